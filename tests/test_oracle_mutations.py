@@ -1,0 +1,68 @@
+"""The oracle's pins have teeth: plausible mistakes planted in a copy of the
+oracle source (on the CPU only) must each fail at least one pin.
+
+Each mutation is a text substitution on ``oracle/mts_oracle.c``; the mutated
+copy is compiled to a temporary library and the pin suites run against it in
+a subprocess.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "mts_oracle.c")
+
+MUTATIONS = {
+    # Eq. 4: headroom charged per running request instead of once per tier
+    "headroom_per_request": [("present[sl[s].tier] = 1;", "present[sl[s].tier] += 1;"),
+                             ("if (present[p]) v256 += x->Hq[rp->group][p];",
+                              "v256 += present[p] * x->Hq[rp->group][p];")],
+    # Eq. 2: head-of-line demand with the wrong sign
+    "hol_sign": [("int64_t v256 = 256 * (phys + demand);", "int64_t v256 = 256 * (phys - demand);")],
+    # Section 3.4: ties in F go to the highest index
+    "dispatch_tie": [("if (best < 0 || f_greater(num[i], den[i], num[best], den[best])) best = (int)i;",
+                      "if (best < 0 || !f_greater(num[best], den[best], num[i], den[i])) best = (int)i;")],
+    # Section 3.4: lowest tier first instead of tier 0 first
+    "dispatch_order": [("for (uint32_t p = 0; p < K; ++p) {\n        for (uint32_t k = 0; k < n; ++k) {",
+                        "for (uint32_t p = K; p-- > 0;) {\n        for (uint32_t k = 0; k < n; ++k) {")],
+    # Eq. 3 reading: the lowest tier keeps its headroom
+    "lowest_tier_headroom": [("if (c->zero_lowest) out[K - 1] = 0;", "")],
+    # preemption takes the oldest instead of the newest request of the worst tier
+    "preempt_order": [("(sl[s].tier == sl[v].tier && sl[s].seq > sl[v].seq)) v = (int)s;",
+                       "(sl[s].tier == sl[v].tier && sl[s].seq < sl[v].seq)) v = (int)s;")],
+    # KV growth one token late
+    "growth_off_by_one": [("if (sl[s].st == ST_RUNNING && sl[s].len % blk == 0) grow++;",
+                           "if (sl[s].st == ST_RUNNING && (sl[s].len + 1) % blk == 0) grow++;")],
+    # Section 3.5: strict instead of non-strict theta threshold
+    "theta_strict": [("if (lhs < rhs) break;", "if (lhs <= rhs) break;")],
+    # Poisson recursion with a wrong index
+    "poisson_index": [("p = p * c->arr_mean / (double)n;", "p = p * c->arr_mean / (double)(n + 1);")],
+    # Philox multiplier typo
+    "philox_constant": [("mulhilo64(0xD2E7470EE14C6C93ULL", "mulhilo64(0xD2E7470EE14C6C95ULL")],
+    # migration candidate: largest instead of smallest KV footprint
+    "candidate_footprint": [("(bs < bc || (bs == bc && sl[s].seq > sl[c].seq))",
+                             "(bs > bc || (bs == bc && sl[s].seq > sl[c].seq))")],
+    # staged copy: commit one stage early
+    "commit_early": [("if (m->copied < b) continue;", "if (m->copied + 1 < b) continue;")],
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_is_caught(name, tmp_path):
+    src = open(SRC).read()
+    for old, new in MUTATIONS[name]:
+        assert src.count(old) == 1, "mutation anchor not found exactly once: %r" % old
+        src = src.replace(old, new)
+    cfile = tmp_path / "mutant.c"
+    cfile.write_text(src)
+    lib = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fPIC", "-shared",
+                           "-o", str(lib), str(cfile), "-lm"])
+    env = dict(os.environ, MTS_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_exact.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, "mutation %s survived every pin:\n%s" % (name, r.stdout[-2000:])
