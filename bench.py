@@ -1,0 +1,161 @@
+"""Benchmark of the multi-tier scheduling step on one MI355X.
+
+A step is one ``mts_step`` call advancing every replica of the workload by
+``--ticks-per-step`` ticks (all phases of the tick: decode/KV accounting,
+admission, freeness, tier-ordered dispatch, migration).  The default workload
+is the K = 1..10 sweep (3840 replicas x 32 instances x 512 slots); 10 timed
+steps of 1000 ticks cover its full 10,000-tick run from an empty cluster.
+Warm-up steps run on a separate handle of the same workload.
+
+Prints one JSON line: replica-ticks/s, slot-updates/s, the roofline of the
+step kernel (HIP-event launch time on the launch stream, algorithmic bytes
+from the run's own counters) and the CPU oracle timed on a bounded sample on
+this host.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def algorithmic_bytes(cfg, R, ticks, d):
+    """Bytes the tick must move per the state layout (meta 1 B per slot per
+    tick; len/rem 8 B read+write per running slot-tick; seq 4 B per waiting
+    slot-tick; 13 B per placed or moved request; 1 B per status change)."""
+    n_slots = R * cfg["n_instances"] * cfg["slots_per_instance"]
+    per = d[:80].reshape(10, 8)
+    dispatched = int(per[:, 2].sum())
+    admitted = int(per[:, 3].sum())
+    finished = int(per[:, 4].sum())
+    preempted = int(per[:, 5].sum())
+    mq, ms, mc, ma = (int(v) for v in d[80:84])
+    run, wait = int(d[84]), int(d[85])
+    placed = dispatched + mq + mc
+    changes = dispatched + admitted + finished + 2 * preempted + 2 * (mq + ms + mc + ma)
+    return n_slots * ticks + 8 * run + 4 * wait + 13 * placed + changes
+
+
+def cpu_baseline(cfg, sample_replicas, sample_ticks):
+    import oracle
+    R = sum(g["n_replicas"] for g in cfg["groups"])
+    stride = max(1, R // sample_replicas)
+    picks = list(range(0, R, stride))[:sample_replicas]
+    t0 = time.perf_counter()
+    for r in picks:
+        o = oracle.Oracle(cfg, r, 1, check=False)
+        o.step(sample_ticks)
+        o.close()
+    dt = time.perf_counter() - t0
+    rt = len(picks) * sample_ticks / dt
+    return {"value": rt, "unit": "replica-ticks/s", "cores": 1, "kind": "oracle",
+            "slot_updates_per_s": rt * cfg["n_instances"] * cfg["slots_per_instance"],
+            "sample": "%d replicas spread over the groups x %d ticks from an empty cluster, single thread, %.1f s"
+                      % (len(picks), sample_ticks, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="sweep")
+    ap.add_argument("--ticks-per-step", type=int, default=1000)
+    ap.add_argument("--threads", type=int, default=0)
+    ap.add_argument("--blocks", type=int, default=0)
+    ap.add_argument("--cpu-replicas", type=int, default=10)
+    ap.add_argument("--cpu-ticks", type=int, default=4000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the replicas are independent, so a multi-GPU run "
+              "is R/N replicas per GPU with no communication; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_16336_amd import Scheduler
+    from workloads import preset
+
+    cfg = preset(args.workload)
+    R = sum(g["n_replicas"] for g in cfg["groups"])
+    T, K, W = args.ticks_per_step, args.steps, args.warmup
+    torch.cuda.set_device(0)
+
+    if W > 0:
+        warm = Scheduler(cfg)
+        if args.threads or args.blocks:
+            warm.set_launch(args.threads, args.blocks)
+        for _ in range(W):
+            warm.step(T)
+        torch.cuda.synchronize()
+        warm.close()
+        del warm
+
+    sch = Scheduler(cfg)
+    if args.threads or args.blocks:
+        sch.set_launch(args.threads, args.blocks)
+    torch.cuda.synchronize()
+    s0 = sch.stats()["raw"].astype(np.int64)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        ev[2 * k].record(stream)
+        sch.step(T, stream=stream)
+        ev[2 * k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    launch_ms = [ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(K)]
+    s1 = sch.stats()
+    d = s1["raw"].astype(np.int64) - s0
+    if d[86] != 0:
+        print("device invariant checks failed: %d" % d[86], file=sys.stderr)
+        sys.exit(1)
+
+    rticks = R * T * K
+    value = rticks / wall
+    slots = cfg["n_instances"] * cfg["slots_per_instance"]
+    b_alg = algorithmic_bytes(cfg, R, T * K, d)
+    avg_launch_s = float(np.mean(launch_ms)) / 1e3
+    achieved = b_alg / K / avg_launch_s / 1e9
+
+    out = {
+        "metric": "replica-ticks/s and request-slot updates/s at 1 MI355X; % of HBM roofline",
+        "value": value,
+        "unit": "replica-ticks/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": wall / K * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic (seeded Philox arrivals, on-device sampling)",
+        "config": {"workload": cfg["name"], "replicas": R, "instances": cfg["n_instances"],
+                   "slots_per_instance": cfg["slots_per_instance"], "ticks_per_step": T,
+                   "ticks_timed": T * K, "parallelism": "replicas across workgroups"},
+        "slot_updates_per_s": value * slots,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "k_step", "avg_launch_ms": avg_launch_s * 1e3,
+                     "algorithmic_bytes_per_launch": b_alg / K},
+        "digest": "%016x" % int(s1["digest"]),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_replicas, args.cpu_ticks)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

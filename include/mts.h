@@ -1,0 +1,220 @@
+/*
+ * mts.h -- multi-tier Llumnix scheduling step on MI355X (gfx950).
+ *
+ * A handle owns R independent simulated clusters ("replicas").  Each replica
+ * has I serving instances with KV capacity M blocks and S request slots each.
+ * mts_step advances every replica by n scheduling ticks on the GPU.  One tick
+ * of one replica:
+ *   A  decode one token per running request; a request whose length is a
+ *      multiple of the block size needs a new KV block; when an instance
+ *      cannot grant every new block it preempts its lowest-priority running
+ *      requests (largest tier, then newest) back to its queue; a request
+ *      whose output is complete finishes and frees its blocks
+ *      (Section 2.1 block-based KV cache, Section 2.2 preemption, Section 3.1)
+ *   A2 a migration whose source request was preempted or finished returns
+ *      its destination reservation (Section 3.5)
+ *   B  each instance admits its head-of-line request (smallest (tier, seq))
+ *      while its blocks fit (Section 3.1; Eq. 2 head-of-line demand)
+ *   C  freeness F = (M - sum_r V(r)) / B with per-tier headroom
+ *      H_p = h0 * gamma^p charged once per present tier (Eq. 1-4)
+ *   D  this tick's arrivals are sampled and dispatched tier 0 first, FCFS
+ *      within a tier, each to the instance with the largest F that has a
+ *      free slot (Section 3.4)
+ *   E  in-flight migrations copy one stage of KV blocks (commit when all are
+ *      copied, abort when a stage does not fit); on interval ticks
+ *      instances are ranked by F and low-F sources (F < 0) are paired with
+ *      high-F destinations while the gap is at least theta; each source
+ *      moves its head-of-line queued request, else starts a staged copy of
+ *      its lowest-priority, smallest running request (Section 3.5, Fig. 4)
+ * All scheduler state and arithmetic is integer; headroom is fixed point at
+ * 1/256 block and freeness values are compared exactly.
+ *
+ * Conventions: every function returns MTS_OK (0) or a negative MTS_E* code
+ * and never throws.  Host pointers are plain CPU memory; the device buffer
+ * passed to mts_create is device memory owned by the caller.  A handle is not
+ * thread-safe; calls on one handle must not overlap.
+ */
+#ifndef MTS_H
+#define MTS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MTS_ABI_VERSION 1
+#define MTS_MAX_TIERS 10
+#define MTS_NSTAT 88
+
+enum {
+    MTS_OK = 0,
+    MTS_EINVAL = -1,  /* bad argument or configuration outside the limits below */
+    MTS_ENOMEM = -2,  /* device buffer too small, or host allocation failed */
+    MTS_EDEVICE = -3, /* a HIP call failed */
+    MTS_ESTATE = -4,  /* a device-side invariant check failed (see mts_stats) */
+    MTS_ERANGE = -5   /* replica range or table index out of range; tick/seq counter would overflow */
+};
+
+/* tier distributions (Section 4.2) */
+enum { MTS_TIERS_UNIFORM = 0,   /* P(k) = 1/K */
+       MTS_TIERS_GAUSS = 1,     /* P(tier <= k) = Phi((k + 1/2 - p0) / p1), tails lumped */
+       MTS_TIERS_GEOMETRIC = 2, /* P(k) proportional to p0^(K-1-k) */
+       MTS_TIERS_EXPLICIT = 3 };/* P(k) proportional to probs[k] */
+/* per-tick arrival count (Section 4.4) */
+enum { MTS_ARRIVAL_POISSON = 0,       /* Poisson(arrival_mean) */
+       MTS_ARRIVAL_GAMMA_POISSON = 1 };/* gamma-mixed Poisson: mean, coefficient of variation */
+/* prompt length in tokens */
+enum { MTS_PROMPT_UNIFORM_INT = 0,    /* uniform on [prompt_lo, prompt_hi] */
+       MTS_PROMPT_LOGNORMAL = 1 };    /* P(len <= n) = Phi((ln(n + 1/2) - mu) / sigma), clipped */
+/* output length in tokens */
+enum { MTS_OUTPUT_GEOMETRIC = 0,      /* support {1, 2, ...}, mean output_param */
+       MTS_OUTPUT_PARETO = 1 };       /* min(floor(output_min * U^(-1/output_param)), output_cap) */
+
+/* A group of consecutive replicas sharing a tier count and tier mix. */
+typedef struct mts_group {
+    uint32_t n_replicas;  /* >= 1 */
+    uint32_t K;           /* tiers, 1..10; tier 0 is the highest priority */
+    uint32_t tier_kind;   /* MTS_TIERS_* */
+    uint32_t reserved;    /* must be 0 */
+    double p0, p1;        /* GAUSS: mu, sigma > 0; GEOMETRIC: ratio in (0, 1] */
+    double probs[MTS_MAX_TIERS]; /* EXPLICIT: K non-negative weights, positive sum */
+} mts_group;
+
+typedef struct mts_cfg {
+    uint32_t abi_version;        /* MTS_ABI_VERSION */
+    uint32_t n_instances;        /* I: 1..256 */
+    uint32_t slots_per_instance; /* S: multiple of 64, 64..4096 */
+    uint32_t kv_blocks;          /* M: 1..2^21 blocks per instance */
+    uint32_t block_tokens;       /* tokens per KV block: power of two, 1..1024 */
+    uint32_t zero_lowest_tier;   /* 1: the lowest tier K-1 gets no headroom */
+    double headroom_base;        /* h0 in blocks (Eq. 3: h0 = M * h_max), >= 0 */
+    double headroom_decay;       /* gamma = e^-lambda, in [0, 1] */
+    uint32_t mig_interval;       /* pairing happens on ticks t with t % interval == 0; >= 1 */
+    uint32_t mig_stage_blocks;   /* B_stage: blocks copied per stage (one stage per tick); >= 1 */
+    uint32_t mig_max_pairs;      /* pairs per round, <= I / 2 */
+    int32_t theta_num, theta_den;/* theta = num/den in blocks per running request; 0 <= num < 2^20, 1 <= den <= 1024 */
+    uint32_t arrival_kind;       /* MTS_ARRIVAL_* */
+    uint32_t prompt_kind;        /* MTS_PROMPT_* */
+    uint32_t output_kind;        /* MTS_OUTPUT_* */
+    uint32_t reserved;           /* must be 0 */
+    double arrival_mean;         /* > 0 */
+    double arrival_cv;           /* GAMMA_POISSON: > 0 */
+    double prompt_mu, prompt_sigma; /* LOGNORMAL */
+    uint32_t prompt_lo, prompt_hi;  /* 1 <= lo <= hi */
+    double output_param;         /* GEOMETRIC: mean >= 1; PARETO: alpha > 0 */
+    uint32_t output_min, output_cap; /* PARETO: 1 <= min <= cap */
+    uint64_t seed;               /* Philox key word 0 */
+    uint64_t replica_id_base;    /* replica r draws with Philox key (seed, replica_id_base + r) */
+    uint32_t n_groups;           /* >= 1 */
+    uint32_t reserved2;          /* must be 0 */
+    const mts_group* groups;     /* n_groups entries, copied by mts_create */
+} mts_cfg;
+
+/* Counters summed over all replicas (mts_stats) or per replica
+ * (mts_export_state).  Index layout of the raw arrays: per_tier[p][f] is
+ * element p * 8 + f, the scalar counters follow at 80..87. */
+enum { MTS_F_ARRIVED = 0, MTS_F_REJECTED, MTS_F_DISPATCHED, MTS_F_ADMITTED,
+       MTS_F_FINISHED, MTS_F_PREEMPTED, MTS_F_QDELAY_SUM, MTS_F_E2E_SUM };
+typedef struct mts_stats_t {
+    uint64_t per_tier[MTS_MAX_TIERS][8];
+    uint64_t mig_queued, mig_started, mig_committed, mig_aborted;
+    uint64_t run_slot_ticks, wait_slot_ticks;  /* running / waiting requests summed over ticks */
+    uint64_t invariant_violations;             /* device-side checks that failed */
+    uint64_t ticks;                            /* replica-ticks executed */
+    uint64_t replicas;
+    uint64_t digest;  /* wrapping sum of the per-replica state digests */
+} mts_stats_t;
+
+/* Host views of the canonical state of replicas [r0, r0 + nr), all arrays
+ * dense in (replica, instance, slot) order:
+ *   meta[nr*I*S]  status | tier << 2 | admitted-once << 6 | migrating-out << 7,
+ *                 status 0 empty, 1 waiting, 2 running, 3 inbound reservation
+ *   lr[nr*I*S]    len | rem << 16 (tokens so far, output tokens left)
+ *   seq[nr*I*S]   per-replica arrival sequence number
+ *   tarr[nr*I*S]  arrival tick
+ *   free[nr*I]    free KV blocks
+ *   mig[nr*I*4]   per source instance: dst (-1 none), src slot, dst slot, blocks copied
+ *   next_seq[nr], stats[nr*MTS_NSTAT]
+ * Empty slots are all-zero. */
+typedef struct mts_state_view {
+    uint8_t* meta;
+    uint32_t* lr;
+    uint32_t* seq;
+    uint32_t* tarr;
+    int32_t* free;
+    int32_t* mig;
+    uint32_t* next_seq;
+    uint64_t* stats;
+} mts_state_view;
+
+typedef struct mts_ctx* mts_handle;
+
+/* Validate cfg and report the device bytes mts_create needs.
+ * Returns MTS_EINVAL for a configuration outside the limits above. */
+int mts_state_bytes(const mts_cfg* cfg, size_t* bytes);
+
+/* Validate cfg, build the sampling and headroom tables (host, double
+ * precision), copy them into dev_buf and initialise every replica to an
+ * empty cluster (all slots empty, free = M, tick 0).  dev_buf is device
+ * memory of at least mts_state_bytes bytes, 256-byte aligned, owned by the
+ * caller and kept alive until mts_destroy.  The initialisation is enqueued
+ * on stream.  On success *out receives the handle. */
+int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stream, mts_handle* out);
+
+/* Enqueue n_ticks ticks of every replica on stream and return after the
+ * launch (asynchronous).  n_ticks = 0 is a no-op.  MTS_ERANGE if the tick or
+ * sequence counters could overflow 32 bits. */
+int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream);
+
+/* Synchronise with the last stream used on h, sum the per-replica counters
+ * and compute the state digest.  Returns MTS_ESTATE (with *out filled) when
+ * a device-side invariant check failed. */
+int mts_stats(mts_handle h, mts_stats_t* out);
+
+/* Per-replica state digests of replicas [r0, r0 + nr) into out[nr]
+ * (wrapping sum of SplitMix64-mixed slot and instance records). */
+int mts_digest(mts_handle h, uint32_t r0, uint32_t nr, uint64_t* out);
+
+/* Copy the canonical state of replicas [r0, r0 + nr) to host arrays
+ * (synchronises with the last stream used). */
+int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* out);
+
+/* Overwrite the state of replicas [r0, r0 + nr) from host arrays in the
+ * canonical layout (synchronous).  The state is taken as given; the device
+ * invariant checks report inconsistencies at the next mts_step. */
+int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* in);
+
+/* The library's own tables, for comparison with an independent build:
+ * which = 0 tier CDF of group g, 1 arrival count, 2 prompt length, 3 output
+ * length.  out[j] = floor(2^32 * CDF(base + j)), last entry 2^32; *len is
+ * the table length (written even when cap is smaller), *base its first value. */
+int mts_get_table(mts_handle h, int which, uint32_t g, uint64_t* out, uint32_t cap,
+                  uint32_t* len, uint32_t* base);
+
+/* Headroom of group g in 1/256 block (Eq. 3 with the lowest tier rule). */
+int mts_get_headroom(mts_handle h, uint32_t g, int32_t out[MTS_MAX_TIERS]);
+
+/* Next tick to execute (ticks done so far). */
+uint64_t mts_tick(mts_handle h);
+
+/* Set the next tick to execute, e.g. after mts_import_state of a state saved
+ * at that tick.  MTS_ERANGE if it does not fit the 32-bit tick fields. */
+int mts_set_tick(mts_handle h, uint64_t tick);
+
+/* Force the launch shape (threads per block, blocks); 0 keeps the automatic
+ * choice.  threads must be a multiple of 64 up to 1024. */
+int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks);
+
+/* Free the handle's host memory.  dev_buf stays with the caller. */
+void mts_destroy(mts_handle h);
+
+const char* mts_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MTS_H */

@@ -1,0 +1,401 @@
+// libmts C ABI: handle management, device buffer layout, launches, state
+// export/import and counter reduction.  See include/mts.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "mts_internal.h"
+
+using namespace mts;
+
+struct mts_ctx {
+    mts_cfg cfg{};
+    std::vector<mts_group> groups;
+    Tables tables;
+    Layout lay{};
+    char* dev = nullptr;
+    size_t bytes = 0;
+    uint32_t R = 0, I = 0, S = 0;
+    uint64_t tick = 0;
+    uint32_t max_arrivals = 0;
+    uint32_t threads = 0, blocks = 0;  // launch shape (auto unless forced)
+    uint32_t scratch_blocks = 0;       // blocks the scratch area is sized for
+    int device = 0;
+    hipStream_t last = nullptr;
+    std::vector<uint16_t> group_of;
+    std::vector<uint32_t> group_K;
+};
+
+namespace {
+
+size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
+
+uint32_t total_replicas(const mts_cfg& c)
+{
+    uint64_t R = 0;
+    for (uint32_t g = 0; g < c.n_groups; ++g) R += c.groups[g].n_replicas;
+    return uint32_t(R);
+}
+
+// blocks of the step kernel the scratch area must serve
+uint32_t scratch_blocks_for(uint32_t R) { return std::min<uint32_t>(R, 8192); }
+
+Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t scratch_blocks, uint32_t max_arrivals)
+{
+    Layout L{};
+    const size_t I = c.n_instances, S = c.slots_per_instance;
+    const size_t N = size_t(R) * I * S;
+    size_t o = 0;
+    L.tier_q = o;   o = up256(o + size_t(c.n_groups) * MTS_MAX_TIERS * 4);
+    L.hq = o;       o = up256(o + size_t(c.n_groups) * MTS_MAX_TIERS * 4);
+    L.group_K = o;  o = up256(o + size_t(c.n_groups) * 4);
+    L.count_q = o;  o = up256(o + T.count.q.size() * 4);
+    L.prompt_q = o; o = up256(o + T.prompt.q.size() * 4);
+    L.output_q = o; o = up256(o + T.output.q.size() * 4);
+    L.group_of = o; o = up256(o + size_t(R) * 2);
+    L.meta = o;     o = up256(o + N);
+    L.lr = o;       o = up256(o + N * 4);
+    L.seq = o;      o = up256(o + N * 4);
+    L.tarr = o;     o = up256(o + N * 4);
+    L.freeb = o;    o = up256(o + size_t(R) * I * 4);
+    L.mig = o;      o = up256(o + size_t(R) * I * 16);
+    L.next_seq = o; o = up256(o + size_t(R) * 4);
+    L.stats = o;    o = up256(o + size_t(R) * MTS_NSTAT * 8);
+    L.digest = o;   o = up256(o + size_t(R) * 8);
+    L.scratch = o;  o = up256(o + size_t(scratch_blocks) * 2 * max_arrivals * 8);
+    L.total = o;
+    return L;
+}
+
+Params make_params(const mts_ctx* h)
+{
+    Params p{};
+    char* d = h->dev;
+    const mts_cfg& c = h->cfg;
+    p.R = h->R; p.I = h->I; p.S = h->S; p.W = h->S / 64;
+    p.M = c.kv_blocks;
+    uint32_t sh = 0;
+    while ((1u << sh) < c.block_tokens) ++sh;
+    p.blk_shift = sh;
+    p.mig_interval = c.mig_interval; p.mig_stage = c.mig_stage_blocks; p.mig_max_pairs = c.mig_max_pairs;
+    p.theta_num = c.theta_num; p.theta_den = c.theta_den;
+    p.count_n = uint32_t(h->tables.count.q.size());
+    p.prompt_n = uint32_t(h->tables.prompt.q.size());
+    p.output_n = uint32_t(h->tables.output.q.size());
+    p.count_base = h->tables.count.base;
+    p.prompt_base = h->tables.prompt.base;
+    p.output_base = h->tables.output.base;
+    p.max_arrivals = h->max_arrivals;
+    p.seed = c.seed;
+    p.id_base = c.replica_id_base;
+    const Layout& L = h->lay;
+    p.tier_q = reinterpret_cast<const uint32_t*>(d + L.tier_q);
+    p.hq = reinterpret_cast<const int32_t*>(d + L.hq);
+    p.group_K32 = reinterpret_cast<const uint32_t*>(d + L.group_K);
+    p.count_q = reinterpret_cast<const uint32_t*>(d + L.count_q);
+    p.prompt_q = reinterpret_cast<const uint32_t*>(d + L.prompt_q);
+    p.output_q = reinterpret_cast<const uint32_t*>(d + L.output_q);
+    p.group_of = reinterpret_cast<const uint16_t*>(d + L.group_of);
+    p.meta = reinterpret_cast<uint8_t*>(d + L.meta);
+    p.lr = reinterpret_cast<uint32_t*>(d + L.lr);
+    p.seq = reinterpret_cast<uint32_t*>(d + L.seq);
+    p.tarr = reinterpret_cast<uint32_t*>(d + L.tarr);
+    p.freeb = reinterpret_cast<int32_t*>(d + L.freeb);
+    p.mig = reinterpret_cast<int32_t*>(d + L.mig);
+    p.next_seq = reinterpret_cast<uint32_t*>(d + L.next_seq);
+    p.stats = reinterpret_cast<unsigned long long*>(d + L.stats);
+    p.digest = reinterpret_cast<unsigned long long*>(d + L.digest);
+    p.scratch = reinterpret_cast<unsigned long long*>(d + L.scratch);
+    return p;
+}
+
+// u32 device image of a table: its first n-1 entries (the last, 2^32, is implicit)
+std::vector<uint32_t> device_table(const Table& t, size_t pad_to = 0)
+{
+    std::vector<uint32_t> v(std::max(t.q.size() - 1, pad_to), 0);
+    for (size_t j = 0; j + 1 < t.q.size(); ++j) v[j] = uint32_t(t.q[j]);
+    return v;
+}
+
+int hip_rc(hipError_t e) { return e == hipSuccess ? MTS_OK : MTS_EDEVICE; }
+
+int prepare(const mts_cfg* cfg, mts_ctx& x)
+{
+    if (!cfg) return MTS_EINVAL;
+    int rc = validate(*cfg);
+    if (rc) return rc;
+    x.cfg = *cfg;
+    x.groups.assign(cfg->groups, cfg->groups + cfg->n_groups);
+    x.cfg.groups = x.groups.data();
+    rc = build_tables(x.cfg, x.tables);
+    if (rc) return rc;
+    x.R = total_replicas(x.cfg);
+    x.I = cfg->n_instances;
+    x.S = cfg->slots_per_instance;
+    x.max_arrivals = uint32_t(x.tables.count.base + x.tables.count.q.size());
+    x.scratch_blocks = scratch_blocks_for(x.R);
+    x.lay = make_layout(x.cfg, x.tables, x.R, x.scratch_blocks, x.max_arrivals);
+    return MTS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mts_strerror(int code)
+{
+    switch (code) {
+    case MTS_OK: return "ok";
+    case MTS_EINVAL: return "invalid argument or configuration";
+    case MTS_ENOMEM: return "buffer too small or out of memory";
+    case MTS_EDEVICE: return "HIP runtime error";
+    case MTS_ESTATE: return "device invariant check failed";
+    case MTS_ERANGE: return "index or counter out of range";
+    default: return "unknown error";
+    }
+}
+
+int mts_state_bytes(const mts_cfg* cfg, size_t* bytes)
+{
+    if (!bytes) return MTS_EINVAL;
+    mts_ctx x;
+    int rc = prepare(cfg, x);
+    if (rc) return rc;
+    *bytes = x.lay.total;
+    return MTS_OK;
+}
+
+int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stream, mts_handle* out)
+{
+    if (!out || !dev_buf || (reinterpret_cast<uintptr_t>(dev_buf) & 255)) return MTS_EINVAL;
+    *out = nullptr;
+    mts_ctx* x = new (std::nothrow) mts_ctx;
+    if (!x) return MTS_ENOMEM;
+    int rc = prepare(cfg, *x);
+    if (rc) { delete x; return rc; }
+    if (bytes < x->lay.total) { delete x; return MTS_ENOMEM; }
+    x->dev = static_cast<char*>(dev_buf);
+    x->bytes = bytes;
+    if (hipGetDevice(&x->device) != hipSuccess) { delete x; return MTS_EDEVICE; }
+    int max_lds = 0;
+    if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, x->device) != hipSuccess) {
+        delete x;
+        return MTS_EDEVICE;
+    }
+    if (lds_bytes(x->I, x->S) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
+
+    // tables and per-replica group index
+    const uint32_t G = x->cfg.n_groups;
+    std::vector<uint32_t> tier(size_t(G) * MTS_MAX_TIERS, 0);
+    for (uint32_t g = 0; g < G; ++g) {
+        const Table& t = x->tables.tier[g];
+        for (size_t j = 0; j + 1 < t.q.size(); ++j) tier[size_t(g) * MTS_MAX_TIERS + j] = uint32_t(t.q[j]);
+        x->group_K.push_back(x->groups[g].K);
+    }
+    for (uint32_t g = 0; g < G; ++g)
+        for (uint32_t k = 0; k < x->groups[g].n_replicas; ++k) x->group_of.push_back(uint16_t(g));
+    const std::vector<uint32_t> cq = device_table(x->tables.count, 1), pq = device_table(x->tables.prompt, 1),
+                                oq = device_table(x->tables.output, 1);
+    const Layout& L = x->lay;
+    hipError_t e = hipSuccess;
+    auto up = [&](size_t off, const void* src, size_t n) {
+        if (e == hipSuccess && n) e = hipMemcpyAsync(x->dev + off, src, n, hipMemcpyHostToDevice, stream);
+    };
+    up(L.tier_q, tier.data(), tier.size() * 4);
+    up(L.hq, x->tables.hq.data(), x->tables.hq.size() * 4);
+    up(L.group_K, x->group_K.data(), x->group_K.size() * 4);
+    up(L.count_q, cq.data(), cq.size() * 4);
+    up(L.prompt_q, pq.data(), pq.size() * 4);
+    up(L.output_q, oq.data(), oq.size() * 4);
+    up(L.group_of, x->group_of.data(), x->group_of.size() * 2);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);  // host vectors go out of scope
+    if (e != hipSuccess) { delete x; return MTS_EDEVICE; }
+    const Params p = make_params(x);
+    if (launch_init(p, stream) != 0) { delete x; return MTS_EDEVICE; }
+    x->last = stream;
+    *out = x;
+    return MTS_OK;
+}
+
+int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks)
+{
+    if (!h) return MTS_EINVAL;
+    if (threads && (threads % 64 || threads > 1024)) return MTS_EINVAL;
+    if (blocks > h->scratch_blocks) return MTS_EINVAL;
+    h->threads = threads;
+    h->blocks = blocks;
+    return MTS_OK;
+}
+
+int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
+{
+    if (!h) return MTS_EINVAL;
+    if (n_ticks == 0) return MTS_OK;
+    // tarr holds a tick in 32 bits; seq grows by at most max_arrivals - 1 per tick
+    const uint64_t end = h->tick + n_ticks;
+    if (end > 0xFFFFFFFFull || end * uint64_t(h->max_arrivals) > 0xFFFFFFFFull) return MTS_ERANGE;
+    Params p = make_params(h);
+    p.tick0 = h->tick;
+    p.n_ticks = n_ticks;
+    uint32_t threads = h->threads ? h->threads : std::min<uint32_t>(1024, std::max<uint32_t>(64, 64 * h->I));
+    uint32_t blocks = h->blocks;
+    if (!blocks) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess) return MTS_EDEVICE;
+        const uint32_t per_cu_waves = 32 / (threads / 64);
+        const size_t lds = lds_bytes(h->I, h->S);
+        const uint32_t per_cu_lds = uint32_t(std::max<size_t>(1, (160 * 1024) / std::max<size_t>(lds, 1)));
+        const uint32_t per_cu = std::max<uint32_t>(1, std::min(per_cu_waves, per_cu_lds));
+        blocks = std::min<uint32_t>(h->R, uint32_t(cus) * per_cu);
+    }
+    blocks = std::min(blocks, h->scratch_blocks);
+    if (launch_step(p, threads, blocks, stream) != 0) return MTS_EDEVICE;
+    h->tick = end;
+    h->last = stream;
+    return MTS_OK;
+}
+
+int mts_digest(mts_handle h, uint32_t r0, uint32_t nr, uint64_t* out)
+{
+    if (!h || !out) return MTS_EINVAL;
+    if (r0 > h->R || nr > h->R - r0) return MTS_ERANGE;
+    const Params p = make_params(h);
+    if (launch_digest(p, r0, nr, h->last) != 0) return MTS_EDEVICE;
+    hipError_t e = hipMemcpyAsync(out, h->dev + h->lay.digest + size_t(r0) * 8, size_t(nr) * 8, hipMemcpyDeviceToHost, h->last);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last);
+    return hip_rc(e);
+}
+
+int mts_stats(mts_handle h, mts_stats_t* out)
+{
+    if (!h || !out) return MTS_EINVAL;
+    std::vector<uint64_t> st(size_t(h->R) * MTS_NSTAT), dg(h->R);
+    hipError_t e = hipStreamSynchronize(h->last);
+    if (e == hipSuccess)
+        e = hipMemcpy(st.data(), h->dev + h->lay.stats, st.size() * 8, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return MTS_EDEVICE;
+    int rc = mts_digest(h, 0, h->R, dg.data());
+    if (rc) return rc;
+    uint64_t sum[MTS_NSTAT] = {0};
+    for (uint32_t r = 0; r < h->R; ++r)
+        for (int k = 0; k < MTS_NSTAT; ++k) sum[k] += st[size_t(r) * MTS_NSTAT + k];
+    std::memset(out, 0, sizeof(*out));
+    std::memcpy(out->per_tier, sum, 80 * 8);
+    out->mig_queued = sum[kMigQueued];
+    out->mig_started = sum[kMigStarted];
+    out->mig_committed = sum[kMigCommitted];
+    out->mig_aborted = sum[kMigAborted];
+    out->run_slot_ticks = sum[kRunSlotTicks];
+    out->wait_slot_ticks = sum[kWaitSlotTicks];
+    out->invariant_violations = sum[kInvariant];
+    out->ticks = sum[kTicks];
+    out->replicas = h->R;
+    uint64_t d = 0;
+    for (uint64_t v : dg) d += v;
+    out->digest = d;
+    return out->invariant_violations ? MTS_ESTATE : MTS_OK;
+}
+
+int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* v)
+{
+    if (!h || !v) return MTS_EINVAL;
+    if (r0 > h->R || nr > h->R - r0) return MTS_ERANGE;
+    const size_t IS = size_t(h->I) * h->S, I = h->I;
+    const Layout& L = h->lay;
+    hipError_t e = hipStreamSynchronize(h->last);
+    auto get = [&](void* dst, size_t off, size_t n) {
+        if (e == hipSuccess && dst && n) e = hipMemcpy(dst, h->dev + off, n, hipMemcpyDeviceToHost);
+    };
+    get(v->meta, L.meta + size_t(r0) * IS, size_t(nr) * IS);
+    get(v->lr, L.lr + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
+    get(v->seq, L.seq + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
+    get(v->tarr, L.tarr + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
+    get(v->free, L.freeb + size_t(r0) * I * 4, size_t(nr) * I * 4);
+    get(v->mig, L.mig + size_t(r0) * I * 16, size_t(nr) * I * 16);
+    get(v->next_seq, L.next_seq + size_t(r0) * 4, size_t(nr) * 4);
+    get(v->stats, L.stats + size_t(r0) * MTS_NSTAT * 8, size_t(nr) * MTS_NSTAT * 8);
+    return hip_rc(e);
+}
+
+int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* v)
+{
+    if (!h || !v || !v->meta || !v->lr || !v->seq || !v->tarr || !v->free || !v->mig || !v->next_seq || !v->stats)
+        return MTS_EINVAL;
+    if (r0 > h->R || nr > h->R - r0) return MTS_ERANGE;
+    const size_t IS = size_t(h->I) * h->S, I = h->I;
+    // structural checks keep every index the kernel derives from the state in range
+    for (uint32_t r = 0; r < nr; ++r) {
+        const uint32_t K = h->group_K[h->group_of[r0 + r]];
+        for (size_t s = 0; s < IS; ++s) {
+            const uint8_t m = v->meta[size_t(r) * IS + s];
+            const uint32_t st = m & 3u, lr = v->lr[size_t(r) * IS + s];
+            if ((st == kWaiting || st == kRunning) && (((m >> 2) & 15u) >= K || (lr & 0xFFFFu) == 0 || (lr >> 16) == 0))
+                return MTS_EINVAL;
+            if (st == kEmpty && m != 0) return MTS_EINVAL;
+        }
+        for (size_t i = 0; i < I; ++i) {
+            const int32_t* m = v->mig + (size_t(r) * I + i) * 4;
+            if (m[0] < -1 || m[0] >= int32_t(I) || m[0] == int32_t(i)) return MTS_EINVAL;
+            if (m[0] >= 0 && (m[1] < 0 || m[1] >= int32_t(h->S) || m[2] < 0 || m[2] >= int32_t(h->S) || m[3] < 0))
+                return MTS_EINVAL;
+            const int32_t f = v->free[size_t(r) * I + i];
+            if (f < -int32_t(h->cfg.kv_blocks) || f > int32_t(h->cfg.kv_blocks)) return MTS_EINVAL;
+        }
+    }
+    const Layout& L = h->lay;
+    hipError_t e = hipStreamSynchronize(h->last);
+    auto put = [&](size_t off, const void* src, size_t n) {
+        if (e == hipSuccess && n) e = hipMemcpy(h->dev + off, src, n, hipMemcpyHostToDevice);
+    };
+    put(L.meta + size_t(r0) * IS, v->meta, size_t(nr) * IS);
+    put(L.lr + size_t(r0) * IS * 4, v->lr, size_t(nr) * IS * 4);
+    put(L.seq + size_t(r0) * IS * 4, v->seq, size_t(nr) * IS * 4);
+    put(L.tarr + size_t(r0) * IS * 4, v->tarr, size_t(nr) * IS * 4);
+    put(L.freeb + size_t(r0) * I * 4, v->free, size_t(nr) * I * 4);
+    put(L.mig + size_t(r0) * I * 16, v->mig, size_t(nr) * I * 16);
+    put(L.next_seq + size_t(r0) * 4, v->next_seq, size_t(nr) * 4);
+    put(L.stats + size_t(r0) * MTS_NSTAT * 8, v->stats, size_t(nr) * MTS_NSTAT * 8);
+    return hip_rc(e);
+}
+
+int mts_get_table(mts_handle h, int which, uint32_t g, uint64_t* out, uint32_t cap, uint32_t* len, uint32_t* base)
+{
+    if (!h || !len || !base || (cap && !out)) return MTS_EINVAL;
+    const Table* t = nullptr;
+    switch (which) {
+    case 0: if (g >= h->cfg.n_groups) return MTS_ERANGE; t = &h->tables.tier[g]; break;
+    case 1: t = &h->tables.count; break;
+    case 2: t = &h->tables.prompt; break;
+    case 3: t = &h->tables.output; break;
+    default: return MTS_ERANGE;
+    }
+    *len = uint32_t(t->q.size());
+    *base = t->base;
+    for (uint32_t j = 0; j < cap && j < t->q.size(); ++j) out[j] = t->q[j];
+    return MTS_OK;
+}
+
+int mts_get_headroom(mts_handle h, uint32_t g, int32_t out[MTS_MAX_TIERS])
+{
+    if (!h || !out) return MTS_EINVAL;
+    if (g >= h->cfg.n_groups) return MTS_ERANGE;
+    std::memcpy(out, &h->tables.hq[size_t(g) * MTS_MAX_TIERS], MTS_MAX_TIERS * 4);
+    return MTS_OK;
+}
+
+uint64_t mts_tick(mts_handle h) { return h ? h->tick : 0; }
+
+int mts_set_tick(mts_handle h, uint64_t tick)
+{
+    if (!h) return MTS_EINVAL;
+    if (tick > 0xFFFFFFFFull) return MTS_ERANGE;
+    h->tick = tick;
+    return MTS_OK;
+}
+
+void mts_destroy(mts_handle h) { delete h; }
+
+}  // extern "C"

@@ -1,0 +1,212 @@
+"""GPU parity: the HIP path against the CPU oracle, bit-exact.
+
+Every comparison is element by element over the canonical state (slot meta,
+len/rem, seq, arrival tick, free blocks, migration records, sequence counter)
+and the per-replica counters, all integers.  Calls go through the C ABI via
+the ctypes binding.
+"""
+import random
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from workloads import preset, scaled  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU-only hosts, never run there
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2608_16336_amd import Scheduler  # noqa: E402
+from paper_2608_16336_amd.mts import MtsError  # noqa: E402
+
+
+def assert_same(gpu, ref, what=""):
+    for k in ref:
+        a, b = gpu[k], ref[k]
+        if not np.array_equal(a, b):
+            idx = np.nonzero(a != b)[0][:8]
+            raise AssertionError("%s field %s differs at %s: gpu %s oracle %s" % (what, k, idx, a[idx], b[idx]))
+
+
+def run_both(cfg, ticks, r_sample=None):
+    g = Scheduler(cfg)
+    g.step(ticks)
+    torch.cuda.synchronize()
+    R = g.R
+    picks = range(R) if r_sample is None else r_sample
+    for r in picks:
+        o = oracle.Oracle(cfg, r, 1)
+        o.step(ticks)
+        assert_same(g.export(r, 1), o.export(), "replica %d" % r)
+        assert np.array_equal(g.digests(r, 1), o.digests())
+    return g
+
+
+@pytest.mark.parametrize("name", ["tiny", "enterprise", "gauss10", "sweep", "wide"])
+def test_tables_match_oracle(name):
+    c = scaled(name, replicas_per_group=1)
+    g = Scheduler(c)
+    o = oracle.Oracle(c, 0, len(c["groups"]))
+    for w in ("count", "prompt", "output"):
+        bg, qg = g.table(w)
+        bo, qo = o.table(w)
+        assert bg == bo and np.array_equal(qg, qo), w
+    for gi in range(len(c["groups"])):
+        bg, qg = g.table("tier", gi)
+        bo, qo = o.table("tier", gi)
+        assert bg == bo and np.array_equal(qg, qo)
+        assert np.array_equal(g.headroom(gi), o.headroom(gi))
+
+
+def test_tiny_full_state_every_tick():
+    cfg = preset("tiny")
+    g = Scheduler(cfg)
+    o = oracle.Oracle(cfg)
+    for t in range(cfg["ticks"]):
+        g.step(1)
+        o.step(1)
+        assert_same(g.export(), o.export(), "tick %d" % t)
+    s = g.stats()
+    assert s["raw"][86] == 0 and s["raw"][87] == cfg["ticks"]
+
+
+@pytest.mark.parametrize("name,rpg,ticks", [
+    ("enterprise", 12, 600),
+    ("gauss10", 12, 600),
+    ("sweep", 1, 400),
+    ("wide", 2, 150),
+])
+def test_presets_reduced(name, rpg, ticks):
+    cfg = scaled(name, replicas_per_group=rpg)
+    g = Scheduler(cfg)
+    g.step(ticks)
+    o = oracle.Oracle(cfg)
+    o.step(ticks)
+    assert_same(g.export(), o.export(), name)
+    assert np.array_equal(g.digests(), o.digests())
+    assert g.stats()["raw"][86] == 0
+
+
+def _random_cfg(case):
+    from test_oracle_exact import _random_cfg as rc
+    return rc(random.Random(1000 + case))
+
+
+@pytest.mark.parametrize("case", range(20))
+def test_random_small_clusters(case):
+    cfg = _random_cfg(case)
+    cfg["groups"][0]["n_replicas"] = 3
+    run_both(cfg, 250)
+
+
+def test_chunking_invariance():
+    cfg = scaled("sweep", replicas_per_group=1)
+    a = Scheduler(cfg)
+    a.step(137)
+    a.step(263)
+    b = Scheduler(cfg)
+    b.step(400)
+    assert_same(a.export(), b.export(), "chunked")
+
+
+@pytest.mark.parametrize("threads,blocks", [(64, 1), (256, 7), (1024, 30), (512, 0)])
+def test_launch_shape_does_not_change_results(threads, blocks):
+    cfg = scaled("sweep", replicas_per_group=1)
+    ref = Scheduler(cfg)
+    ref.step(300)
+    g = Scheduler(cfg)
+    g.set_launch(threads, blocks)
+    g.step(300)
+    assert_same(g.export(), ref.export(), "launch %d x %d" % (threads, blocks))
+
+
+def test_replica_alone_equals_replica_in_batch():
+    cfg = scaled("gauss10", replicas_per_group=16)
+    batch = Scheduler(cfg)
+    batch.step(300)
+    for r in (0, 7, 15):
+        one = scaled("gauss10", replicas_per_group=1)
+        one["replica_id_base"] = r
+        alone = Scheduler(one)
+        alone.step(300)
+        assert_same(alone.export(), batch.export(r, 1), "replica %d" % r)
+
+
+def test_zero_ticks_is_a_noop():
+    cfg = preset("tiny")
+    g = Scheduler(cfg)
+    g.step(0)
+    assert g.tick == 0
+    assert g.stats()["raw"].sum() == 0
+
+
+def test_export_import_roundtrip_resumes_exactly():
+    cfg = scaled("enterprise", replicas_per_group=4)
+    a = Scheduler(cfg)
+    a.step(300)
+    st = a.export()
+    b = Scheduler(cfg)
+    b.import_state(st)
+    b.tick = 300
+    a.step(200)
+    b.step(200)
+    assert_same(b.export(), a.export(), "resumed vs uninterrupted")
+    o = oracle.Oracle(cfg)
+    o.import_state(st)
+    o.tick = 300
+    o.step(200)
+    assert_same(a.export(), o.export(), "resumed oracle")
+
+
+def test_corrupted_state_is_reported():
+    cfg = preset("tiny")
+    g = Scheduler(cfg)
+    g.step(100)
+    st = g.export()
+    st["free"][2] += 1  # a block appears from nowhere
+    g.import_state(st)
+    g.step(1)
+    with pytest.raises(MtsError) as e:
+        g.stats()
+    assert e.value.code == -4
+
+
+def test_out_of_range_import_is_rejected():
+    cfg = preset("tiny")
+    g = Scheduler(cfg)
+    st = g.export()
+    st["mig"][0:4] = [7, 0, 0, 0]  # destination instance 7 of 4
+    with pytest.raises(MtsError) as e:
+        g.import_state(st)
+    assert e.value.code == -1
+
+
+def test_single_instance_and_no_pairs():
+    for over in (dict(n_instances=1, mig_max_pairs=0), dict(mig_max_pairs=0)):
+        cfg = preset("tiny")
+        cfg.update(over)
+        run_both(cfg, 300)
+
+
+def test_near_zero_arrivals():
+    cfg = preset("tiny")
+    cfg["arrival"] = dict(kind="poisson", mean=1e-3)
+    run_both(cfg, 500)
+
+
+def test_overloaded_rejections():
+    cfg = preset("tiny")
+    cfg["slots_per_instance"] = 64
+    cfg["arrival"] = dict(kind="poisson", mean=9.0)
+    g = run_both(cfg, 400)
+    assert g.stats()["raw"][1:80:8].sum() > 0
+
+
+def test_largest_instance_table():
+    # I = 256 instances of S = 2048 slots: the widest replica this build serves
+    cfg = scaled("wide", replicas_per_group=1)
+    run_both(cfg, 60)

@@ -69,7 +69,7 @@ def _random_cfg(rng):
         n_instances=I, slots_per_instance=64, kv_blocks=M, block_tokens=blk,
         headroom_base=rng.choice([0.0, 0.1, 0.25, 0.6, 1.2]) * M, headroom_decay=rng.choice([0.3, 0.5, 0.9]),
         zero_lowest_tier=rng.choice([0, 1]), mig_interval=rng.choice([1, 2, 3]),
-        mig_stage_blocks=rng.choice([1, 3, 32]), mig_max_pairs=rng.randint(0, max(I // 2, 0) + 1),
+        mig_stage_blocks=rng.choice([1, 3, 32]), mig_max_pairs=rng.randint(0, I // 2),
         theta_num=rng.choice([0, 3, 20]), theta_den=10,
         arrival=dict(kind="poisson", mean=rng.choice([0.3, 1.0, 2.0, 5.0])),
         prompt=dict(kind="uniform_int", lo=1, hi=rng.choice([8, 64, 300, 800])),
