@@ -82,8 +82,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="sweep")
     ap.add_argument("--ticks-per-step", type=int, default=1000)
-    ap.add_argument("--threads", type=int, default=0)
-    ap.add_argument("--blocks", type=int, default=0)
+    ap.add_argument("--blocks", type=int, default=0, help="waves of the step kernel (0: automatic)")
     ap.add_argument("--cpu-replicas", type=int, default=16)
     ap.add_argument("--cpu-ticks", type=int, default=10000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -108,8 +107,8 @@ def main():
 
     if W > 0:
         warm = Scheduler(cfg)
-        if args.threads or args.blocks:
-            warm.set_launch(args.threads, args.blocks)
+        if args.blocks:
+            warm.set_launch(64, args.blocks)
         for _ in range(W):
             warm.step(T)
         torch.cuda.synchronize()
@@ -124,8 +123,8 @@ def main():
         del src, dst
 
     sch = Scheduler(cfg)
-    if args.threads or args.blocks:
-        sch.set_launch(args.threads, args.blocks)
+    if args.blocks:
+        sch.set_launch(64, args.blocks)
     torch.cuda.synchronize()
     s0 = sch.stats()["raw"].astype(np.int64)
     stream = torch.cuda.current_stream()

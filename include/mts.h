@@ -87,9 +87,9 @@ typedef struct mts_group {
 typedef struct mts_cfg {
     uint32_t abi_version;        /* MTS_ABI_VERSION */
     uint32_t n_instances;        /* I: 1..256 */
-    uint32_t slots_per_instance; /* S: multiple of 64, 64..4096 */
+    uint32_t slots_per_instance; /* S: multiple of 64, 64..2048 */
     uint32_t kv_blocks;          /* M: 1..2^21 blocks per instance */
-    uint32_t block_tokens;       /* tokens per KV block: power of two, 1..1024 */
+    uint32_t block_tokens;       /* tokens per KV block: power of two, 1..64 */
     uint32_t zero_lowest_tier;   /* 1: the lowest tier K-1 gets no headroom */
     double headroom_base;        /* h0 in blocks (Eq. 3: h0 = M * h_max), >= 0 */
     double headroom_decay;       /* gamma = e^-lambda, in [0, 1] */
@@ -106,7 +106,7 @@ typedef struct mts_cfg {
     double prompt_mu, prompt_sigma; /* LOGNORMAL */
     uint32_t prompt_lo, prompt_hi;  /* 1 <= lo <= hi */
     double output_param;         /* GEOMETRIC: mean >= 1; PARETO: alpha > 0 */
-    uint32_t output_min, output_cap; /* PARETO: 1 <= min <= cap */
+    uint32_t output_min, output_cap; /* PARETO: 1 <= min <= cap; every output length <= 16383 */
     uint64_t seed;               /* Philox key word 0 */
     uint64_t replica_id_base;    /* replica r draws with Philox key (seed, replica_id_base + r) */
     uint32_t n_groups;           /* >= 1 */
@@ -184,8 +184,10 @@ int mts_digest(mts_handle h, uint32_t r0, uint32_t nr, uint64_t* out);
 int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* out);
 
 /* Overwrite the state of replicas [r0, r0 + nr) from host arrays in the
- * canonical layout (synchronous).  The state is taken as given; the device
- * invariant checks report inconsistencies at the next mts_step. */
+ * canonical layout (synchronous).  The state is taken as given at the
+ * handle's current tick; the device invariant checks report inconsistencies
+ * at the next mts_step.  MTS_EINVAL for indices out of range, a tier >= K, a
+ * live request with len or rem 0, rem > 16383 or len + rem > 65535. */
 int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* in);
 
 /* The library's own tables, for comparison with an independent build:
@@ -202,11 +204,14 @@ int mts_get_headroom(mts_handle h, uint32_t g, int32_t out[MTS_MAX_TIERS]);
 uint64_t mts_tick(mts_handle h);
 
 /* Set the next tick to execute, e.g. after mts_import_state of a state saved
- * at that tick.  MTS_ERANGE if it does not fit the 32-bit tick fields. */
+ * at that tick.  The canonical state (every request's length and remaining
+ * output) is unchanged; only the clock moves (synchronous).  MTS_ERANGE if
+ * the tick does not fit the 32-bit tick fields. */
 int mts_set_tick(mts_handle h, uint64_t tick);
 
-/* Force the launch shape (threads per block, blocks); 0 keeps the automatic
- * choice.  threads must be a multiple of 64 up to 1024. */
+/* Force the launch shape of the step kernel: threads per block (0 or 64:
+ * one wave per replica) and number of blocks (0: automatic, else at most the
+ * replica count; each wave runs replicas r, r + blocks, ...). */
 int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks);
 
 /* Free the handle's host memory.  dev_buf stays with the caller. */

@@ -20,9 +20,9 @@ struct mts_ctx {
     size_t bytes = 0;
     uint32_t R = 0, I = 0, S = 0;
     uint64_t tick = 0;
-    uint32_t max_arrivals = 0;
-    uint32_t threads = 0, blocks = 0;  // launch shape (auto unless forced)
-    uint32_t scratch_blocks = 0;       // blocks the scratch area is sized for
+    uint32_t arr_cap = 0;              // arrival records per (replica, tick)
+    uint32_t chunk = 0;                // ticks per arrival batch
+    uint32_t blocks = 0;               // step-kernel blocks (one wave each); 0 = automatic
     int device = 0;
     hipStream_t last = nullptr;
     std::vector<uint16_t> group_of;
@@ -40,10 +40,16 @@ uint32_t total_replicas(const mts_cfg& c)
     return uint32_t(R);
 }
 
-// blocks of the step kernel the scratch area must serve
-uint32_t scratch_blocks_for(uint32_t R) { return std::min<uint32_t>(R, 8192); }
+// device bytes reserved for pre-sampled arrivals; sets the ticks per batch
+constexpr size_t kArrivalBudget = size_t(512) << 20;
 
-Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t scratch_blocks, uint32_t max_arrivals)
+uint32_t chunk_for(uint32_t R, uint32_t cap)
+{
+    const size_t per_tick = size_t(R) * cap * 8 + size_t(R) * 4;
+    return uint32_t(std::max<size_t>(1, std::min<size_t>(1024, kArrivalBudget / per_tick)));
+}
+
+Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk, uint32_t cap)
 {
     Layout L{};
     const size_t I = c.n_instances, S = c.slots_per_instance;
@@ -57,7 +63,7 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t scrat
     L.output_q = o; o = up256(o + T.output.q.size() * 4);
     L.group_of = o; o = up256(o + size_t(R) * 2);
     L.meta = o;     o = up256(o + N);
-    L.lr = o;       o = up256(o + N * 4);
+    L.hot = o;      o = up256(o + N * 4);
     L.seq = o;      o = up256(o + N * 4);
     L.tarr = o;     o = up256(o + N * 4);
     L.freeb = o;    o = up256(o + size_t(R) * I * 4);
@@ -65,7 +71,8 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t scrat
     L.next_seq = o; o = up256(o + size_t(R) * 4);
     L.stats = o;    o = up256(o + size_t(R) * MTS_NSTAT * 8);
     L.digest = o;   o = up256(o + size_t(R) * 8);
-    L.scratch = o;  o = up256(o + size_t(scratch_blocks) * 2 * max_arrivals * 8);
+    L.arr_cnt = o;  o = up256(o + size_t(R) * chunk * 4);
+    L.arr_rec = o;  o = up256(o + size_t(R) * chunk * cap * 8);
     L.total = o;
     return L;
 }
@@ -80,6 +87,7 @@ Params make_params(const mts_ctx* h)
     uint32_t sh = 0;
     while ((1u << sh) < c.block_tokens) ++sh;
     p.blk_shift = sh;
+    p.RB = c.block_tokens;
     p.mig_interval = c.mig_interval; p.mig_stage = c.mig_stage_blocks; p.mig_max_pairs = c.mig_max_pairs;
     p.theta_num = c.theta_num; p.theta_den = c.theta_den;
     p.count_n = uint32_t(h->tables.count.q.size());
@@ -88,7 +96,8 @@ Params make_params(const mts_ctx* h)
     p.count_base = h->tables.count.base;
     p.prompt_base = h->tables.prompt.base;
     p.output_base = h->tables.output.base;
-    p.max_arrivals = h->max_arrivals;
+    p.chunk = h->chunk;
+    p.arr_cap = h->arr_cap;
     p.seed = c.seed;
     p.id_base = c.replica_id_base;
     const Layout& L = h->lay;
@@ -100,7 +109,7 @@ Params make_params(const mts_ctx* h)
     p.output_q = reinterpret_cast<const uint32_t*>(d + L.output_q);
     p.group_of = reinterpret_cast<const uint16_t*>(d + L.group_of);
     p.meta = reinterpret_cast<uint8_t*>(d + L.meta);
-    p.lr = reinterpret_cast<uint32_t*>(d + L.lr);
+    p.hot = reinterpret_cast<uint32_t*>(d + L.hot);
     p.seq = reinterpret_cast<uint32_t*>(d + L.seq);
     p.tarr = reinterpret_cast<uint32_t*>(d + L.tarr);
     p.freeb = reinterpret_cast<int32_t*>(d + L.freeb);
@@ -108,7 +117,8 @@ Params make_params(const mts_ctx* h)
     p.next_seq = reinterpret_cast<uint32_t*>(d + L.next_seq);
     p.stats = reinterpret_cast<unsigned long long*>(d + L.stats);
     p.digest = reinterpret_cast<unsigned long long*>(d + L.digest);
-    p.scratch = reinterpret_cast<unsigned long long*>(d + L.scratch);
+    p.arr_cnt = reinterpret_cast<uint32_t*>(d + L.arr_cnt);
+    p.arr_rec = reinterpret_cast<unsigned long long*>(d + L.arr_rec);
     return p;
 }
 
@@ -135,9 +145,9 @@ int prepare(const mts_cfg* cfg, mts_ctx& x)
     x.R = total_replicas(x.cfg);
     x.I = cfg->n_instances;
     x.S = cfg->slots_per_instance;
-    x.max_arrivals = uint32_t(x.tables.count.base + x.tables.count.q.size());
-    x.scratch_blocks = scratch_blocks_for(x.R);
-    x.lay = make_layout(x.cfg, x.tables, x.R, x.scratch_blocks, x.max_arrivals);
+    x.arr_cap = uint32_t(x.tables.count.base + x.tables.count.q.size());
+    x.chunk = chunk_for(x.R, x.arr_cap);
+    x.lay = make_layout(x.cfg, x.tables, x.R, x.chunk, x.arr_cap);
     return MTS_OK;
 }
 
@@ -185,7 +195,7 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
         delete x;
         return MTS_EDEVICE;
     }
-    if (lds_bytes(x->I, x->S) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
+    if (lds_bytes(x->I, x->S, x->cfg.block_tokens) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
 
     // tables and per-replica group index
     const uint32_t G = x->cfg.n_groups;
@@ -223,9 +233,8 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
 int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks)
 {
     if (!h) return MTS_EINVAL;
-    if (threads && (threads % 64 || threads > 1024)) return MTS_EINVAL;
-    if (blocks > h->scratch_blocks) return MTS_EINVAL;
-    h->threads = threads;
+    if (threads != 0 && threads != 64) return MTS_EINVAL;  // one wave per replica
+    if (blocks > h->R) return MTS_EINVAL;
     h->blocks = blocks;
     return MTS_OK;
 }
@@ -234,25 +243,24 @@ int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
 {
     if (!h) return MTS_EINVAL;
     if (n_ticks == 0) return MTS_OK;
-    // tarr holds a tick in 32 bits; seq grows by at most max_arrivals - 1 per tick
+    // ticks are 32-bit on the device and the sequence counter grows by at
+    // most arr_cap - 1 per tick
     const uint64_t end = h->tick + n_ticks;
-    if (end > 0xFFFFFFFFull || end * uint64_t(h->max_arrivals) > 0xFFFFFFFFull) return MTS_ERANGE;
-    Params p = make_params(h);
-    p.tick0 = h->tick;
-    p.n_ticks = n_ticks;
-    uint32_t threads = h->threads ? h->threads : std::min<uint32_t>(1024, std::max<uint32_t>(64, 64 * h->I));
+    if (end > 0xFFFF0000ull || end * uint64_t(h->arr_cap) > 0xFFFFFFFFull) return MTS_ERANGE;
+    const Params p = make_params(h);
     uint32_t blocks = h->blocks;
     if (!blocks) {
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess) return MTS_EDEVICE;
-        const uint32_t per_cu_waves = 32 / (threads / 64);
-        const size_t lds = lds_bytes(h->I, h->S);
-        const uint32_t per_cu_lds = uint32_t(std::max<size_t>(1, (160 * 1024) / std::max<size_t>(lds, 1)));
-        const uint32_t per_cu = std::max<uint32_t>(1, std::min(per_cu_waves, per_cu_lds));
+        const size_t lds = lds_bytes(h->I, h->S, h->cfg.block_tokens);
+        const uint32_t per_cu = uint32_t(std::max<size_t>(1, std::min<size_t>(16, (160 * 1024) / lds)));
         blocks = std::min<uint32_t>(h->R, uint32_t(cus) * per_cu);
     }
-    blocks = std::min(blocks, h->scratch_blocks);
-    if (launch_step(p, threads, blocks, stream) != 0) return MTS_EDEVICE;
+    for (uint64_t t = h->tick; t < end; t += h->chunk) {
+        const uint32_t nt = uint32_t(std::min<uint64_t>(h->chunk, end - t));
+        if (launch_arrivals(p, t, nt, stream) != 0) return MTS_EDEVICE;
+        if (launch_step(p, t, nt, blocks, stream) != 0) return MTS_EDEVICE;
+    }
     h->tick = end;
     h->last = stream;
     return MTS_OK;
@@ -263,7 +271,7 @@ int mts_digest(mts_handle h, uint32_t r0, uint32_t nr, uint64_t* out)
     if (!h || !out) return MTS_EINVAL;
     if (r0 > h->R || nr > h->R - r0) return MTS_ERANGE;
     const Params p = make_params(h);
-    if (launch_digest(p, r0, nr, h->last) != 0) return MTS_EDEVICE;
+    if (launch_digest(p, r0, nr, uint32_t(h->tick), h->last) != 0) return MTS_EDEVICE;
     hipError_t e = hipMemcpyAsync(out, h->dev + h->lay.digest + size_t(r0) * 8, size_t(nr) * 8, hipMemcpyDeviceToHost, h->last);
     if (e == hipSuccess) e = hipStreamSynchronize(h->last);
     return hip_rc(e);
@@ -299,6 +307,22 @@ int mts_stats(mts_handle h, mts_stats_t* out)
     return out->invariant_violations ? MTS_ESTATE : MTS_OK;
 }
 
+namespace {
+
+// canonical len | rem << 16 of a slot word at the next tick to run
+uint32_t word_to_lr(uint32_t w, uint64_t tick)
+{
+    const uint32_t st = w >> 30, lo = w & 0xFFFFu, mid = (w >> 16) & 0x3FFFu;
+    if (st == kWaiting) return lo | (mid << 16);
+    if (st == kRunning) {
+        const uint32_t rem = (mid - uint32_t(tick) + 1u) & 0x3FFFu;
+        return (lo - rem) | (rem << 16);
+    }
+    return 0;
+}
+
+}  // namespace
+
 int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* v)
 {
     if (!h || !v) return MTS_EINVAL;
@@ -309,8 +333,13 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     auto get = [&](void* dst, size_t off, size_t n) {
         if (e == hipSuccess && dst && n) e = hipMemcpy(dst, h->dev + off, n, hipMemcpyDeviceToHost);
     };
+    if (v->lr) {
+        std::vector<uint32_t> w(size_t(nr) * IS);
+        get(w.data(), L.hot + size_t(r0) * IS * 4, w.size() * 4);
+        if (e == hipSuccess)
+            for (size_t k = 0; k < w.size(); ++k) v->lr[k] = word_to_lr(w[k], h->tick);
+    }
     get(v->meta, L.meta + size_t(r0) * IS, size_t(nr) * IS);
-    get(v->lr, L.lr + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
     get(v->seq, L.seq + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
     get(v->tarr, L.tarr + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
     get(v->free, L.freeb + size_t(r0) * I * 4, size_t(nr) * I * 4);
@@ -326,15 +355,30 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
         return MTS_EINVAL;
     if (r0 > h->R || nr > h->R - r0) return MTS_ERANGE;
     const size_t IS = size_t(h->I) * h->S, I = h->I;
-    // structural checks keep every index the kernel derives from the state in range
+    std::vector<uint32_t> w(size_t(nr) * IS);
+    // structural checks keep every index the kernel derives from the state in
+    // range; running requests are re-encoded relative to the handle's tick
     for (uint32_t r = 0; r < nr; ++r) {
         const uint32_t K = h->group_K[h->group_of[r0 + r]];
         for (size_t s = 0; s < IS; ++s) {
-            const uint8_t m = v->meta[size_t(r) * IS + s];
-            const uint32_t st = m & 3u, lr = v->lr[size_t(r) * IS + s];
-            if ((st == kWaiting || st == kRunning) && (((m >> 2) & 15u) >= K || (lr & 0xFFFFu) == 0 || (lr >> 16) == 0))
-                return MTS_EINVAL;
-            if (st == kEmpty && m != 0) return MTS_EINVAL;
+            const size_t k = size_t(r) * IS + s;
+            const uint8_t m = v->meta[k];
+            const uint32_t st = m & 3u, lr = v->lr[k], len = lr & 0xFFFFu, rem = lr >> 16;
+            if (st == kEmpty) {
+                if (m != 0) return MTS_EINVAL;
+                w[k] = 0;
+            } else if (st == kInbound) {
+                w[k] = 3u << 30;
+            } else {
+                if (((m >> 2) & 15u) >= K || len == 0 || rem == 0 || rem > kMaxOutput) return MTS_EINVAL;
+                if (st == kWaiting) {
+                    w[k] = (1u << 30) | (rem << 16) | len;
+                } else {
+                    if (len + rem > 65535u) return MTS_EINVAL;
+                    const uint32_t fin = uint32_t(h->tick) - 1u + rem;
+                    w[k] = (2u << 30) | ((fin & 0x3FFFu) << 16) | (len + rem);
+                }
+            }
         }
         for (size_t i = 0; i < I; ++i) {
             const int32_t* m = v->mig + (size_t(r) * I + i) * 4;
@@ -351,7 +395,7 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
         if (e == hipSuccess && n) e = hipMemcpy(h->dev + off, src, n, hipMemcpyHostToDevice);
     };
     put(L.meta + size_t(r0) * IS, v->meta, size_t(nr) * IS);
-    put(L.lr + size_t(r0) * IS * 4, v->lr, size_t(nr) * IS * 4);
+    put(L.hot + size_t(r0) * IS * 4, w.data(), w.size() * 4);
     put(L.seq + size_t(r0) * IS * 4, v->seq, size_t(nr) * IS * 4);
     put(L.tarr + size_t(r0) * IS * 4, v->tarr, size_t(nr) * IS * 4);
     put(L.freeb + size_t(r0) * I * 4, v->free, size_t(nr) * I * 4);
@@ -391,7 +435,10 @@ uint64_t mts_tick(mts_handle h) { return h ? h->tick : 0; }
 int mts_set_tick(mts_handle h, uint64_t tick)
 {
     if (!h) return MTS_EINVAL;
-    if (tick > 0xFFFFFFFFull) return MTS_ERANGE;
+    if (tick > 0xFFFF0000ull) return MTS_ERANGE;
+    const Params p = make_params(h);
+    if (launch_shift_clock(p, uint32_t(tick - h->tick), h->last) != 0) return MTS_EDEVICE;
+    if (hipStreamSynchronize(h->last) != hipSuccess) return MTS_EDEVICE;
     h->tick = tick;
     return MTS_OK;
 }

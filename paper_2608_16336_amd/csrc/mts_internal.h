@@ -12,7 +12,9 @@
 namespace mts {
 
 constexpr uint32_t kMaxInstances = 256;
-constexpr uint32_t kMaxSlots = 4096;
+constexpr uint32_t kMaxSlots = 2048;
+constexpr uint32_t kMaxBlockTokens = 64;
+constexpr uint32_t kMaxOutput = 16383;
 constexpr uint32_t kMaxBlocks = 1u << 21;
 constexpr uint32_t kMaxGroups = 4096;
 constexpr uint64_t kMaxReplicas = 1u << 20;
@@ -44,33 +46,33 @@ int build_tables(const mts_cfg& c, Tables& T);
 
 // Device buffer layout: byte offsets of every array inside dev_buf.
 struct Layout {
-    size_t tier_q, hq, group_K, count_q, prompt_q, output_q, group_of;   // tables
-    size_t meta, lr, seq, tarr;                                  // [R][I][S]
-    size_t freeb, mig;                                           // [R][I], [R][I][4]
-    size_t next_seq, stats, digest;                              // [R], [R][NSTAT], [R]
-    size_t scratch;                                              // per block: 2 * max_arrivals u64
+    size_t tier_q, hq, group_K, count_q, prompt_q, output_q, group_of;  // tables
+    size_t meta, hot, seq, tarr;                                        // [R][I][S]
+    size_t freeb, mig;                                                  // [R][I], [R][I][4]
+    size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
+    size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
     size_t total;
 };
 
 // Everything a kernel launch needs, passed by value.
 struct Params {
     uint32_t R, I, S, W;           // W = S / 64 occupancy words per instance
-    uint32_t M, blk_shift;
+    uint32_t M, blk_shift, RB;     // RB = block_tokens growth residues
     uint32_t mig_interval, mig_stage, mig_max_pairs;
     int32_t theta_num, theta_den;
     uint32_t count_n, prompt_n, output_n;  // table lengths (entries incl. the implicit 2^32)
     uint32_t count_base, prompt_base, output_base;
-    uint32_t max_arrivals;         // scratch capacity per block
+    uint32_t chunk, arr_cap;       // ticks per arrival batch, records per tick
     uint64_t seed, id_base;
-    uint64_t tick0, n_ticks;
     const uint32_t* tier_q;        // [group][MTS_MAX_TIERS]
     const int32_t* hq;             // [group][MTS_MAX_TIERS]
+    const uint32_t* group_K32;     // [group] tier count
     const uint32_t* count_q;
     const uint32_t* prompt_q;
     const uint32_t* output_q;
     const uint16_t* group_of;      // [R]
     uint8_t* meta;
-    uint32_t* lr;
+    uint32_t* hot;
     uint32_t* seq;
     uint32_t* tarr;
     int32_t* freeb;
@@ -78,16 +80,18 @@ struct Params {
     uint32_t* next_seq;
     unsigned long long* stats;
     unsigned long long* digest;
-    unsigned long long* scratch;
-    const uint32_t* group_K32;     // [group] tier count
+    uint32_t* arr_cnt;
+    unsigned long long* arr_rec;
 };
 
-// LDS bytes one block of the step kernel needs for a replica of I x S.
-size_t lds_bytes(uint32_t I, uint32_t S);
+// LDS bytes of one wave (one replica) of the step kernel
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB);
 
 // kernel launches (mts_kernels.hip); return hipError_t as int
 int launch_init(const Params& p, hipStream_t stream);
-int launch_step(const Params& p, uint32_t threads, uint32_t blocks, hipStream_t stream);
-int launch_digest(const Params& p, uint32_t r0, uint32_t nr, hipStream_t stream);
+int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStream_t stream);
+int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream);
+int launch_digest(const Params& p, uint32_t r0, uint32_t nr, uint32_t tick, hipStream_t stream);
+int launch_shift_clock(const Params& p, uint32_t delta, hipStream_t stream);
 
 }  // namespace mts

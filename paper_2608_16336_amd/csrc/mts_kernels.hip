@@ -1,15 +1,27 @@
-// Device code of libmts: the persistent multi-tick scheduling kernel, the
-// state initialiser and the state digest.
+// Device code of libmts.
 //
-// Mapping.  One block owns one replica at a time and runs all n_ticks ticks
-// of it before taking the next replica (replicas never interact, so there is
-// no grid-wide synchronisation).  Within a block, wave w handles instances
-// w, w + nwaves, ... in the per-instance phases (A, B, C); wave 0 runs the
-// replica-wide serial phases (A2, D, E).  Slot state lives in HBM in the
-// canonical SoA layout (meta u8, lr u32, seq u32, tarr u32, each [R][I][S]),
-// scanned 64 consecutive slots per wave instruction.  Per-instance summaries,
-// the slot occupancy bitmap and the replica's counters live in LDS for the
-// whole launch.
+//   k_arrivals  samples every arrival of a chunk of ticks for every replica
+//               (Philox4x64-10 + inverse-CDF tables) and sorts each tick's
+//               arrivals by tier, one wave per (replica, tick).
+//   k_step      the scheduling tick, one wave per replica for a whole chunk
+//               of ticks: per-instance summaries live in LDS, per-instance
+//               O(1) work is lane-parallel (lane i <-> instance i), slot
+//               state lives in HBM and is touched only by events.
+//   k_init      empty clusters; k_digest the canonical state digest.
+//
+// Slot word ("hot", u32, bits 31..30 = status):
+//   waiting   01 | rem (14 bits) | len (16 bits)
+//   running   10 | fin mod 2^14  | final length (16 bits)
+//   inbound   11 | 0
+//   empty     0
+// A running request's word never changes while it runs: the tick at which it
+// emits its last token (fin) and its final length determine its length at
+// any tick t (final - (fin - t + 1) before the decode of t), so decoding
+// writes nothing.  Its KV growth falls on ticks t with
+// (final - fin - 1 + t) mod block = 0: per instance, counters indexed by that
+// residue give the number of requests that need a new block at tick t in
+// O(1).  Each instance tracks a lower bound of its next finish tick and scans
+// its slots only when it is due.
 #include <hip/hip_runtime.h>
 
 #include "mts_internal.h"
@@ -20,92 +32,124 @@ namespace {
 constexpr int kNstat = MTS_NSTAT;
 constexpr int kTiers = MTS_MAX_TIERS;
 constexpr unsigned long long kNone = ~0ull;
+constexpr uint32_t kWaitW = 1u << 30, kRunW = 2u << 30, kInbW = 3u << 30;
+constexpr uint32_t kFin = 0x3FFFu;
+constexpr uint32_t kInf = 0xFFFFFFFFu;
+constexpr int kNoHol = -1, kHolUnknown = -2, kHolPending = -3;
+constexpr int kFlagAbort = 1, kFlagBusy = 2;
+
+__device__ __forceinline__ uint32_t wst(uint32_t v) { return v >> 30; }
+__device__ __forceinline__ uint32_t wlo(uint32_t v) { return v & 0xFFFFu; }
+__device__ __forceinline__ uint32_t wmid(uint32_t v) { return (v >> 16) & kFin; }
 
 // ---------------------------------------------------------------------------
-// LDS layout of one block (sizes depend on I and W = S / 64)
+// LDS of one wave (one replica)
 // ---------------------------------------------------------------------------
+constexpr int kInts = 17;
+
 struct LdsLayout {
-    uint32_t stats, occ, q, ints, tcnt, bytes, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, total;
 };
 
-constexpr int kIntArrays = 17;  // see Lds below
-constexpr int kMisc = 16;
+__host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
 
-__host__ __device__ inline uint32_t align8(uint32_t x) { return (x + 7u) & ~7u; }
-
-__host__ __device__ inline LdsLayout lds_layout(uint32_t I, uint32_t W)
+__host__ __device__ inline LdsLayout lds_layout(uint32_t I, uint32_t W, uint32_t RB)
 {
     LdsLayout L;
     uint32_t o = 0;
     L.stats = o; o += kNstat * 8;
     L.occ = o;   o += I * W * 8;
-    L.q = o;     o += I * 8;
-    L.ints = o;  o += (I * kIntArrays + kTiers + kMisc) * 4; o = align8(o);
-    L.tcnt = o;  o += I * kTiers * 2; o = align8(o);
-    L.bytes = o; o += I * 2; o = align8(o);
-    L.total = o;
+    L.holk = o;  o += I * 8;
+    L.fd = o;    o += I * 8;
+    L.ints = o;  o += I * kInts * 4;
+    L.res = o;   o += I * RB * 4;
+    L.tcnt = o;  o += I * kTiers * 4;
+    L.mig = o;   o += I * 16;
+    L.total = al8(o);
     return L;
 }
 
-struct Lds {
-    unsigned long long* stats;  // [88] this replica's counters
-    unsigned long long* occ;    // [I][W] bit s%64 of word s/64: slot s not empty
-    long long* q;               // [I] floor(num * 2^24 / den): exact order key of F
-    int* freeb;                 // [I] free blocks
-    int* B;                     // [I] running requests
-    int* live;                  // [I] non-empty slots
-    int* hwm;                   // [I] 1 + highest non-empty slot
-    int* hol_slot;              // [I] head-of-line slot or -1
-    int* hol_tier;
-    unsigned* hol_seq;
-    int* hol_dem;               // [I] head-of-line demand in blocks (0 if none)
-    int* num;                   // [I] freeness numerator, 1/256 block
-    int* den;                   // [I] max(B, 1)
-    int* inb;                   // [I] blocks copied into this instance's inbound reservation
-    int* mig;                   // [I][4] dst, src slot, dst slot, copied
-    int* order;                 // [I] instances ranked for pairing
-    int* hl;                    // [10] headroom of this replica's group
-    int* misc;                  // [16] block-wide scalars
-    unsigned short* tcnt;       // [I][10] running requests per tier
-    unsigned char* abort_;      // [I] source migration must be released
-    unsigned char* busy;        // [I] in a migration
+struct Ctx {
+    // LDS
+    unsigned long long* stats;
+    unsigned long long* occ;   // [I][W] slot not empty
+    unsigned long long* holk;  // [I] head-of-line key tier << 32 | seq
+    double* fd;                // [I] freeness num / den (exact order for S <= 2048)
+    int *freeb, *B, *live, *nwait, *hwm, *hols, *hold, *num, *den, *held, *inb, *tmask, *flags, *gtmp, *order, *pend;
+    unsigned* nfin;            // [I] lower bound of the next finish tick
+    unsigned* res;             // [I][RB] running requests per growth residue
+    unsigned* tcnt;            // [I][10] running requests per tier
+    int* mig;                  // [I][4] dst, src slot, dst slot, copied
+    // HBM slot arrays of this replica
+    uint32_t* hot;
+    uint8_t* meta;
+    uint32_t* seq;
+    uint32_t* tarr;
+    uint32_t I, S, W, RB, shift, bmask, M, K;
+    int hq[kTiers];
 };
 
-__device__ inline Lds carve(char* base, uint32_t I, uint32_t W)
+__device__ inline Ctx carve(char* base, const Params& P)
 {
-    const LdsLayout Y = lds_layout(I, W);
-    Lds L;
-    L.stats = reinterpret_cast<unsigned long long*>(base + Y.stats);
-    L.occ = reinterpret_cast<unsigned long long*>(base + Y.occ);
-    L.q = reinterpret_cast<long long*>(base + Y.q);
+    const LdsLayout Y = lds_layout(P.I, P.W, P.RB);
+    Ctx C;
+    C.stats = reinterpret_cast<unsigned long long*>(base + Y.stats);
+    C.occ = reinterpret_cast<unsigned long long*>(base + Y.occ);
+    C.holk = reinterpret_cast<unsigned long long*>(base + Y.holk);
+    C.fd = reinterpret_cast<double*>(base + Y.fd);
     int* p = reinterpret_cast<int*>(base + Y.ints);
-    L.freeb = p; p += I;
-    L.B = p; p += I;
-    L.live = p; p += I;
-    L.hwm = p; p += I;
-    L.hol_slot = p; p += I;
-    L.hol_tier = p; p += I;
-    L.hol_seq = reinterpret_cast<unsigned*>(p); p += I;
-    L.hol_dem = p; p += I;
-    L.num = p; p += I;
-    L.den = p; p += I;
-    L.inb = p; p += I;
-    L.mig = p; p += 4 * I;
-    L.order = p; p += I;
-    L.hl = p; p += kTiers;
-    L.misc = p; p += kMisc;
-    L.tcnt = reinterpret_cast<unsigned short*>(base + Y.tcnt);
-    L.abort_ = reinterpret_cast<unsigned char*>(base + Y.bytes);
-    L.busy = L.abort_ + I;
-    return L;
+    const uint32_t I = P.I;
+    C.freeb = p; p += I;
+    C.B = p; p += I;
+    C.live = p; p += I;
+    C.nwait = p; p += I;
+    C.hwm = p; p += I;
+    C.hols = p; p += I;
+    C.hold = p; p += I;
+    C.num = p; p += I;
+    C.den = p; p += I;
+    C.held = p; p += I;
+    C.inb = p; p += I;
+    C.tmask = p; p += I;
+    C.flags = p; p += I;
+    C.gtmp = p; p += I;
+    C.order = p; p += I;
+    C.pend = p; p += I;
+    C.nfin = reinterpret_cast<unsigned*>(p); p += I;
+    C.res = reinterpret_cast<unsigned*>(base + Y.res);
+    C.tcnt = reinterpret_cast<unsigned*>(base + Y.tcnt);
+    C.mig = reinterpret_cast<int*>(base + Y.mig);
+    C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
+    C.shift = P.blk_shift;
+    C.bmask = (1u << P.blk_shift) - 1u;
+    C.M = P.M;
+    return C;
 }
 
 // ---------------------------------------------------------------------------
-// wave helpers (wave64)
+// wave helpers
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
 __device__ __forceinline__ unsigned long long ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ unsigned long long lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+__device__ __forceinline__ int ffs64(unsigned long long m) { return __ffsll(static_cast<long long>(m)) - 1; }
+
+__device__ __forceinline__ int rl(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ unsigned rlu(unsigned v, int l) { return unsigned(__builtin_amdgcn_readlane(int(v), l)); }
+__device__ __forceinline__ unsigned long long rl64(unsigned long long v, int l)
+{
+    const unsigned lo = rlu(unsigned(v), l), hi = rlu(unsigned(v >> 32), l);
+    return (static_cast<unsigned long long>(hi) << 32) | lo;
+}
+
+// Lanes of the wave exchange values through LDS and HBM: every write by a
+// subset of lanes that other lanes read later is followed by this point, so
+// that no later load is moved above it and every later load sees the write.
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+}
 
 __device__ __forceinline__ int wsum(int x)
 {
@@ -113,30 +157,102 @@ __device__ __forceinline__ int wsum(int x)
     for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
     return x;
 }
-
+__device__ __forceinline__ unsigned long long wsum64(unsigned long long x)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    return x;
+}
 __device__ __forceinline__ unsigned long long wmax64(unsigned long long x)
 {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-        unsigned long long y = __shfl_xor(x, o);
+        const unsigned long long y = __shfl_xor(x, o);
         x = y > x ? y : x;
     }
     return x;
 }
-
 __device__ __forceinline__ unsigned long long wmin64(unsigned long long x)
 {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-        unsigned long long y = __shfl_xor(x, o);
+        const unsigned long long y = __shfl_xor(x, o);
         x = y < x ? y : x;
     }
     return x;
 }
 
+// wave-wide max of a double through DPP lane moves; every lane gets the result
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ double dpp_f64(double v)
+{
+    const int lo = __double2loint(v), hi = __double2hiint(v);
+    const int lo2 = __builtin_amdgcn_update_dpp(lo, lo, kCtrl, kRowMask, 0xF, false);
+    const int hi2 = __builtin_amdgcn_update_dpp(hi, hi, kCtrl, kRowMask, 0xF, false);
+    return __hiloint2double(hi2, lo2);
+}
+__device__ __forceinline__ double wave_max_f64(double v)
+{
+    v = fmax(v, dpp_f64<0xB1, 0xF>(v));   // quad_perm 1,0,3,2
+    v = fmax(v, dpp_f64<0x4E, 0xF>(v));   // quad_perm 2,3,0,1
+    v = fmax(v, dpp_f64<0x141, 0xF>(v));  // row_half_mirror
+    v = fmax(v, dpp_f64<0x140, 0xF>(v));  // row_mirror
+    v = fmax(v, dpp_f64<0x142, 0xA>(v));  // row_bcast:15
+    v = fmax(v, dpp_f64<0x143, 0xC>(v));  // row_bcast:31
+    const int lo = __builtin_amdgcn_readlane(__double2loint(v), 63);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(v), 63);
+    return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ int blocks_of(uint32_t len, uint32_t shift)
+{
+    return int((len + (1u << shift) - 1u) >> shift);
+}
+
+// full finish tick of a running word, given that it has not finished before t
+__device__ __forceinline__ uint32_t fin_of(uint32_t v, uint32_t t) { return t + ((wmid(v) - t) & kFin); }
+
+// Freeness of instance i (Eq. 1-4): num = 256 (free - hol demand) - sum of H_p
+// over the tiers with a running request, den = max(B, 1).
+__device__ inline void set_f(const Ctx& C, int i)
+{
+    int hs = 0;
+    const int tm = C.tmask[i];
+#pragma unroll
+    for (int p = 0; p < kTiers; ++p) hs += (tm >> p) & 1 ? C.hq[p] : 0;
+    const int num = 256 * (C.freeb[i] - C.hold[i]) - hs;
+    const int den = C.B[i] > 0 ? C.B[i] : 1;
+    C.num[i] = num;
+    C.den[i] = den;
+    C.fd[i] = double(num) / double(den);
+}
+
+__device__ __forceinline__ void tier_dec(const Ctx& C, int i, int tier)
+{
+    if (atomicSub(&C.tcnt[i * kTiers + tier], 1u) == 1u) atomicAnd(&C.tmask[i], ~(1 << tier));
+}
+__device__ __forceinline__ void tier_inc(const Ctx& C, int i, int tier)
+{
+    atomicAdd(&C.tcnt[i * kTiers + tier], 1u);
+    atomicOr(&C.tmask[i], 1 << tier);
+}
+
+__device__ __forceinline__ void stat(const Ctx& C, int idx, unsigned long long v) { atomicAdd(&C.stats[idx], v); }
+
+// lowest empty slot of instance i (one exists); uniform
+__device__ inline int lowest_empty(const Ctx& C, int i, int lane)
+{
+    const unsigned long long w = lane < int(C.W) ? C.occ[i * C.W + lane] : kNone;
+    const unsigned long long fm = ballot(w != kNone);
+    if (fm == 0) return -1;
+    const int c0 = ffs64(fm);
+    const unsigned long long w0 = rl64(w, c0);
+    return c0 * 64 + ffs64(~w0);
+}
+
 // ---------------------------------------------------------------------------
-// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011), written from the
-// published round function and Weyl key schedule.
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011) from its published
+// round function and Weyl key schedule; inverse-CDF table search.
 // ---------------------------------------------------------------------------
 __device__ inline void philox4x64_10(unsigned long long x[4], unsigned long long k0, unsigned long long k1)
 {
@@ -152,7 +268,6 @@ __device__ inline void philox4x64_10(unsigned long long x[4], unsigned long long
     }
 }
 
-// base + min{j : u < q[j]} over a table of n entries whose last (2^32) is implicit
 __device__ inline uint32_t sample(const uint32_t* q, uint32_t n, uint32_t u)
 {
     uint32_t lo = 0, hi = n - 1;
@@ -163,542 +278,729 @@ __device__ inline uint32_t sample(const uint32_t* q, uint32_t n, uint32_t u)
     return lo;
 }
 
-__device__ __forceinline__ int blocks_of(uint32_t len, uint32_t shift)
+// ---------------------------------------------------------------------------
+// k_arrivals: one wave per (replica, tick of the chunk)
+// record = prompt | out << 16 | tier << 32 | k << 36, sorted by tier (stable)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t0, uint32_t nt)
 {
-    return int((len + (1u << shift) - 1u) >> shift);
-}
-
-// Freeness of instance i (Eq. 1-4): num = 256 (free - hol) - sum of H_p over
-// the tiers with a running request, den = max(B, 1); q orders F exactly.
-__device__ inline void set_f(const Lds& L, int i, int K)
-{
-    int hs = 0;
-    for (int p = 0; p < K; ++p) hs += L.tcnt[i * kTiers + p] ? L.hl[p] : 0;
-    const long long num = 256ll * (L.freeb[i] - L.hol_dem[i]) - hs;
-    const int den = L.B[i] > 0 ? L.B[i] : 1;
-    const long long n = num * (1ll << 24);
-    const long long q = n >= 0 ? n / den : -((-n + den - 1) / den);
-    L.num[i] = int(num);
-    L.den[i] = den;
-    L.q[i] = q;
-}
-
-// dispatch key: larger F first, then smaller index; 0 is never a valid key
-__device__ __forceinline__ unsigned long long dkey(long long q, int i)
-{
-    return (static_cast<unsigned long long>(q + (1ll << 54) + 1) << 8) | unsigned(255 - i);
-}
-
-// pairing key: smaller F first, then smaller index
-__device__ __forceinline__ unsigned long long pkey(long long q, int i)
-{
-    return (static_cast<unsigned long long>(q + (1ll << 54) + 1) << 8) | unsigned(i);
-}
-
-// lowest empty slot of instance i (caller guarantees one exists); uniform
-__device__ inline int lowest_empty(const Lds& L, int i, uint32_t W, int lane, int* word, unsigned long long* wval)
-{
-    const unsigned long long w = lane < int(W) ? L.occ[i * W + lane] : kNone;
-    const unsigned long long fm = ballot(w != kNone);
-    const int c0 = __ffsll(static_cast<long long>(fm)) - 1;
-    if (c0 < 0) return -1;
-    const unsigned long long w0 = __shfl(w, c0);
-    const int bit = __ffsll(static_cast<long long>(~w0)) - 1;
-    *word = c0;
-    *wval = w0;
-    return c0 * 64 + bit;
-}
-
-__device__ inline void stat_add(const Lds& L, int idx, unsigned long long v)
-{
-    atomicAdd(&L.stats[idx], v);
+    const uint32_t item = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (item >= P.R * nt) return;
+    const int lane = lane_id();
+    const uint32_t r = item / nt, tl = item % nt;
+    const unsigned long long t = t0 + tl;
+    const unsigned long long gid = P.id_base + r;
+    const uint32_t g = P.group_of[r];
+    const int K = int(P.group_K32[g]);
+    const uint32_t* tq = P.tier_q + size_t(g) * kTiers;
+    unsigned long long x[4] = {t, 0, 0, 0};
+    philox4x64_10(x, P.seed, gid);
+    const uint32_t n = P.count_base + sample(P.count_q, P.count_n, uint32_t(x[0]));
+    unsigned long long* out = P.arr_rec + (size_t(r) * P.chunk + tl) * P.arr_cap;
+    if (lane == 0) P.arr_cnt[size_t(r) * P.chunk + tl] = n;
+    if (n == 0) return;
+    // pass 1: tier counts
+    int cnt[kTiers];
+#pragma unroll
+    for (int p = 0; p < kTiers; ++p) cnt[p] = 0;
+    for (uint32_t k0 = 0; k0 < n; k0 += 64) {
+        const uint32_t k = k0 + lane;
+        int tier = -1;
+        if (k < n) {
+            unsigned long long y[4] = {t, k, 1, 0};
+            philox4x64_10(y, P.seed, gid);
+            tier = int(sample(tq, uint32_t(K), uint32_t(y[0])));
+        }
+#pragma unroll
+        for (int p = 0; p < kTiers; ++p)
+            if (p < K) cnt[p] += __popcll(ballot(tier == p));
+    }
+    int off[kTiers];
+    int acc = 0;
+#pragma unroll
+    for (int p = 0; p < kTiers; ++p) { off[p] = acc; acc += cnt[p]; }
+    // pass 2: draw again and scatter in tier order (a lane's draws are its own)
+    for (uint32_t k0 = 0; k0 < n; k0 += 64) {
+        const uint32_t k = k0 + lane;
+        int tier = -1;
+        unsigned long long rec = 0;
+        if (k < n) {
+            unsigned long long y[4] = {t, k, 1, 0};
+            philox4x64_10(y, P.seed, gid);
+            tier = int(sample(tq, uint32_t(K), uint32_t(y[0])));
+            const uint32_t prompt = P.prompt_base + sample(P.prompt_q, P.prompt_n, uint32_t(y[1]));
+            const uint32_t outl = P.output_base + sample(P.output_q, P.output_n, uint32_t(y[2]));
+            rec = static_cast<unsigned long long>(prompt) | (static_cast<unsigned long long>(outl) << 16) |
+                  (static_cast<unsigned long long>(tier) << 32) | (static_cast<unsigned long long>(k) << 36);
+        }
+        int pos = 0;
+#pragma unroll
+        for (int p = 0; p < kTiers; ++p) {
+            if (p >= K) continue;
+            const unsigned long long b = ballot(tier == p);
+            if (tier == p) pos = off[p] + __popcll(b & lanemask_lt());
+            off[p] += __popcll(b);
+        }
+        if (k < n) out[pos] = rec;
+    }
 }
 
 // ---------------------------------------------------------------------------
-// The step kernel
+// per-instance event handlers (uniform: the whole wave works on instance i)
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_step(Params P)
+
+// head of line of instance i from its slots: smallest (tier, seq) waiting
+__device__ inline void rescan_hol(const Ctx& C, int i, int lane)
+{
+    const size_t b = size_t(i) * C.S;
+    const int nch = (C.hwm[i] + 63) >> 6;
+    unsigned long long bk = kNone;
+    int bs = 0;
+    uint32_t bv = 0;
+    for (int c = 0; c < nch; ++c) {
+        const int s = c * 64 + lane;
+        const uint32_t v = C.hot[b + s];
+        if (wst(v) == 1u) {
+            const unsigned long long k = (static_cast<unsigned long long>((C.meta[b + s] >> 2) & 15u) << 32) | C.seq[b + s];
+            if (k < bk) { bk = k; bs = s; bv = v; }
+        }
+    }
+    const unsigned long long mn = wmin64(bk);
+    if (lane == 0 && mn == kNone) { C.hols[i] = kNoHol; C.holk[i] = kNone; C.hold[i] = 0; }
+    if (mn == kNone) { wave_sync(); return; }
+    const int wl = ffs64(ballot(bk == mn));
+    const int h = rl(bs, wl);
+    const uint32_t v = rlu(bv, wl);
+    if (lane == 0) { C.hols[i] = h; C.holk[i] = mn; C.hold[i] = blocks_of(wlo(v), C.shift); }
+    wave_sync();
+}
+
+// memory pressure: preempt the largest (tier, seq) running request until the
+// growth of this tick fits (Section 2.2; recompute semantics)
+__device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
+{
+    const size_t b = size_t(i) * C.S;
+    int G = C.gtmp[i], fr = C.freeb[i];
+    while (G > fr) {
+        const int nch = (C.hwm[i] + 63) >> 6;
+        unsigned long long bk = 0;
+        int bs = 0;
+        for (int c = 0; c < nch; ++c) {
+            const int s = c * 64 + lane;
+            const uint32_t v = C.hot[b + s];
+            if (wst(v) == 2u) {
+                const unsigned long long k = (static_cast<unsigned long long>(((C.meta[b + s] >> 2) & 15u) + 1u) << 32) | C.seq[b + s];
+                if (k > bk) { bk = k; bs = s; }
+            }
+        }
+        const unsigned long long mx = wmax64(bk);
+        if (mx == 0) break;
+        const int vs = rl(bs, ffs64(ballot(bk == mx)));
+        const int owner = vs & 63;
+        int vb = 0, vg = 0, vt = 0, vr = 0, vm = 0;
+        if (lane == owner) {
+            const uint32_t v = C.hot[b + vs];
+            const uint32_t lenf = wlo(v), fin = fin_of(v, t);
+            const uint32_t remb = fin - t + 1u, lenb = lenf - remb;
+            C.hot[b + vs] = kWaitW | (remb << 16) | lenb;
+            const uint32_t m = C.meta[b + vs];
+            C.meta[b + vs] = uint8_t((m & ~(3u | kMigrating)) | kWaiting);
+            vb = blocks_of(lenb, C.shift);
+            vg = (lenb & C.bmask) == 0;
+            vt = int((m >> 2) & 15u);
+            vr = int((lenf - fin - 1u) & C.bmask);
+            vm = (m & kMigrating) ? 1 : 0;
+        }
+        vb = rl(vb, owner); vg = rl(vg, owner); vt = rl(vt, owner); vr = rl(vr, owner); vm = rl(vm, owner);
+        fr += vb;
+        G -= vg;
+        if (lane == 0) {
+            C.held[i] -= vb;
+            C.B[i] -= 1;
+            C.nwait[i] += 1;
+            C.res[i * C.RB + vr] -= 1u;
+            tier_dec(C, i, vt);
+            stat(C, vt * 8 + kPreempted, 1);
+            if (vm) C.flags[i] |= kFlagAbort;
+            const unsigned long long key = (static_cast<unsigned long long>(vt) << 32) | static_cast<unsigned>(mx);
+            if (C.hols[i] != kHolUnknown && (C.hols[i] == kNoHol || key < C.holk[i])) {
+                C.hols[i] = vs; C.holk[i] = key; C.hold[i] = vb;
+            }
+        }
+        wave_sync();
+    }
+    if (lane == 0) { C.gtmp[i] = G; C.freeb[i] = fr; }
+    wave_sync();
+}
+
+// requests of instance i that emit their last token at tick t finish and free
+// their blocks
+__device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
+{
+    const size_t b = size_t(i) * C.S;
+    const int nch = (C.hwm[i] + 63) >> 6;
+    const uint32_t t14 = t & kFin;
+    int freed = 0, nf = 0, top = -1;
+    uint32_t nmin = kInf;
+    bool ab = false;
+    for (int c = 0; c < nch; ++c) {
+        const int s = c * 64 + lane;
+        const uint32_t v = C.hot[b + s];
+        const bool run = wst(v) == 2u;
+        const bool f = run && wmid(v) == t14;
+        if (f) {
+            const uint32_t lenf = wlo(v);
+            freed += blocks_of(lenf, C.shift);
+            const uint32_t m = C.meta[b + s];
+            const int tier = int((m >> 2) & 15u);
+            stat(C, tier * 8 + kFinished, 1);
+            stat(C, tier * 8 + kE2e, t - C.tarr[b + s]);
+            atomicSub(&C.res[i * C.RB + ((lenf - t - 1u) & C.bmask)], 1u);
+            tier_dec(C, i, tier);
+            if (m & kMigrating) ab = true;
+            C.hot[b + s] = 0; C.meta[b + s] = 0; C.seq[b + s] = 0; C.tarr[b + s] = 0;
+        } else if (run) {
+            const uint32_t rel = (wmid(v) - t - 1u) & kFin;
+            nmin = rel < nmin ? rel : nmin;
+        }
+        const unsigned long long fb = ballot(f);
+        const unsigned long long ow = ballot(v != 0 && !f);
+        nf += __popcll(fb);
+        if (ow) top = c * 64 + 63 - __clzll(static_cast<long long>(ow));
+        if (lane == 0) C.occ[i * C.W + c] = ow;
+    }
+    freed = wsum(freed);
+    nmin = unsigned(wmin64(nmin));
+    const bool any_ab = ballot(ab) != 0;
+    if (lane == 0) {
+        C.freeb[i] += freed;
+        C.held[i] -= freed;
+        C.B[i] -= nf;
+        C.live[i] -= nf;
+        C.hwm[i] = top + 1;
+        C.nfin[i] = nmin == kInf ? kInf : t + 1u + nmin;
+        if (any_ab) C.flags[i] |= kFlagAbort;
+    }
+    wave_sync();
+}
+
+// admit the head of line while its blocks fit (Section 3.1, Eq. 2)
+__device__ inline void admit(const Ctx& C, int i, uint32_t t, int lane)
+{
+    const size_t b = size_t(i) * C.S;
+    if (C.hols[i] == kHolUnknown) rescan_hol(C, i, lane);
+    while (C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]) {
+        const int h = C.hols[i];
+        const int owner = h & 63;
+        uint32_t fin = 0, first = 0, ta = 0;
+        int tier = 0, r = 0;
+        if (lane == owner) {
+            const uint32_t v = C.hot[b + h];
+            const uint32_t len = wlo(v), rem = wmid(v);
+            fin = t + rem;
+            C.hot[b + h] = kRunW | ((fin & kFin) << 16) | (len + rem);
+            const uint32_t m = C.meta[b + h];
+            C.meta[b + h] = uint8_t((m & ~3u) | kRunning | kAdmitted);
+            tier = int((m >> 2) & 15u);
+            first = (m & kAdmitted) ? 0u : 1u;
+            ta = first ? C.tarr[b + h] : 0u;
+            r = int((len - t - 1u) & C.bmask);
+        }
+        fin = rlu(fin, owner); first = rlu(first, owner); ta = rlu(ta, owner);
+        tier = rl(tier, owner); r = rl(r, owner);
+        if (lane == 0) {
+            const int dem = C.hold[i];
+            C.freeb[i] -= dem;
+            C.held[i] += dem;
+            C.B[i] += 1;
+            C.nwait[i] -= 1;
+            C.res[i * C.RB + r] += 1u;
+            tier_inc(C, i, tier);
+            if (fin < C.nfin[i]) C.nfin[i] = fin;
+            if (first) {
+                stat(C, tier * 8 + kAdmittedCnt, 1);
+                stat(C, tier * 8 + kQdelay, t - ta);
+            }
+            if (C.nwait[i] == 0) { C.hols[i] = kNoHol; C.holk[i] = kNone; C.hold[i] = 0; }
+            else C.hols[i] = kHolUnknown;
+        }
+        wave_sync();
+        if (C.hols[i] == kHolUnknown) rescan_hol(C, i, lane);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_step
+// ---------------------------------------------------------------------------
+template <int IPL>
+__global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, uint32_t nt)
 {
     extern __shared__ __align__(16) char lds_raw[];
-    const uint32_t I = P.I, S = P.S, W = P.W;
-    const Lds L = carve(lds_raw, I, W);
+    Ctx C = carve(lds_raw, P);
     const int lane = lane_id();
-    const int wave = threadIdx.x >> 6;
-    const int nwaves = blockDim.x >> 6;
-    const uint32_t shift = P.blk_shift;
-    const uint32_t bmask = (1u << shift) - 1u;
+    const uint32_t I = P.I, S = P.S, W = P.W;
 
     for (uint32_t r = blockIdx.x; r < P.R; r += gridDim.x) {
         const uint32_t g = P.group_of[r];
-        const int K = int(P.group_K32[g]);
-        const unsigned long long gid = P.id_base + r;
-        const size_t rbase = size_t(r) * I * S;
+        C.K = P.group_K32[g];
+#pragma unroll
+        for (int p = 0; p < kTiers; ++p) C.hq[p] = P.hq[g * kTiers + p];
+        const size_t rb = size_t(r) * I * S;
+        C.hot = P.hot + rb; C.meta = P.meta + rb; C.seq = P.seq + rb; C.tarr = P.tarr + rb;
 
-        // ---- load the replica ----
-        for (int j = threadIdx.x; j < kNstat; j += blockDim.x) L.stats[j] = P.stats[size_t(r) * kNstat + j];
-        for (int j = threadIdx.x; j < kTiers; j += blockDim.x) L.hl[j] = P.hq[g * kTiers + j];
-        for (uint32_t i = threadIdx.x; i < I; i += blockDim.x) {
-            L.freeb[i] = P.freeb[size_t(r) * I + i];
-            for (int k = 0; k < 4; ++k) L.mig[4 * i + k] = P.mig[(size_t(r) * I + i) * 4 + k];
-            L.abort_[i] = 0;
+        // ---------------- prologue: derived per-instance state ----------------
+        for (int j = lane; j < kNstat; j += 64) C.stats[j] = P.stats[size_t(r) * kNstat + j];
+        for (uint32_t i = lane; i < I; i += 64) {
+            C.freeb[i] = P.freeb[size_t(r) * I + i];
+            for (int k = 0; k < 4; ++k) C.mig[4 * i + k] = P.mig[(size_t(r) * I + i) * 4 + k];
+            C.inb[i] = 0;
+            C.flags[i] = 0;
+            C.tmask[i] = 0;
+            for (uint32_t q = 0; q < C.RB; ++q) C.res[i * C.RB + q] = 0;
+            for (int q = 0; q < kTiers; ++q) C.tcnt[i * kTiers + q] = 0;
         }
-        // high-water marks from a full scan
-        for (uint32_t i = wave; i < I; i += nwaves) {
-            const uint8_t* mt = P.meta + rbase + size_t(i) * S;
-            int top = -1;
+        wave_sync();
+        for (uint32_t i = lane; i < I; i += 64) {
+            const int d = C.mig[4 * i];
+            if (d >= 0) C.inb[d] = C.mig[4 * i + 3];
+        }
+        wave_sync();
+        const uint32_t t0u = uint32_t(t0);
+        for (uint32_t i = 0; i < I; ++i) {
+            const size_t b = size_t(i) * S;
+            int nB = 0, nlive = 0, nw = 0, top = -1, held = 0;
+            uint32_t nmin = kInf;
+            unsigned long long bk = kNone;
+            int bs = 0;
+            uint32_t bv = 0;
             for (uint32_t c = 0; c < W; ++c) {
-                const unsigned long long b = ballot(mt[c * 64 + lane] != 0);
-                if (b) top = int(c * 64 + 63 - __clzll(static_cast<long long>(b)));
+                const int s = int(c) * 64 + lane;
+                const uint32_t v = C.hot[b + s];
+                const uint32_t st = wst(v);
+                const unsigned long long ow = ballot(v != 0);
+                nlive += __popcll(ow);
+                nB += __popcll(ballot(st == 2u));
+                nw += __popcll(ballot(st == 1u));
+                if (ow) top = int(c) * 64 + 63 - __clzll(static_cast<long long>(ow));
+                if (lane == 0) C.occ[i * W + c] = ow;
+                if (st == 2u) {
+                    const uint32_t lenf = wlo(v), fin = fin_of(v, t0u);
+                    held += blocks_of(lenf - (fin - t0u + 1u), C.shift);
+                    atomicAdd(&C.res[i * C.RB + ((lenf - fin - 1u) & C.bmask)], 1u);
+                    const int tier = int((C.meta[b + s] >> 2) & 15u);
+                    atomicAdd(&C.tcnt[i * kTiers + tier], 1u);
+                    nmin = fin < nmin ? fin : nmin;
+                } else if (st == 1u) {
+                    const unsigned long long k = (static_cast<unsigned long long>((C.meta[b + s] >> 2) & 15u) << 32) | C.seq[b + s];
+                    if (k < bk) { bk = k; bs = s; bv = v; }
+                }
             }
-            if (lane == 0) L.hwm[i] = top + 1;
+            held = wsum(held);
+            nmin = unsigned(wmin64(nmin));
+            const unsigned long long mn = wmin64(bk);
+            int hs = kNoHol, hd = 0;
+            if (mn != kNone) {
+                const int wl = ffs64(ballot(bk == mn));
+                hs = rl(bs, wl);
+                hd = blocks_of(wlo(rlu(bv, wl)), C.shift);
+            }
+            if (lane == 0) {
+                C.B[i] = nB; C.live[i] = nlive; C.nwait[i] = nw; C.hwm[i] = top + 1;
+                C.held[i] = held; C.nfin[i] = nmin;
+                C.hols[i] = hs; C.holk[i] = mn; C.hold[i] = hd;
+                int tm = 0;
+                for (int p = 0; p < kTiers; ++p) tm |= C.tcnt[i * kTiers + p] ? (1 << p) : 0;
+                C.tmask[i] = tm;
+            }
+            wave_sync();
         }
         unsigned next_seq = P.next_seq[r];
-        __syncthreads();
+        unsigned long long run_acc = 0, wait_acc = 0;
+        const unsigned long long* recs = P.arr_rec + size_t(r) * P.chunk * P.arr_cap;
+        const uint32_t* cnts = P.arr_cnt + size_t(r) * P.chunk;
+        wave_sync();
 
-        for (unsigned long long t = P.tick0; t < P.tick0 + P.n_ticks; ++t) {
-            // ================= A: decode, growth, preemption, finish =================
-            for (uint32_t i = wave; i < I; i += nwaves) {
-                const size_t ib = rbase + size_t(i) * S;
-                uint8_t* mt = P.meta + ib;
-                uint32_t* lr = P.lr + ib;
-                uint32_t* sq = P.seq + ib;
-                uint32_t* ta = P.tarr + ib;
-                const int nch = (L.hwm[i] + 63) >> 6;
-                int grow = 0;
-                for (int c = 0; c < nch; ++c) {
-                    const int s = c * 64 + lane;
-                    bool gr = false;
-                    if ((mt[s] & 3u) == kRunning) gr = (lr[s] & bmask) == 0;
-                    grow += __popcll(ballot(gr));
+        for (uint32_t tl = 0; tl < nt; ++tl) {
+            const uint32_t t = t0u + tl;
+            const uint32_t n = cnts[tl];
+            const unsigned long long* rec = recs + size_t(tl) * P.arr_cap;
+            unsigned long long a0 = lane < int(n) ? rec[lane] : 0;
+
+            // ===================== A: growth, preemption, finish =====================
+            const uint32_t cres = (0u - t) & C.bmask;
+            unsigned long long pre[IPL], due[IPL];
+#pragma unroll
+            for (int j = 0; j < IPL; ++j) {
+                const uint32_t i = lane + 64 * j;
+                bool np = false, dd = false;
+                if (i < I) {
+                    const int G = int(C.res[i * C.RB + cres]);
+                    C.gtmp[i] = G;
+                    np = G > C.freeb[i];
+                    dd = C.nfin[i] <= t;
                 }
-                int fr = L.freeb[i];
-                while (grow > fr) {
-                    // victim: the running request with the largest (tier, seq)
-                    unsigned long long bk = 0;
-                    int bs = 0;
-                    for (int c = 0; c < nch; ++c) {
-                        const int s = c * 64 + lane;
-                        const unsigned m = mt[s];
-                        if ((m & 3u) == kRunning) {
-                            const unsigned long long k = (static_cast<unsigned long long>(((m >> 2) & 15u) + 1u) << 32) | sq[s];
-                            if (k > bk) { bk = k; bs = s; }
-                        }
-                    }
-                    const unsigned long long mx = wmax64(bk);
-                    if (mx == 0) break;
-                    const int wl = __ffsll(static_cast<long long>(ballot(bk == mx))) - 1;
-                    const int v = __shfl(bs, wl);
-                    int vb = 0, vg = 0, vt = 0, vm = 0;
-                    if (lane == (v & 63)) {
-                        const unsigned m = mt[v];
-                        const unsigned len = lr[v] & 0xFFFFu;
-                        vt = int((m >> 2) & 15u);
-                        vm = (m & kMigrating) ? 1 : 0;
-                        mt[v] = uint8_t((m & ~(3u | kMigrating)) | kWaiting);
-                        vb = blocks_of(len, shift);
-                        vg = (len & bmask) == 0;
-                    }
-                    vb = __shfl(vb, v & 63);
-                    vg = __shfl(vg, v & 63);
-                    vt = __shfl(vt, v & 63);
-                    vm = __shfl(vm, v & 63);
-                    fr += vb;
-                    grow -= vg;
-                    if (lane == 0) {
-                        stat_add(L, vt * 8 + kPreempted, 1);
-                        if (vm) L.abort_[i] = 1;
-                    }
-                }
-                fr -= grow;
-                int freed = 0;
-                bool ab = false;
-                for (int c = 0; c < nch; ++c) {
-                    const int s = c * 64 + lane;
-                    const unsigned m = mt[s];
-                    if ((m & 3u) != kRunning) continue;
-                    const unsigned v = lr[s];
-                    const unsigned len = (v & 0xFFFFu) + 1u, rem = (v >> 16) - 1u;
-                    if (rem == 0) {
-                        freed += blocks_of(len, shift);
-                        const int tier = int((m >> 2) & 15u);
-                        stat_add(L, tier * 8 + kFinished, 1);
-                        stat_add(L, tier * 8 + kE2e, t - ta[s]);
-                        if (m & kMigrating) ab = true;
-                        mt[s] = 0; lr[s] = 0; sq[s] = 0; ta[s] = 0;
-                    } else {
-                        lr[s] = len | (rem << 16);
-                    }
-                }
-                fr += wsum(freed);
-                const bool any_ab = ballot(ab) != 0;
-                if (lane == 0) {
-                    L.freeb[i] = fr;
-                    if (any_ab) L.abort_[i] = 1;
-                }
+                pre[j] = ballot(np);
+                due[j] = ballot(dd);
             }
-            __syncthreads();
-
-            // ================= A2: release aborted reservations =================
-            if (wave == 0) {
+            wave_sync();
+#pragma unroll
+            for (int j = 0; j < IPL; ++j)
+                for (unsigned long long m = pre[j]; m; m &= m - 1) preempt(C, 64 * j + ffs64(m), t, lane);
+            for (uint32_t i = lane; i < I; i += 64) {
+                const int G = C.gtmp[i];
+                C.freeb[i] -= G;
+                C.held[i] += G;
+            }
+            wave_sync();
+            bool any_abort = false;
+#pragma unroll
+            for (int j = 0; j < IPL; ++j)
+                for (unsigned long long m = due[j]; m; m &= m - 1) finish_scan(C, 64 * j + ffs64(m), t, lane);
+            for (uint32_t i = lane; i < I; i += 64) any_abort |= (C.flags[i] & kFlagAbort) != 0;
+            // ===================== A2: release reservations of aborted migrations =====================
+            if (ballot(any_abort)) {
                 for (uint32_t i = lane; i < I; i += 64) {
-                    if (!L.abort_[i]) continue;
-                    L.abort_[i] = 0;
-                    int* m = &L.mig[4 * i];
+                    if (!(C.flags[i] & kFlagAbort)) continue;
+                    C.flags[i] &= ~kFlagAbort;
+                    int* m = &C.mig[4 * i];
                     const int d = m[0];
                     if (d < 0) continue;
-                    L.freeb[d] += m[3];
-                    const size_t db = rbase + size_t(d) * S + m[2];
-                    P.meta[db] = 0; P.lr[db] = 0; P.seq[db] = 0; P.tarr[db] = 0;
+                    C.freeb[d] += m[3];
+                    C.inb[d] = 0;
+                    const size_t db = size_t(d) * S + m[2];
+                    C.hot[db] = 0; C.meta[db] = 0;
+                    C.occ[d * W + (m[2] >> 6)] &= ~(1ull << (m[2] & 63));
+                    C.live[d] -= 1;
                     m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
-                    stat_add(L, kMigAborted, 1);
-                }
-                for (uint32_t i = lane; i < I; i += 64) L.inb[i] = 0;
-                for (uint32_t i = lane; i < I; i += 64) {
-                    const int d = L.mig[4 * i];
-                    if (d >= 0) L.inb[d] = L.mig[4 * i + 3];
+                    stat(C, kMigAborted, 1);
                 }
             }
-            __syncthreads();
+            wave_sync();
 
-            // ================= B: admission, C: per-instance summary =================
-            for (uint32_t i = wave; i < I; i += nwaves) {
-                const size_t ib = rbase + size_t(i) * S;
-                uint8_t* mt = P.meta + ib;
-                uint32_t* lr = P.lr + ib;
-                uint32_t* sq = P.seq + ib;
-                uint32_t* ta = P.tarr + ib;
-                const int nch = (L.hwm[i] + 63) >> 6;
-                int fr = L.freeb[i];
-                int hslot = -1, hdem = 0;
-                unsigned long long hkey = kNone;
-                for (;;) {
-                    unsigned long long bk = kNone;
-                    int bs = 0;
-                    for (int c = 0; c < nch; ++c) {
-                        const int s = c * 64 + lane;
-                        const unsigned m = mt[s];
-                        if ((m & 3u) == kWaiting) {
-                            const unsigned long long k = (static_cast<unsigned long long>((m >> 2) & 15u) << 32) | sq[s];
-                            if (k < bk) { bk = k; bs = s; }
-                        }
-                    }
-                    const unsigned long long mn = wmin64(bk);
-                    if (mn == kNone) break;
-                    const int wl = __ffsll(static_cast<long long>(ballot(bk == mn))) - 1;
-                    const int h = __shfl(bs, wl);
-                    int need = 0;
-                    if (lane == (h & 63)) need = blocks_of(lr[h] & 0xFFFFu, shift);
-                    need = __shfl(need, h & 63);
-                    if (need > fr) { hslot = h; hdem = need; hkey = mn; break; }
-                    fr -= need;
-                    if (lane == (h & 63)) {
-                        const unsigned m = mt[h];
-                        mt[h] = uint8_t((m & ~3u) | kRunning | kAdmitted);
-                        if (!(m & kAdmitted)) {
-                            const int tier = int((m >> 2) & 15u);
-                            stat_add(L, tier * 8 + kAdmittedCnt, 1);
-                            stat_add(L, tier * 8 + kQdelay, t - ta[h]);
-                        }
-                    }
-                }
-                // C: summary scan
-                int nB = 0, nlive = 0, nwait = 0, held = 0, top = -1;
-                int tc[kTiers];
+            // ===================== B: admission; C: freeness =====================
+            {
+                unsigned long long cand[IPL];
 #pragma unroll
-                for (int p = 0; p < kTiers; ++p) tc[p] = 0;
-                for (int c = 0; c < nch; ++c) {
-                    const int s = c * 64 + lane;
-                    const unsigned m = mt[s];
-                    const unsigned st = m & 3u;
-                    const bool run = st == kRunning;
-                    const unsigned long long ow = ballot(st != kEmpty);
-                    nB += __popcll(ballot(run));
-                    nlive += __popcll(ow);
-                    nwait += __popcll(ballot(st == kWaiting));
-                    if (run) held += blocks_of(lr[s] & 0xFFFFu, shift);
-                    const int tier = int((m >> 2) & 15u);
+                for (int j = 0; j < IPL; ++j) {
+                    const uint32_t i = lane + 64 * j;
+                    bool c = false;
+                    if (i < I) c = C.hols[i] == kHolUnknown || (C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]);
+                    cand[j] = ballot(c);
+                }
 #pragma unroll
-                    for (int p = 0; p < kTiers; ++p)
-                        if (p < K) tc[p] += __popcll(ballot(run && tier == p));
-                    if (ow) top = c * 64 + 63 - __clzll(static_cast<long long>(ow));
-                    if (lane == 0) L.occ[i * W + c] = ow;
-                }
-                for (uint32_t c = nch + lane; c < W; c += 64) L.occ[i * W + c] = 0;
-                held = wsum(held);
-                if (lane == 0) {
-                    L.freeb[i] = fr;
-                    L.B[i] = nB;
-                    L.live[i] = nlive;
-                    L.hwm[i] = top + 1;
-                    for (int p = 0; p < kTiers; ++p) L.tcnt[i * kTiers + p] = (unsigned short)(p < K ? tc[p] : 0);
-                    L.hol_slot[i] = hslot;
-                    L.hol_tier[i] = int(hkey >> 32);
-                    L.hol_seq[i] = unsigned(hkey);
-                    L.hol_dem[i] = hslot >= 0 ? hdem : 0;
-                    if (fr < 0 || fr + held + L.inb[i] != int(P.M)) stat_add(L, kInvariant, 1);
-                    set_f(L, int(i), K);
-                    stat_add(L, kRunSlotTicks, nB);
-                    stat_add(L, kWaitSlotTicks, nwait);
-                }
+                for (int j = 0; j < IPL; ++j)
+                    for (unsigned long long m = cand[j]; m; m &= m - 1) admit(C, 64 * j + ffs64(m), t, lane);
             }
-            __syncthreads();
+            for (uint32_t i = lane; i < I; i += 64) {
+                set_f(C, int(i));
+                if (C.freeb[i] < 0 || C.freeb[i] + C.held[i] + C.inb[i] != int(C.M)) stat(C, kInvariant, 1);
+            }
+            wave_sync();
 
-            // ================= D: arrivals and tier-ordered dispatch =================
-            if (wave == 0) {
-                unsigned long long x[4] = {t, 0, 0, 0};
-                philox4x64_10(x, P.seed, gid);
-                const uint32_t n = P.count_base + sample(P.count_q, P.count_n, uint32_t(x[0]));
+            // ===================== D: tier-ordered dispatch =====================
+            if (n > 0) {
+                // arrivals per tier
+                for (uint32_t k0 = 0; k0 < n; k0 += 64) {
+                    const unsigned long long a = k0 == 0 ? a0 : (k0 + lane < n ? rec[k0 + lane] : 0);
+                    const int tier = k0 + lane < n ? int((a >> 32) & 15u) : -1;
+                    for (int p = 0; p < int(C.K); ++p) {
+                        const int c = __popcll(ballot(tier == p));
+                        if (lane == 0 && c) stat(C, p * 8 + kArrived, c);
+                    }
+                }
                 const unsigned seq0 = next_seq;
                 next_seq += n;
-                unsigned long long* raw = P.scratch + size_t(blockIdx.x) * 2 * P.max_arrivals;
-                unsigned long long* sorted = raw + P.max_arrivals;
-                const uint32_t* tq = P.tier_q + size_t(g) * kTiers;
-                int cnt[kTiers];
+                double key[IPL];
 #pragma unroll
-                for (int p = 0; p < kTiers; ++p) cnt[p] = 0;
-                for (uint32_t k0 = 0; k0 < n; k0 += 64) {
-                    const uint32_t k = k0 + lane;
-                    const bool ok = k < n;
-                    int tier = 0;
-                    if (ok) {
-                        unsigned long long y[4] = {t, k, 1, 0};
-                        philox4x64_10(y, P.seed, gid);
-                        tier = int(sample(tq, uint32_t(K), uint32_t(y[0])));
-                        const uint32_t prompt = P.prompt_base + sample(P.prompt_q, P.prompt_n, uint32_t(y[1]));
-                        const uint32_t out = P.output_base + sample(P.output_q, P.output_n, uint32_t(y[2]));
-                        raw[k] = static_cast<unsigned long long>(prompt) | (static_cast<unsigned long long>(out) << 16) |
-                                 (static_cast<unsigned long long>(tier) << 32) | (static_cast<unsigned long long>(k) << 36);
-                    }
-#pragma unroll
-                    for (int p = 0; p < kTiers; ++p)
-                        if (p < K) cnt[p] += __popcll(ballot(ok && tier == p));
+                for (int j = 0; j < IPL; ++j) {
+                    const uint32_t i = lane + 64 * j;
+                    key[j] = (i < I && C.live[i] < int(S)) ? C.fd[i] : -__builtin_inf();
                 }
-                int off[kTiers];
-                int acc = 0;
-#pragma unroll
-                for (int p = 0; p < kTiers; ++p) {
-                    off[p] = acc;
-                    acc += p < K ? cnt[p] : 0;
-                    if (lane == 0 && p < K && cnt[p]) stat_add(L, p * 8 + kArrived, cnt[p]);
-                }
-                // stable scatter by tier (a lane reads back only what it wrote)
-                for (uint32_t k0 = 0; k0 < n; k0 += 64) {
-                    const uint32_t k = k0 + lane;
-                    const bool ok = k < n;
-                    const unsigned long long a = ok ? raw[k] : 0;
-                    const int tier = int((a >> 32) & 15u);
-                    int pos = 0;
-#pragma unroll
-                    for (int p = 0; p < kTiers; ++p) {
-                        if (p >= K) continue;
-                        const unsigned long long b = ballot(ok && tier == p);
-                        if (ok && tier == p) pos = off[p] + __popcll(b & lanemask_lt());
-                        off[p] += __popcll(b);
-                    }
-                    if (ok) sorted[pos] = a;
-                }
-                __threadfence_block();
-
                 int cur = -1;
-                for (uint32_t j = 0; j < n; ++j) {
-                    const unsigned long long a = sorted[j];
-                    const int tier = int((a >> 32) & 15u);
-                    if (cur < 0) {
-                        unsigned long long best = 0;
-                        for (uint32_t i = lane; i < I; i += 64)
-                            if (L.live[i] < int(S)) {
-                                const unsigned long long k = dkey(L.q[i], int(i));
-                                best = k > best ? k : best;
+                bool full = false;
+                for (uint32_t k0 = 0; k0 < n; k0 += 64) {
+                    const uint32_t cn = n - k0 < 64 ? n - k0 : 64;
+                    const unsigned long long a = k0 == 0 ? a0 : (lane < int(cn) ? rec[k0 + lane] : 0);
+                    int tgt = -1;
+                    for (uint32_t k = 0; k < cn && !full; ++k) {
+                        const unsigned long long ak = rl64(a, int(k));
+                        const int tier = int((ak >> 32) & 15u);
+                        if (cur < 0) {
+                            double lb = key[0];
+                            int lj = 0;
+#pragma unroll
+                            for (int j = 1; j < IPL; ++j)
+                                if (key[j] > lb) { lb = key[j]; lj = j; }
+                            (void)lj;
+                            const double mv = wave_max_f64(lb);
+                            if (mv == -__builtin_inf()) { full = true; break; }
+#pragma unroll
+                            for (int j = 0; j < IPL; ++j) {
+                                const unsigned long long bm = ballot(key[j] == mv);
+                                if (bm && cur < 0) cur = 64 * j + ffs64(bm);
                             }
-                        best = wmax64(best);
-                        if (best == 0) {
-                            // no free slot anywhere: the rest of this tick's arrivals are rejected
-                            for (uint32_t jj = j + lane; jj < n; jj += 64)
-                                stat_add(L, int((sorted[jj] >> 32) & 15u) * 8 + kRejected, 1);
-                            break;
                         }
-                        cur = 255 - int(best & 255u);
-                    }
-                    int c0;
-                    unsigned long long w0;
-                    const int s = lowest_empty(L, cur, W, lane, &c0, &w0);
-                    if (s < 0) {  // occupancy and live count disagree: flag and drop the arrival
-                        if (lane == 0) { stat_add(L, kInvariant, 1); stat_add(L, tier * 8 + kRejected, 1); L.live[cur] = int(S); }
-                        cur = -1;
-                        continue;
-                    }
-                    const unsigned seqv = seq0 + unsigned(a >> 36);
-                    const uint32_t prompt = uint32_t(a & 0xFFFFu);
-                    const bool becomes = L.hol_slot[cur] < 0 || tier < L.hol_tier[cur] ||
-                                         (tier == L.hol_tier[cur] && seqv < L.hol_seq[cur]);
-                    if (lane == 0) {
-                        const size_t sb = rbase + size_t(cur) * S + s;
-                        P.meta[sb] = uint8_t(kWaiting | (unsigned(tier) << 2));
-                        P.lr[sb] = uint32_t(a & 0xFFFFFFFFu);
-                        P.seq[sb] = seqv;
-                        P.tarr[sb] = uint32_t(t);
-                        L.occ[cur * W + c0] = w0 | (1ull << (s & 63));
-                        L.live[cur] += 1;
-                        if (s + 1 > L.hwm[cur]) L.hwm[cur] = s + 1;
-                        stat_add(L, tier * 8 + kDispatched, 1);
-                        stat_add(L, kWaitSlotTicks, 1);
-                        if (becomes) {
-                            L.hol_slot[cur] = s;
-                            L.hol_tier[cur] = tier;
-                            L.hol_seq[cur] = seqv;
-                            L.hol_dem[cur] = blocks_of(prompt, shift);
-                            set_f(L, cur, K);
-                        }
-                    }
-                    if (becomes || L.live[cur] >= int(S)) cur = -1;
-                }
-            }
-            __syncthreads();
-
-            // ================= E1: staged copies =================
-            if (wave == 0) {
-                for (uint32_t i = lane; i < I; i += 64) {
-                    int* m = &L.mig[4 * i];
-                    const int d = m[0];
-                    if (d < 0) continue;
-                    const size_t sb = rbase + size_t(i) * S + m[1];
-                    const size_t db = rbase + size_t(d) * S + m[2];
-                    const unsigned v = P.lr[sb];
-                    const int b = blocks_of(v & 0xFFFFu, shift);
-                    int w = b - m[3];
-                    if (w > int(P.mig_stage)) w = int(P.mig_stage);
-                    if (w > L.freeb[d]) {
-                        L.freeb[d] += m[3];
-                        P.meta[db] = 0;
-                        L.occ[d * W + (m[2] >> 6)] &= ~(1ull << (m[2] & 63));
-                        L.live[d] -= 1;
-                        P.meta[sb] = uint8_t(P.meta[sb] & ~kMigrating);
-                        m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
-                        stat_add(L, kMigAborted, 1);
-                        set_f(L, d, K);
-                        continue;
-                    }
-                    L.freeb[d] -= w;
-                    m[3] += w;
-                    if (m[3] == b) {
-                        const unsigned mm = P.meta[sb];
-                        const int tier = int((mm >> 2) & 15u);
-                        P.meta[db] = uint8_t((mm & ~(3u | kMigrating)) | kRunning);
-                        P.lr[db] = v;
-                        P.seq[db] = P.seq[sb];
-                        P.tarr[db] = P.tarr[sb];
-                        P.meta[sb] = 0; P.lr[sb] = 0; P.seq[sb] = 0; P.tarr[sb] = 0;
-                        L.occ[i * W + (m[1] >> 6)] &= ~(1ull << (m[1] & 63));
-                        L.live[i] -= 1;
-                        L.freeb[i] += b;
-                        L.B[i] -= 1;
-                        L.B[d] += 1;
-                        L.tcnt[i * kTiers + tier] -= 1;
-                        L.tcnt[d * kTiers + tier] += 1;
-                        m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
-                        stat_add(L, kMigCommitted, 1);
-                        set_f(L, int(i), K);
-                    }
-                    set_f(L, d, K);
-                }
-            }
-            __syncthreads();
-
-            // ================= E2: pairing on interval ticks =================
-            if (wave == 0 && t % P.mig_interval == 0) {
-                for (uint32_t i = lane; i < I; i += 64) L.busy[i] = 0;
-                for (uint32_t i = lane; i < I; i += 64) {
-                    const int d = L.mig[4 * i];
-                    if (d >= 0) { L.busy[i] = 1; L.busy[d] = 1; }
-                }
-                int mine = 0;
-                for (uint32_t i = lane; i < I; i += 64) {
-                    if (L.busy[i]) continue;
-                    ++mine;
-                    const unsigned long long ki = pkey(L.q[i], int(i));
-                    int rank = 0;
-                    for (uint32_t j = 0; j < I; ++j)
-                        if (!L.busy[j] && pkey(L.q[j], int(j)) < ki) ++rank;
-                    L.order[rank] = int(i);
-                }
-                const int n = wsum(mine);
-                for (int k = 0; k < int(P.mig_max_pairs) && k < n - 1 - k; ++k) {
-                    const int src = L.order[k], dst = L.order[n - 1 - k];
-                    if (L.num[src] >= 0) break;
-                    const long long lhs = (long long)P.theta_den *
-                        ((long long)L.num[dst] * L.den[src] - (long long)L.num[src] * L.den[dst]);
-                    const long long rhs = (long long)P.theta_num * 256 * L.den[src] * L.den[dst];
-                    if (lhs < rhs) break;
-                    if (L.live[dst] >= int(S)) continue;
-                    int c0;
-                    unsigned long long w0;
-                    const int ds = lowest_empty(L, dst, W, lane, &c0, &w0);
-                    if (ds < 0) {
-                        if (lane == 0) stat_add(L, kInvariant, 1);
-                        continue;
-                    }
-                    const size_t dsb = rbase + size_t(dst) * S + ds;
-                    const int h = L.hol_slot[src];
-                    if (h >= 0) {
+                        if (lane == int(k)) tgt = cur;
+                        const unsigned seqv = seq0 + unsigned(ak >> 36);
+                        const unsigned long long hk = (static_cast<unsigned long long>(tier) << 32) | seqv;
+                        const bool becomes = C.hols[cur] == kNoHol || hk < C.holk[cur];
+                        const int nl = C.live[cur] + 1;
                         if (lane == 0) {
-                            const size_t hb = rbase + size_t(src) * S + h;
-                            P.meta[dsb] = P.meta[hb]; P.lr[dsb] = P.lr[hb];
-                            P.seq[dsb] = P.seq[hb]; P.tarr[dsb] = P.tarr[hb];
-                            P.meta[hb] = 0; P.lr[hb] = 0; P.seq[hb] = 0; P.tarr[hb] = 0;
-                            L.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
-                            L.live[src] -= 1;
-                            L.occ[dst * W + c0] = w0 | (1ull << (ds & 63));
-                            L.live[dst] += 1;
-                            if (ds + 1 > L.hwm[dst]) L.hwm[dst] = ds + 1;
-                            stat_add(L, kMigQueued, 1);
+                            C.live[cur] = nl;
+                            C.nwait[cur] += 1;
+                            if (becomes) {
+                                C.holk[cur] = hk;
+                                C.hols[cur] = kHolPending;
+                                C.pend[cur] = int(k0 + k);
+                                C.hold[cur] = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
+                                set_f(C, cur);
+                            }
                         }
-                        continue;
-                    }
-                    // running candidate: largest tier, then fewest blocks, then newest
-                    const uint8_t* mt = P.meta + rbase + size_t(src) * S;
-                    const uint32_t* lr = P.lr + rbase + size_t(src) * S;
-                    const uint32_t* sq = P.seq + rbase + size_t(src) * S;
-                    const int nch = (L.hwm[src] + 63) >> 6;
-                    unsigned long long bk = 0;
-                    int bs = 0;
-                    for (int c = 0; c < nch; ++c) {
-                        const int s = c * 64 + lane;
-                        const unsigned m = mt[s];
-                        if ((m & 3u) == kRunning && !(m & kMigrating)) {
-                            const unsigned long long kk =
-                                (static_cast<unsigned long long>(((m >> 2) & 15u) + 1u) << 48) |
-                                (static_cast<unsigned long long>(65535 - blocks_of(lr[s] & 0xFFFFu, shift)) << 32) | sq[s];
-                            if (kk > bk) { bk = kk; bs = s; }
+                        wave_sync();
+                        if (becomes || nl >= int(S)) {
+                            const double nk = nl >= int(S) ? -__builtin_inf() : C.fd[cur];
+#pragma unroll
+                            for (int j = 0; j < IPL; ++j)
+                                if (cur >> 6 == j && lane == (cur & 63)) key[j] = nk;
+                            cur = -1;
                         }
                     }
-                    const unsigned long long mx = wmax64(bk);
-                    if (mx == 0) continue;  // unreachable: F < 0 implies a request
-                    const int cs = __shfl(bs, __ffsll(static_cast<long long>(ballot(bk == mx))) - 1);
-                    if (lane == 0) {
-                        P.meta[dsb] = uint8_t(kInbound);
-                        L.occ[dst * W + c0] = w0 | (1ull << (ds & 63));
-                        L.live[dst] += 1;
-                        if (ds + 1 > L.hwm[dst]) L.hwm[dst] = ds + 1;
-                        const size_t cb = rbase + size_t(src) * S + cs;
-                        P.meta[cb] = uint8_t(P.meta[cb] | kMigrating);
-                        int* m = &L.mig[4 * src];
-                        m[0] = dst; m[1] = cs; m[2] = ds; m[3] = 0;
-                        stat_add(L, kMigStarted, 1);
+                    // slot assignment: the arrivals bound for one instance take its
+                    // lowest empty slots in arrival order
+                    wave_sync();
+                    int rank = 0;
+                    for (unsigned long long pend = ballot(tgt >= 0); pend;) {
+                        const int tv = rl(tgt, ffs64(pend));
+                        const unsigned long long same = ballot(tgt == tv);
+                        if (tgt == tv) rank = __popcll(same & lanemask_lt());
+                        pend &= ~same;
                     }
+                    const int tier = int((a >> 32) & 15u);
+                    if (tgt >= 0) {
+                        // the rank-th empty slot must exist
+                        int z_total = 0;
+                        for (uint32_t w = 0; w < W; ++w) z_total += 64 - __popcll(C.occ[tgt * W + w]);
+                        const int s = rank < z_total ? 0 : -1;
+                        if (s < 0) {  // occupancy and live count disagree: flag, drop the arrival
+                            stat(C, kInvariant, 1);
+                            stat(C, tier * 8 + kRejected, 1);
+                            tgt = -2;
+                        }
+                    }
+                    if (tgt >= 0) {
+                        int s = -1;
+                        {
+                            int rk = rank;
+                            for (uint32_t w = 0; w < W && s < 0; ++w) {
+                                const unsigned long long word = C.occ[tgt * W + w];
+                                const int z = 64 - __popcll(word);
+                                if (rk < z) {
+                                    unsigned long long free_bits = ~word;
+                                    for (int q = 0; q < rk; ++q) free_bits &= free_bits - 1;
+                                    s = int(w) * 64 + ffs64(free_bits);
+                                } else {
+                                    rk -= z;
+                                }
+                            }
+                        }
+                        atomicOr(&C.occ[tgt * W + (s >> 6)], 1ull << (s & 63));
+                        atomicMax(&C.hwm[tgt], s + 1);
+                        const size_t sb = size_t(tgt) * S + s;
+                        C.hot[sb] = kWaitW | (uint32_t((a >> 16) & 0xFFFFu) << 16) | uint32_t(a & 0xFFFFu);
+                        C.meta[sb] = uint8_t(kWaiting | (unsigned(tier) << 2));
+                        C.seq[sb] = seq0 + unsigned(a >> 36);
+                        C.tarr[sb] = t;
+                        if (C.hols[tgt] == kHolPending && C.pend[tgt] == int(k0) + lane) C.hols[tgt] = s;
+                    }
+                    for (int p = 0; p < int(C.K); ++p) {
+                        const int cd = __popcll(ballot(tgt >= 0 && tier == p));
+                        const int cr = __popcll(ballot(tgt == -1 && lane < int(cn) && tier == p));
+                        if (lane == 0 && cd) stat(C, p * 8 + kDispatched, cd);
+                        if (lane == 0 && cr) stat(C, p * 8 + kRejected, cr);
+                    }
+                    wave_sync();
                 }
             }
-            if (threadIdx.x == 0) stat_add(L, kTicks, 1);
-            __syncthreads();
+            wave_sync();
+
+            // ===================== E1: staged copies =====================
+            for (uint32_t i = lane; i < I; i += 64) {
+                int* m = &C.mig[4 * i];
+                const int d = m[0];
+                if (d < 0) continue;
+                const size_t sb = size_t(i) * S + m[1], db = size_t(d) * S + m[2];
+                const uint32_t v = C.hot[sb];
+                const uint32_t fin = fin_of(v, t);
+                const int bl = blocks_of(wlo(v) - (fin - t), C.shift);
+                int w = bl - m[3];
+                if (w > int(P.mig_stage)) w = int(P.mig_stage);
+                if (w > C.freeb[d]) {
+                    C.freeb[d] += m[3];
+                    C.inb[d] = 0;
+                    C.hot[db] = 0; C.meta[db] = 0;
+                    C.occ[d * W + (m[2] >> 6)] &= ~(1ull << (m[2] & 63));
+                    C.live[d] -= 1;
+                    C.meta[sb] = uint8_t(C.meta[sb] & ~kMigrating);
+                    m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
+                    stat(C, kMigAborted, 1);
+                    set_f(C, d);
+                    continue;
+                }
+                C.freeb[d] -= w;
+                m[3] += w;
+                C.inb[d] += w;
+                if (m[3] == bl) {
+                    const uint32_t mm = C.meta[sb];
+                    const int tier = int((mm >> 2) & 15u);
+                    const int rr = int((wlo(v) - fin - 1u) & C.bmask);
+                    C.hot[db] = v;
+                    C.meta[db] = uint8_t((mm & ~(3u | kMigrating)) | kRunning);
+                    C.seq[db] = C.seq[sb];
+                    C.tarr[db] = C.tarr[sb];
+                    C.hot[sb] = 0; C.meta[sb] = 0; C.seq[sb] = 0; C.tarr[sb] = 0;
+                    C.occ[i * W + (m[1] >> 6)] &= ~(1ull << (m[1] & 63));
+                    C.live[i] -= 1;
+                    C.freeb[i] += bl;
+                    C.held[i] -= bl;
+                    C.held[d] += bl;
+                    C.inb[d] = 0;
+                    C.B[i] -= 1;
+                    C.B[d] += 1;
+                    C.res[i * C.RB + rr] -= 1u;
+                    C.res[d * C.RB + rr] += 1u;
+                    tier_dec(C, int(i), tier);
+                    tier_inc(C, d, tier);
+                    if (fin < C.nfin[d]) C.nfin[d] = fin;
+                    m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
+                    stat(C, kMigCommitted, 1);
+                    set_f(C, int(i));
+                }
+                set_f(C, d);
+            }
+            wave_sync();
+
+            // ===================== E2: pairing on interval ticks =====================
+            if (t % P.mig_interval == 0) {
+                for (uint32_t i = lane; i < I; i += 64) C.flags[i] &= ~kFlagBusy;
+                wave_sync();
+                for (uint32_t i = lane; i < I; i += 64) {
+                    const int d = C.mig[4 * i];
+                    if (d >= 0) { atomicOr(&C.flags[i], kFlagBusy); atomicOr(&C.flags[d], kFlagBusy); }
+                }
+                wave_sync();
+                bool neg = false;
+                for (uint32_t i = lane; i < I; i += 64) neg |= !(C.flags[i] & kFlagBusy) && C.num[i] < 0;
+                if (ballot(neg)) {
+                    int mine = 0;
+                    for (uint32_t i = lane; i < I; i += 64) {
+                        if (C.flags[i] & kFlagBusy) continue;
+                        ++mine;
+                        const double fi = C.fd[i];
+                        int rank = 0;
+                        for (uint32_t j = 0; j < I; ++j) {
+                            if (C.flags[j] & kFlagBusy) continue;
+                            const double fj = C.fd[j];
+                            rank += (fj < fi || (fj == fi && j < i)) ? 1 : 0;
+                        }
+                        C.order[rank] = int(i);
+                    }
+                    const int n2 = wsum(mine);
+                    wave_sync();
+                    for (int k = 0; k < int(P.mig_max_pairs) && k < n2 - 1 - k; ++k) {
+                        const int src = C.order[k], dst = C.order[n2 - 1 - k];
+                        if (C.num[src] >= 0) break;
+                        const long long lhs = (long long)P.theta_den *
+                            ((long long)C.num[dst] * C.den[src] - (long long)C.num[src] * C.den[dst]);
+                        const long long rhs = (long long)P.theta_num * 256 * C.den[src] * C.den[dst];
+                        if (lhs < rhs) break;
+                        if (C.live[dst] >= int(S)) continue;
+                        const int ds = lowest_empty(C, dst, lane);
+                        if (ds < 0) continue;
+                        const size_t dsb = size_t(dst) * S + ds;
+                        const int h = C.hols[src];
+                        if (h >= 0) {
+                            if (lane == 0) {
+                                const size_t hb = size_t(src) * S + h;
+                                C.hot[dsb] = C.hot[hb]; C.meta[dsb] = C.meta[hb];
+                                C.seq[dsb] = C.seq[hb]; C.tarr[dsb] = C.tarr[hb];
+                                C.hot[hb] = 0; C.meta[hb] = 0; C.seq[hb] = 0; C.tarr[hb] = 0;
+                                C.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
+                                C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
+                                C.live[src] -= 1; C.nwait[src] -= 1;
+                                C.live[dst] += 1; C.nwait[dst] += 1;
+                                if (ds + 1 > C.hwm[dst]) C.hwm[dst] = ds + 1;
+                                const unsigned long long key = C.holk[src];
+                                if (C.hols[dst] == kNoHol || key < C.holk[dst]) {
+                                    C.hols[dst] = ds; C.holk[dst] = key; C.hold[dst] = C.hold[src];
+                                }
+                                if (C.nwait[src] == 0) { C.hols[src] = kNoHol; C.holk[src] = kNone; C.hold[src] = 0; }
+                                else C.hols[src] = kHolUnknown;
+                                stat(C, kMigQueued, 1);
+                            }
+                            wave_sync();
+                            continue;
+                        }
+                        // running candidate: largest tier, then fewest blocks, then newest
+                        const size_t sbase = size_t(src) * S;
+                        const int nch = (C.hwm[src] + 63) >> 6;
+                        unsigned long long bk = 0;
+                        int bs = 0;
+                        for (int c = 0; c < nch; ++c) {
+                            const int s = c * 64 + lane;
+                            const uint32_t v = C.hot[sbase + s];
+                            const uint32_t m = C.meta[sbase + s];
+                            if (wst(v) == 2u && !(m & kMigrating)) {
+                                const uint32_t fin = fin_of(v, t);
+                                const unsigned long long kk =
+                                    (static_cast<unsigned long long>(((m >> 2) & 15u) + 1u) << 48) |
+                                    (static_cast<unsigned long long>(65535 - blocks_of(wlo(v) - (fin - t), C.shift)) << 32) |
+                                    C.seq[sbase + s];
+                                if (kk > bk) { bk = kk; bs = s; }
+                            }
+                        }
+                        const unsigned long long mx = wmax64(bk);
+                        if (mx == 0) continue;
+                        const int cs = rl(bs, ffs64(ballot(bk == mx)));
+                        if (lane == 0) {
+                            C.hot[dsb] = kInbW;
+                            C.meta[dsb] = uint8_t(kInbound);
+                            C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
+                            C.live[dst] += 1;
+                            if (ds + 1 > C.hwm[dst]) C.hwm[dst] = ds + 1;
+                            C.meta[sbase + cs] = uint8_t(C.meta[sbase + cs] | kMigrating);
+                            int* m = &C.mig[4 * src];
+                            m[0] = dst; m[1] = cs; m[2] = ds; m[3] = 0;
+                            stat(C, kMigStarted, 1);
+                        }
+                        wave_sync();
+                    }
+                }
+                wave_sync();
+            }
+
+            // ===================== end of tick =====================
+            for (uint32_t i = lane; i < I; i += 64) {
+                run_acc += unsigned(C.B[i]);
+                wait_acc += unsigned(C.nwait[i]);
+            }
+            if (lane == 0) C.stats[kTicks] += 1;
         }
 
-        // ---- store the replica ----
-        for (int j = threadIdx.x; j < kNstat; j += blockDim.x) P.stats[size_t(r) * kNstat + j] = L.stats[j];
-        for (uint32_t i = threadIdx.x; i < I; i += blockDim.x) {
-            P.freeb[size_t(r) * I + i] = L.freeb[i];
-            for (int k = 0; k < 4; ++k) P.mig[(size_t(r) * I + i) * 4 + k] = L.mig[4 * i + k];
+        // ---------------- epilogue ----------------
+        run_acc = wsum64(run_acc);
+        wait_acc = wsum64(wait_acc);
+        if (lane == 0) {
+            C.stats[kRunSlotTicks] += run_acc;
+            C.stats[kWaitSlotTicks] += wait_acc;
         }
-        if (threadIdx.x == 0) P.next_seq[r] = next_seq;
-        __syncthreads();
+        wave_sync();
+        for (int j = lane; j < kNstat; j += 64) P.stats[size_t(r) * kNstat + j] = C.stats[j];
+        for (uint32_t i = lane; i < I; i += 64) {
+            P.freeb[size_t(r) * I + i] = C.freeb[i];
+            for (int k = 0; k < 4; ++k) P.mig[(size_t(r) * I + i) * 4 + k] = C.mig[4 * i + k];
+        }
+        if (lane == 0) P.next_seq[r] = next_seq;
+        wave_sync();
     }
 }
 
@@ -710,7 +1012,7 @@ __global__ void k_init(Params P)
     const size_t nslots = size_t(P.R) * P.I * P.S;
     const size_t stride = size_t(gridDim.x) * blockDim.x;
     const size_t t0 = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    for (size_t s = t0; s < nslots; s += stride) { P.meta[s] = 0; P.lr[s] = 0; P.seq[s] = 0; P.tarr[s] = 0; }
+    for (size_t s = t0; s < nslots; s += stride) { P.meta[s] = 0; P.hot[s] = 0; P.seq[s] = 0; P.tarr[s] = 0; }
     for (size_t j = t0; j < size_t(P.R) * P.I; j += stride) {
         P.freeb[j] = int32_t(P.M);
         P.mig[4 * j] = -1; P.mig[4 * j + 1] = 0; P.mig[4 * j + 2] = 0; P.mig[4 * j + 3] = 0;
@@ -720,8 +1022,23 @@ __global__ void k_init(Params P)
 }
 
 // ---------------------------------------------------------------------------
-// per-replica digest: wrapping sum of SplitMix64-finalised slot and instance
-// records (Steele, Lea, Flood, OOPSLA 2014); one block per replica
+// moving the clock by delta ticks keeps every running request's remaining
+// output: its finish tick moves by the same delta
+// ---------------------------------------------------------------------------
+__global__ void k_shift_clock(Params P, uint32_t delta)
+{
+    const size_t nslots = size_t(P.R) * P.I * P.S;
+    const size_t stride = size_t(gridDim.x) * blockDim.x;
+    for (size_t s = size_t(blockIdx.x) * blockDim.x + threadIdx.x; s < nslots; s += stride) {
+        const uint32_t v = P.hot[s];
+        if (wst(v) == 2u) P.hot[s] = (v & ~(kFin << 16)) | (((wmid(v) + delta) & kFin) << 16);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// per-replica digest of the canonical state at tick `tick` (the next tick to
+// run): wrapping sum of SplitMix64-finalised slot and instance records
+// (Steele, Lea, Flood, OOPSLA 2014); one block per replica
 // ---------------------------------------------------------------------------
 __device__ inline unsigned long long mix64(unsigned long long z)
 {
@@ -730,7 +1047,18 @@ __device__ inline unsigned long long mix64(unsigned long long z)
     return z ^ (z >> 31);
 }
 
-__global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0)
+// canonical len | rem << 16 of a slot word at tick `tick`
+__device__ inline uint32_t canonical_lr(uint32_t v, uint32_t tick)
+{
+    if (wst(v) == 1u) return wlo(v) | (wmid(v) << 16);
+    if (wst(v) == 2u) {
+        const uint32_t rem = (wmid(v) - tick + 1u) & kFin;
+        return (wlo(v) - rem) | (rem << 16);
+    }
+    return 0;
+}
+
+__global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t tick)
 {
     __shared__ unsigned long long part[4];
     const uint32_t r = r0 + blockIdx.x;
@@ -741,7 +1069,7 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0)
     for (size_t s = threadIdx.x; s < IS; s += blockDim.x) {
         const unsigned m = P.meta[rb + s];
         if ((m & 3u) == kEmpty) continue;
-        const unsigned long long a = static_cast<unsigned long long>(P.lr[rb + s]) |
+        const unsigned long long a = static_cast<unsigned long long>(canonical_lr(P.hot[rb + s], tick)) |
                                      (static_cast<unsigned long long>(P.seq[rb + s]) << 32);
         const unsigned long long b = static_cast<unsigned long long>(P.tarr[rb + s]) |
                                      (static_cast<unsigned long long>(m) << 32);
@@ -765,7 +1093,7 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0)
 
 }  // namespace
 
-size_t lds_bytes(uint32_t I, uint32_t S) { return lds_layout(I, S / 64).total; }
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB) { return lds_layout(I, S / 64, RB).total; }
 
 int launch_init(const Params& p, hipStream_t stream)
 {
@@ -773,23 +1101,41 @@ int launch_init(const Params& p, hipStream_t stream)
     return int(hipGetLastError());
 }
 
-int launch_step(const Params& p, uint32_t threads, uint32_t blocks, hipStream_t stream)
+int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStream_t stream)
 {
-    const size_t lds = lds_bytes(p.I, p.S);
-    if (lds > 64 * 1024) {
-        // raise the dynamic LDS limit; the launch below reports a real failure
-        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_step),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-        (void)hipGetLastError();
-    }
-    hipLaunchKernelGGL(k_step, dim3(blocks), dim3(threads), lds, stream, p);
+    const uint32_t items = p.R * nt;
+    hipLaunchKernelGGL(k_arrivals, dim3((items + 3) / 4), dim3(256), 0, stream, p, t0, nt);
     return int(hipGetLastError());
 }
 
-int launch_digest(const Params& p, uint32_t r0, uint32_t nr, hipStream_t stream)
+int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream)
+{
+    const size_t lds = lds_bytes(p.I, p.S, p.RB);
+    const int ipl = int((p.I + 63) / 64);
+    const void* fn = ipl <= 1 ? reinterpret_cast<const void*>(&k_step<1>)
+                   : ipl <= 2 ? reinterpret_cast<const void*>(&k_step<2>)
+                              : reinterpret_cast<const void*>(&k_step<4>);
+    if (lds > 64 * 1024) {
+        // raise the dynamic LDS limit; a real failure shows up at the launch
+        (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+        (void)hipGetLastError();
+    }
+    if (ipl <= 1) hipLaunchKernelGGL(k_step<1>, dim3(blocks), dim3(64), lds, stream, p, t0, nt);
+    else if (ipl <= 2) hipLaunchKernelGGL(k_step<2>, dim3(blocks), dim3(64), lds, stream, p, t0, nt);
+    else hipLaunchKernelGGL(k_step<4>, dim3(blocks), dim3(64), lds, stream, p, t0, nt);
+    return int(hipGetLastError());
+}
+
+int launch_shift_clock(const Params& p, uint32_t delta, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_shift_clock, dim3(1024), dim3(256), 0, stream, p, delta);
+    return int(hipGetLastError());
+}
+
+int launch_digest(const Params& p, uint32_t r0, uint32_t nr, uint32_t tick, hipStream_t stream)
 {
     if (nr == 0) return 0;
-    hipLaunchKernelGGL(k_digest, dim3(nr), dim3(256), 0, stream, p, r0);
+    hipLaunchKernelGGL(k_digest, dim3(nr), dim3(256), 0, stream, p, r0, tick);
     return int(hipGetLastError());
 }
 

@@ -130,7 +130,7 @@ int validate(const mts_cfg& c)
     if (c.n_instances < 1 || c.n_instances > kMaxInstances) return MTS_EINVAL;
     if (c.slots_per_instance < 64 || c.slots_per_instance > kMaxSlots || c.slots_per_instance % 64) return MTS_EINVAL;
     if (c.kv_blocks < 1 || c.kv_blocks > kMaxBlocks) return MTS_EINVAL;
-    if (c.block_tokens < 1 || c.block_tokens > 1024 || (c.block_tokens & (c.block_tokens - 1))) return MTS_EINVAL;
+    if (c.block_tokens < 1 || c.block_tokens > kMaxBlockTokens || (c.block_tokens & (c.block_tokens - 1))) return MTS_EINVAL;
     if (c.zero_lowest_tier > 1) return MTS_EINVAL;
     if (!std::isfinite(c.headroom_base) || c.headroom_base < 0.0) return MTS_EINVAL;
     if (!std::isfinite(c.headroom_decay) || c.headroom_decay < 0.0 || c.headroom_decay > 1.0) return MTS_EINVAL;
@@ -197,8 +197,10 @@ int build_tables(const mts_cfg& c, Tables& T)
     if (!rc) rc = prompt_table(c, T.prompt);
     if (!rc) rc = output_table(c, T.output);
     if (rc) return rc;
-    const uint64_t maxlen = uint64_t(T.prompt.base) + T.prompt.q.size() - 1 + T.output.base + T.output.q.size() - 1;
-    if (maxlen > 65535) return MTS_EINVAL;
+    // a request's length fits 16 bits and its remaining output 14 bits
+    const uint64_t maxout = uint64_t(T.output.base) + T.output.q.size() - 1;
+    const uint64_t maxlen = uint64_t(T.prompt.base) + T.prompt.q.size() - 1 + maxout;
+    if (maxlen > 65535 || maxout > kMaxOutput) return MTS_EINVAL;
     return MTS_OK;
 }
 
