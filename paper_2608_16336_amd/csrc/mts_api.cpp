@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -22,6 +23,7 @@ struct mts_ctx {
     uint64_t tick = 0;
     uint32_t arr_cap = 0;              // arrival records per (replica, tick)
     uint32_t chunk = 0;                // ticks per arrival batch
+    uint32_t wsz = 0, wcap = 0;        // finish wheel: buckets, entries per bucket
     uint32_t blocks = 0;               // step-kernel blocks (one wave each); 0 = automatic
     int device = 0;
     hipStream_t last = nullptr;
@@ -49,7 +51,23 @@ uint32_t chunk_for(uint32_t R, uint32_t cap)
     return uint32_t(std::max<size_t>(1, std::min<size_t>(1024, kArrivalBudget / per_tick)));
 }
 
-Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk, uint32_t cap)
+// Finish wheel of one replica: a running request is filed under bucket
+// fin mod wsz.  Buckets hold the finishes of one tick plus the few longer
+// requests that share the bucket and are carried to its next visit; entries
+// per bucket give a wide margin over the arrival rate, and a bucket that
+// overflows is rebuilt by an exact scan.
+void wheel_size(const mts_cfg& c, const Tables& T, uint32_t& wsz, uint32_t& wcap)
+{
+    const uint32_t maxout = T.output.base + uint32_t(T.output.q.size()) - 1;
+    wsz = 1;
+    while (wsz <= maxout && wsz < 1024) wsz <<= 1;
+    const double cv = c.arrival_kind == MTS_ARRIVAL_GAMMA_POISSON ? c.arrival_cv : 0.0;
+    const double want = 2.0 * c.arrival_mean * (1.0 + cv) + 24.0;
+    wcap = uint32_t(std::min(2048.0, std::ceil(want / 16.0) * 16.0));
+}
+
+Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk, uint32_t cap,
+                   uint32_t wsz, uint32_t wcap)
 {
     Layout L{};
     const size_t I = c.n_instances, S = c.slots_per_instance;
@@ -73,6 +91,8 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.digest = o;   o = up256(o + size_t(R) * 8);
     L.arr_cnt = o;  o = up256(o + size_t(R) * chunk * 4);
     L.arr_rec = o;  o = up256(o + size_t(R) * chunk * cap * 8);
+    L.wcnt = o;     o = up256(o + size_t(R) * wsz * 4);
+    L.wheel = o;    o = up256(o + size_t(R) * wsz * wcap * 4);
     L.total = o;
     return L;
 }
@@ -98,6 +118,8 @@ Params make_params(const mts_ctx* h)
     p.output_base = h->tables.output.base;
     p.chunk = h->chunk;
     p.arr_cap = h->arr_cap;
+    p.wsz = h->wsz;
+    p.wcap = h->wcap;
     p.seed = c.seed;
     p.id_base = c.replica_id_base;
     const Layout& L = h->lay;
@@ -119,6 +141,8 @@ Params make_params(const mts_ctx* h)
     p.digest = reinterpret_cast<unsigned long long*>(d + L.digest);
     p.arr_cnt = reinterpret_cast<uint32_t*>(d + L.arr_cnt);
     p.arr_rec = reinterpret_cast<unsigned long long*>(d + L.arr_rec);
+    p.wcnt = reinterpret_cast<uint32_t*>(d + L.wcnt);
+    p.wheel = reinterpret_cast<uint32_t*>(d + L.wheel);
     return p;
 }
 
@@ -147,7 +171,8 @@ int prepare(const mts_cfg* cfg, mts_ctx& x)
     x.S = cfg->slots_per_instance;
     x.arr_cap = uint32_t(x.tables.count.base + x.tables.count.q.size());
     x.chunk = chunk_for(x.R, x.arr_cap);
-    x.lay = make_layout(x.cfg, x.tables, x.R, x.chunk, x.arr_cap);
+    wheel_size(x.cfg, x.tables, x.wsz, x.wcap);
+    x.lay = make_layout(x.cfg, x.tables, x.R, x.chunk, x.arr_cap, x.wsz, x.wcap);
     return MTS_OK;
 }
 

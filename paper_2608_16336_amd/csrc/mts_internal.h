@@ -51,6 +51,7 @@ struct Layout {
     size_t freeb, mig;                                                  // [R][I], [R][I][4]
     size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
     size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
+    size_t wcnt, wheel;                                                 // [R][wsz], [R][wsz][wcap]
     size_t total;
 };
 
@@ -63,6 +64,7 @@ struct Params {
     uint32_t count_n, prompt_n, output_n;  // table lengths (entries incl. the implicit 2^32)
     uint32_t count_base, prompt_base, output_base;
     uint32_t chunk, arr_cap;       // ticks per arrival batch, records per tick
+    uint32_t wsz, wcap;            // finish wheel: buckets (power of two), entries per bucket
     uint64_t seed, id_base;
     const uint32_t* tier_q;        // [group][MTS_MAX_TIERS]
     const int32_t* hq;             // [group][MTS_MAX_TIERS]
@@ -82,6 +84,8 @@ struct Params {
     unsigned long long* digest;
     uint32_t* arr_cnt;
     unsigned long long* arr_rec;
+    uint32_t* wcnt;
+    uint32_t* wheel;
 };
 
 // LDS bytes of one wave (one replica) of the step kernel

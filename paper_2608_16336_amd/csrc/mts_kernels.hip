@@ -20,8 +20,10 @@
 // writes nothing.  Its KV growth falls on ticks t with
 // (final - fin - 1 + t) mod block = 0: per instance, counters indexed by that
 // residue give the number of requests that need a new block at tick t in
-// O(1).  Each instance tracks a lower bound of its next finish tick and scans
-// its slots only when it is due.
+// O(1).  A request that starts running is filed under its finish tick in a
+// per-replica timing wheel, so a tick visits exactly the requests that
+// finish in it.  The head of line of every instance is cached in LDS (slot,
+// key, slot word, meta, arrival tick), so admission reads no HBM.
 #include <hip/hip_runtime.h>
 
 #include "mts_internal.h"
@@ -45,7 +47,7 @@ __device__ __forceinline__ uint32_t wmid(uint32_t v) { return (v >> 16) & kFin; 
 // ---------------------------------------------------------------------------
 // LDS of one wave (one replica)
 // ---------------------------------------------------------------------------
-constexpr int kInts = 17;
+constexpr int kInts = 18;
 
 struct LdsLayout {
     uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, total;
@@ -75,12 +77,15 @@ struct Ctx {
     unsigned long long* occ;   // [I][W] slot not empty
     unsigned long long* holk;  // [I] head-of-line key tier << 32 | seq
     double* fd;                // [I] freeness num / den (exact order for S <= 2048)
-    int *freeb, *B, *live, *nwait, *hwm, *hols, *hold, *num, *den, *held, *inb, *tmask, *flags, *gtmp, *order, *pend;
-    unsigned* nfin;            // [I] lower bound of the next finish tick
+    int *freeb, *B, *live, *nwait, *hols, *hold, *num, *den, *held, *inb, *tmask, *flags, *gtmp, *order, *pend;
+    unsigned *hwd, *hmt, *hta; // [I] head of line: slot word, meta, arrival tick
     unsigned* res;             // [I][RB] running requests per growth residue
     unsigned* tcnt;            // [I][10] running requests per tier
     int* mig;                  // [I][4] dst, src slot, dst slot, copied
-    // HBM slot arrays of this replica
+    // HBM: timing wheel of this replica, slot arrays
+    uint32_t* wcnt;            // [Wsz] requests filed per bucket
+    uint32_t* wheel;           // [Wsz][wcap] instance << 16 | slot
+    uint32_t wmask, wcap;
     uint32_t* hot;
     uint8_t* meta;
     uint32_t* seq;
@@ -103,7 +108,6 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.B = p; p += I;
     C.live = p; p += I;
     C.nwait = p; p += I;
-    C.hwm = p; p += I;
     C.hols = p; p += I;
     C.hold = p; p += I;
     C.num = p; p += I;
@@ -115,7 +119,9 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.gtmp = p; p += I;
     C.order = p; p += I;
     C.pend = p; p += I;
-    C.nfin = reinterpret_cast<unsigned*>(p); p += I;
+    C.hwd = reinterpret_cast<unsigned*>(p); p += I;
+    C.hmt = reinterpret_cast<unsigned*>(p); p += I;
+    C.hta = reinterpret_cast<unsigned*>(p); p += I;
     C.res = reinterpret_cast<unsigned*>(base + Y.res);
     C.tcnt = reinterpret_cast<unsigned*>(base + Y.tcnt);
     C.mig = reinterpret_cast<int*>(base + Y.mig);
@@ -123,6 +129,8 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
     C.M = P.M;
+    C.wmask = P.wsz - 1u;
+    C.wcap = P.wcap;
     return C;
 }
 
@@ -250,6 +258,37 @@ __device__ inline int lowest_empty(const Ctx& C, int i, int lane)
     return c0 * 64 + ffs64(~w0);
 }
 
+// number of 64-slot chunks of instance i up to its highest non-empty one; uniform
+__device__ __forceinline__ int live_chunks(const Ctx& C, int i, int lane)
+{
+    const unsigned long long w = lane < int(C.W) ? C.occ[i * C.W + lane] : 0ull;
+    const unsigned long long nz = ballot(w != 0);
+    return nz ? 64 - __clzll(static_cast<long long>(nz)) : 0;
+}
+
+// position of the k-th (from 0) set bit of m; m has more than k set bits
+__device__ __forceinline__ int kth_set_bit(unsigned long long m, int k)
+{
+    int pos = 0;
+#pragma unroll
+    for (int w = 32; w >= 1; w >>= 1) {
+        const int c = __popcll((m >> pos) & ((1ull << w) - 1ull));
+        if (k >= c) { k -= c; pos += w; }
+    }
+    return pos;
+}
+
+// inclusive prefix sum over the lanes of the wave
+__device__ __forceinline__ int wscan(int x, int lane)
+{
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+
 // ---------------------------------------------------------------------------
 // Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011) from its published
 // round function and Weyl key schedule; inverse-CDF table search.
@@ -349,29 +388,63 @@ __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t
 // per-instance event handlers (uniform: the whole wave works on instance i)
 // ---------------------------------------------------------------------------
 
+__device__ __forceinline__ void clear_hol(const Ctx& C, int i)
+{
+    C.hols[i] = kNoHol; C.holk[i] = kNone; C.hold[i] = 0;
+}
+
+__device__ __forceinline__ void set_hol(const Ctx& C, int i, int slot, unsigned long long key, uint32_t word,
+                                        uint32_t meta, uint32_t tarr)
+{
+    C.hols[i] = slot; C.holk[i] = key; C.hold[i] = blocks_of(wlo(word), C.shift);
+    C.hwd[i] = word; C.hmt[i] = meta; C.hta[i] = tarr;
+}
+
+// file a running request under its finish tick
+__device__ __forceinline__ void wheel_put(const Ctx& C, uint32_t fin, int i, int s)
+{
+    const uint32_t b = fin & C.wmask;
+    const uint32_t k = atomicAdd(&C.wcnt[b], 1u);
+    if (k < C.wcap) C.wheel[size_t(b) * C.wcap + k] = (uint32_t(i) << 16) | uint32_t(s);
+}
+
 // head of line of instance i from its slots: smallest (tier, seq) waiting
 __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
 {
     const size_t b = size_t(i) * C.S;
-    const int nch = (C.hwm[i] + 63) >> 6;
+    const int nch = live_chunks(C, i, lane);
     unsigned long long bk = kNone;
     int bs = 0;
-    uint32_t bv = 0;
-    for (int c = 0; c < nch; ++c) {
-        const int s = c * 64 + lane;
-        const uint32_t v = C.hot[b + s];
-        if (wst(v) == 1u) {
-            const unsigned long long k = (static_cast<unsigned long long>((C.meta[b + s] >> 2) & 15u) << 32) | C.seq[b + s];
-            if (k < bk) { bk = k; bs = s; bv = v; }
+    uint32_t bv = 0, bm = 0;
+    for (int c0 = 0; c0 < nch; c0 += 4) {
+        uint32_t v[4], m[4], q[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) v[g] = c0 + g < nch ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const bool w = wst(v[g]) == 1u;
+            m[g] = w ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
+            q[g] = w ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            if (wst(v[g]) != 1u) continue;
+            const unsigned long long k = (static_cast<unsigned long long>((m[g] >> 2) & 15u) << 32) | q[g];
+            if (k < bk) { bk = k; bs = (c0 + g) * 64 + lane; bv = v[g]; bm = m[g]; }
         }
     }
     const unsigned long long mn = wmin64(bk);
-    if (lane == 0 && mn == kNone) { C.hols[i] = kNoHol; C.holk[i] = kNone; C.hold[i] = 0; }
-    if (mn == kNone) { wave_sync(); return; }
+    if (mn == kNone) {
+        if (lane == 0) clear_hol(C, i);
+        wave_sync();
+        return;
+    }
     const int wl = ffs64(ballot(bk == mn));
+    uint32_t ta = lane == wl ? C.tarr[b + bs] : 0u;
     const int h = rl(bs, wl);
-    const uint32_t v = rlu(bv, wl);
-    if (lane == 0) { C.hols[i] = h; C.holk[i] = mn; C.hold[i] = blocks_of(wlo(v), C.shift); }
+    const uint32_t word = rlu(bv, wl), meta = rlu(bm, wl);
+    ta = rlu(ta, wl);
+    if (lane == 0) set_hol(C, i, h, mn, word, meta, ta);
     wave_sync();
 }
 
@@ -382,7 +455,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
     const size_t b = size_t(i) * C.S;
     int G = C.gtmp[i], fr = C.freeb[i];
     while (G > fr) {
-        const int nch = (C.hwm[i] + 63) >> 6;
+        const int nch = live_chunks(C, i, lane);
         unsigned long long bk = 0;
         int bs = 0;
         for (int c = 0; c < nch; ++c) {
@@ -398,13 +471,17 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
         const int vs = rl(bs, ffs64(ballot(bk == mx)));
         const int owner = vs & 63;
         int vb = 0, vg = 0, vt = 0, vr = 0, vm = 0;
+        uint32_t vw = 0, vmeta = 0, vta = 0;
         if (lane == owner) {
             const uint32_t v = C.hot[b + vs];
             const uint32_t lenf = wlo(v), fin = fin_of(v, t);
             const uint32_t remb = fin - t + 1u, lenb = lenf - remb;
-            C.hot[b + vs] = kWaitW | (remb << 16) | lenb;
+            vw = kWaitW | (remb << 16) | lenb;
+            C.hot[b + vs] = vw;
             const uint32_t m = C.meta[b + vs];
-            C.meta[b + vs] = uint8_t((m & ~(3u | kMigrating)) | kWaiting);
+            vmeta = (m & ~(3u | kMigrating)) | kWaiting;
+            C.meta[b + vs] = uint8_t(vmeta);
+            vta = C.tarr[b + vs];
             vb = blocks_of(lenb, C.shift);
             vg = (lenb & C.bmask) == 0;
             vt = int((m >> 2) & 15u);
@@ -412,6 +489,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             vm = (m & kMigrating) ? 1 : 0;
         }
         vb = rl(vb, owner); vg = rl(vg, owner); vt = rl(vt, owner); vr = rl(vr, owner); vm = rl(vm, owner);
+        vw = rlu(vw, owner); vmeta = rlu(vmeta, owner); vta = rlu(vta, owner);
         fr += vb;
         G -= vg;
         if (lane == 0) {
@@ -423,9 +501,8 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             stat(C, vt * 8 + kPreempted, 1);
             if (vm) C.flags[i] |= kFlagAbort;
             const unsigned long long key = (static_cast<unsigned long long>(vt) << 32) | static_cast<unsigned>(mx);
-            if (C.hols[i] != kHolUnknown && (C.hols[i] == kNoHol || key < C.holk[i])) {
-                C.hols[i] = vs; C.holk[i] = key; C.hold[i] = vb;
-            }
+            if (C.hols[i] != kHolUnknown && (C.hols[i] == kNoHol || key < C.holk[i]))
+                set_hol(C, i, vs, key, vw, vmeta, vta);
         }
         wave_sync();
     }
@@ -433,21 +510,22 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
     wave_sync();
 }
 
-// requests of instance i that emit their last token at tick t finish and free
-// their blocks
+// Exact finish scan of instance i, used when a wheel bucket overflowed:
+// finishes the requests whose last token is at t and files again the running
+// requests that share the bucket of t but finish later.
 __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
 {
     const size_t b = size_t(i) * C.S;
-    const int nch = (C.hwm[i] + 63) >> 6;
-    const uint32_t t14 = t & kFin;
-    int freed = 0, nf = 0, top = -1;
-    uint32_t nmin = kInf;
+    const int nch = live_chunks(C, i, lane);
+    const uint32_t bk = t & C.wmask;
+    int freed = 0, nf = 0;
     bool ab = false;
     for (int c = 0; c < nch; ++c) {
         const int s = c * 64 + lane;
         const uint32_t v = C.hot[b + s];
         const bool run = wst(v) == 2u;
-        const bool f = run && wmid(v) == t14;
+        const uint32_t fin = fin_of(v, t);
+        const bool f = run && fin == t;
         if (f) {
             const uint32_t lenf = wlo(v);
             freed += blocks_of(lenf, C.shift);
@@ -459,86 +537,199 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
             tier_dec(C, i, tier);
             if (m & kMigrating) ab = true;
             C.hot[b + s] = 0; C.meta[b + s] = 0; C.seq[b + s] = 0; C.tarr[b + s] = 0;
-        } else if (run) {
-            const uint32_t rel = (wmid(v) - t - 1u) & kFin;
-            nmin = rel < nmin ? rel : nmin;
+        } else if (run && (fin & C.wmask) == bk) {
+            wheel_put(C, fin, i, s);
         }
         const unsigned long long fb = ballot(f);
         const unsigned long long ow = ballot(v != 0 && !f);
         nf += __popcll(fb);
-        if (ow) top = c * 64 + 63 - __clzll(static_cast<long long>(ow));
         if (lane == 0) C.occ[i * C.W + c] = ow;
     }
     freed = wsum(freed);
-    nmin = unsigned(wmin64(nmin));
     const bool any_ab = ballot(ab) != 0;
     if (lane == 0) {
         C.freeb[i] += freed;
         C.held[i] -= freed;
         C.B[i] -= nf;
         C.live[i] -= nf;
-        C.hwm[i] = top + 1;
-        C.nfin[i] = nmin == kInf ? kInf : t + 1u + nmin;
         if (any_ab) C.flags[i] |= kFlagAbort;
     }
     wave_sync();
 }
 
-// admit the head of line while its blocks fit (Section 3.1, Eq. 2)
-__device__ inline void admit(const Ctx& C, int i, uint32_t t, int lane)
+// Requests that emit their last token at tick t.  The bucket t mod wsz lists
+// every running request with fin = t (mod wsz): those with fin = t finish,
+// those with a later fin stay in the bucket (compacted in place), entries of
+// slots whose request has left are dropped.
+__device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
 {
-    const size_t b = size_t(i) * C.S;
-    if (C.hols[i] == kHolUnknown) rescan_hol(C, i, lane);
-    while (C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]) {
-        const int h = C.hols[i];
-        const int owner = h & 63;
-        uint32_t fin = 0, first = 0, ta = 0;
-        int tier = 0, r = 0;
-        if (lane == owner) {
-            const uint32_t v = C.hot[b + h];
-            const uint32_t len = wlo(v), rem = wmid(v);
-            fin = t + rem;
-            C.hot[b + h] = kRunW | ((fin & kFin) << 16) | (len + rem);
-            const uint32_t m = C.meta[b + h];
-            C.meta[b + h] = uint8_t((m & ~3u) | kRunning | kAdmitted);
-            tier = int((m >> 2) & 15u);
-            first = (m & kAdmitted) ? 0u : 1u;
-            ta = first ? C.tarr[b + h] : 0u;
-            r = int((len - t - 1u) & C.bmask);
+    const uint32_t bk = t & C.wmask;
+    const uint32_t n = __hip_atomic_load(&C.wcnt[bk], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (n > C.wcap) {
+        // the bucket overflowed: rebuild it by scanning every instance with running requests
+        if (lane == 0) C.wcnt[bk] = 0;
+        wave_sync();
+        for (uint32_t j = 0; j < (C.I + 63) / 64; ++j) {
+            const uint32_t i = lane + 64 * j;
+            for (unsigned long long m = ballot(i < C.I && C.B[i] > 0); m; m &= m - 1)
+                finish_scan(C, int(64 * j + ffs64(m)), t, lane);
         }
-        fin = rlu(fin, owner); first = rlu(first, owner); ta = rlu(ta, owner);
-        tier = rl(tier, owner); r = rl(r, owner);
-        if (lane == 0) {
-            const int dem = C.hold[i];
-            C.freeb[i] -= dem;
-            C.held[i] += dem;
-            C.B[i] += 1;
-            C.nwait[i] -= 1;
-            C.res[i * C.RB + r] += 1u;
-            tier_inc(C, i, tier);
-            if (fin < C.nfin[i]) C.nfin[i] = fin;
-            if (first) {
-                stat(C, tier * 8 + kAdmittedCnt, 1);
-                stat(C, tier * 8 + kQdelay, t - ta);
-            }
-            if (C.nwait[i] == 0) { C.hols[i] = kNoHol; C.holk[i] = kNone; C.hold[i] = 0; }
-            else C.hols[i] = kHolUnknown;
+        return;
+    }
+    uint32_t* ent = C.wheel + size_t(bk) * C.wcap;
+    uint32_t kept = 0;
+    for (uint32_t e0 = 0; e0 < n; e0 += 64) {
+        const uint32_t e = e0 + lane < n ? ent[e0 + lane] : 0u;
+        const int i = int(e >> 16), s = int(e & 0xFFFFu);
+        const bool valid = e0 + lane < n && uint32_t(i) < C.I && uint32_t(s) < C.S;
+        const size_t idx = size_t(i) * C.S + s;
+        const uint32_t v = valid ? C.hot[idx] : 0u;
+        const uint32_t fin = fin_of(v, t);
+        bool f = valid && wst(v) == 2u && fin == t;
+        bool k = valid && wst(v) == 2u && fin != t && (fin & C.wmask) == bk;
+        // a slot listed twice in this batch is handled once
+        bool first = false;
+        for (unsigned long long pend = ballot(f || k); pend;) {
+            const int l = ffs64(pend);
+            const uint32_t ev = rlu(e, l);
+            const unsigned long long same = ballot((f || k) && e == ev);
+            if (lane == l) first = true;
+            pend &= ~same;
+        }
+        f = f && first;
+        k = k && first;
+        const unsigned long long km = ballot(k);
+        if (k) ent[kept + __popcll(km & lanemask_lt())] = e;
+        kept += __popcll(km);
+        uint32_t m = 0, ta = 0;
+        if (f) { m = C.meta[idx]; ta = C.tarr[idx]; }
+        if (f) {
+            const uint32_t lenf = wlo(v);
+            const int bl = blocks_of(lenf, C.shift);
+            const int tier = int((m >> 2) & 15u);
+            stat(C, tier * 8 + kFinished, 1);
+            stat(C, tier * 8 + kE2e, t - ta);
+            atomicSub(&C.res[i * C.RB + ((lenf - t - 1u) & C.bmask)], 1u);
+            tier_dec(C, i, tier);
+            if (m & kMigrating) atomicOr(&C.flags[i], kFlagAbort);
+            atomicAnd(&C.occ[i * C.W + (s >> 6)], ~(1ull << (s & 63)));
+            atomicAdd(&C.freeb[i], bl);
+            atomicSub(&C.held[i], bl);
+            atomicSub(&C.B[i], 1);
+            atomicSub(&C.live[i], 1);
+            C.hot[idx] = 0; C.meta[idx] = 0; C.seq[idx] = 0; C.tarr[idx] = 0;
         }
         wave_sync();
-        if (C.hols[i] == kHolUnknown) rescan_hol(C, i, lane);
     }
+    if (lane == 0) C.wcnt[bk] = kept;
+    wave_sync();
+}
+
+// Admission of instance i when its head of line fits and 2..64 requests wait
+// (Section 3.1: the local queue is served in priority order while the head
+// fits).  The waiting requests are gathered into lanes, ranked by (tier, seq),
+// and the longest prefix of the ranked list whose summed demand fits is
+// admitted in one step; the next ranked request becomes the head of line.
+// The result equals admitting the head of line one request at a time.
+__device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
+{
+    const size_t b = size_t(i) * C.S;
+    const int nch = live_chunks(C, i, lane);
+    unsigned long long key = kNone;
+    uint32_t word = 0, meta = 0, ta = 0;
+    int slot = 0, w = 0;
+    for (int c0 = 0; c0 < nch; c0 += 4) {
+        uint32_t v[4], m[4], q[4], a[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) v[g] = c0 + g < nch ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const bool wt = wst(v[g]) == 1u;
+            const size_t sb = b + (c0 + g) * 64 + lane;
+            m[g] = wt ? C.meta[sb] : 0u;
+            q[g] = wt ? C.seq[sb] : 0u;
+            a[g] = wt ? C.tarr[sb] : 0u;
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const unsigned long long wm = ballot(wst(v[g]) == 1u);
+            if (!wm) continue;
+            const int cnt = __popcll(wm);
+            const int k = lane - w;
+            const bool take = k >= 0 && k < cnt;
+            const int src = kth_set_bit(wm, take ? k : 0);
+            const uint32_t pv = __shfl(v[g], src), pm = __shfl(m[g], src), pq = __shfl(q[g], src),
+                           pa = __shfl(a[g], src);
+            if (take) {
+                word = pv; meta = pm; ta = pa;
+                key = (static_cast<unsigned long long>((pm >> 2) & 15u) << 32) | pq;
+                slot = (c0 + g) * 64 + src;
+            }
+            w += cnt;
+        }
+    }
+    if (w > 64) w = 64;  // callers guarantee at most 64 waiting requests
+    // rank among the gathered keys (all distinct: seq is unique per replica)
+    int rank = 0;
+    for (int j = 0; j < w; ++j) rank += rl64(key, j) < key ? 1 : 0;
+    if (lane >= w) rank = lane;
+    // sort: lane r receives the request of rank r
+    const int ad = rank * 4;
+    const uint32_t k_lo = uint32_t(__builtin_amdgcn_ds_permute(ad, int(uint32_t(key))));
+    const uint32_t k_hi = uint32_t(__builtin_amdgcn_ds_permute(ad, int(uint32_t(key >> 32))));
+    word = uint32_t(__builtin_amdgcn_ds_permute(ad, int(word)));
+    meta = uint32_t(__builtin_amdgcn_ds_permute(ad, int(meta)));
+    ta = uint32_t(__builtin_amdgcn_ds_permute(ad, int(ta)));
+    slot = __builtin_amdgcn_ds_permute(ad, slot);
+    key = (static_cast<unsigned long long>(k_hi) << 32) | k_lo;
+    const int dem = lane < w ? blocks_of(wlo(word), C.shift) : 0;
+    const int pre = wscan(dem, lane);
+    const int fr = C.freeb[i];
+    const bool adm = lane < w && pre <= fr && uint32_t(slot) < C.S;
+    const int na = __popcll(ballot(adm));
+    if (adm) {
+        const uint32_t len = wlo(word), rem = wmid(word);
+        const uint32_t fin = t + rem;
+        const size_t hb = b + slot;
+        C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
+        C.meta[hb] = uint8_t((meta & ~3u) | kRunning | kAdmitted);
+        const int tier = int((meta >> 2) & 15u);
+        if (!(meta & kAdmitted)) {
+            stat(C, tier * 8 + kAdmittedCnt, 1);
+            stat(C, tier * 8 + kQdelay, t - ta);
+        }
+        atomicAdd(&C.res[i * C.RB + ((len - t - 1u) & C.bmask)], 1u);
+        tier_inc(C, i, tier);
+        wheel_put(C, fin, i, slot);
+    }
+    const int used = na > 0 ? rl(pre, na - 1) : 0;
+    const int hs = rl(slot, na < w ? na : 0);
+    const unsigned long long hk = rl64(key, na < w ? na : 0);
+    const uint32_t hw = rlu(word, na < w ? na : 0), hm = rlu(meta, na < w ? na : 0),
+                   ht = rlu(ta, na < w ? na : 0);
+    if (lane == 0) {
+        C.freeb[i] -= used;
+        C.held[i] += used;
+        C.B[i] += na;
+        C.nwait[i] -= na;
+        if (w != C.nwait[i] + na) stat(C, kInvariant, 1);
+        if (na < w) set_hol(C, i, hs, hk, hw, hm, ht);
+        else clear_hol(C, i);
+    }
+    wave_sync();
 }
 
 // ---------------------------------------------------------------------------
 // k_step
 // ---------------------------------------------------------------------------
 template <int IPL>
-__global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, uint32_t nt)
+__global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigned long long t0, uint32_t nt)
 {
     extern __shared__ __align__(16) char lds_raw[];
     Ctx C = carve(lds_raw, P);
     const int lane = lane_id();
     const uint32_t I = P.I, S = P.S, W = P.W;
+    const uint32_t wsz = P.wsz;
 
     for (uint32_t r = blockIdx.x; r < P.R; r += gridDim.x) {
         const uint32_t g = P.group_of[r];
@@ -547,6 +738,8 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
         for (int p = 0; p < kTiers; ++p) C.hq[p] = P.hq[g * kTiers + p];
         const size_t rb = size_t(r) * I * S;
         C.hot = P.hot + rb; C.meta = P.meta + rb; C.seq = P.seq + rb; C.tarr = P.tarr + rb;
+        C.wcnt = P.wcnt + size_t(r) * wsz;
+        C.wheel = P.wheel + size_t(r) * wsz * P.wcap;
 
         // ---------------- prologue: derived per-instance state ----------------
         for (int j = lane; j < kNstat; j += 64) C.stats[j] = P.stats[size_t(r) * kNstat + j];
@@ -559,6 +752,7 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
             for (uint32_t q = 0; q < C.RB; ++q) C.res[i * C.RB + q] = 0;
             for (int q = 0; q < kTiers; ++q) C.tcnt[i * kTiers + q] = 0;
         }
+        for (uint32_t b = lane; b < wsz; b += 64) C.wcnt[b] = 0;
         wave_sync();
         for (uint32_t i = lane; i < I; i += 64) {
             const int d = C.mig[4 * i];
@@ -568,11 +762,10 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
         const uint32_t t0u = uint32_t(t0);
         for (uint32_t i = 0; i < I; ++i) {
             const size_t b = size_t(i) * S;
-            int nB = 0, nlive = 0, nw = 0, top = -1, held = 0;
-            uint32_t nmin = kInf;
+            int nB = 0, nlive = 0, nw = 0, held = 0;
             unsigned long long bk = kNone;
             int bs = 0;
-            uint32_t bv = 0;
+            uint32_t bv = 0, bm = 0;
             for (uint32_t c = 0; c < W; ++c) {
                 const int s = int(c) * 64 + lane;
                 const uint32_t v = C.hot[b + s];
@@ -581,7 +774,6 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                 nlive += __popcll(ow);
                 nB += __popcll(ballot(st == 2u));
                 nw += __popcll(ballot(st == 1u));
-                if (ow) top = int(c) * 64 + 63 - __clzll(static_cast<long long>(ow));
                 if (lane == 0) C.occ[i * W + c] = ow;
                 if (st == 2u) {
                     const uint32_t lenf = wlo(v), fin = fin_of(v, t0u);
@@ -589,25 +781,29 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                     atomicAdd(&C.res[i * C.RB + ((lenf - fin - 1u) & C.bmask)], 1u);
                     const int tier = int((C.meta[b + s] >> 2) & 15u);
                     atomicAdd(&C.tcnt[i * kTiers + tier], 1u);
-                    nmin = fin < nmin ? fin : nmin;
+                    wheel_put(C, fin, int(i), s);
                 } else if (st == 1u) {
-                    const unsigned long long k = (static_cast<unsigned long long>((C.meta[b + s] >> 2) & 15u) << 32) | C.seq[b + s];
-                    if (k < bk) { bk = k; bs = s; bv = v; }
+                    const uint32_t m = C.meta[b + s];
+                    const unsigned long long k = (static_cast<unsigned long long>((m >> 2) & 15u) << 32) | C.seq[b + s];
+                    if (k < bk) { bk = k; bs = s; bv = v; bm = m; }
                 }
             }
             held = wsum(held);
-            nmin = unsigned(wmin64(nmin));
             const unsigned long long mn = wmin64(bk);
-            int hs = kNoHol, hd = 0;
+            int hs = kNoHol;
+            uint32_t hw = 0, hm = 0, ht = 0;
             if (mn != kNone) {
                 const int wl = ffs64(ballot(bk == mn));
                 hs = rl(bs, wl);
-                hd = blocks_of(wlo(rlu(bv, wl)), C.shift);
+                hw = rlu(bv, wl);
+                hm = rlu(bm, wl);
+                ht = rlu(lane == wl ? C.tarr[b + bs] : 0u, wl);
             }
             if (lane == 0) {
-                C.B[i] = nB; C.live[i] = nlive; C.nwait[i] = nw; C.hwm[i] = top + 1;
-                C.held[i] = held; C.nfin[i] = nmin;
-                C.hols[i] = hs; C.holk[i] = mn; C.hold[i] = hd;
+                C.B[i] = nB; C.live[i] = nlive; C.nwait[i] = nw;
+                C.held[i] = held;
+                if (hs >= 0) set_hol(C, int(i), hs, mn, hw, hm, ht);
+                else clear_hol(C, int(i));
                 int tm = 0;
                 for (int p = 0; p < kTiers; ++p) tm |= C.tcnt[i * kTiers + p] ? (1 << p) : 0;
                 C.tmask[i] = tm;
@@ -615,7 +811,7 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
             wave_sync();
         }
         unsigned next_seq = P.next_seq[r];
-        unsigned long long run_acc = 0, wait_acc = 0;
+        uint32_t run_acc = 0, wait_acc = 0;  // per lane, at most 1024 ticks x 4 x 2048
         const unsigned long long* recs = P.arr_rec + size_t(r) * P.chunk * P.arr_cap;
         const uint32_t* cnts = P.arr_cnt + size_t(r) * P.chunk;
         wave_sync();
@@ -624,23 +820,21 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
             const uint32_t t = t0u + tl;
             const uint32_t n = cnts[tl];
             const unsigned long long* rec = recs + size_t(tl) * P.arr_cap;
-            unsigned long long a0 = lane < int(n) ? rec[lane] : 0;
+            const unsigned long long a0 = lane < int(n) ? rec[lane] : 0;
 
             // ===================== A: growth, preemption, finish =====================
             const uint32_t cres = (0u - t) & C.bmask;
-            unsigned long long pre[IPL], due[IPL];
+            unsigned long long pre[IPL];
 #pragma unroll
             for (int j = 0; j < IPL; ++j) {
                 const uint32_t i = lane + 64 * j;
-                bool np = false, dd = false;
+                bool np = false;
                 if (i < I) {
                     const int G = int(C.res[i * C.RB + cres]);
                     C.gtmp[i] = G;
                     np = G > C.freeb[i];
-                    dd = C.nfin[i] <= t;
                 }
                 pre[j] = ballot(np);
-                due[j] = ballot(dd);
             }
             wave_sync();
 #pragma unroll
@@ -652,10 +846,8 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                 C.held[i] += G;
             }
             wave_sync();
+            finish_tick(C, t, lane);
             bool any_abort = false;
-#pragma unroll
-            for (int j = 0; j < IPL; ++j)
-                for (unsigned long long m = due[j]; m; m &= m - 1) finish_scan(C, 64 * j + ffs64(m), t, lane);
             for (uint32_t i = lane; i < I; i += 64) any_abort |= (C.flags[i] & kFlagAbort) != 0;
             // ===================== A2: release reservations of aborted migrations =====================
             if (ballot(any_abort)) {
@@ -674,22 +866,62 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                     m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
                     stat(C, kMigAborted, 1);
                 }
+                wave_sync();
             }
-            wave_sync();
 
-            // ===================== B: admission; C: freeness =====================
-            {
-                unsigned long long cand[IPL];
+            // ===================== B: admission (lane-parallel rounds); C: freeness =====================
+            for (;;) {
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
                     const uint32_t i = lane + 64 * j;
-                    bool c = false;
-                    if (i < I) c = C.hols[i] == kHolUnknown || (C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]);
-                    cand[j] = ballot(c);
+                    for (unsigned long long m = ballot(i < I && C.hols[i] == kHolUnknown); m; m &= m - 1)
+                        rescan_hol(C, 64 * j + ffs64(m), lane);
                 }
+                bool any = false;
+                unsigned long long bat[IPL];
+#pragma unroll
+                for (int j = 0; j < IPL; ++j) {
+                    const uint32_t i = lane + 64 * j;
+                    bool batch = false;
+                    if (i < I && C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]) {
+                        const int nw = C.nwait[i];
+                        if (nw >= 2 && nw <= 64) {
+                            batch = true;
+                        } else {
+                            // the only waiting request, or a queue longer than a wave:
+                            // admit the head of line alone
+                            any = any || nw > 1;
+                            const int h = C.hols[i], dem = C.hold[i];
+                            const uint32_t w = C.hwd[i], m = C.hmt[i];
+                            const uint32_t len = wlo(w), rem = wmid(w);
+                            const uint32_t fin = t + rem;
+                            const size_t hb = size_t(i) * S + h;
+                            C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
+                            C.meta[hb] = uint8_t((m & ~3u) | kRunning | kAdmitted);
+                            const int tier = int((m >> 2) & 15u);
+                            if (!(m & kAdmitted)) {
+                                stat(C, tier * 8 + kAdmittedCnt, 1);
+                                stat(C, tier * 8 + kQdelay, t - C.hta[i]);
+                            }
+                            C.freeb[i] -= dem;
+                            C.held[i] += dem;
+                            C.B[i] += 1;
+                            C.nwait[i] -= 1;
+                            C.res[i * C.RB + ((len - t - 1u) & C.bmask)] += 1u;
+                            C.tcnt[i * kTiers + tier] += 1u;
+                            C.tmask[i] |= 1 << tier;
+                            wheel_put(C, fin, int(i), h);
+                            if (C.nwait[i] == 0) clear_hol(C, int(i));
+                            else C.hols[i] = kHolUnknown;
+                        }
+                    }
+                    bat[j] = ballot(batch);
+                }
+                wave_sync();
 #pragma unroll
                 for (int j = 0; j < IPL; ++j)
-                    for (unsigned long long m = cand[j]; m; m &= m - 1) admit(C, 64 * j + ffs64(m), t, lane);
+                    for (unsigned long long m = bat[j]; m; m &= m - 1) admit_batch(C, 64 * j + ffs64(m), t, lane);
+                if (!ballot(any)) break;
             }
             for (uint32_t i = lane; i < I; i += 64) {
                 set_f(C, int(i));
@@ -699,7 +931,6 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
 
             // ===================== D: tier-ordered dispatch =====================
             if (n > 0) {
-                // arrivals per tier
                 for (uint32_t k0 = 0; k0 < n; k0 += 64) {
                     const unsigned long long a = k0 == 0 ? a0 : (k0 + lane < n ? rec[k0 + lane] : 0);
                     const int tier = k0 + lane < n ? int((a >> 32) & 15u) : -1;
@@ -710,11 +941,31 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                 }
                 const unsigned seq0 = next_seq;
                 next_seq += n;
+                // per-instance dispatch state in registers: lane l, register j <-> instance 64 j + l
                 double key[IPL];
+                int live_r[IPL], fr_r[IPL], hs_r[IPL], den_r[IPL], dem_r[IPL], nadd[IPL], pend_r[IPL];
+                unsigned long long hk_r[IPL];
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
                     const uint32_t i = lane + 64 * j;
-                    key[j] = (i < I && C.live[i] < int(S)) ? C.fd[i] : -__builtin_inf();
+                    nadd[j] = 0;
+                    pend_r[j] = -1;
+                    if (i < I) {
+                        live_r[j] = C.live[i];
+                        fr_r[j] = C.freeb[i];
+                        den_r[j] = C.den[i];
+                        dem_r[j] = C.hold[i];
+                        int hs = 0;
+                        const int tm = C.tmask[i];
+#pragma unroll
+                        for (int p = 0; p < kTiers; ++p) hs += (tm >> p) & 1 ? C.hq[p] : 0;
+                        hs_r[j] = hs;
+                        hk_r[j] = C.hols[i] == kNoHol ? kNone : C.holk[i];
+                        key[j] = live_r[j] < int(S) ? C.fd[i] : -__builtin_inf();
+                    } else {
+                        live_r[j] = int(S); fr_r[j] = 0; den_r[j] = 1; dem_r[j] = 0; hs_r[j] = 0; hk_r[j] = 0;
+                        key[j] = -__builtin_inf();
+                    }
                 }
                 int cur = -1;
                 bool full = false;
@@ -727,47 +978,67 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                         const int tier = int((ak >> 32) & 15u);
                         if (cur < 0) {
                             double lb = key[0];
-                            int lj = 0;
 #pragma unroll
-                            for (int j = 1; j < IPL; ++j)
-                                if (key[j] > lb) { lb = key[j]; lj = j; }
-                            (void)lj;
+                            for (int j = 1; j < IPL; ++j) lb = fmax(lb, key[j]);
                             const double mv = wave_max_f64(lb);
                             if (mv == -__builtin_inf()) { full = true; break; }
 #pragma unroll
-                            for (int j = 0; j < IPL; ++j) {
+                            for (int j = IPL - 1; j >= 0; --j) {
                                 const unsigned long long bm = ballot(key[j] == mv);
-                                if (bm && cur < 0) cur = 64 * j + ffs64(bm);
+                                if (bm) cur = 64 * j + ffs64(bm);
+                            }
+                        }
+                        const int jc = cur >> 6, lc = cur & 63;
+                        int lv = 0;
+                        unsigned long long hkc = 0;
+#pragma unroll
+                        for (int j = 0; j < IPL; ++j)
+                            if (j == jc) { lv = rl(live_r[j], lc); hkc = rl64(hk_r[j], lc); }
+                        const unsigned seqv = seq0 + unsigned(ak >> 36);
+                        const unsigned long long hk = (static_cast<unsigned long long>(tier) << 32) | seqv;
+                        const bool becomes = hk < hkc;
+                        const int nl = lv + 1;
+                        if (lane == lc) {
+#pragma unroll
+                            for (int j = 0; j < IPL; ++j) {
+                                if (j != jc) continue;
+                                live_r[j] = nl;
+                                nadd[j] += 1;
+                                if (becomes) {
+                                    hk_r[j] = hk;
+                                    pend_r[j] = int(k0 + k);
+                                    dem_r[j] = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
+                                    const int num = 256 * (fr_r[j] - dem_r[j]) - hs_r[j];
+                                    key[j] = double(num) / double(den_r[j]);
+                                }
+                                if (nl >= int(S)) key[j] = -__builtin_inf();
                             }
                         }
                         if (lane == int(k)) tgt = cur;
-                        const unsigned seqv = seq0 + unsigned(ak >> 36);
-                        const unsigned long long hk = (static_cast<unsigned long long>(tier) << 32) | seqv;
-                        const bool becomes = C.hols[cur] == kNoHol || hk < C.holk[cur];
-                        const int nl = C.live[cur] + 1;
-                        if (lane == 0) {
-                            C.live[cur] = nl;
-                            C.nwait[cur] += 1;
-                            if (becomes) {
-                                C.holk[cur] = hk;
-                                C.hols[cur] = kHolPending;
-                                C.pend[cur] = int(k0 + k);
-                                C.hold[cur] = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
-                                set_f(C, cur);
-                            }
-                        }
-                        wave_sync();
-                        if (becomes || nl >= int(S)) {
-                            const double nk = nl >= int(S) ? -__builtin_inf() : C.fd[cur];
+                        if (becomes || nl >= int(S)) cur = -1;
+                    }
+                    // write the dispatch state back for the slot assignment and later phases
 #pragma unroll
-                            for (int j = 0; j < IPL; ++j)
-                                if (cur >> 6 == j && lane == (cur & 63)) key[j] = nk;
-                            cur = -1;
+                    for (int j = 0; j < IPL; ++j) {
+                        const uint32_t i = lane + 64 * j;
+                        if (i >= I) continue;
+                        C.live[i] = live_r[j];
+                        C.nwait[i] += nadd[j];
+                        nadd[j] = 0;
+                        if (pend_r[j] >= 0) {
+                            C.hols[i] = kHolPending;
+                            C.pend[i] = pend_r[j];
+                            C.holk[i] = hk_r[j];
+                            C.hold[i] = dem_r[j];
+                            const int num = 256 * (fr_r[j] - dem_r[j]) - hs_r[j];
+                            C.num[i] = num;
+                            C.fd[i] = double(num) / double(den_r[j]);
+                            pend_r[j] = -1;
                         }
                     }
+                    wave_sync();
                     // slot assignment: the arrivals bound for one instance take its
                     // lowest empty slots in arrival order
-                    wave_sync();
                     int rank = 0;
                     for (unsigned long long pend = ballot(tgt >= 0); pend;) {
                         const int tv = rl(tgt, ffs64(pend));
@@ -776,41 +1047,42 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                         pend &= ~same;
                     }
                     const int tier = int((a >> 32) & 15u);
+                    int s = -1;
                     if (tgt >= 0) {
-                        // the rank-th empty slot must exist
-                        int z_total = 0;
-                        for (uint32_t w = 0; w < W; ++w) z_total += 64 - __popcll(C.occ[tgt * W + w]);
-                        const int s = rank < z_total ? 0 : -1;
+                        int rk = rank;
+                        for (uint32_t w = 0; w < W && s < 0; ++w) {
+                            const unsigned long long word = C.occ[tgt * W + w];
+                            const int z = 64 - __popcll(word);
+                            if (rk < z) {
+                                unsigned long long free_bits = ~word;
+                                for (int q = 0; q < rk; ++q) free_bits &= free_bits - 1;
+                                s = int(w) * 64 + ffs64(free_bits);
+                            } else {
+                                rk -= z;
+                            }
+                        }
                         if (s < 0) {  // occupancy and live count disagree: flag, drop the arrival
                             stat(C, kInvariant, 1);
                             stat(C, tier * 8 + kRejected, 1);
                             tgt = -2;
                         }
                     }
+                    wave_sync();
                     if (tgt >= 0) {
-                        int s = -1;
-                        {
-                            int rk = rank;
-                            for (uint32_t w = 0; w < W && s < 0; ++w) {
-                                const unsigned long long word = C.occ[tgt * W + w];
-                                const int z = 64 - __popcll(word);
-                                if (rk < z) {
-                                    unsigned long long free_bits = ~word;
-                                    for (int q = 0; q < rk; ++q) free_bits &= free_bits - 1;
-                                    s = int(w) * 64 + ffs64(free_bits);
-                                } else {
-                                    rk -= z;
-                                }
-                            }
-                        }
                         atomicOr(&C.occ[tgt * W + (s >> 6)], 1ull << (s & 63));
-                        atomicMax(&C.hwm[tgt], s + 1);
                         const size_t sb = size_t(tgt) * S + s;
-                        C.hot[sb] = kWaitW | (uint32_t((a >> 16) & 0xFFFFu) << 16) | uint32_t(a & 0xFFFFu);
-                        C.meta[sb] = uint8_t(kWaiting | (unsigned(tier) << 2));
+                        const uint32_t word = kWaitW | (uint32_t((a >> 16) & 0xFFFFu) << 16) | uint32_t(a & 0xFFFFu);
+                        const uint32_t meta = kWaiting | (unsigned(tier) << 2);
+                        C.hot[sb] = word;
+                        C.meta[sb] = uint8_t(meta);
                         C.seq[sb] = seq0 + unsigned(a >> 36);
                         C.tarr[sb] = t;
-                        if (C.hols[tgt] == kHolPending && C.pend[tgt] == int(k0) + lane) C.hols[tgt] = s;
+                        if (C.hols[tgt] == kHolPending && C.pend[tgt] == int(k0) + lane) {
+                            C.hols[tgt] = s;
+                            C.hwd[tgt] = word;
+                            C.hmt[tgt] = meta;
+                            C.hta[tgt] = t;
+                        }
                     }
                     for (int p = 0; p < int(C.K); ++p) {
                         const int cd = __popcll(ballot(tgt >= 0 && tier == p));
@@ -821,7 +1093,6 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                     wave_sync();
                 }
             }
-            wave_sync();
 
             // ===================== E1: staged copies =====================
             for (uint32_t i = lane; i < I; i += 64) {
@@ -870,7 +1141,7 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                     C.res[d * C.RB + rr] += 1u;
                     tier_dec(C, int(i), tier);
                     tier_inc(C, d, tier);
-                    if (fin < C.nfin[d]) C.nfin[d] = fin;
+                    wheel_put(C, fin, d, m[2]);
                     m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
                     stat(C, kMigCommitted, 1);
                     set_f(C, int(i));
@@ -881,16 +1152,16 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
 
             // ===================== E2: pairing on interval ticks =====================
             if (t % P.mig_interval == 0) {
-                for (uint32_t i = lane; i < I; i += 64) C.flags[i] &= ~kFlagBusy;
-                wave_sync();
-                for (uint32_t i = lane; i < I; i += 64) {
-                    const int d = C.mig[4 * i];
-                    if (d >= 0) { atomicOr(&C.flags[i], kFlagBusy); atomicOr(&C.flags[d], kFlagBusy); }
-                }
-                wave_sync();
                 bool neg = false;
-                for (uint32_t i = lane; i < I; i += 64) neg |= !(C.flags[i] & kFlagBusy) && C.num[i] < 0;
+                for (uint32_t i = lane; i < I; i += 64) neg |= C.num[i] < 0;
                 if (ballot(neg)) {
+                    for (uint32_t i = lane; i < I; i += 64) C.flags[i] &= ~kFlagBusy;
+                    wave_sync();
+                    for (uint32_t i = lane; i < I; i += 64) {
+                        const int d = C.mig[4 * i];
+                        if (d >= 0) { atomicOr(&C.flags[i], kFlagBusy); atomicOr(&C.flags[d], kFlagBusy); }
+                    }
+                    wave_sync();
                     int mine = 0;
                     for (uint32_t i = lane; i < I; i += 64) {
                         if (C.flags[i] & kFlagBusy) continue;
@@ -921,19 +1192,17 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                         if (h >= 0) {
                             if (lane == 0) {
                                 const size_t hb = size_t(src) * S + h;
-                                C.hot[dsb] = C.hot[hb]; C.meta[dsb] = C.meta[hb];
-                                C.seq[dsb] = C.seq[hb]; C.tarr[dsb] = C.tarr[hb];
+                                const uint32_t hw = C.hot[hb], hm = C.meta[hb], ht = C.tarr[hb];
+                                C.hot[dsb] = hw; C.meta[dsb] = uint8_t(hm);
+                                C.seq[dsb] = C.seq[hb]; C.tarr[dsb] = ht;
                                 C.hot[hb] = 0; C.meta[hb] = 0; C.seq[hb] = 0; C.tarr[hb] = 0;
                                 C.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
                                 C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
                                 C.live[src] -= 1; C.nwait[src] -= 1;
                                 C.live[dst] += 1; C.nwait[dst] += 1;
-                                if (ds + 1 > C.hwm[dst]) C.hwm[dst] = ds + 1;
                                 const unsigned long long key = C.holk[src];
-                                if (C.hols[dst] == kNoHol || key < C.holk[dst]) {
-                                    C.hols[dst] = ds; C.holk[dst] = key; C.hold[dst] = C.hold[src];
-                                }
-                                if (C.nwait[src] == 0) { C.hols[src] = kNoHol; C.holk[src] = kNone; C.hold[src] = 0; }
+                                if (C.hols[dst] == kNoHol || key < C.holk[dst]) set_hol(C, dst, ds, key, hw, hm, ht);
+                                if (C.nwait[src] == 0) clear_hol(C, src);
                                 else C.hols[src] = kHolUnknown;
                                 stat(C, kMigQueued, 1);
                             }
@@ -942,7 +1211,7 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                         }
                         // running candidate: largest tier, then fewest blocks, then newest
                         const size_t sbase = size_t(src) * S;
-                        const int nch = (C.hwm[src] + 63) >> 6;
+                        const int nch = live_chunks(C, src, lane);
                         unsigned long long bk = 0;
                         int bs = 0;
                         for (int c = 0; c < nch; ++c) {
@@ -966,7 +1235,6 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
                             C.meta[dsb] = uint8_t(kInbound);
                             C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
                             C.live[dst] += 1;
-                            if (ds + 1 > C.hwm[dst]) C.hwm[dst] = ds + 1;
                             C.meta[sbase + cs] = uint8_t(C.meta[sbase + cs] | kMigrating);
                             int* m = &C.mig[4 * src];
                             m[0] = dst; m[1] = cs; m[2] = ds; m[3] = 0;
@@ -987,11 +1255,10 @@ __global__ __launch_bounds__(64) void k_step(Params P, unsigned long long t0, ui
         }
 
         // ---------------- epilogue ----------------
-        run_acc = wsum64(run_acc);
-        wait_acc = wsum64(wait_acc);
+        const unsigned long long run_sum = wsum64(run_acc), wait_sum = wsum64(wait_acc);
         if (lane == 0) {
-            C.stats[kRunSlotTicks] += run_acc;
-            C.stats[kWaitSlotTicks] += wait_acc;
+            C.stats[kRunSlotTicks] += run_sum;
+            C.stats[kWaitSlotTicks] += wait_sum;
         }
         wave_sync();
         for (int j = lane; j < kNstat; j += 64) P.stats[size_t(r) * kNstat + j] = C.stats[j];

@@ -2,6 +2,7 @@
 symbol include/mts.h declares, sizes every workload and rejects
 configurations outside its documented limits."""
 import copy
+import math
 import os
 import re
 
@@ -44,8 +45,13 @@ def test_state_bytes(name):
     R = sum(g["n_replicas"] for g in c["groups"])
     n_slots = R * c["n_instances"] * c["slots_per_instance"]
     b = mts.mts_state_bytes(c)
-    # slot arrays (13 B per slot) plus at most 512 MiB of pre-sampled arrivals and small tables
-    assert 13 * n_slots <= b < 13 * n_slots + 600 * 2**20
+    # slot arrays (13 B per slot), at most 512 MiB of pre-sampled arrivals, a
+    # finish wheel of at most 1024 buckets per replica and small tables
+    a = c["arrival"]
+    cv = a.get("cv", 0.0) if a["kind"] == "gamma_poisson" else 0.0
+    wcap = min(2048, math.ceil((2 * a["mean"] * (1 + cv) + 24) / 16) * 16)
+    wheel = R * 1024 * (wcap + 1) * 4
+    assert 13 * n_slots <= b < 13 * n_slots + wheel + 600 * 2**20
 
 
 def _bad(**over):
