@@ -166,7 +166,8 @@ def main():
         "data": "synthetic (seeded Philox arrivals, on-device sampling)",
         "config": {"workload": cfg["name"], "replicas": R, "instances": cfg["n_instances"],
                    "slots_per_instance": cfg["slots_per_instance"], "ticks_per_step": T,
-                   "ticks_timed": T * K, "parallelism": "replicas across workgroups"},
+                   "ticks_timed": T * K, "parallelism": "replicas across workgroups",
+                   "blocks": sch.launch()[1], "threads_per_block": 64},
         "slot_updates_per_s": value * slots,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,

@@ -214,6 +214,11 @@ int mts_set_tick(mts_handle h, uint64_t tick);
  * replica count; each wave runs replicas r, r + blocks, ...). */
 int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks);
 
+/* Launch shape mts_step uses now: *threads = 64 and *blocks = the forced
+ * count, or the automatic one (replicas, capped at the step-kernel blocks the
+ * device holds at once).  Queries the current device's occupancy. */
+int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks);
+
 /* Free the handle's host memory.  dev_buf stays with the caller. */
 void mts_destroy(mts_handle h);
 

@@ -51,6 +51,34 @@ uint32_t chunk_for(uint32_t R, uint32_t cap)
     return uint32_t(std::max<size_t>(1, std::min<size_t>(1024, kArrivalBudget / per_tick)));
 }
 
+// Guide table of an inverse-CDF table q (Chen and Asau's indexed search):
+// bucket j of the 32-bit uniforms, [j 2^shift, (j+1) 2^shift), holds samples in
+// [g[j], g[j+1]], where g[j] = min{n : j 2^shift < q[n]} and g[G] = n - 1.  The
+// device searches only that range, so it returns exactly min{n : u < q[n]}.
+uint32_t guide_shift(const Table& t)
+{
+    uint32_t lg = 1;
+    while ((size_t(1) << lg) < t.q.size() && lg < 16) ++lg;
+    return 32 - lg;
+}
+
+std::vector<uint32_t> guide_table(const Table& t)
+{
+    const uint32_t sh = guide_shift(t);
+    const size_t G = size_t(1) << (32 - sh);
+    std::vector<uint32_t> g(G + 1);
+    size_t n = 0;
+    for (size_t j = 0; j < G; ++j) {
+        const uint64_t thr = uint64_t(j) << sh;
+        while (t.q[n] <= thr) ++n;
+        g[j] = uint32_t(n);
+    }
+    g[G] = uint32_t(t.q.size() - 1);
+    return g;
+}
+
+size_t guide_bytes(const Table& t) { return ((size_t(1) << (32 - guide_shift(t))) + 1) * 4; }
+
 // Finish wheel of one replica: a running request is filed under bucket
 // fin mod wsz.  Buckets hold the finishes of one tick plus the few longer
 // requests that share the bucket and are carried to its next visit; entries
@@ -60,7 +88,7 @@ void wheel_size(const mts_cfg& c, const Tables& T, uint32_t& wsz, uint32_t& wcap
 {
     const uint32_t maxout = T.output.base + uint32_t(T.output.q.size()) - 1;
     wsz = 1;
-    while (wsz <= maxout && wsz < 1024) wsz <<= 1;
+    while (wsz <= maxout && wsz < 512) wsz <<= 1;
     const double cv = c.arrival_kind == MTS_ARRIVAL_GAMMA_POISSON ? c.arrival_cv : 0.0;
     const double want = 2.0 * c.arrival_mean * (1.0 + cv) + 24.0;
     wcap = uint32_t(std::min(2048.0, std::ceil(want / 16.0) * 16.0));
@@ -79,6 +107,9 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.count_q = o;  o = up256(o + T.count.q.size() * 4);
     L.prompt_q = o; o = up256(o + T.prompt.q.size() * 4);
     L.output_q = o; o = up256(o + T.output.q.size() * 4);
+    L.count_g = o;  o = up256(o + guide_bytes(T.count));
+    L.prompt_g = o; o = up256(o + guide_bytes(T.prompt));
+    L.output_g = o; o = up256(o + guide_bytes(T.output));
     L.group_of = o; o = up256(o + size_t(R) * 2);
     L.meta = o;     o = up256(o + N);
     L.hot = o;      o = up256(o + N * 4);
@@ -91,7 +122,6 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.digest = o;   o = up256(o + size_t(R) * 8);
     L.arr_cnt = o;  o = up256(o + size_t(R) * chunk * 4);
     L.arr_rec = o;  o = up256(o + size_t(R) * chunk * cap * 8);
-    L.wcnt = o;     o = up256(o + size_t(R) * wsz * 4);
     L.wheel = o;    o = up256(o + size_t(R) * wsz * wcap * 4);
     L.total = o;
     return L;
@@ -116,6 +146,9 @@ Params make_params(const mts_ctx* h)
     p.count_base = h->tables.count.base;
     p.prompt_base = h->tables.prompt.base;
     p.output_base = h->tables.output.base;
+    p.count_gs = guide_shift(h->tables.count);
+    p.prompt_gs = guide_shift(h->tables.prompt);
+    p.output_gs = guide_shift(h->tables.output);
     p.chunk = h->chunk;
     p.arr_cap = h->arr_cap;
     p.wsz = h->wsz;
@@ -129,6 +162,9 @@ Params make_params(const mts_ctx* h)
     p.count_q = reinterpret_cast<const uint32_t*>(d + L.count_q);
     p.prompt_q = reinterpret_cast<const uint32_t*>(d + L.prompt_q);
     p.output_q = reinterpret_cast<const uint32_t*>(d + L.output_q);
+    p.count_g = reinterpret_cast<const uint32_t*>(d + L.count_g);
+    p.prompt_g = reinterpret_cast<const uint32_t*>(d + L.prompt_g);
+    p.output_g = reinterpret_cast<const uint32_t*>(d + L.output_g);
     p.group_of = reinterpret_cast<const uint16_t*>(d + L.group_of);
     p.meta = reinterpret_cast<uint8_t*>(d + L.meta);
     p.hot = reinterpret_cast<uint32_t*>(d + L.hot);
@@ -141,7 +177,6 @@ Params make_params(const mts_ctx* h)
     p.digest = reinterpret_cast<unsigned long long*>(d + L.digest);
     p.arr_cnt = reinterpret_cast<uint32_t*>(d + L.arr_cnt);
     p.arr_rec = reinterpret_cast<unsigned long long*>(d + L.arr_rec);
-    p.wcnt = reinterpret_cast<uint32_t*>(d + L.wcnt);
     p.wheel = reinterpret_cast<uint32_t*>(d + L.wheel);
     return p;
 }
@@ -220,7 +255,7 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
         delete x;
         return MTS_EDEVICE;
     }
-    if (lds_bytes(x->I, x->S, x->cfg.block_tokens) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
+    if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
 
     // tables and per-replica group index
     const uint32_t G = x->cfg.n_groups;
@@ -245,6 +280,11 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
     up(L.count_q, cq.data(), cq.size() * 4);
     up(L.prompt_q, pq.data(), pq.size() * 4);
     up(L.output_q, oq.data(), oq.size() * 4);
+    const std::vector<uint32_t> cg = guide_table(x->tables.count), pg = guide_table(x->tables.prompt),
+                                og = guide_table(x->tables.output);
+    up(L.count_g, cg.data(), cg.size() * 4);
+    up(L.prompt_g, pg.data(), pg.size() * 4);
+    up(L.output_g, og.data(), og.size() * 4);
     up(L.group_of, x->group_of.data(), x->group_of.size() * 2);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);  // host vectors go out of scope
     if (e != hipSuccess) { delete x; return MTS_EDEVICE; }
@@ -264,6 +304,29 @@ int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks)
     return MTS_OK;
 }
 
+namespace {
+
+int auto_blocks(mts_handle h, const Params& p, uint32_t* blocks)
+{
+    if (h->blocks) { *blocks = h->blocks; return MTS_OK; }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess) return MTS_EDEVICE;
+    // every replica resident at once when the CUs hold them all; else one
+    // full wave of resident blocks striding over the replicas
+    const uint32_t per_cu = uint32_t(std::max(1, step_blocks_per_cu(p)));
+    *blocks = std::min<uint32_t>(h->R, uint32_t(cus) * per_cu);
+    return MTS_OK;
+}
+
+}  // namespace
+
+int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks)
+{
+    if (!h || !threads || !blocks) return MTS_EINVAL;
+    *threads = 64;
+    return auto_blocks(h, make_params(h), blocks);
+}
+
 int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
 {
     if (!h) return MTS_EINVAL;
@@ -273,14 +336,9 @@ int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
     const uint64_t end = h->tick + n_ticks;
     if (end > 0xFFFF0000ull || end * uint64_t(h->arr_cap) > 0xFFFFFFFFull) return MTS_ERANGE;
     const Params p = make_params(h);
-    uint32_t blocks = h->blocks;
-    if (!blocks) {
-        int cus = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess) return MTS_EDEVICE;
-        const size_t lds = lds_bytes(h->I, h->S, h->cfg.block_tokens);
-        const uint32_t per_cu = uint32_t(std::max<size_t>(1, std::min<size_t>(16, (160 * 1024) / lds)));
-        blocks = std::min<uint32_t>(h->R, uint32_t(cus) * per_cu);
-    }
+    uint32_t blocks = 0;
+    const int rc = auto_blocks(h, p, &blocks);
+    if (rc) return rc;
     for (uint64_t t = h->tick; t < end; t += h->chunk) {
         const uint32_t nt = uint32_t(std::min<uint64_t>(h->chunk, end - t));
         if (launch_arrivals(p, t, nt, stream) != 0) return MTS_EDEVICE;

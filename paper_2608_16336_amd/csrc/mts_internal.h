@@ -47,11 +47,12 @@ int build_tables(const mts_cfg& c, Tables& T);
 // Device buffer layout: byte offsets of every array inside dev_buf.
 struct Layout {
     size_t tier_q, hq, group_K, count_q, prompt_q, output_q, group_of;  // tables
+    size_t count_g, prompt_g, output_g;                                 // guide tables
     size_t meta, hot, seq, tarr;                                        // [R][I][S]
     size_t freeb, mig;                                                  // [R][I], [R][I][4]
     size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
     size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
-    size_t wcnt, wheel;                                                 // [R][wsz], [R][wsz][wcap]
+    size_t wheel;                                                       // [R][wsz][wcap]
     size_t total;
 };
 
@@ -63,6 +64,7 @@ struct Params {
     int32_t theta_num, theta_den;
     uint32_t count_n, prompt_n, output_n;  // table lengths (entries incl. the implicit 2^32)
     uint32_t count_base, prompt_base, output_base;
+    uint32_t count_gs, prompt_gs, output_gs;  // guide shift: bucket = u >> shift
     uint32_t chunk, arr_cap;       // ticks per arrival batch, records per tick
     uint32_t wsz, wcap;            // finish wheel: buckets (power of two), entries per bucket
     uint64_t seed, id_base;
@@ -72,6 +74,9 @@ struct Params {
     const uint32_t* count_q;
     const uint32_t* prompt_q;
     const uint32_t* output_q;
+    const uint32_t* count_g;       // guide tables, 2^(32 - shift) + 1 entries
+    const uint32_t* prompt_g;
+    const uint32_t* output_g;
     const uint16_t* group_of;      // [R]
     uint8_t* meta;
     uint32_t* hot;
@@ -84,17 +89,18 @@ struct Params {
     unsigned long long* digest;
     uint32_t* arr_cnt;
     unsigned long long* arr_rec;
-    uint32_t* wcnt;
     uint32_t* wheel;
 };
 
 // LDS bytes of one wave (one replica) of the step kernel
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB);
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz);
 
 // kernel launches (mts_kernels.hip); return hipError_t as int
 int launch_init(const Params& p, hipStream_t stream);
 int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStream_t stream);
 int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream);
+// resident step-kernel blocks per CU (0 if the runtime cannot tell)
+int step_blocks_per_cu(const Params& p);
 int launch_digest(const Params& p, uint32_t r0, uint32_t nr, uint32_t tick, hipStream_t stream);
 int launch_shift_clock(const Params& p, uint32_t delta, hipStream_t stream);
 

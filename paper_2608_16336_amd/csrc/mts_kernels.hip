@@ -50,23 +50,34 @@ __device__ __forceinline__ uint32_t wmid(uint32_t v) { return (v >> 16) & kFin; 
 constexpr int kInts = 18;
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, wc, wov, total;
 };
 
 __host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
 
-__host__ __device__ inline LdsLayout lds_layout(uint32_t I, uint32_t W, uint32_t RB)
+// Per-instance arrays are sized for IM instances (a power of two >= I, at
+// least 16) and come first, so that their offsets are compile-time constants
+// of the kernel instantiation; the arrays whose size depends on S, the block
+// size or the wheel follow.
+__host__ __device__ constexpr uint32_t imax_for(uint32_t I)
+{
+    return I <= 16 ? 16 : I <= 32 ? 32 : I <= 64 ? 64 : I <= 128 ? 128 : 256;
+}
+
+__host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_t W, uint32_t RB, uint32_t wsz)
 {
     LdsLayout L;
     uint32_t o = 0;
     L.stats = o; o += kNstat * 8;
+    L.holk = o;  o += IM * 8;
+    L.fd = o;    o += IM * 8;
+    L.ints = o;  o += IM * kInts * 4;
+    L.tcnt = o;  o += IM * kTiers / 2 * 4;
+    L.mig = o;   o += IM * 16;
     L.occ = o;   o += I * W * 8;
-    L.holk = o;  o += I * 8;
-    L.fd = o;    o += I * 8;
-    L.ints = o;  o += I * kInts * 4;
-    L.res = o;   o += I * RB * 4;
-    L.tcnt = o;  o += I * kTiers * 4;
-    L.mig = o;   o += I * 16;
+    L.res = o;   o += ((I * RB + 1) / 2) * 4;
+    L.wc = o;    o += (wsz / 2) * 4;
+    L.wov = o;   o += ((wsz + 31) / 32) * 4;
     L.total = al8(o);
     return L;
 }
@@ -79,12 +90,13 @@ struct Ctx {
     double* fd;                // [I] freeness num / den (exact order for S <= 2048)
     int *freeb, *B, *live, *nwait, *hols, *hold, *num, *den, *held, *inb, *tmask, *flags, *gtmp, *order, *pend;
     unsigned *hwd, *hmt, *hta; // [I] head of line: slot word, meta, arrival tick
-    unsigned* res;             // [I][RB] running requests per growth residue
-    unsigned* tcnt;            // [I][10] running requests per tier
+    unsigned* res;             // [I][RB] running requests per growth residue (u16 pairs)
+    unsigned* tcnt;            // [I][10] running requests per tier (u16 pairs)
     int* mig;                  // [I][4] dst, src slot, dst slot, copied
+    unsigned* wc;              // [wsz / 2] entries filed per wheel bucket, two u16 per word
+    unsigned* wov;             // [wsz / 32] bucket overflowed since its last visit
     // HBM: timing wheel of this replica, slot arrays
-    uint32_t* wcnt;            // [Wsz] requests filed per bucket
-    uint32_t* wheel;           // [Wsz][wcap] instance << 16 | slot
+    uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t wmask, wcap;
     uint32_t* hot;
     uint8_t* meta;
@@ -94,37 +106,39 @@ struct Ctx {
     int hq[kTiers];
 };
 
+template <int IM>
 __device__ inline Ctx carve(char* base, const Params& P)
 {
-    const LdsLayout Y = lds_layout(P.I, P.W, P.RB);
+    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz);
     Ctx C;
     C.stats = reinterpret_cast<unsigned long long*>(base + Y.stats);
     C.occ = reinterpret_cast<unsigned long long*>(base + Y.occ);
     C.holk = reinterpret_cast<unsigned long long*>(base + Y.holk);
     C.fd = reinterpret_cast<double*>(base + Y.fd);
     int* p = reinterpret_cast<int*>(base + Y.ints);
-    const uint32_t I = P.I;
-    C.freeb = p; p += I;
-    C.B = p; p += I;
-    C.live = p; p += I;
-    C.nwait = p; p += I;
-    C.hols = p; p += I;
-    C.hold = p; p += I;
-    C.num = p; p += I;
-    C.den = p; p += I;
-    C.held = p; p += I;
-    C.inb = p; p += I;
-    C.tmask = p; p += I;
-    C.flags = p; p += I;
-    C.gtmp = p; p += I;
-    C.order = p; p += I;
-    C.pend = p; p += I;
-    C.hwd = reinterpret_cast<unsigned*>(p); p += I;
-    C.hmt = reinterpret_cast<unsigned*>(p); p += I;
-    C.hta = reinterpret_cast<unsigned*>(p); p += I;
+    C.freeb = p; p += IM;
+    C.B = p; p += IM;
+    C.live = p; p += IM;
+    C.nwait = p; p += IM;
+    C.hols = p; p += IM;
+    C.hold = p; p += IM;
+    C.num = p; p += IM;
+    C.den = p; p += IM;
+    C.held = p; p += IM;
+    C.inb = p; p += IM;
+    C.tmask = p; p += IM;
+    C.flags = p; p += IM;
+    C.gtmp = p; p += IM;
+    C.order = p; p += IM;
+    C.pend = p; p += IM;
+    C.hwd = reinterpret_cast<unsigned*>(p); p += IM;
+    C.hmt = reinterpret_cast<unsigned*>(p); p += IM;
+    C.hta = reinterpret_cast<unsigned*>(p); p += IM;
     C.res = reinterpret_cast<unsigned*>(base + Y.res);
     C.tcnt = reinterpret_cast<unsigned*>(base + Y.tcnt);
     C.mig = reinterpret_cast<int*>(base + Y.mig);
+    C.wc = reinterpret_cast<unsigned*>(base + Y.wc);
+    C.wov = reinterpret_cast<unsigned*>(base + Y.wov);
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
@@ -235,13 +249,31 @@ __device__ inline void set_f(const Ctx& C, int i)
     C.fd[i] = double(num) / double(den);
 }
 
+// Counters of running requests, two u16 per LDS word (an instance holds at
+// most 2048 running requests, so no half ever carries into the other).  All
+// updates are atomic: lanes that work on different instances may share a word.
+__device__ __forceinline__ uint32_t c16_get(const unsigned* a, uint32_t idx)
+{
+    return (a[idx >> 1] >> ((idx & 1u) * 16u)) & 0xFFFFu;
+}
+__device__ __forceinline__ uint32_t c16_inc(unsigned* a, uint32_t idx)
+{
+    const uint32_t sh = (idx & 1u) * 16u;
+    return (atomicAdd(&a[idx >> 1], 1u << sh) >> sh) & 0xFFFFu;
+}
+__device__ __forceinline__ uint32_t c16_dec(unsigned* a, uint32_t idx)
+{
+    const uint32_t sh = (idx & 1u) * 16u;
+    return (atomicSub(&a[idx >> 1], 1u << sh) >> sh) & 0xFFFFu;
+}
+
 __device__ __forceinline__ void tier_dec(const Ctx& C, int i, int tier)
 {
-    if (atomicSub(&C.tcnt[i * kTiers + tier], 1u) == 1u) atomicAnd(&C.tmask[i], ~(1 << tier));
+    if (c16_dec(C.tcnt, uint32_t(i * kTiers + tier)) == 1u) atomicAnd(&C.tmask[i], ~(1 << tier));
 }
 __device__ __forceinline__ void tier_inc(const Ctx& C, int i, int tier)
 {
-    atomicAdd(&C.tcnt[i * kTiers + tier], 1u);
+    c16_inc(C.tcnt, uint32_t(i * kTiers + tier));
     atomicOr(&C.tmask[i], 1 << tier);
 }
 
@@ -307,9 +339,13 @@ __device__ inline void philox4x64_10(unsigned long long x[4], unsigned long long
     }
 }
 
-__device__ inline uint32_t sample(const uint32_t* q, uint32_t n, uint32_t u)
+// min{n : u < q[n]} with q's last entry 2^32 implicit: the guide table g
+// bounds the answer to [g[u >> shift], g[(u >> shift) + 1]] (indexed search,
+// Chen and Asau 1974), a binary search finishes inside that range
+__device__ __forceinline__ uint32_t sample(const uint32_t* q, const uint32_t* g, uint32_t shift, uint32_t u)
 {
-    uint32_t lo = 0, hi = n - 1;
+    const uint32_t j = u >> shift;
+    uint32_t lo = g[j], hi = g[j + 1];
     while (lo < hi) {
         const uint32_t mid = (lo + hi) >> 1;
         if (u < q[mid]) hi = mid; else lo = mid + 1;
@@ -321,6 +357,29 @@ __device__ inline uint32_t sample(const uint32_t* q, uint32_t n, uint32_t u)
 // k_arrivals: one wave per (replica, tick of the chunk)
 // record = prompt | out << 16 | tier << 32 | k << 36, sorted by tier (stable)
 // ---------------------------------------------------------------------------
+struct Draw {
+    uint32_t tier;
+    unsigned long long rec;
+};
+
+__device__ __forceinline__ Draw draw_arrival(const Params& P, unsigned long long t, unsigned long long gid, uint32_t k,
+                                             const uint32_t* tq, int K)
+{
+    unsigned long long y[4] = {t, k, 1, 0};
+    philox4x64_10(y, P.seed, gid);
+    const uint32_t ut = uint32_t(y[0]);
+    uint32_t tier = 0;
+#pragma unroll
+    for (int j = 0; j < kTiers - 1; ++j) tier += (j < K - 1 && tq[j] <= ut) ? 1u : 0u;
+    const uint32_t prompt = P.prompt_base + sample(P.prompt_q, P.prompt_g, P.prompt_gs, uint32_t(y[1]));
+    const uint32_t outl = P.output_base + sample(P.output_q, P.output_g, P.output_gs, uint32_t(y[2]));
+    Draw d;
+    d.tier = tier;
+    d.rec = static_cast<unsigned long long>(prompt) | (static_cast<unsigned long long>(outl) << 16) |
+            (static_cast<unsigned long long>(tier) << 32) | (static_cast<unsigned long long>(k) << 36);
+    return d;
+}
+
 __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t0, uint32_t nt)
 {
     const uint32_t item = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -334,10 +393,25 @@ __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t
     const uint32_t* tq = P.tier_q + size_t(g) * kTiers;
     unsigned long long x[4] = {t, 0, 0, 0};
     philox4x64_10(x, P.seed, gid);
-    const uint32_t n = P.count_base + sample(P.count_q, P.count_n, uint32_t(x[0]));
+    const uint32_t n = P.count_base + sample(P.count_q, P.count_g, P.count_gs, uint32_t(x[0]));
     unsigned long long* out = P.arr_rec + (size_t(r) * P.chunk + tl) * P.arr_cap;
     if (lane == 0) P.arr_cnt[size_t(r) * P.chunk + tl] = n;
     if (n == 0) return;
+    if (n <= 64) {
+        // one draw per lane, scattered in tier order
+        Draw d{~0u, 0};
+        if (uint32_t(lane) < n) d = draw_arrival(P, t, gid, uint32_t(lane), tq, K);
+        int pos = 0, off = 0;
+#pragma unroll
+        for (int p = 0; p < kTiers; ++p) {
+            if (p >= K) continue;
+            const unsigned long long b = ballot(d.tier == uint32_t(p));
+            if (d.tier == uint32_t(p)) pos = off + __popcll(b & lanemask_lt());
+            off += __popcll(b);
+        }
+        if (uint32_t(lane) < n) out[pos] = d.rec;
+        return;
+    }
     // pass 1: tier counts
     int cnt[kTiers];
 #pragma unroll
@@ -348,7 +422,10 @@ __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t
         if (k < n) {
             unsigned long long y[4] = {t, k, 1, 0};
             philox4x64_10(y, P.seed, gid);
-            tier = int(sample(tq, uint32_t(K), uint32_t(y[0])));
+            const uint32_t ut = uint32_t(y[0]);
+            tier = 0;
+#pragma unroll
+            for (int j = 0; j < kTiers - 1; ++j) tier += (j < K - 1 && tq[j] <= ut) ? 1 : 0;
         }
 #pragma unroll
         for (int p = 0; p < kTiers; ++p)
@@ -361,26 +438,17 @@ __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t
     // pass 2: draw again and scatter in tier order (a lane's draws are its own)
     for (uint32_t k0 = 0; k0 < n; k0 += 64) {
         const uint32_t k = k0 + lane;
-        int tier = -1;
-        unsigned long long rec = 0;
-        if (k < n) {
-            unsigned long long y[4] = {t, k, 1, 0};
-            philox4x64_10(y, P.seed, gid);
-            tier = int(sample(tq, uint32_t(K), uint32_t(y[0])));
-            const uint32_t prompt = P.prompt_base + sample(P.prompt_q, P.prompt_n, uint32_t(y[1]));
-            const uint32_t outl = P.output_base + sample(P.output_q, P.output_n, uint32_t(y[2]));
-            rec = static_cast<unsigned long long>(prompt) | (static_cast<unsigned long long>(outl) << 16) |
-                  (static_cast<unsigned long long>(tier) << 32) | (static_cast<unsigned long long>(k) << 36);
-        }
+        Draw d{~0u, 0};
+        if (k < n) d = draw_arrival(P, t, gid, k, tq, K);
         int pos = 0;
 #pragma unroll
         for (int p = 0; p < kTiers; ++p) {
             if (p >= K) continue;
-            const unsigned long long b = ballot(tier == p);
-            if (tier == p) pos = off[p] + __popcll(b & lanemask_lt());
+            const unsigned long long b = ballot(d.tier == uint32_t(p));
+            if (d.tier == uint32_t(p)) pos = off[p] + __popcll(b & lanemask_lt());
             off[p] += __popcll(b);
         }
-        if (k < n) out[pos] = rec;
+        if (k < n) out[pos] = d.rec;
     }
 }
 
@@ -404,8 +472,15 @@ __device__ __forceinline__ void set_hol(const Ctx& C, int i, int slot, unsigned 
 __device__ __forceinline__ void wheel_put(const Ctx& C, uint32_t fin, int i, int s)
 {
     const uint32_t b = fin & C.wmask;
-    const uint32_t k = atomicAdd(&C.wcnt[b], 1u);
-    if (k < C.wcap) C.wheel[size_t(b) * C.wcap + k] = (uint32_t(i) << 16) | uint32_t(s);
+    const uint32_t sh = (b & 1u) * 16u;
+    const uint32_t k = (atomicAdd(&C.wc[b >> 1], 1u << sh) >> sh) & 0xFFFFu;
+    if (k < C.wcap) {
+        C.wheel[size_t(b) * C.wcap + k] = (uint32_t(i) << 16) | uint32_t(s);
+    } else {
+        // full: keep the count at wcap and mark the bucket for an exact rebuild
+        atomicSub(&C.wc[b >> 1], 1u << sh);
+        atomicOr(&C.wov[b >> 5], 1u << (b & 31u));
+    }
 }
 
 // head of line of instance i from its slots: smallest (tier, seq) waiting
@@ -419,12 +494,11 @@ __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
     for (int c0 = 0; c0 < nch; c0 += 4) {
         uint32_t v[4], m[4], q[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) v[g] = c0 + g < nch ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
-#pragma unroll
         for (int g = 0; g < 4; ++g) {
-            const bool w = wst(v[g]) == 1u;
-            m[g] = w ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
-            q[g] = w ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
+            const bool in = c0 + g < nch;
+            v[g] = in ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
+            m[g] = in ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
+            q[g] = in ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
         }
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -496,7 +570,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             C.held[i] -= vb;
             C.B[i] -= 1;
             C.nwait[i] += 1;
-            C.res[i * C.RB + vr] -= 1u;
+            c16_dec(C.res, i * C.RB + vr);
             tier_dec(C, i, vt);
             stat(C, vt * 8 + kPreempted, 1);
             if (vm) C.flags[i] |= kFlagAbort;
@@ -533,7 +607,7 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
             const int tier = int((m >> 2) & 15u);
             stat(C, tier * 8 + kFinished, 1);
             stat(C, tier * 8 + kE2e, t - C.tarr[b + s]);
-            atomicSub(&C.res[i * C.RB + ((lenf - t - 1u) & C.bmask)], 1u);
+            c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
             if (m & kMigrating) ab = true;
             C.hot[b + s] = 0; C.meta[b + s] = 0; C.seq[b + s] = 0; C.tarr[b + s] = 0;
@@ -564,10 +638,14 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
 __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
 {
     const uint32_t bk = t & C.wmask;
-    const uint32_t n = __hip_atomic_load(&C.wcnt[bk], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (n > C.wcap) {
+    const uint32_t sh = (bk & 1u) * 16u;
+    const uint32_t n = (C.wc[bk >> 1] >> sh) & 0xFFFFu;
+    if ((C.wov[bk >> 5] >> (bk & 31u)) & 1u) {
         // the bucket overflowed: rebuild it by scanning every instance with running requests
-        if (lane == 0) C.wcnt[bk] = 0;
+        if (lane == 0) {
+            C.wc[bk >> 1] &= ~(0xFFFFu << sh);
+            C.wov[bk >> 5] &= ~(1u << (bk & 31u));
+        }
         wave_sync();
         for (uint32_t j = 0; j < (C.I + 63) / 64; ++j) {
             const uint32_t i = lane + 64 * j;
@@ -583,7 +661,8 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
         const int i = int(e >> 16), s = int(e & 0xFFFFu);
         const bool valid = e0 + lane < n && uint32_t(i) < C.I && uint32_t(s) < C.S;
         const size_t idx = size_t(i) * C.S + s;
-        const uint32_t v = valid ? C.hot[idx] : 0u;
+        uint32_t v = 0, m = 0, ta = 0;
+        if (valid) { v = C.hot[idx]; m = C.meta[idx]; ta = C.tarr[idx]; }
         const uint32_t fin = fin_of(v, t);
         bool f = valid && wst(v) == 2u && fin == t;
         bool k = valid && wst(v) == 2u && fin != t && (fin & C.wmask) == bk;
@@ -601,15 +680,13 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
         const unsigned long long km = ballot(k);
         if (k) ent[kept + __popcll(km & lanemask_lt())] = e;
         kept += __popcll(km);
-        uint32_t m = 0, ta = 0;
-        if (f) { m = C.meta[idx]; ta = C.tarr[idx]; }
         if (f) {
             const uint32_t lenf = wlo(v);
             const int bl = blocks_of(lenf, C.shift);
             const int tier = int((m >> 2) & 15u);
             stat(C, tier * 8 + kFinished, 1);
             stat(C, tier * 8 + kE2e, t - ta);
-            atomicSub(&C.res[i * C.RB + ((lenf - t - 1u) & C.bmask)], 1u);
+            c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
             if (m & kMigrating) atomicOr(&C.flags[i], kFlagAbort);
             atomicAnd(&C.occ[i * C.W + (s >> 6)], ~(1ull << (s & 63)));
@@ -621,8 +698,25 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
         }
         wave_sync();
     }
-    if (lane == 0) C.wcnt[bk] = kept;
+    if (lane == 0) C.wc[bk >> 1] = (C.wc[bk >> 1] & ~(0xFFFFu << sh)) | (kept << sh);
     wave_sync();
+}
+
+// Adds to stats[tier * 8 + field], for every tier, the number of lanes with f
+// set among the lanes of that tier.  The lanes' tiers are non-decreasing
+// (arrivals are sorted by tier); lanes that hold no arrival carry tier 15.
+__device__ __forceinline__ void tier_stat(const Ctx& C, int tier, bool f, int field, int lane)
+{
+    const int tn = __shfl_down(tier, 1);
+    const bool last = lane == 63 || tn != tier;
+    const unsigned long long bm = ballot(last), fm = ballot(f);
+    if (last && tier < kTiers) {
+        const unsigned long long below = bm & lanemask_lt();
+        const int start = below ? 64 - __clzll(static_cast<long long>(below)) : 0;
+        const unsigned long long upto = lane == 63 ? ~0ull : (1ull << (lane + 1)) - 1ull;
+        const int c = __popcll(fm & upto & ~((1ull << start) - 1ull));
+        if (c) stat(C, tier * 8 + field, c);
+    }
 }
 
 // Admission of instance i when its head of line fits and 2..64 requests wait
@@ -640,15 +734,15 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
     int slot = 0, w = 0;
     for (int c0 = 0; c0 < nch; c0 += 4) {
         uint32_t v[4], m[4], q[4], a[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) v[g] = c0 + g < nch ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
+        // all loads of the group are issued together (one memory round trip)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            const bool wt = wst(v[g]) == 1u;
+            const bool in = c0 + g < nch;
             const size_t sb = b + (c0 + g) * 64 + lane;
-            m[g] = wt ? C.meta[sb] : 0u;
-            q[g] = wt ? C.seq[sb] : 0u;
-            a[g] = wt ? C.tarr[sb] : 0u;
+            v[g] = in ? C.hot[sb] : 0u;
+            m[g] = in ? C.meta[sb] : 0u;
+            q[g] = in ? C.seq[sb] : 0u;
+            a[g] = in ? C.tarr[sb] : 0u;
         }
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -698,7 +792,7 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
             stat(C, tier * 8 + kAdmittedCnt, 1);
             stat(C, tier * 8 + kQdelay, t - ta);
         }
-        atomicAdd(&C.res[i * C.RB + ((len - t - 1u) & C.bmask)], 1u);
+        c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
         tier_inc(C, i, tier);
         wheel_put(C, fin, i, slot);
     }
@@ -722,11 +816,12 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
 // ---------------------------------------------------------------------------
 // k_step
 // ---------------------------------------------------------------------------
-template <int IPL>
-__global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigned long long t0, uint32_t nt)
+template <int IM>
+__global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigned long long t0, uint32_t nt)
 {
+    constexpr int IPL = (IM + 63) / 64;
     extern __shared__ __align__(16) char lds_raw[];
-    Ctx C = carve(lds_raw, P);
+    Ctx C = carve<IM>(lds_raw, P);
     const int lane = lane_id();
     const uint32_t I = P.I, S = P.S, W = P.W;
     const uint32_t wsz = P.wsz;
@@ -738,7 +833,6 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
         for (int p = 0; p < kTiers; ++p) C.hq[p] = P.hq[g * kTiers + p];
         const size_t rb = size_t(r) * I * S;
         C.hot = P.hot + rb; C.meta = P.meta + rb; C.seq = P.seq + rb; C.tarr = P.tarr + rb;
-        C.wcnt = P.wcnt + size_t(r) * wsz;
         C.wheel = P.wheel + size_t(r) * wsz * P.wcap;
 
         // ---------------- prologue: derived per-instance state ----------------
@@ -749,10 +843,11 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
             C.inb[i] = 0;
             C.flags[i] = 0;
             C.tmask[i] = 0;
-            for (uint32_t q = 0; q < C.RB; ++q) C.res[i * C.RB + q] = 0;
-            for (int q = 0; q < kTiers; ++q) C.tcnt[i * kTiers + q] = 0;
         }
-        for (uint32_t b = lane; b < wsz; b += 64) C.wcnt[b] = 0;
+        for (uint32_t b = lane; b < wsz / 2; b += 64) C.wc[b] = 0;
+        for (uint32_t b = lane; b < (I * C.RB + 1) / 2; b += 64) C.res[b] = 0;
+        for (uint32_t b = lane; b < (I * kTiers + 1) / 2; b += 64) C.tcnt[b] = 0;
+        for (uint32_t b = lane; b < (wsz + 31) / 32; b += 64) C.wov[b] = 0;
         wave_sync();
         for (uint32_t i = lane; i < I; i += 64) {
             const int d = C.mig[4 * i];
@@ -778,9 +873,9 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                 if (st == 2u) {
                     const uint32_t lenf = wlo(v), fin = fin_of(v, t0u);
                     held += blocks_of(lenf - (fin - t0u + 1u), C.shift);
-                    atomicAdd(&C.res[i * C.RB + ((lenf - fin - 1u) & C.bmask)], 1u);
+                    c16_inc(C.res, i * C.RB + ((lenf - fin - 1u) & C.bmask));
                     const int tier = int((C.meta[b + s] >> 2) & 15u);
-                    atomicAdd(&C.tcnt[i * kTiers + tier], 1u);
+                    c16_inc(C.tcnt, i * kTiers + tier);
                     wheel_put(C, fin, int(i), s);
                 } else if (st == 1u) {
                     const uint32_t m = C.meta[b + s];
@@ -805,7 +900,7 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                 if (hs >= 0) set_hol(C, int(i), hs, mn, hw, hm, ht);
                 else clear_hol(C, int(i));
                 int tm = 0;
-                for (int p = 0; p < kTiers; ++p) tm |= C.tcnt[i * kTiers + p] ? (1 << p) : 0;
+                for (int p = 0; p < kTiers; ++p) tm |= c16_get(C.tcnt, i * kTiers + p) ? (1 << p) : 0;
                 C.tmask[i] = tm;
             }
             wave_sync();
@@ -816,11 +911,16 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
         const uint32_t* cnts = P.arr_cnt + size_t(r) * P.chunk;
         wave_sync();
 
+        // the arrivals of the next tick are loaded one tick ahead; records past
+        // the tick's count are never used
+        const uint32_t lim = P.arr_cap < 64u ? P.arr_cap : 64u;
+        uint32_t n_nx = cnts[0];
+        unsigned long long a_nx = uint32_t(lane) < lim ? recs[lane] : 0ull;
         for (uint32_t tl = 0; tl < nt; ++tl) {
             const uint32_t t = t0u + tl;
-            const uint32_t n = cnts[tl];
+            const uint32_t n = n_nx;
             const unsigned long long* rec = recs + size_t(tl) * P.arr_cap;
-            const unsigned long long a0 = lane < int(n) ? rec[lane] : 0;
+            const unsigned long long a0 = a_nx;
 
             // ===================== A: growth, preemption, finish =====================
             const uint32_t cres = (0u - t) & C.bmask;
@@ -830,7 +930,7 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                 const uint32_t i = lane + 64 * j;
                 bool np = false;
                 if (i < I) {
-                    const int G = int(C.res[i * C.RB + cres]);
+                    const int G = int(c16_get(C.res, i * C.RB + cres));
                     C.gtmp[i] = G;
                     np = G > C.freeb[i];
                 }
@@ -907,9 +1007,8 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                             C.held[i] += dem;
                             C.B[i] += 1;
                             C.nwait[i] -= 1;
-                            C.res[i * C.RB + ((len - t - 1u) & C.bmask)] += 1u;
-                            C.tcnt[i * kTiers + tier] += 1u;
-                            C.tmask[i] |= 1 << tier;
+                            c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
+                            tier_inc(C, int(i), tier);
                             wheel_put(C, fin, int(i), h);
                             if (C.nwait[i] == 0) clear_hol(C, int(i));
                             else C.hols[i] = kHolUnknown;
@@ -933,11 +1032,8 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
             if (n > 0) {
                 for (uint32_t k0 = 0; k0 < n; k0 += 64) {
                     const unsigned long long a = k0 == 0 ? a0 : (k0 + lane < n ? rec[k0 + lane] : 0);
-                    const int tier = k0 + lane < n ? int((a >> 32) & 15u) : -1;
-                    for (int p = 0; p < int(C.K); ++p) {
-                        const int c = __popcll(ballot(tier == p));
-                        if (lane == 0 && c) stat(C, p * 8 + kArrived, c);
-                    }
+                    const int tier = k0 + lane < n ? int((a >> 32) & 15u) : 15;
+                    tier_stat(C, tier, true, kArrived, lane);
                 }
                 const unsigned seq0 = next_seq;
                 next_seq += n;
@@ -973,9 +1069,8 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                     const uint32_t cn = n - k0 < 64 ? n - k0 : 64;
                     const unsigned long long a = k0 == 0 ? a0 : (lane < int(cn) ? rec[k0 + lane] : 0);
                     int tgt = -1;
-                    for (uint32_t k = 0; k < cn && !full; ++k) {
-                        const unsigned long long ak = rl64(a, int(k));
-                        const int tier = int((ak >> 32) & 15u);
+                    uint32_t k = 0;
+                    while (k < cn && !full) {
                         if (cur < 0) {
                             double lb = key[0];
 #pragma unroll
@@ -994,16 +1089,22 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
 #pragma unroll
                         for (int j = 0; j < IPL; ++j)
                             if (j == jc) { lv = rl(live_r[j], lc); hkc = rl64(hk_r[j], lc); }
-                        const unsigned seqv = seq0 + unsigned(ak >> 36);
-                        const unsigned long long hk = (static_cast<unsigned long long>(tier) << 32) | seqv;
+                        const unsigned long long ak = rl64(a, int(k));
+                        const unsigned long long hk = ((ak >> 32) & 15u) << 32 | (seq0 + unsigned(ak >> 36));
                         const bool becomes = hk < hkc;
-                        const int nl = lv + 1;
+                        // Arrival k goes to cur.  If it becomes cur's head of line, F of cur
+                        // changes and the argmax is taken again.  Otherwise F stays, and
+                        // so does the argmax for the following arrivals, none of which can
+                        // become the head of line (keys increase along the arrival order):
+                        // they all go to cur until its slots run out.
+                        const int m = becomes ? 1 : min(int(cn - k), int(S) - lv);
+                        const int nl = lv + m;
                         if (lane == lc) {
 #pragma unroll
                             for (int j = 0; j < IPL; ++j) {
                                 if (j != jc) continue;
                                 live_r[j] = nl;
-                                nadd[j] += 1;
+                                nadd[j] += m;
                                 if (becomes) {
                                     hk_r[j] = hk;
                                     pend_r[j] = int(k0 + k);
@@ -1014,8 +1115,9 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                                 if (nl >= int(S)) key[j] = -__builtin_inf();
                             }
                         }
-                        if (lane == int(k)) tgt = cur;
+                        if (lane >= int(k) && lane < int(k) + m) tgt = cur;
                         if (becomes || nl >= int(S)) cur = -1;
+                        k += uint32_t(m);
                     }
                     // write the dispatch state back for the slot assignment and later phases
 #pragma unroll
@@ -1054,9 +1156,7 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                             const unsigned long long word = C.occ[tgt * W + w];
                             const int z = 64 - __popcll(word);
                             if (rk < z) {
-                                unsigned long long free_bits = ~word;
-                                for (int q = 0; q < rk; ++q) free_bits &= free_bits - 1;
-                                s = int(w) * 64 + ffs64(free_bits);
+                                s = int(w) * 64 + kth_set_bit(~word, rk);
                             } else {
                                 rk -= z;
                             }
@@ -1084,14 +1184,16 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                             C.hta[tgt] = t;
                         }
                     }
-                    for (int p = 0; p < int(C.K); ++p) {
-                        const int cd = __popcll(ballot(tgt >= 0 && tier == p));
-                        const int cr = __popcll(ballot(tgt == -1 && lane < int(cn) && tier == p));
-                        if (lane == 0 && cd) stat(C, p * 8 + kDispatched, cd);
-                        if (lane == 0 && cr) stat(C, p * 8 + kRejected, cr);
-                    }
+                    const int vt = lane < int(cn) ? tier : 15;
+                    tier_stat(C, vt, tgt >= 0, kDispatched, lane);
+                    tier_stat(C, vt, tgt == -1 && lane < int(cn), kRejected, lane);
                     wave_sync();
                 }
+            }
+
+            if (tl + 1 < nt) {
+                n_nx = cnts[tl + 1];
+                a_nx = uint32_t(lane) < lim ? rec[P.arr_cap + lane] : 0ull;
             }
 
             // ===================== E1: staged copies =====================
@@ -1137,8 +1239,8 @@ __global__ __launch_bounds__(64, IPL == 1 ? 4 : 1) void k_step(Params P, unsigne
                     C.inb[d] = 0;
                     C.B[i] -= 1;
                     C.B[d] += 1;
-                    C.res[i * C.RB + rr] -= 1u;
-                    C.res[d * C.RB + rr] += 1u;
+                    c16_dec(C.res, i * C.RB + rr);
+                    c16_inc(C.res, d * C.RB + rr);
                     tier_dec(C, int(i), tier);
                     tier_inc(C, d, tier);
                     wheel_put(C, fin, d, m[2]);
@@ -1360,7 +1462,10 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t 
 
 }  // namespace
 
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB) { return lds_layout(I, S / 64, RB).total; }
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz)
+{
+    return lds_layout(imax_for(I), I, S / 64, RB, wsz).total;
+}
 
 int launch_init(const Params& p, hipStream_t stream)
 {
@@ -1375,21 +1480,53 @@ int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStre
     return int(hipGetLastError());
 }
 
-int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream)
+namespace {
+
+const void* step_fn(const Params& p)
 {
-    const size_t lds = lds_bytes(p.I, p.S, p.RB);
-    const int ipl = int((p.I + 63) / 64);
-    const void* fn = ipl <= 1 ? reinterpret_cast<const void*>(&k_step<1>)
-                   : ipl <= 2 ? reinterpret_cast<const void*>(&k_step<2>)
-                              : reinterpret_cast<const void*>(&k_step<4>);
+    switch (imax_for(p.I)) {
+    case 16: return reinterpret_cast<const void*>(&k_step<16>);
+    case 32: return reinterpret_cast<const void*>(&k_step<32>);
+    case 64: return reinterpret_cast<const void*>(&k_step<64>);
+    case 128: return reinterpret_cast<const void*>(&k_step<128>);
+    default: return reinterpret_cast<const void*>(&k_step<256>);
+    }
+}
+
+size_t step_lds(const Params& p)
+{
+    const size_t lds = lds_bytes(p.I, p.S, p.RB, p.wsz);
     if (lds > 64 * 1024) {
         // raise the dynamic LDS limit; a real failure shows up at the launch
-        (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+        (void)hipFuncSetAttribute(step_fn(p), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
         (void)hipGetLastError();
     }
-    if (ipl <= 1) hipLaunchKernelGGL(k_step<1>, dim3(blocks), dim3(64), lds, stream, p, t0, nt);
-    else if (ipl <= 2) hipLaunchKernelGGL(k_step<2>, dim3(blocks), dim3(64), lds, stream, p, t0, nt);
-    else hipLaunchKernelGGL(k_step<4>, dim3(blocks), dim3(64), lds, stream, p, t0, nt);
+    return lds;
+}
+
+}  // namespace
+
+int step_blocks_per_cu(const Params& p)
+{
+    const size_t lds = step_lds(p);
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, step_fn(p), 64, lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return nb;
+}
+
+int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream)
+{
+    const size_t lds = step_lds(p);
+    switch (imax_for(p.I)) {
+    case 16: hipLaunchKernelGGL(k_step<16>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 32: hipLaunchKernelGGL(k_step<32>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 64: hipLaunchKernelGGL(k_step<64>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 128: hipLaunchKernelGGL(k_step<128>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    default: hipLaunchKernelGGL(k_step<256>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    }
     return int(hipGetLastError());
 }
 

@@ -74,7 +74,7 @@ class mts_state_view(ctypes.Structure):
 
 EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest",
             "mts_export_state", "mts_import_state", "mts_get_table", "mts_get_headroom",
-            "mts_tick", "mts_set_tick", "mts_set_launch", "mts_destroy", "mts_strerror")
+            "mts_tick", "mts_set_tick", "mts_set_launch", "mts_get_launch", "mts_destroy", "mts_strerror")
 
 _lib = None
 
@@ -103,12 +103,13 @@ def load_library(path=LIB_PATH):
     L.mts_set_tick.argtypes = [vp, u64]
     L.mts_set_tick.restype = ci
     L.mts_set_launch.argtypes = [vp, u32, u32]
+    L.mts_get_launch.argtypes = [vp, ctypes.POINTER(u32), ctypes.POINTER(u32)]
     L.mts_destroy.argtypes = [vp]
     L.mts_destroy.restype = None
     L.mts_strerror.argtypes = [ci]
     L.mts_strerror.restype = ctypes.c_char_p
     for f in ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest", "mts_export_state",
-              "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch"):
+              "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch", "mts_get_launch"):
         getattr(L, f).restype = ci
     _lib = L
     return L
@@ -228,6 +229,12 @@ class Scheduler:
 
     def set_launch(self, threads=0, blocks=0):
         _check("mts_set_launch", load_library().mts_set_launch(self._h, threads, blocks))
+
+    def launch(self):
+        """(threads, blocks) of the step kernel as mts_step launches it."""
+        th, bl = ctypes.c_uint32(0), ctypes.c_uint32(0)
+        _check("mts_get_launch", load_library().mts_get_launch(self._h, ctypes.byref(th), ctypes.byref(bl)))
+        return th.value, bl.value
 
     def stats(self, allow_violations=False):
         st = mts_stats_t()
