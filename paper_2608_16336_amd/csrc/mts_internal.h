@@ -66,6 +66,7 @@ struct Params {
     uint32_t count_base, prompt_base, output_base;
     uint32_t count_gs, prompt_gs, output_gs;  // guide shift: bucket = u >> shift
     uint32_t chunk, arr_cap;       // ticks per arrival batch, records per tick
+    uint32_t arr_group;            // lanes per tick in the arrival kernel (16, 32 or 64)
     uint32_t wsz, wcap;            // finish wheel: buckets (power of two), entries per bucket
     uint64_t seed, id_base;
     const uint32_t* tier_q;        // [group][MTS_MAX_TIERS]
@@ -95,7 +96,7 @@ struct Params {
 // LDS bytes of one wave (one replica) of the step kernel
 size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz);
 
-// kernel launches (mts_kernels.hip); return hipError_t as int
+// kernel launches (mts_kernels.hip, mts_arrivals.hip); return hipError_t as int
 int launch_init(const Params& p, hipStream_t stream);
 int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStream_t stream);
 int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream);

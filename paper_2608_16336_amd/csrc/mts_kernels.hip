@@ -1,8 +1,7 @@
 // Device code of libmts.
 //
-//   k_arrivals  samples every arrival of a chunk of ticks for every replica
-//               (Philox4x64-10 + inverse-CDF tables) and sorts each tick's
-//               arrivals by tier, one wave per (replica, tick).
+//   k_arrivals  (mts_arrivals.hip) samples every arrival of a chunk of ticks
+//               and sorts each tick's arrivals by tier.
 //   k_step      the scheduling tick, one wave per replica for a whole chunk
 //               of ticks: per-instance summaries live in LDS, per-instance
 //               O(1) work is lane-parallel (lane i <-> instance i), slot
@@ -27,6 +26,7 @@
 #include <hip/hip_runtime.h>
 
 #include "mts_internal.h"
+#include "mts_wave.h"
 
 namespace mts {
 namespace {
@@ -148,21 +148,7 @@ __device__ inline Ctx carve(char* base, const Params& P)
     return C;
 }
 
-// ---------------------------------------------------------------------------
-// wave helpers
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ int lane_id() { return __lane_id(); }
-__device__ __forceinline__ unsigned long long ballot(bool p) { return __ballot(p); }
-__device__ __forceinline__ unsigned long long lanemask_lt() { return (1ull << lane_id()) - 1ull; }
-__device__ __forceinline__ int ffs64(unsigned long long m) { return __ffsll(static_cast<long long>(m)) - 1; }
-
-__device__ __forceinline__ int rl(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
-__device__ __forceinline__ unsigned rlu(unsigned v, int l) { return unsigned(__builtin_amdgcn_readlane(int(v), l)); }
-__device__ __forceinline__ unsigned long long rl64(unsigned long long v, int l)
-{
-    const unsigned lo = rlu(unsigned(v), l), hi = rlu(unsigned(v >> 32), l);
-    return (static_cast<unsigned long long>(hi) << 32) | lo;
-}
+using namespace wave;
 
 // Lanes of the wave exchange values through LDS and HBM: every write by a
 // subset of lanes that other lanes read later is followed by this point, so
@@ -319,137 +305,6 @@ __device__ __forceinline__ int wscan(int x, int lane)
         if (lane >= o) x += y;
     }
     return x;
-}
-
-// ---------------------------------------------------------------------------
-// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011) from its published
-// round function and Weyl key schedule; inverse-CDF table search.
-// ---------------------------------------------------------------------------
-__device__ inline void philox4x64_10(unsigned long long x[4], unsigned long long k0, unsigned long long k1)
-{
-    constexpr unsigned long long M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
-    constexpr unsigned long long W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
-#pragma unroll
-    for (int r = 0; r < 10; ++r) {
-        const unsigned long long lo0 = M0 * x[0], hi0 = __umul64hi(M0, x[0]);
-        const unsigned long long lo1 = M1 * x[2], hi1 = __umul64hi(M1, x[2]);
-        const unsigned long long n0 = hi1 ^ x[1] ^ k0, n2 = hi0 ^ x[3] ^ k1;
-        x[0] = n0; x[1] = lo1; x[2] = n2; x[3] = lo0;
-        k0 += W0; k1 += W1;
-    }
-}
-
-// min{n : u < q[n]} with q's last entry 2^32 implicit: the guide table g
-// bounds the answer to [g[u >> shift], g[(u >> shift) + 1]] (indexed search,
-// Chen and Asau 1974), a binary search finishes inside that range
-__device__ __forceinline__ uint32_t sample(const uint32_t* q, const uint32_t* g, uint32_t shift, uint32_t u)
-{
-    const uint32_t j = u >> shift;
-    uint32_t lo = g[j], hi = g[j + 1];
-    while (lo < hi) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (u < q[mid]) hi = mid; else lo = mid + 1;
-    }
-    return lo;
-}
-
-// ---------------------------------------------------------------------------
-// k_arrivals: one wave per (replica, tick of the chunk)
-// record = prompt | out << 16 | tier << 32 | k << 36, sorted by tier (stable)
-// ---------------------------------------------------------------------------
-struct Draw {
-    uint32_t tier;
-    unsigned long long rec;
-};
-
-__device__ __forceinline__ Draw draw_arrival(const Params& P, unsigned long long t, unsigned long long gid, uint32_t k,
-                                             const uint32_t* tq, int K)
-{
-    unsigned long long y[4] = {t, k, 1, 0};
-    philox4x64_10(y, P.seed, gid);
-    const uint32_t ut = uint32_t(y[0]);
-    uint32_t tier = 0;
-#pragma unroll
-    for (int j = 0; j < kTiers - 1; ++j) tier += (j < K - 1 && tq[j] <= ut) ? 1u : 0u;
-    const uint32_t prompt = P.prompt_base + sample(P.prompt_q, P.prompt_g, P.prompt_gs, uint32_t(y[1]));
-    const uint32_t outl = P.output_base + sample(P.output_q, P.output_g, P.output_gs, uint32_t(y[2]));
-    Draw d;
-    d.tier = tier;
-    d.rec = static_cast<unsigned long long>(prompt) | (static_cast<unsigned long long>(outl) << 16) |
-            (static_cast<unsigned long long>(tier) << 32) | (static_cast<unsigned long long>(k) << 36);
-    return d;
-}
-
-__global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t0, uint32_t nt)
-{
-    const uint32_t item = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (item >= P.R * nt) return;
-    const int lane = lane_id();
-    const uint32_t r = item / nt, tl = item % nt;
-    const unsigned long long t = t0 + tl;
-    const unsigned long long gid = P.id_base + r;
-    const uint32_t g = P.group_of[r];
-    const int K = int(P.group_K32[g]);
-    const uint32_t* tq = P.tier_q + size_t(g) * kTiers;
-    unsigned long long x[4] = {t, 0, 0, 0};
-    philox4x64_10(x, P.seed, gid);
-    const uint32_t n = P.count_base + sample(P.count_q, P.count_g, P.count_gs, uint32_t(x[0]));
-    unsigned long long* out = P.arr_rec + (size_t(r) * P.chunk + tl) * P.arr_cap;
-    if (lane == 0) P.arr_cnt[size_t(r) * P.chunk + tl] = n;
-    if (n == 0) return;
-    if (n <= 64) {
-        // one draw per lane, scattered in tier order
-        Draw d{~0u, 0};
-        if (uint32_t(lane) < n) d = draw_arrival(P, t, gid, uint32_t(lane), tq, K);
-        int pos = 0, off = 0;
-#pragma unroll
-        for (int p = 0; p < kTiers; ++p) {
-            if (p >= K) continue;
-            const unsigned long long b = ballot(d.tier == uint32_t(p));
-            if (d.tier == uint32_t(p)) pos = off + __popcll(b & lanemask_lt());
-            off += __popcll(b);
-        }
-        if (uint32_t(lane) < n) out[pos] = d.rec;
-        return;
-    }
-    // pass 1: tier counts
-    int cnt[kTiers];
-#pragma unroll
-    for (int p = 0; p < kTiers; ++p) cnt[p] = 0;
-    for (uint32_t k0 = 0; k0 < n; k0 += 64) {
-        const uint32_t k = k0 + lane;
-        int tier = -1;
-        if (k < n) {
-            unsigned long long y[4] = {t, k, 1, 0};
-            philox4x64_10(y, P.seed, gid);
-            const uint32_t ut = uint32_t(y[0]);
-            tier = 0;
-#pragma unroll
-            for (int j = 0; j < kTiers - 1; ++j) tier += (j < K - 1 && tq[j] <= ut) ? 1 : 0;
-        }
-#pragma unroll
-        for (int p = 0; p < kTiers; ++p)
-            if (p < K) cnt[p] += __popcll(ballot(tier == p));
-    }
-    int off[kTiers];
-    int acc = 0;
-#pragma unroll
-    for (int p = 0; p < kTiers; ++p) { off[p] = acc; acc += cnt[p]; }
-    // pass 2: draw again and scatter in tier order (a lane's draws are its own)
-    for (uint32_t k0 = 0; k0 < n; k0 += 64) {
-        const uint32_t k = k0 + lane;
-        Draw d{~0u, 0};
-        if (k < n) d = draw_arrival(P, t, gid, k, tq, K);
-        int pos = 0;
-#pragma unroll
-        for (int p = 0; p < kTiers; ++p) {
-            if (p >= K) continue;
-            const unsigned long long b = ballot(d.tier == uint32_t(p));
-            if (d.tier == uint32_t(p)) pos = off[p] + __popcll(b & lanemask_lt());
-            off[p] += __popcll(b);
-        }
-        if (k < n) out[pos] = d.rec;
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1473,12 +1328,6 @@ int launch_init(const Params& p, hipStream_t stream)
     return int(hipGetLastError());
 }
 
-int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStream_t stream)
-{
-    const uint32_t items = p.R * nt;
-    hipLaunchKernelGGL(k_arrivals, dim3((items + 3) / 4), dim3(256), 0, stream, p, t0, nt);
-    return int(hipGetLastError());
-}
 
 namespace {
 

@@ -1,0 +1,24 @@
+// Wave-level helpers shared by the device sources of libmts (one wave of 64
+// lanes; gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace mts {
+namespace wave {
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+__device__ __forceinline__ unsigned long long ballot(bool p) { return __ballot(p); }
+__device__ __forceinline__ unsigned long long lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+__device__ __forceinline__ int ffs64(unsigned long long m) { return __ffsll(static_cast<long long>(m)) - 1; }
+
+__device__ __forceinline__ int rl(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ unsigned rlu(unsigned v, int l) { return unsigned(__builtin_amdgcn_readlane(int(v), l)); }
+__device__ __forceinline__ unsigned long long rl64(unsigned long long v, int l)
+{
+    const unsigned lo = rlu(unsigned(v), l), hi = rlu(unsigned(v >> 32), l);
+    return (static_cast<unsigned long long>(hi) << 32) | lo;
+}
+
+}  // namespace wave
+}  // namespace mts

@@ -209,6 +209,7 @@ class Scheduler:
         if getattr(self, "_h", None) and self._h.value:
             load_library().mts_destroy(self._h)
             self._h = ctypes.c_void_p(0)
+            self.buf = None
 
     def __del__(self):
         try:
