@@ -219,6 +219,15 @@ int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks);
  * device holds at once).  Queries the current device's occupancy. */
 int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks);
 
+/* Kernel timing with HIP events recorded on the launch stream (off by
+ * default; costs three events per chunk of ticks).  With on = 1, every later
+ * mts_step records the duration of each arrival-kernel and step-kernel
+ * launch.  mts_get_timing waits for the recorded launches, returns the
+ * summed durations in milliseconds and the number of step-kernel launches,
+ * and starts a new sum.  Any pointer may be NULL. */
+int mts_set_timing(mts_handle h, int on);
+int mts_get_timing(mts_handle h, double* step_ms, double* arrivals_ms, uint32_t* step_launches);
+
 /* Free the handle's host memory.  dev_buf stays with the caller. */
 void mts_destroy(mts_handle h);
 

@@ -30,6 +30,12 @@ struct mts_ctx {
     hipStream_t last = nullptr;
     std::vector<uint16_t> group_of;
     std::vector<uint32_t> group_K;
+    bool timing = false;
+    std::vector<hipEvent_t> ev;        // 3 per timed chunk: before arrivals, before step, after step
+    ~mts_ctx()
+    {
+        for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    }
 };
 
 namespace {
@@ -357,8 +363,17 @@ int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
     if (rc) return rc;
     for (uint64_t t = h->tick; t < end; t += h->chunk) {
         const uint32_t nt = uint32_t(std::min<uint64_t>(h->chunk, end - t));
+        hipEvent_t e[3] = {nullptr, nullptr, nullptr};
+        if (h->timing) {
+            for (hipEvent_t& x : e)
+                if (hipEventCreate(&x) != hipSuccess) return MTS_EDEVICE;
+            h->ev.insert(h->ev.end(), e, e + 3);
+            if (hipEventRecord(e[0], stream) != hipSuccess) return MTS_EDEVICE;
+        }
         if (launch_arrivals(p, t, nt, stream) != 0) return MTS_EDEVICE;
+        if (h->timing && hipEventRecord(e[1], stream) != hipSuccess) return MTS_EDEVICE;
         if (launch_step(p, t, nt, blocks, stream) != 0) return MTS_EDEVICE;
+        if (h->timing && hipEventRecord(e[2], stream) != hipSuccess) return MTS_EDEVICE;
     }
     h->tick = end;
     h->last = stream;
@@ -540,6 +555,35 @@ int mts_set_tick(mts_handle h, uint64_t tick)
     if (hipStreamSynchronize(h->last) != hipSuccess) return MTS_EDEVICE;
     h->tick = tick;
     return MTS_OK;
+}
+
+int mts_set_timing(mts_handle h, int on)
+{
+    if (!h || (on != 0 && on != 1)) return MTS_EINVAL;
+    h->timing = on == 1;
+    return MTS_OK;
+}
+
+int mts_get_timing(mts_handle h, double* step_ms, double* arrivals_ms, uint32_t* step_launches)
+{
+    if (!h) return MTS_EINVAL;
+    double st = 0.0, ar = 0.0;
+    int rc = MTS_OK;
+    for (size_t k = 0; k + 2 < h->ev.size() && rc == MTS_OK; k += 3) {
+        float a = 0.0f, b = 0.0f;
+        if (hipEventSynchronize(h->ev[k + 2]) != hipSuccess || hipEventElapsedTime(&a, h->ev[k], h->ev[k + 1]) != hipSuccess ||
+            hipEventElapsedTime(&b, h->ev[k + 1], h->ev[k + 2]) != hipSuccess)
+            rc = MTS_EDEVICE;
+        ar += a;
+        st += b;
+    }
+    const uint32_t n = uint32_t(h->ev.size() / 3);
+    for (hipEvent_t e : h->ev) (void)hipEventDestroy(e);
+    h->ev.clear();
+    if (step_ms) *step_ms = st;
+    if (arrivals_ms) *arrivals_ms = ar;
+    if (step_launches) *step_launches = n;
+    return rc;
 }
 
 void mts_destroy(mts_handle h) { delete h; }

@@ -74,7 +74,8 @@ class mts_state_view(ctypes.Structure):
 
 EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest",
             "mts_export_state", "mts_import_state", "mts_get_table", "mts_get_headroom",
-            "mts_tick", "mts_set_tick", "mts_set_launch", "mts_get_launch", "mts_destroy", "mts_strerror")
+            "mts_tick", "mts_set_tick", "mts_set_launch", "mts_get_launch", "mts_set_timing",
+            "mts_get_timing", "mts_destroy", "mts_strerror")
 
 _lib = None
 
@@ -104,12 +105,16 @@ def load_library(path=LIB_PATH):
     L.mts_set_tick.restype = ci
     L.mts_set_launch.argtypes = [vp, u32, u32]
     L.mts_get_launch.argtypes = [vp, ctypes.POINTER(u32), ctypes.POINTER(u32)]
+    L.mts_set_timing.argtypes = [vp, ci]
+    L.mts_get_timing.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                 ctypes.POINTER(u32)]
     L.mts_destroy.argtypes = [vp]
     L.mts_destroy.restype = None
     L.mts_strerror.argtypes = [ci]
     L.mts_strerror.restype = ctypes.c_char_p
     for f in ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest", "mts_export_state",
-              "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch", "mts_get_launch"):
+              "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch", "mts_get_launch",
+              "mts_set_timing", "mts_get_timing"):
         getattr(L, f).restype = ci
     _lib = L
     return L
@@ -230,6 +235,17 @@ class Scheduler:
 
     def set_launch(self, threads=0, blocks=0):
         _check("mts_set_launch", load_library().mts_set_launch(self._h, threads, blocks))
+
+    def set_timing(self, on=True):
+        """Record HIP events around every kernel launch of later steps."""
+        _check("mts_set_timing", load_library().mts_set_timing(self._h, 1 if on else 0))
+
+    def timing(self):
+        """(step-kernel ms, arrival-kernel ms, step-kernel launches) since the last call."""
+        st, ar, n = ctypes.c_double(0), ctypes.c_double(0), ctypes.c_uint32(0)
+        _check("mts_get_timing", load_library().mts_get_timing(self._h, ctypes.byref(st), ctypes.byref(ar),
+                                                               ctypes.byref(n)))
+        return st.value, ar.value, n.value
 
     def launch(self):
         """(threads, blocks) of the step kernel as mts_step launches it."""

@@ -225,3 +225,17 @@ def test_largest_instance_table():
     # I = 256 instances of S = 2048 slots: the widest replica this build serves
     cfg = scaled("wide", replicas_per_group=1)
     run_both(cfg, 60)
+
+
+def test_kernel_timing_counts_launches_and_changes_nothing():
+    cfg = scaled("sweep", replicas_per_group=1)
+    g = Scheduler(cfg)
+    g.set_timing(True)
+    g.step(700)
+    st, ar, n = g.timing()
+    assert n >= 1 and st > 0.0 and ar > 0.0
+    assert g.timing() == (0.0, 0.0, 0)
+    ref = Scheduler(cfg)
+    ref.step(700)
+    assert_same(g.export(), ref.export(), "timed vs untimed")
+    assert g.launch()[1] == min(g.R, g.launch()[1])
