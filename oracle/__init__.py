@@ -22,12 +22,13 @@ SRC = os.path.join(HERE, "mts_oracle.c")
 # broken build of the oracle
 LIB = os.environ.get("MTS_ORACLE_LIB") or os.path.join(HERE, "_build", "libmts_oracle.so")
 
-NSTAT = 88
+NSTAT = 96
 MAX_TIERS = 10
 STAT_FIELDS = ("arrived", "rejected", "dispatched", "admitted", "finished",
                "preempted", "qdelay_sum", "e2e_sum")
 STAT_GLOBALS = ("mig_queued", "mig_started", "mig_committed", "mig_aborted",
-                "run_slot_ticks", "wait_slot_ticks", "invariant_violations", "ticks")
+                "run_slot_ticks", "wait_slot_ticks", "invariant_violations", "ticks",
+                "scale_out_ticks", "scale_in_ticks", "drain_fallback_dispatches")
 
 _TIER_KIND = {"uniform": 0, "gauss": 1, "geometric": 2, "explicit": 3}
 _ARR_KIND = {"poisson": 0, "gamma_poisson": 1}
@@ -91,9 +92,9 @@ def lib():
         L.or_tick_now.argtypes = [vp]
         L.or_set_tick.argtypes = [vp, u64]
         L.or_export.restype = ctypes.c_int
-        L.or_export.argtypes = [vp, u32, u32] + [vp] * 8
+        L.or_export.argtypes = [vp, u32, u32] + [vp] * 9
         L.or_import.restype = ctypes.c_int
-        L.or_import.argtypes = [vp, u32, u32] + [vp] * 8
+        L.or_import.argtypes = [vp, u32, u32] + [vp] * 9
         L.or_digest.argtypes = [vp, vp]
         L.or_table.restype = ctypes.c_int
         L.or_table.argtypes = [vp, ctypes.c_int, u32, vp, u32, ctypes.POINTER(u32)]
@@ -104,6 +105,12 @@ def lib():
         L.or_check.restype = u64
         L.or_check.argtypes = [vp, u32]
         L.or_philox4x64_10.argtypes = [vp, vp, vp]
+        L.or_set_drain.restype = ctypes.c_int
+        L.or_set_drain.argtypes = [vp, u32, u32, ctypes.c_int]
+        L.or_freeness_normal.argtypes = [vp, u32, u32, ctypes.POINTER(ctypes.c_int64),
+                                         ctypes.POINTER(ctypes.c_int64)]
+        L.or_autoscale.restype = ctypes.c_int
+        L.or_autoscale.argtypes = [vp, u32, ctypes.POINTER(ctypes.c_int64)]
         _lib = L
     return _lib
 
@@ -219,9 +226,10 @@ class Oracle:
         return dict(meta=np.zeros(nr * IS, np.uint8), lr=np.zeros(nr * IS, np.uint32),
                     seq=np.zeros(nr * IS, np.uint32), tarr=np.zeros(nr * IS, np.uint32),
                     free=np.zeros(nr * self.I, np.int32), mig=np.zeros(nr * self.I * 4, np.int32),
-                    next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64))
+                    next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
+                    drain=np.zeros(nr * self.I, np.uint8))
 
-    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats")
+    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")
 
     def export(self, r0=0, nr=None):
         """Canonical state of local replicas [r0, r0+nr) as flat numpy arrays."""
@@ -261,6 +269,23 @@ class Oracle:
         out = np.zeros(MAX_TIERS, np.int32)
         lib().or_headroom(self._h, g, _ptr(out))
         return out
+
+    def set_drain(self, r, i, on=True):
+        """Mark instance i of local replica r as draining (or not)."""
+        if lib().or_set_drain(self._h, r, i, 1 if on else 0):
+            raise OracleError("set_drain range")
+
+    def freeness_normal(self, r, i):
+        """(num, den): F_normal = num / (256 den) blocks per running request, no headroom."""
+        n, d = ctypes.c_int64(0), ctypes.c_int64(0)
+        lib().or_freeness_normal(self._h, r, i, ctypes.byref(n), ctypes.byref(d))
+        return n.value, d.value
+
+    def autoscale(self, r=0):
+        """(signal, fixed-point sum): -1 scale out, +1 scale in, 0 none, for the current state."""
+        v = ctypes.c_int64(0)
+        sig = lib().or_autoscale(self._h, r, ctypes.byref(v))
+        return sig, v.value
 
     def freeness(self, r, i):
         num, den = ctypes.c_int64(0), ctypes.c_int64(0)

@@ -19,6 +19,16 @@
  *   D  arrival sampling and tier-ordered dispatch to argmax F.  (Section 3.4)
  *   E  migration: staged copies, then pairing of low-F sources with high-F
  *      destinations.  (Section 3.5, Fig. 4)
+ * Draining (Section 3.5, last paragraph; Section 3.4): a draining instance
+ * carries an infinite-virtual-usage sentinel, so its full freeness is minus
+ * infinity: it receives no dispatch while another instance can take the
+ * request, it is the first migration source and never a destination; when
+ * every instance with a free slot is draining, dispatch falls back to the
+ * least loaded of them (largest freeness without the sentinel).
+ * Auto-scaling (Section 3.6): every tick, after admission, the cluster
+ * average of the normal-priority freeness F_normal (Eq. 1 without headroom)
+ * is compared with the scale-out (-0.5) and scale-in (1.5) thresholds; the
+ * ticks that signal either are counted.
  * Every quantity is an integer.  The headroom H_p is quantised to 1/256 block
  * and freeness values are compared by exact 64-bit cross-multiplication.
  *
@@ -38,7 +48,7 @@
 #include <string.h>
 
 #define OR_MAX_TIERS 10
-#define OR_NSTAT 88
+#define OR_NSTAT 96
 #define OR_TABLE_CAP (1u << 17)
 
 /* per-tier counters: stats[tier * 8 + field] */
@@ -46,7 +56,8 @@ enum { F_ARRIVED = 0, F_REJECTED, F_DISPATCHED, F_ADMITTED, F_FINISHED,
        F_PREEMPTED, F_QDELAY, F_E2E };
 /* replica-wide counters */
 enum { S_MIG_QUEUED = 80, S_MIG_STARTED, S_MIG_COMMITTED, S_MIG_ABORTED,
-       S_RUN_SLOT_TICKS, S_WAIT_SLOT_TICKS, S_INVARIANT, S_TICKS };
+       S_RUN_SLOT_TICKS, S_WAIT_SLOT_TICKS, S_INVARIANT, S_TICKS,
+       S_SCALE_OUT, S_SCALE_IN, S_DRAIN_FALLBACK };
 
 enum { ST_EMPTY = 0, ST_WAITING = 1, ST_RUNNING = 2, ST_INBOUND = 3 };
 
@@ -98,6 +109,7 @@ typedef struct {
     slot_t *slot;     /* [I][S] */
     int64_t *freeb;   /* [I] free KV blocks */
     mig_t *mig;       /* [I] */
+    uint8_t *drain;   /* [I] 1: the instance is draining */
     uint32_t next_seq;
     uint64_t stats[OR_NSTAT];
     uint32_t n_arr, cap_arr;
@@ -364,6 +376,57 @@ static void freeness(const or_ctx *x, replica_t *rp, uint32_t i, int64_t *num, i
 /* F_a > F_b, exact */
 static int f_greater(int64_t na, int64_t da, int64_t nb, int64_t db) { return na * db > nb * da; }
 
+/* Normal-priority freeness (Section 3.4): Eq. 1 with the virtual usage of
+ * Eq. 2 but without any headroom term -- physical blocks of the running
+ * requests, blocks copied into inbound reservations, the head of line's
+ * demand.  num / (256 den) as for freeness(); the draining sentinel does not
+ * enter it. */
+static void freeness_normal(const or_ctx *x, replica_t *rp, uint32_t i, int64_t *num, int64_t *den)
+{
+    slot_t *sl = inst_slots(x, rp, i);
+    int64_t phys = 0, running = 0;
+    for (uint32_t s = 0; s < x->S; ++s) {
+        if (sl[s].st == ST_RUNNING) {
+            phys += blocks(x, sl[s].len);
+            running += 1;
+        }
+    }
+    for (uint32_t j = 0; j < x->I; ++j)
+        if (rp->mig[j].dst == (int32_t)i) phys += rp->mig[j].copied;
+    int h = head_of_line(x, rp, i);
+    int64_t demand = h >= 0 ? blocks(x, sl[h].len) : 0;
+    *num = 256 * ((int64_t)x->cfg.kv_blocks - phys - demand);
+    *den = running > 0 ? running : 1;
+}
+
+/* floor(a / b) for b > 0 */
+static int64_t floor_div(int64_t a, int64_t b)
+{
+    int64_t q = a / b;
+    if (a % b != 0 && a < 0) q -= 1;
+    return q;
+}
+
+/* Auto-scaling signal (Section 3.6) of the current state: the cluster
+ * average of F_normal against -1/2 (scale out) and 3/2 (scale in).  Each
+ * instance's F_normal = num / (256 den) enters in fixed point as
+ * floor(F_normal * 2^20); the sum over the instances is exact.  Returns -1
+ * (scale out), +1 (scale in) or 0; *sum receives the fixed-point sum. */
+static int autoscale_signal(const or_ctx *x, replica_t *rp, int64_t *sum)
+{
+    int64_t acc = 0;
+    for (uint32_t i = 0; i < x->I; ++i) {
+        int64_t num, den;
+        freeness_normal(x, rp, i, &num, &den);
+        acc += floor_div(num * 4096, den);  /* num * 2^20 / (256 den) */
+    }
+    *sum = acc;
+    const int64_t half = (int64_t)x->I << 19;  /* I * 2^20 / 2 */
+    if (acc < -half) return -1;
+    if (acc > 3 * half) return 1;
+    return 0;
+}
+
 /* ------------------------------------------------------------------ */
 /* Phase A: decode one token per running request                      */
 /* ------------------------------------------------------------------ */
@@ -487,12 +550,24 @@ static void phase_dispatch(or_ctx *x, replica_t *rp, uint64_t t)
         for (uint32_t k = 0; k < n; ++k) {
             const uint32_t *a = rp->arr + 3 * (size_t)k;
             if (a[0] != p) continue;
-            int best = -1;
+            /* argmax F over the instances with a free slot; a draining
+             * instance's F is minus infinity */
+            int best = -1, fallback = 0;
             for (uint32_t i = 0; i < x->I; ++i) {
-                if (nempty[i] == 0) continue;
+                if (nempty[i] == 0 || rp->drain[i]) continue;
                 if (best < 0 || f_greater(num[i], den[i], num[best], den[best])) best = (int)i;
             }
+            if (best < 0) {
+                /* every instance that can take the request is draining: the
+                 * least loaded of them, by freeness without the sentinel */
+                for (uint32_t j = 0; j < x->I; ++j) {
+                    if (nempty[j] == 0) continue;
+                    if (best < 0 || f_greater(num[j], den[j], num[best], den[best])) best = (int)j;
+                }
+                fallback = best >= 0;
+            }
             if (best < 0) { rp->stats[p * 8 + F_REJECTED]++; continue; }
+            if (fallback) rp->stats[S_DRAIN_FALLBACK]++;
             int s = lowest_empty(x, rp, (uint32_t)best);
             slot_t *sl = &inst_slots(x, rp, (uint32_t)best)[s];
             sl->st = ST_WAITING; sl->tier = (uint8_t)p; sl->admitted = 0; sl->migrating = 0;
@@ -562,20 +637,33 @@ static void phase_migrate(or_ctx *x, replica_t *rp, uint64_t t)
         freeness(x, rp, i, &num[i], &den[i]);
         if (!in_migration(x, rp, i)) L[n++] = i;
     }
-    /* insertion sort by (F ascending, index ascending) */
+    /* insertion sort by (F ascending, index ascending); a draining
+     * instance's F is minus infinity, so draining instances come first */
     for (uint32_t a = 1; a < n; ++a) {
         uint32_t v = L[a];
         int b = (int)a - 1;
-        while (b >= 0 && f_greater(num[L[b]], den[L[b]], num[v], den[v])) { L[b + 1] = L[b]; --b; }
+        for (; b >= 0; --b) {
+            uint32_t u = L[b];
+            int after = rp->drain[u] != rp->drain[v] ? !rp->drain[u]
+                      : (!rp->drain[u] && f_greater(num[u], den[u], num[v], den[v]));
+            if (!after) break;
+            L[b + 1] = L[b];
+        }
         L[b + 1] = v;
     }
     for (uint32_t k = 0; k < x->cfg.mig_max_pairs && k + 1 + k < n; ++k) {
         uint32_t src = L[k], dst = L[n - 1 - k];
-        if (num[src] >= 0) break;
-        /* F_dst - F_src >= theta_num / theta_den with F = num / (256 den) */
-        __int128 lhs = (__int128)x->cfg.theta_den * ((__int128)num[dst] * den[src] - (__int128)num[src] * den[dst]);
-        __int128 rhs = (__int128)x->cfg.theta_num * 256 * den[src] * den[dst];
-        if (lhs < rhs) break;
+        /* a draining destination means every instance left is draining */
+        if (rp->drain[dst]) break;
+        if (!rp->drain[src]) {
+            /* a draining source has F = minus infinity: overloaded, and any
+             * destination is more than theta freer */
+            if (num[src] >= 0) break;
+            /* F_dst - F_src >= theta_num / theta_den with F = num / (256 den) */
+            __int128 lhs = (__int128)x->cfg.theta_den * ((__int128)num[dst] * den[src] - (__int128)num[src] * den[dst]);
+            __int128 rhs = (__int128)x->cfg.theta_num * 256 * den[src] * den[dst];
+            if (lhs < rhs) break;
+        }
         int ds = lowest_empty(x, rp, dst);
         if (ds < 0) continue;
         slot_t *dsl = &inst_slots(x, rp, dst)[ds];
@@ -596,6 +684,9 @@ static void phase_migrate(or_ctx *x, replica_t *rp, uint64_t t)
                     (sl[s].tier == sl[c].tier && (bs < bc || (bs == bc && sl[s].seq > sl[c].seq))))
                     c = (int)s;
             }
+            /* nothing to move: only a draining source can be empty; its pair
+             * is skipped like one with a full destination */
+            if (c < 0) continue;
             clear_slot(dsl);
             dsl->st = ST_INBOUND;
             sl[c].migrating = 1;
@@ -658,6 +749,10 @@ static void tick_replica(or_ctx *x, replica_t *rp, uint64_t t, uint8_t *abort_pe
     phase_release(x, rp, abort_pending);
     phase_admit(x, rp, t);
     if (x->check) rp->stats[S_INVARIANT] += check_invariants(x, rp);
+    int64_t fsum;
+    int sig = autoscale_signal(x, rp, &fsum);
+    if (sig < 0) rp->stats[S_SCALE_OUT]++;
+    if (sig > 0) rp->stats[S_SCALE_IN]++;
     phase_dispatch(x, rp, t);
     phase_migrate(x, rp, t);
     uint64_t run = 0, wait = 0;
@@ -725,7 +820,8 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
         rp->slot = (slot_t *)calloc((size_t)x->I * x->S, sizeof(slot_t));
         rp->freeb = (int64_t *)calloc(x->I, sizeof(int64_t));
         rp->mig = (mig_t *)calloc(x->I, sizeof(mig_t));
-        if (!rp->slot || !rp->freeb || !rp->mig) { *err = -2; or_destroy(x); return NULL; }
+        rp->drain = (uint8_t *)calloc(x->I, 1);
+        if (!rp->slot || !rp->freeb || !rp->mig || !rp->drain) { *err = -2; or_destroy(x); return NULL; }
         for (uint32_t i = 0; i < x->I; ++i) { rp->freeb[i] = cfg->kv_blocks; rp->mig[i].dst = -1; }
     }
     *err = 0;
@@ -738,6 +834,7 @@ void or_destroy(or_ctx *x)
     if (x->rep)
         for (uint32_t r = 0; r < x->r_count; ++r) {
             free(x->rep[r].slot); free(x->rep[r].freeb); free(x->rep[r].mig); free(x->rep[r].arr);
+            free(x->rep[r].drain);
         }
     free(x->rep);
     if (x->tier_tab) for (uint32_t g = 0; g < x->cfg.n_groups; ++g) free(x->tier_tab[g].q);
@@ -765,7 +862,7 @@ void or_set_tick(or_ctx *x, uint64_t t) { x->tick = t; }
  * lr   = len | rem << 16
  * mig  = dst, src_slot, dst_slot, copied (dst = -1: none) */
 int or_export(const or_ctx *x, uint32_t r0, uint32_t nr, uint8_t *meta, uint32_t *lr, uint32_t *seq,
-              uint32_t *tarr, int32_t *freeb, int32_t *mig, uint32_t *next_seq, uint64_t *stats)
+              uint32_t *tarr, int32_t *freeb, int32_t *mig, uint32_t *next_seq, uint64_t *stats, uint8_t *drain)
 {
     if (r0 > x->r_count || nr > x->r_count - r0) return -1;
     size_t IS = (size_t)x->I * x->S;
@@ -783,6 +880,7 @@ int or_export(const or_ctx *x, uint32_t r0, uint32_t nr, uint8_t *meta, uint32_t
             freeb[(size_t)r * x->I + i] = (int32_t)rp->freeb[i];
             int32_t *m = mig + ((size_t)r * x->I + i) * 4;
             m[0] = rp->mig[i].dst; m[1] = rp->mig[i].src_slot; m[2] = rp->mig[i].dst_slot; m[3] = rp->mig[i].copied;
+            drain[(size_t)r * x->I + i] = rp->drain[i];
         }
         next_seq[r] = rp->next_seq;
         memcpy(stats + (size_t)r * OR_NSTAT, rp->stats, sizeof(rp->stats));
@@ -792,7 +890,7 @@ int or_export(const or_ctx *x, uint32_t r0, uint32_t nr, uint8_t *meta, uint32_t
 
 int or_import(or_ctx *x, uint32_t r0, uint32_t nr, const uint8_t *meta, const uint32_t *lr, const uint32_t *seq,
               const uint32_t *tarr, const int32_t *freeb, const int32_t *mig, const uint32_t *next_seq,
-              const uint64_t *stats)
+              const uint64_t *stats, const uint8_t *drain)
 {
     if (r0 > x->r_count || nr > x->r_count - r0) return -1;
     size_t IS = (size_t)x->I * x->S;
@@ -810,6 +908,7 @@ int or_import(or_ctx *x, uint32_t r0, uint32_t nr, const uint8_t *meta, const ui
             rp->freeb[i] = freeb[(size_t)r * x->I + i];
             const int32_t *m = mig + ((size_t)r * x->I + i) * 4;
             rp->mig[i].dst = m[0]; rp->mig[i].src_slot = m[1]; rp->mig[i].dst_slot = m[2]; rp->mig[i].copied = m[3];
+            rp->drain[i] = drain[(size_t)r * x->I + i] ? 1 : 0;
         }
         rp->next_seq = next_seq[r];
         memcpy(rp->stats, stats + (size_t)r * OR_NSTAT, sizeof(rp->stats));
@@ -847,7 +946,7 @@ void or_digest(const or_ctx *x, uint64_t *out)
             uint64_t p = mix64(g + 2 * ((uint64_t)IS + i) + 1);
             uint64_t c = (uint64_t)(uint32_t)rp->freeb[i] | (uint64_t)(uint32_t)m->dst << 32;
             uint64_t e = (uint64_t)(uint32_t)m->src_slot | (uint64_t)(uint32_t)m->dst_slot << 32;
-            d += mix64(p ^ c) + mix64(p ^ e) + mix64(p ^ (uint64_t)(uint32_t)m->copied);
+            d += mix64(p ^ c) + mix64(p ^ e) + mix64(p ^ ((uint64_t)(uint32_t)m->copied | (uint64_t)rp->drain[i] << 32));
         }
         out[r] = d;
     }
@@ -885,3 +984,23 @@ int or_last_arrivals(const or_ctx *x, uint32_t r, uint32_t *out, uint32_t cap)
 }
 
 uint64_t or_check(or_ctx *x, uint32_t r) { return check_invariants(x, &x->rep[r]); }
+
+/* draining flag of instance i of local replica r (a host decision: scale-in
+ * or graceful shutdown) */
+int or_set_drain(or_ctx *x, uint32_t r, uint32_t i, int on)
+{
+    if (r >= x->r_count || i >= x->I) return -1;
+    x->rep[r].drain[i] = on ? 1 : 0;
+    return 0;
+}
+
+void or_freeness_normal(const or_ctx *x, uint32_t r, uint32_t i, int64_t *num, int64_t *den)
+{
+    freeness_normal(x, &x->rep[r], i, num, den);
+}
+
+/* auto-scaling signal of the current state of local replica r */
+int or_autoscale(const or_ctx *x, uint32_t r, int64_t *sum)
+{
+    return autoscale_signal(x, &x->rep[r], sum);
+}

@@ -13,13 +13,23 @@ Eq. 3 instead of the oracle's repeated double multiplication.
 The arrivals of each tick are inputs: the caller passes the (tier, prompt,
 output) triples the oracle sampled, so this simulator covers the scheduling
 decisions and the accounting, not the sampler.
+
+Draining (Sections 3.4, 3.5) is modelled literally: a draining instance's
+full freeness is ``-inf`` (the infinite-usage sentinel), dispatch takes the
+argmax over the non-draining instances with room and, only when there is
+none, the least loaded draining one; pairing sorts draining instances first
+and never uses one as a destination.  The auto-scaling signal (Section 3.6)
+averages F_normal -- Eq. 1 with no headroom at all -- in fixed point with
+floor(F * 2^20) per instance.
 """
+import math
 from fractions import Fraction
 
 EMPTY, WAITING, RUNNING, INBOUND = 0, 1, 2, 3
-NSTAT = 88
+NSTAT = 96
 F_ARRIVED, F_REJECTED, F_DISPATCHED, F_ADMITTED, F_FINISHED, F_PREEMPTED, F_QDELAY, F_E2E = range(8)
 MIG_QUEUED, MIG_STARTED, MIG_COMMITTED, MIG_ABORTED, RUN_TICKS, WAIT_TICKS, INVARIANT, TICKS = range(80, 88)
+SCALE_OUT, SCALE_IN, DRAIN_FALLBACK = range(88, 91)
 
 
 def exact_headroom(h0, gamma, K, zero_lowest):
@@ -58,6 +68,7 @@ class ExactSim:
         self.slots = [[None] * self.S for _ in range(self.I)]
         self.free = [self.M] * self.I
         self.mig = [None] * self.I  # per source: [dst, src_slot, dst_slot, copied]
+        self.drain = [0] * self.I
         self.next_seq = 0
         self.stats = [0] * NSTAT
         self.t = 0
@@ -95,6 +106,29 @@ class ExactSim:
             if m is not None and m[0] == i:
                 V += m[3]
         return (self.M - V) / max(len(running), 1)
+
+    def freeness_normal(self, i):
+        """Eq. 1 without headroom: physical usage and head-of-line demand only."""
+        running = self.requests(i, RUNNING)
+        V = sum(self.blocks(r.len) for _, r in running)
+        h = self.hol(i)
+        if h is not None:
+            V += self.blocks(self.slots[i][h].len)
+        for m in self.mig:
+            if m is not None and m[0] == i:
+                V += m[3]
+        return Fraction(self.M - V, max(len(running), 1))
+
+    def full_freeness(self, i):
+        return -math.inf if self.drain[i] else self.freeness(i)
+
+    def autoscale(self):
+        total = sum(math.floor(self.freeness_normal(i) * 2**20) for i in range(self.I))
+        if total < -self.I * 2**19:
+            return -1, total
+        if total > 3 * self.I * 2**19:
+            return 1, total
+        return 0, total
 
     # -- the tick ---------------------------------------------------------
     def tick(self, arrivals):
@@ -149,6 +183,12 @@ class ExactSim:
                     r.admitted = 1
                     st[r.tier * 8 + F_ADMITTED] += 1
                     st[r.tier * 8 + F_QDELAY] += t - r.tarr
+        # C': auto-scaling signal
+        sig, _ = self.autoscale()
+        if sig < 0:
+            st[SCALE_OUT] += 1
+        elif sig > 0:
+            st[SCALE_IN] += 1
         # D: dispatch in (tier, seq) order to the freest instance with room
         seq0 = self.next_seq
         self.next_seq += len(arrivals)
@@ -157,10 +197,14 @@ class ExactSim:
         order = sorted(range(len(arrivals)), key=lambda k: (arrivals[k][0], k))
         for k in order:
             tier, prompt, out = arrivals[k]
-            cands = [i for i in range(self.I) if self.lowest_empty(i) is not None]
-            if not cands:
+            room = [i for i in range(self.I) if self.lowest_empty(i) is not None]
+            if not room:
                 st[tier * 8 + F_REJECTED] += 1
                 continue
+            cands = [i for i in room if not self.drain[i]]
+            if not cands:
+                cands = room  # all draining: the least loaded one
+                st[DRAIN_FALLBACK] += 1
             F = {i: self.freeness(i) for i in cands}
             best = max(F.values())
             i = min(j for j in cands if F[j] == best)
@@ -200,13 +244,15 @@ class ExactSim:
                     busy.add(i)
                     busy.add(m[0])
             L = [i for i in range(self.I) if i not in busy]
-            F = {i: self.freeness(i) for i in L}
+            F = {i: self.full_freeness(i) for i in L}
             L.sort(key=lambda i: (F[i], i))
             n = len(L)
             for k in range(n):
                 if k >= self.cfg["mig_max_pairs"] or k >= n - 1 - k:
                     break
                 src, dst = L[k], L[n - 1 - k]
+                if self.drain[dst]:
+                    break
                 if F[src] >= 0 or F[dst] - F[src] < self.theta:
                     break
                 ds = self.lowest_empty(dst)
@@ -219,6 +265,8 @@ class ExactSim:
                     st[MIG_QUEUED] += 1
                 else:
                     run = [(s, r) for s, r in self.requests(src, RUNNING) if not r.migrating]
+                    if not run:  # an empty draining source: nothing to move
+                        continue
                     c, rc = max(run, key=lambda sr: (sr[1].tier, -self.blocks(sr[1].len), sr[1].seq))
                     self.slots[dst][ds] = Request(INBOUND, 0, 0, 0, 0, 0)
                     rc.migrating = 1
@@ -254,4 +302,4 @@ class ExactSim:
         return dict(meta=meta, lr=lr, seq=seq, tarr=tarr,
                     free=np.array(self.free, np.int32), mig=mig,
                     next_seq=np.array([self.next_seq], np.uint32),
-                    stats=np.array(self.stats, np.uint64))
+                    stats=np.array(self.stats, np.uint64), drain=np.array(self.drain, np.uint8))

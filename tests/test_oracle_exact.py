@@ -5,7 +5,8 @@ K = 2 to Llumnix's binary headroom h / numHighPriorityRequests (Section 3.3);
 the exact simulator implements both literally (per-request headroom shares,
 exhaustive argmax over exact fractions).  Random small clusters, overloaded
 on purpose, drive every branch: preemption, rejection, queued moves and staged
-copies that commit or abort.
+copies that commit or abort; random draining schedules drive the sentinel,
+the all-draining fallback and the auto-scaling counters.
 """
 import random
 
@@ -17,11 +18,15 @@ from exact_sim import ExactSim
 from workloads import preset
 
 
-def run_pair(cfg, ticks):
+def run_pair(cfg, ticks, drain_plan=None):
+    """drain_plan: {tick: [(instance, on), ...]} applied before that tick."""
     K = cfg["groups"][0]["K"]
     o = oracle.Oracle(cfg, 0, 1, check=True)
     sim = ExactSim(cfg, K)
     for t in range(ticks):
+        for i, on in (drain_plan or {}).get(t, []):
+            o.set_drain(0, i, on)
+            sim.drain[i] = 1 if on else 0
         o.step(1)
         arrivals = [tuple(int(v) for v in a) for a in o.last_arrivals(0)]
         # dispatch order log invariant: (tier, seq) order is what both use;
@@ -88,7 +93,7 @@ def test_random_small_clusters(case):
 
 
 def test_random_clusters_reach_every_branch():
-    seen = np.zeros(88, np.int64)
+    seen = np.zeros(oracle.NSTAT, np.int64)
     for case in range(20):
         c = _random_cfg(random.Random(1000 + case))
         o = oracle.Oracle(c, 0, 1)
@@ -99,3 +104,45 @@ def test_random_clusters_reach_every_branch():
     assert per[:, 5].sum() > 0, "no preemption"
     for k in (80, 81, 82, 83):
         assert seen[k] > 0, "migration counter %d never moved" % k
+
+
+def _random_drain_plan(rng, I, ticks):
+    plan = {}
+    for _ in range(rng.randint(1, 6)):
+        t = rng.randrange(ticks)
+        plan.setdefault(t, []).append((rng.randrange(I), rng.random() < 0.7))
+    return plan
+
+
+@pytest.mark.parametrize("case", range(16))
+def test_random_clusters_with_draining(case):
+    rng = random.Random(5000 + case)
+    c = _random_cfg(rng)
+    plan = _random_drain_plan(rng, c["n_instances"], 250)
+    s = run_pair(c, 250, plan)
+    assert s[86] == 0
+
+
+def test_every_instance_draining_falls_back_to_the_least_loaded():
+    c = preset("tiny")
+    plan = {0: [(i, True) for i in range(4)], 200: [(1, False)], 300: [(1, True)]}
+    s = run_pair(c, 400, plan)
+    assert s[90] > 0  # dispatches went to draining instances
+    assert s[86] == 0
+
+
+def test_draining_branches_are_reached():
+    seen = np.zeros(oracle.NSTAT, np.int64)
+    for case in range(16):
+        rng = random.Random(5000 + case)
+        c = _random_cfg(rng)
+        plan = _random_drain_plan(rng, c["n_instances"], 250)
+        o = oracle.Oracle(c, 0, 1)
+        for t in range(250):
+            for i, on in plan.get(t, []):
+                o.set_drain(0, i, on)
+            o.step(1)
+        seen += o.export()["stats"].astype(np.int64)
+    assert seen[88] > 0, "no scale-out signal"
+    assert seen[89] > 0, "no scale-in signal"
+    assert seen[80] > 0 and seen[81] > 0

@@ -46,6 +46,18 @@ MUTATIONS = {
                              "(bs > bc || (bs == bc && sl[s].seq > sl[c].seq))")],
     # staged copy: commit one stage early
     "commit_early": [("if (m->copied < b) continue;", "if (m->copied + 1 < b) continue;")],
+    # Section 3.4: a draining instance still takes dispatches
+    "drain_dispatchable": [("if (nempty[i] == 0 || rp->drain[i]) continue;", "if (nempty[i] == 0) continue;")],
+    # Section 3.4: all-draining fallback picks the lowest index, not the least loaded
+    "drain_fallback_first": [("if (best < 0 || f_greater(num[j], den[j], num[best], den[best])) best = (int)j;",
+                              "if (best < 0) best = (int)j;")],
+    # Section 3.5: a draining instance accepted as a migration destination
+    "drain_destination": [("        if (rp->drain[dst]) break;\n", "")],
+    # Section 3.4: F_normal charged with tier-0 headroom
+    "fnormal_headroom": [("*num = 256 * ((int64_t)x->cfg.kv_blocks - phys - demand);",
+                          "*num = 256 * ((int64_t)x->cfg.kv_blocks - phys - demand) - x->Hq[rp->group][0];")],
+    # Section 3.6: scale-out at an average of exactly -0.5
+    "scale_out_inclusive": [("if (acc < -half) return -1;", "if (acc <= -half) return -1;")],
 }
 
 
@@ -63,6 +75,7 @@ def test_mutation_is_caught(name, tmp_path):
     env = dict(os.environ, MTS_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_drain_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_exact.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, "mutation %s survived every pin:\n%s" % (name, r.stdout[-2000:])

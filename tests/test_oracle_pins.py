@@ -295,7 +295,7 @@ def test_invariants_hold_every_tick(name, ticks):
     o = oracle.Oracle(c, 0, R, check=True)
     o.step(ticks)
     st = o.export()
-    stats = st["stats"].reshape(R, 88).astype(np.int64)
+    stats = st["stats"].reshape(R, oracle.NSTAT).astype(np.int64)
     assert np.all(stats[:, 86] == 0), "block/migration invariants violated"
     assert np.all(stats[:, 87] == ticks)
     I, S = c["n_instances"], c["slots_per_instance"]
