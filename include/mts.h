@@ -46,9 +46,9 @@
 extern "C" {
 #endif
 
-#define MTS_ABI_VERSION 1
+#define MTS_ABI_VERSION 2
 #define MTS_MAX_TIERS 10
-#define MTS_NSTAT 88
+#define MTS_NSTAT 96
 
 enum {
     MTS_OK = 0,
@@ -116,7 +116,8 @@ typedef struct mts_cfg {
 
 /* Counters summed over all replicas (mts_stats) or per replica
  * (mts_export_state).  Index layout of the raw arrays: per_tier[p][f] is
- * element p * 8 + f, the scalar counters follow at 80..87. */
+ * element p * 8 + f, the scalar counters follow at 80..90 in the order of
+ * the fields below, 91..95 are zero. */
 enum { MTS_F_ARRIVED = 0, MTS_F_REJECTED, MTS_F_DISPATCHED, MTS_F_ADMITTED,
        MTS_F_FINISHED, MTS_F_PREEMPTED, MTS_F_QDELAY_SUM, MTS_F_E2E_SUM };
 typedef struct mts_stats_t {
@@ -125,6 +126,14 @@ typedef struct mts_stats_t {
     uint64_t run_slot_ticks, wait_slot_ticks;  /* running / waiting requests summed over ticks */
     uint64_t invariant_violations;             /* device-side checks that failed */
     uint64_t ticks;                            /* replica-ticks executed */
+    /* Section 3.6: replica-ticks whose cluster-average normal-priority
+     * freeness (Eq. 1 without headroom, fixed point floor(F * 2^20) per
+     * instance) is below -1/2 (scale out) or above 3/2 (scale in); evaluated
+     * after admission */
+    uint64_t scale_out_ticks, scale_in_ticks;
+    /* Section 3.4: arrivals placed on a draining instance because every
+     * instance with a free slot was draining */
+    uint64_t drain_fallback_dispatches;
     uint64_t replicas;
     uint64_t digest;  /* wrapping sum of the per-replica state digests */
 } mts_stats_t;
@@ -139,6 +148,7 @@ typedef struct mts_stats_t {
  *   free[nr*I]    free KV blocks
  *   mig[nr*I*4]   per source instance: dst (-1 none), src slot, dst slot, blocks copied
  *   next_seq[nr], stats[nr*MTS_NSTAT]
+ *   drain[nr*I]   1 if the instance is draining (see mts_set_draining)
  * Empty slots are all-zero. */
 typedef struct mts_state_view {
     uint8_t* meta;
@@ -149,6 +159,7 @@ typedef struct mts_state_view {
     int32_t* mig;
     uint32_t* next_seq;
     uint64_t* stats;
+    uint8_t* drain;
 } mts_state_view;
 
 typedef struct mts_ctx* mts_handle;
@@ -189,6 +200,18 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
  * at the next mts_step.  MTS_EINVAL for indices out of range, a tier >= K, a
  * live request with len or rem 0, rem > 16383 or len + rem > 65535. */
 int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_view* in);
+
+/* Mark instances as draining (scale-in or graceful shutdown; Section 3.5):
+ * flags[nr*I], 1 = draining, for replicas [r0, r0 + nr).  A draining
+ * instance carries an infinite virtual-usage sentinel: its full freeness is
+ * minus infinity, so it receives no dispatch while any other instance has a
+ * free slot (when every instance with a free slot drains, the least loaded
+ * of them -- largest freeness without the sentinel -- takes the arrival),
+ * it is paired first as a migration source and never as a destination, and
+ * its requests leave by migration.  It keeps decoding and admitting its own
+ * queue.  Synchronous; applies from the next tick.  MTS_ERANGE for a
+ * replica range outside the handle, MTS_EINVAL for a flag other than 0 or 1. */
+int mts_set_draining(mts_handle h, uint32_t r0, uint32_t nr, const uint8_t* flags);
 
 /* The library's own tables, for comparison with an independent build:
  * which = 0 tier CDF of group g, 1 arrival count, 2 prompt length, 3 output

@@ -124,6 +124,7 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.tarr = o;     o = up256(o + N * 4);
     L.freeb = o;    o = up256(o + size_t(R) * I * 4);
     L.mig = o;      o = up256(o + size_t(R) * I * 16);
+    L.drain = o;    o = up256(o + size_t(R) * I);
     L.next_seq = o; o = up256(o + size_t(R) * 4);
     L.stats = o;    o = up256(o + size_t(R) * MTS_NSTAT * 8);
     L.digest = o;   o = up256(o + size_t(R) * 8);
@@ -180,6 +181,7 @@ Params make_params(const mts_ctx* h)
     p.tarr = reinterpret_cast<uint32_t*>(d + L.tarr);
     p.freeb = reinterpret_cast<int32_t*>(d + L.freeb);
     p.mig = reinterpret_cast<int32_t*>(d + L.mig);
+    p.drain = reinterpret_cast<uint8_t*>(d + L.drain);
     p.next_seq = reinterpret_cast<uint32_t*>(d + L.next_seq);
     p.stats = reinterpret_cast<unsigned long long*>(d + L.stats);
     p.digest = reinterpret_cast<unsigned long long*>(d + L.digest);
@@ -414,6 +416,9 @@ int mts_stats(mts_handle h, mts_stats_t* out)
     out->wait_slot_ticks = sum[kWaitSlotTicks];
     out->invariant_violations = sum[kInvariant];
     out->ticks = sum[kTicks];
+    out->scale_out_ticks = sum[kScaleOut];
+    out->scale_in_ticks = sum[kScaleIn];
+    out->drain_fallback_dispatches = sum[kDrainFallback];
     out->replicas = h->R;
     uint64_t d = 0;
     for (uint64_t v : dg) d += v;
@@ -460,6 +465,7 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     get(v->mig, L.mig + size_t(r0) * I * 16, size_t(nr) * I * 16);
     get(v->next_seq, L.next_seq + size_t(r0) * 4, size_t(nr) * 4);
     get(v->stats, L.stats + size_t(r0) * MTS_NSTAT * 8, size_t(nr) * MTS_NSTAT * 8);
+    get(v->drain, L.drain + size_t(r0) * I, size_t(nr) * I);
     return hip_rc(e);
 }
 
@@ -501,6 +507,7 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
                 return MTS_EINVAL;
             const int32_t f = v->free[size_t(r) * I + i];
             if (f < -int32_t(h->cfg.kv_blocks) || f > int32_t(h->cfg.kv_blocks)) return MTS_EINVAL;
+            if (v->drain && v->drain[size_t(r) * I + i] > 1) return MTS_EINVAL;
         }
     }
     const Layout& L = h->lay;
@@ -516,6 +523,24 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     put(L.mig + size_t(r0) * I * 16, v->mig, size_t(nr) * I * 16);
     put(L.next_seq + size_t(r0) * 4, v->next_seq, size_t(nr) * 4);
     put(L.stats + size_t(r0) * MTS_NSTAT * 8, v->stats, size_t(nr) * MTS_NSTAT * 8);
+    if (v->drain) {
+        put(L.drain + size_t(r0) * I, v->drain, size_t(nr) * I);
+    } else {
+        const std::vector<uint8_t> none(size_t(nr) * I, 0);
+        put(L.drain + size_t(r0) * I, none.data(), none.size());
+    }
+    return hip_rc(e);
+}
+
+int mts_set_draining(mts_handle h, uint32_t r0, uint32_t nr, const uint8_t* flags)
+{
+    if (!h || (!flags && nr)) return MTS_EINVAL;
+    if (r0 > h->R || nr > h->R - r0) return MTS_ERANGE;
+    const size_t n = size_t(nr) * h->I;
+    for (size_t k = 0; k < n; ++k)
+        if (flags[k] > 1) return MTS_EINVAL;
+    hipError_t e = hipStreamSynchronize(h->last);
+    if (e == hipSuccess && n) e = hipMemcpy(h->dev + h->lay.drain + size_t(r0) * h->I, flags, n, hipMemcpyHostToDevice);
     return hip_rc(e);
 }
 

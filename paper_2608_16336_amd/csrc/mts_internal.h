@@ -28,7 +28,8 @@ constexpr uint32_t kAdmitted = 0x40, kMigrating = 0x80;
 constexpr int kArrived = 0, kRejected = 1, kDispatched = 2, kAdmittedCnt = 3, kFinished = 4,
               kPreempted = 5, kQdelay = 6, kE2e = 7;
 constexpr int kMigQueued = 80, kMigStarted = 81, kMigCommitted = 82, kMigAborted = 83,
-              kRunSlotTicks = 84, kWaitSlotTicks = 85, kInvariant = 86, kTicks = 87;
+              kRunSlotTicks = 84, kWaitSlotTicks = 85, kInvariant = 86, kTicks = 87,
+              kScaleOut = 88, kScaleIn = 89, kDrainFallback = 90;
 
 struct Table {
     uint32_t base = 0;
@@ -49,7 +50,7 @@ struct Layout {
     size_t tier_q, hq, group_K, count_q, prompt_q, output_q, group_of;  // tables
     size_t count_g, prompt_g, output_g;                                 // guide tables
     size_t meta, hot, seq, tarr;                                        // [R][I][S]
-    size_t freeb, mig;                                                  // [R][I], [R][I][4]
+    size_t freeb, mig, drain;                                           // [R][I], [R][I][4], [R][I] u8
     size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
     size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
     size_t wheel;                                                       // [R][wsz][wcap]
@@ -85,6 +86,7 @@ struct Params {
     uint32_t* tarr;
     int32_t* freeb;
     int32_t* mig;
+    uint8_t* drain;
     uint32_t* next_seq;
     unsigned long long* stats;
     unsigned long long* digest;

@@ -47,7 +47,7 @@ __device__ __forceinline__ uint32_t wmid(uint32_t v) { return (v >> 16) & kFin; 
 // ---------------------------------------------------------------------------
 // LDS of one wave (one replica)
 // ---------------------------------------------------------------------------
-constexpr int kInts = 18;
+constexpr int kInts = 19;
 
 struct LdsLayout {
     uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, wc, wov, total;
@@ -89,6 +89,7 @@ struct Ctx {
     unsigned long long* holk;  // [I] head-of-line key tier << 32 | seq
     double* fd;                // [I] freeness num / den (exact order for S <= 2048)
     int *freeb, *B, *live, *nwait, *hols, *hold, *num, *den, *held, *inb, *tmask, *flags, *gtmp, *order, *pend;
+    int* drn;                  // [I] draining (infinite virtual-usage sentinel)
     unsigned *hwd, *hmt, *hta; // [I] head of line: slot word, meta, arrival tick
     unsigned* res;             // [I][RB] running requests per growth residue (u16 pairs)
     unsigned* tcnt;            // [I][10] running requests per tier (u16 pairs)
@@ -131,6 +132,7 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.gtmp = p; p += IM;
     C.order = p; p += IM;
     C.pend = p; p += IM;
+    C.drn = p; p += IM;
     C.hwd = reinterpret_cast<unsigned*>(p); p += IM;
     C.hmt = reinterpret_cast<unsigned*>(p); p += IM;
     C.hta = reinterpret_cast<unsigned*>(p); p += IM;
@@ -694,6 +696,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         for (int j = lane; j < kNstat; j += 64) C.stats[j] = P.stats[size_t(r) * kNstat + j];
         for (uint32_t i = lane; i < I; i += 64) {
             C.freeb[i] = P.freeb[size_t(r) * I + i];
+            C.drn[i] = P.drain[size_t(r) * I + i];
             for (int k = 0; k < 4; ++k) C.mig[4 * i + k] = P.mig[(size_t(r) * I + i) * 4 + k];
             C.inb[i] = 0;
             C.flags[i] = 0;
@@ -877,9 +880,25 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     for (unsigned long long m = bat[j]; m; m &= m - 1) admit_batch(C, 64 * j + ffs64(m), t, lane);
                 if (!ballot(any)) break;
             }
+            // auto-scaling signal (Section 3.6): the cluster average of the
+            // normal-priority freeness F_normal = (free - head-of-line demand) /
+            // max(B, 1) -- no headroom, no draining sentinel -- in fixed point,
+            // floor(F_normal * 2^20) per instance, against -1/2 and 3/2
+            long long fsum = 0;
             for (uint32_t i = lane; i < I; i += 64) {
                 set_f(C, int(i));
                 if (C.freeb[i] < 0 || C.freeb[i] + C.held[i] + C.inb[i] != int(C.M)) stat(C, kInvariant, 1);
+                const long long a = static_cast<long long>(C.freeb[i] - C.hold[i]) * 1048576ll;
+                const long long d = C.den[i];
+                long long q = a / d;
+                if (q * d != a && a < 0) q -= 1;
+                fsum += q;
+            }
+            fsum = static_cast<long long>(wsum64(static_cast<unsigned long long>(fsum)));
+            if (lane == 0) {
+                const long long half = static_cast<long long>(I) << 19;
+                if (fsum < -half) stat(C, kScaleOut, 1);
+                else if (fsum > 3 * half) stat(C, kScaleIn, 1);
             }
             wave_sync();
 
@@ -893,8 +912,10 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 const unsigned seq0 = next_seq;
                 next_seq += n;
                 // per-instance dispatch state in registers: lane l, register j <-> instance 64 j + l
+                // key: F of the instances that can take an arrival (minus infinity
+                // for a full instance and, in the first mode, for a draining one)
                 double key[IPL];
-                int live_r[IPL], fr_r[IPL], hs_r[IPL], den_r[IPL], dem_r[IPL], nadd[IPL], pend_r[IPL];
+                int live_r[IPL], fr_r[IPL], hs_r[IPL], den_r[IPL], dem_r[IPL], nadd[IPL], pend_r[IPL], drn_r[IPL];
                 unsigned long long hk_r[IPL];
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
@@ -912,14 +933,18 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         for (int p = 0; p < kTiers; ++p) hs += (tm >> p) & 1 ? C.hq[p] : 0;
                         hs_r[j] = hs;
                         hk_r[j] = C.hols[i] == kNoHol ? kNone : C.holk[i];
-                        key[j] = live_r[j] < int(S) ? C.fd[i] : -__builtin_inf();
+                        drn_r[j] = C.drn[i];
+                        key[j] = live_r[j] < int(S) && !drn_r[j] ? C.fd[i] : -__builtin_inf();
                     } else {
                         live_r[j] = int(S); fr_r[j] = 0; den_r[j] = 1; dem_r[j] = 0; hs_r[j] = 0; hk_r[j] = 0;
+                        drn_r[j] = 0;
                         key[j] = -__builtin_inf();
                     }
                 }
                 int cur = -1;
                 bool full = false;
+                bool drain_mode = false;  // every instance with room is draining (Section 3.4 fallback)
+                int nfall = 0;
                 for (uint32_t k0 = 0; k0 < n; k0 += 64) {
                     const uint32_t cn = n - k0 < 64 ? n - k0 : 64;
                     const unsigned long long a = k0 == 0 ? a0 : (lane < int(cn) ? rec[k0 + lane] : 0);
@@ -930,7 +955,22 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             double lb = key[0];
 #pragma unroll
                             for (int j = 1; j < IPL; ++j) lb = fmax(lb, key[j]);
-                            const double mv = wave_max_f64(lb);
+                            double mv = wave_max_f64(lb);
+                            if (mv == -__builtin_inf() && !drain_mode) {
+                                // no non-draining instance has a free slot: the least
+                                // loaded draining one (largest F without the sentinel);
+                                // slots only fill up, so the mode holds for the tick
+                                drain_mode = true;
+#pragma unroll
+                                for (int j = 0; j < IPL; ++j) {
+                                    const uint32_t i = lane + 64 * j;
+                                    key[j] = i < I && live_r[j] < int(S) && drn_r[j] ? C.fd[i] : -__builtin_inf();
+                                }
+                                lb = key[0];
+#pragma unroll
+                                for (int j = 1; j < IPL; ++j) lb = fmax(lb, key[j]);
+                                mv = wave_max_f64(lb);
+                            }
                             if (mv == -__builtin_inf()) { full = true; break; }
 #pragma unroll
                             for (int j = IPL - 1; j >= 0; --j) {
@@ -972,6 +1012,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         }
                         if (lane >= int(k) && lane < int(k) + m) tgt = cur;
                         if (becomes || nl >= int(S)) cur = -1;
+                        if (drain_mode) nfall += m;
                         k += uint32_t(m);
                     }
                     // write the dispatch state back for the slot assignment and later phases
@@ -1044,6 +1085,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     tier_stat(C, vt, tgt == -1 && lane < int(cn), kRejected, lane);
                     wave_sync();
                 }
+                if (lane == 0 && nfall) stat(C, kDrainFallback, unsigned(nfall));
             }
 
             if (tl + 1 < nt) {
@@ -1110,7 +1152,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             // ===================== E2: pairing on interval ticks =====================
             if (t % P.mig_interval == 0) {
                 bool neg = false;
-                for (uint32_t i = lane; i < I; i += 64) neg |= C.num[i] < 0;
+                for (uint32_t i = lane; i < I; i += 64) neg |= C.num[i] < 0 || C.drn[i];
                 if (ballot(neg)) {
                     for (uint32_t i = lane; i < I; i += 64) C.flags[i] &= ~kFlagBusy;
                     wave_sync();
@@ -1123,11 +1165,12 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     for (uint32_t i = lane; i < I; i += 64) {
                         if (C.flags[i] & kFlagBusy) continue;
                         ++mine;
-                        const double fi = C.fd[i];
+                        // a draining instance's F is minus infinity (sentinel)
+                        const double fi = C.drn[i] ? -__builtin_inf() : C.fd[i];
                         int rank = 0;
                         for (uint32_t j = 0; j < I; ++j) {
                             if (C.flags[j] & kFlagBusy) continue;
-                            const double fj = C.fd[j];
+                            const double fj = C.drn[j] ? -__builtin_inf() : C.fd[j];
                             rank += (fj < fi || (fj == fi && j < i)) ? 1 : 0;
                         }
                         C.order[rank] = int(i);
@@ -1136,11 +1179,17 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     wave_sync();
                     for (int k = 0; k < int(P.mig_max_pairs) && k < n2 - 1 - k; ++k) {
                         const int src = C.order[k], dst = C.order[n2 - 1 - k];
-                        if (C.num[src] >= 0) break;
-                        const long long lhs = (long long)P.theta_den *
-                            ((long long)C.num[dst] * C.den[src] - (long long)C.num[src] * C.den[dst]);
-                        const long long rhs = (long long)P.theta_num * 256 * C.den[src] * C.den[dst];
-                        if (lhs < rhs) break;
+                        // a draining destination: every instance left is draining
+                        if (C.drn[dst]) break;
+                        if (!C.drn[src]) {
+                            // (a draining source is overloaded and any destination is
+                            // more than theta freer)
+                            if (C.num[src] >= 0) break;
+                            const long long lhs = (long long)P.theta_den *
+                                ((long long)C.num[dst] * C.den[src] - (long long)C.num[src] * C.den[dst]);
+                            const long long rhs = (long long)P.theta_num * 256 * C.den[src] * C.den[dst];
+                            if (lhs < rhs) break;
+                        }
                         if (C.live[dst] >= int(S)) continue;
                         const int ds = lowest_empty(C, dst, lane);
                         if (ds < 0) continue;
@@ -1240,6 +1289,7 @@ __global__ void k_init(Params P)
     for (size_t j = t0; j < size_t(P.R) * P.I; j += stride) {
         P.freeb[j] = int32_t(P.M);
         P.mig[4 * j] = -1; P.mig[4 * j + 1] = 0; P.mig[4 * j + 2] = 0; P.mig[4 * j + 3] = 0;
+        P.drain[j] = 0;
     }
     for (size_t j = t0; j < size_t(P.R) * kNstat; j += stride) P.stats[j] = 0;
     for (size_t j = t0; j < P.R; j += stride) { P.next_seq[j] = 0; P.digest[j] = 0; }
@@ -1307,7 +1357,9 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t 
                                      (static_cast<unsigned long long>(uint32_t(m[0])) << 32);
         const unsigned long long e = static_cast<unsigned long long>(uint32_t(m[1])) |
                                      (static_cast<unsigned long long>(uint32_t(m[2])) << 32);
-        d += mix64(p ^ c) + mix64(p ^ e) + mix64(p ^ static_cast<unsigned long long>(uint32_t(m[3])));
+        const unsigned long long f = static_cast<unsigned long long>(uint32_t(m[3])) |
+                                     (static_cast<unsigned long long>(P.drain[size_t(r) * P.I + i]) << 32);
+        d += mix64(p ^ c) + mix64(p ^ e) + mix64(p ^ f);
     }
     for (int o = 32; o > 0; o >>= 1) d += __shfl_xor(d, o);
     if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = d;

@@ -12,9 +12,9 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libmts.so")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 MAX_TIERS = 10
-NSTAT = 88
+NSTAT = 96
 
 TIER_KINDS = {"uniform": 0, "gauss": 1, "geometric": 2, "explicit": 3}
 ARRIVAL_KINDS = {"poisson": 0, "gamma_poisson": 1}
@@ -64,18 +64,20 @@ class mts_stats_t(ctypes.Structure):
                 ("mig_committed", ctypes.c_uint64), ("mig_aborted", ctypes.c_uint64),
                 ("run_slot_ticks", ctypes.c_uint64), ("wait_slot_ticks", ctypes.c_uint64),
                 ("invariant_violations", ctypes.c_uint64), ("ticks", ctypes.c_uint64),
+                ("scale_out_ticks", ctypes.c_uint64), ("scale_in_ticks", ctypes.c_uint64),
+                ("drain_fallback_dispatches", ctypes.c_uint64),
                 ("replicas", ctypes.c_uint64), ("digest", ctypes.c_uint64)]
 
 
 class mts_state_view(ctypes.Structure):
     _fields_ = [(k, ctypes.c_void_p) for k in
-                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats")]
+                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")]
 
 
 EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest",
             "mts_export_state", "mts_import_state", "mts_get_table", "mts_get_headroom",
             "mts_tick", "mts_set_tick", "mts_set_launch", "mts_get_launch", "mts_set_timing",
-            "mts_get_timing", "mts_destroy", "mts_strerror")
+            "mts_get_timing", "mts_set_draining", "mts_destroy", "mts_strerror")
 
 _lib = None
 
@@ -106,6 +108,7 @@ def load_library(path=LIB_PATH):
     L.mts_set_launch.argtypes = [vp, u32, u32]
     L.mts_get_launch.argtypes = [vp, ctypes.POINTER(u32), ctypes.POINTER(u32)]
     L.mts_set_timing.argtypes = [vp, ci]
+    L.mts_set_draining.argtypes = [vp, u32, u32, vp]
     L.mts_get_timing.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                  ctypes.POINTER(u32)]
     L.mts_destroy.argtypes = [vp]
@@ -114,7 +117,7 @@ def load_library(path=LIB_PATH):
     L.mts_strerror.restype = ctypes.c_char_p
     for f in ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest", "mts_export_state",
               "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch", "mts_get_launch",
-              "mts_set_timing", "mts_get_timing"):
+              "mts_set_timing", "mts_get_timing", "mts_set_draining"):
         getattr(L, f).restype = ci
     _lib = L
     return L
@@ -191,7 +194,7 @@ def _stream_handle(stream):
 class Scheduler:
     """R replicas of a workload on one GPU, advanced by ``step``."""
 
-    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats")
+    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")
 
     def __init__(self, cfg, device="cuda", stream=None):
         import torch
@@ -262,8 +265,9 @@ class Scheduler:
         for p in range(MAX_TIERS):
             for f in range(8):
                 raw[p * 8 + f] = st.per_tier[p][f]
-        raw[80:88] = [st.mig_queued, st.mig_started, st.mig_committed, st.mig_aborted,
-                      st.run_slot_ticks, st.wait_slot_ticks, st.invariant_violations, st.ticks]
+        raw[80:91] = [st.mig_queued, st.mig_started, st.mig_committed, st.mig_aborted,
+                      st.run_slot_ticks, st.wait_slot_ticks, st.invariant_violations, st.ticks,
+                      st.scale_out_ticks, st.scale_in_ticks, st.drain_fallback_dispatches]
         return dict(raw=raw, replicas=st.replicas, digest=st.digest)
 
     def digests(self, r0=0, nr=None):
@@ -277,7 +281,16 @@ class Scheduler:
         return dict(meta=np.zeros(nr * IS, np.uint8), lr=np.zeros(nr * IS, np.uint32),
                     seq=np.zeros(nr * IS, np.uint32), tarr=np.zeros(nr * IS, np.uint32),
                     free=np.zeros(nr * self.I, np.int32), mig=np.zeros(nr * self.I * 4, np.int32),
-                    next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64))
+                    next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
+                    drain=np.zeros(nr * self.I, np.uint8))
+
+    def set_draining(self, flags, r0=0, nr=None):
+        """flags: 0/1 per (replica, instance) of replicas [r0, r0 + nr)."""
+        f = np.ascontiguousarray(flags, dtype=np.uint8).ravel()
+        nr = len(f) // self.I if nr is None else nr
+        if len(f) != nr * self.I:
+            raise ValueError("need %d flags" % (nr * self.I))
+        _check("mts_set_draining", load_library().mts_set_draining(self._h, r0, nr, f.ctypes.data))
 
     def export(self, r0=0, nr=None):
         nr = self.R - r0 if nr is None else nr

@@ -84,3 +84,34 @@ def test_full_sweep_is_deterministic_across_launch_shapes():
     db = b.digests()
     b.close()
     assert np.array_equal(da, db)
+
+
+def test_full_sweep_with_draining_instances():
+    # two instances of every replica drain from tick 200 on, one returns at 600
+    cfg = preset("sweep")
+    g = Scheduler(cfg)
+    R, I = g.R, cfg["n_instances"]
+    g.step(200)
+    flags = np.zeros((R, I), np.uint8)
+    flags[:, 3] = 1
+    flags[:, 17] = 1
+    g.set_draining(flags)
+    g.step(400)
+    flags[:, 17] = 0
+    g.set_draining(flags)
+    g.step(200)
+    torch.cuda.synchronize()
+    s = g.stats()
+    assert s["raw"][86] == 0
+    for r in sample_replicas(cfg, 3):
+        o = oracle.Oracle(cfg, r, 1)
+        o.step(200)
+        o.set_drain(0, 3, True)
+        o.set_drain(0, 17, True)
+        o.step(400)
+        o.set_drain(0, 17, False)
+        o.step(200)
+        assert_same(g.export(r, 1), o.export(), "sweep replica %d with draining" % r)
+        assert np.array_equal(g.digests(r, 1), o.digests())
+        o.close()
+    g.close()

@@ -239,3 +239,70 @@ def test_kernel_timing_counts_launches_and_changes_nothing():
     ref.step(700)
     assert_same(g.export(), ref.export(), "timed vs untimed")
     assert g.launch()[1] == min(g.R, g.launch()[1])
+
+
+# ---------------------------------------------------------------------------
+# draining (Sections 3.4, 3.5) and auto-scaling signals (Section 3.6)
+# ---------------------------------------------------------------------------
+def run_plan_both(cfg, ticks, plan, replicas=None):
+    """plan: {tick: [(instance, on), ...]} applied to every replica before that tick."""
+    g = Scheduler(cfg)
+    R, I = g.R, cfg["n_instances"]
+    picks = range(R) if replicas is None else replicas
+    orc = {r: oracle.Oracle(cfg, r, 1) for r in picks}
+    flags = np.zeros((R, I), np.uint8)
+    t = 0
+    for stop in sorted([k for k in plan if k < ticks]) + [ticks]:
+        if stop > t:
+            g.step(stop - t)
+            for o in orc.values():
+                o.step(stop - t)
+            t = stop
+        if stop in plan:
+            for i, on in plan[stop]:
+                flags[:, i] = 1 if on else 0
+                for o in orc.values():
+                    o.set_drain(0, i, on)
+            g.set_draining(flags)
+    for r, o in orc.items():
+        assert_same(g.export(r, 1), o.export(), "replica %d" % r)
+        assert np.array_equal(g.digests(r, 1), o.digests())
+    return g
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_clusters_with_draining(case):
+    from test_oracle_exact import _random_cfg as rc, _random_drain_plan
+    rng = random.Random(5000 + case)
+    cfg = rc(rng)
+    plan = _random_drain_plan(rng, cfg["n_instances"], 250)
+    cfg["groups"][0]["n_replicas"] = 3
+    run_plan_both(cfg, 250, plan)
+
+
+def test_every_instance_draining_falls_back_to_the_least_loaded():
+    cfg = preset("tiny")
+    plan = {0: [(i, True) for i in range(4)], 200: [(1, False)], 300: [(1, True)]}
+    g = run_plan_both(cfg, 400, plan)
+    s = g.stats()["raw"]
+    assert s[90] > 0 and s[86] == 0
+
+
+def test_drain_empties_an_instance_and_signals_are_counted():
+    cfg = scaled("enterprise", replicas_per_group=6)
+    plan = {100: [(0, True), (5, True)], 400: [(5, False)]}
+    g = run_plan_both(cfg, 600, plan)
+    s = g.stats()["raw"]
+    assert s[86] == 0 and s[88] + s[89] > 0
+    st = g.export()
+    S, I = cfg["slots_per_instance"], cfg["n_instances"]
+    meta = st["meta"].reshape(g.R, I, S)
+    assert not np.any(meta[:, 0, :] & 3), "a draining instance still holds requests"
+    assert np.all(st["drain"].reshape(g.R, I)[:, 0] == 1)
+
+
+def test_draining_flags_are_validated():
+    g = Scheduler(preset("tiny"))
+    with pytest.raises(MtsError) as e:
+        g.set_draining(np.array([0, 2, 0, 0], np.uint8))
+    assert e.value.code == -1
