@@ -24,6 +24,7 @@ LIB = os.environ.get("MTS_ORACLE_LIB") or os.path.join(HERE, "_build", "libmts_o
 
 NSTAT = 96
 MAX_TIERS = 10
+HBINS = 240  # latency histogram bins per (metric, tier)
 STAT_FIELDS = ("arrived", "rejected", "dispatched", "admitted", "finished",
                "preempted", "qdelay_sum", "e2e_sum")
 STAT_GLOBALS = ("mig_queued", "mig_started", "mig_committed", "mig_aborted",
@@ -111,6 +112,12 @@ def lib():
                                          ctypes.POINTER(ctypes.c_int64)]
         L.or_autoscale.restype = ctypes.c_int
         L.or_autoscale.argtypes = [vp, u32, ctypes.POINTER(ctypes.c_int64)]
+        L.or_hist_get.restype = ctypes.c_int
+        L.or_hist_get.argtypes = [vp, u32, u32, vp]
+        L.or_hist_set.restype = ctypes.c_int
+        L.or_hist_set.argtypes = [vp, u32, u32, vp]
+        L.or_hist_bin.restype = u32
+        L.or_hist_bin.argtypes = [u64]
         _lib = L
     return _lib
 
@@ -227,7 +234,8 @@ class Oracle:
                     seq=np.zeros(nr * IS, np.uint32), tarr=np.zeros(nr * IS, np.uint32),
                     free=np.zeros(nr * self.I, np.int32), mig=np.zeros(nr * self.I * 4, np.int32),
                     next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
-                    drain=np.zeros(nr * self.I, np.uint8))
+                    drain=np.zeros(nr * self.I, np.uint8),
+                    hist=np.zeros(nr * 2 * MAX_TIERS * HBINS, np.uint32))
 
     _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")
 
@@ -237,16 +245,18 @@ class Oracle:
             nr = self.r_count - r0
         a = self._arrays(nr)
         rc = lib().or_export(self._h, r0, nr, *[_ptr(a[k]) for k in self._ORDER])
-        if rc:
+        if rc or lib().or_hist_get(self._h, r0, nr, _ptr(a["hist"])):
             raise OracleError("export range")
         return a
 
     def import_state(self, a, r0=0, nr=None):
         if nr is None:
             nr = len(a["next_seq"])
-        b = {k: np.ascontiguousarray(a[k], dtype=v.dtype) for k, v in self._arrays(nr).items()}
+        b = {k: np.ascontiguousarray(a[k], dtype=v.dtype) if k in a else v for k, v in self._arrays(nr).items()}
+        if "hist" not in a:
+            b["hist"][:] = 0
         rc = lib().or_import(self._h, r0, nr, *[_ptr(b[k]) for k in self._ORDER])
-        if rc:
+        if rc or lib().or_hist_set(self._h, r0, nr, _ptr(b["hist"])):
             raise OracleError("import range")
 
     def digests(self):
@@ -308,3 +318,13 @@ def stat_index(tier, field):
 
 def stat_global(name):
     return 80 + STAT_GLOBALS.index(name)
+
+
+def hist_bin(v):
+    """The oracle's histogram bin of a latency of v ticks."""
+    return int(lib().or_hist_bin(int(v)))
+
+
+def hist_view(h, nr):
+    """Flat histogram array -> [replica][metric (0 queue delay, 1 end-to-end)][tier][bin]."""
+    return np.asarray(h).reshape(nr, 2, MAX_TIERS, HBINS)

@@ -25,6 +25,13 @@
  * request, it is the first migration source and never a destination; when
  * every instance with a free slot is draining, dispatch falls back to the
  * least loaded of them (largest freeness without the sentinel).
+ * Latency histograms (the per-tier latency distributions of Section 5.1,
+ * in ticks): each request's queue delay (arrival to first admission, the
+ * scheduler's share of the time to first token) and end-to-end time
+ * (arrival to the tick of its last token) is counted per tier in a
+ * log-linear histogram: values 0..15 have a bin each; a larger value v with
+ * 2^e <= v < 2^(e+1) falls into one of eight equal sub-ranges of that
+ * octave, bin 16 + 8 (e - 4) + (floor(v / 2^(e-3)) - 8), up to bin 239.
  * Auto-scaling (Section 3.6): every tick, after admission, the cluster
  * average of the normal-priority freeness F_normal (Eq. 1 without headroom)
  * is compared with the scale-out (-0.5) and scale-in (1.5) thresholds; the
@@ -50,6 +57,8 @@
 #define OR_MAX_TIERS 10
 #define OR_NSTAT 96
 #define OR_TABLE_CAP (1u << 17)
+#define OR_HBINS 240
+enum { H_QDELAY = 0, H_E2E = 1 };
 
 /* per-tier counters: stats[tier * 8 + field] */
 enum { F_ARRIVED = 0, F_REJECTED, F_DISPATCHED, F_ADMITTED, F_FINISHED,
@@ -112,6 +121,7 @@ typedef struct {
     uint8_t *drain;   /* [I] 1: the instance is draining */
     uint32_t next_seq;
     uint64_t stats[OR_NSTAT];
+    uint32_t (*hist)[OR_MAX_TIERS][OR_HBINS];  /* [2]: queue delay, end-to-end */
     uint32_t n_arr, cap_arr;
     uint32_t *arr;    /* last tick's arrivals in sampling order: tier, prompt, out */
 } replica_t;
@@ -427,6 +437,23 @@ static int autoscale_signal(const or_ctx *x, replica_t *rp, int64_t *sum)
     return 0;
 }
 
+/* Histogram bin of a latency of v ticks: v itself below 16; above, the
+ * octave [2^e, 2^(e+1)) is split into eight sub-ranges of width 2^(e-3). */
+static uint32_t hist_bin(uint64_t v)
+{
+    if (v < 16) return (uint32_t)v;
+    uint32_t e = 4;
+    while (e < 63 && (v >> (e + 1)) != 0) e++;
+    uint64_t sub = (v >> (e - 3)) - 8;  /* 0..7 */
+    uint64_t b = 16 + 8 * (uint64_t)(e - 4) + sub;
+    return b < OR_HBINS ? (uint32_t)b : OR_HBINS - 1;
+}
+
+static void hist_add(replica_t *rp, int which, uint32_t tier, uint64_t v)
+{
+    rp->hist[which][tier][hist_bin(v)]++;
+}
+
 /* ------------------------------------------------------------------ */
 /* Phase A: decode one token per running request                      */
 /* ------------------------------------------------------------------ */
@@ -465,6 +492,7 @@ static void phase_decode(or_ctx *x, replica_t *rp, uint64_t t, uint8_t *abort_pe
                 rp->freeb[i] += blocks(x, sl[s].len);
                 rp->stats[sl[s].tier * 8 + F_FINISHED]++;
                 rp->stats[sl[s].tier * 8 + F_E2E] += t - sl[s].tarr;
+                hist_add(rp, H_E2E, sl[s].tier, t - sl[s].tarr);
                 if (sl[s].migrating) abort_pending[i] = 1;
                 clear_slot(&sl[s]);
             }
@@ -504,6 +532,7 @@ static void phase_admit(or_ctx *x, replica_t *rp, uint64_t t)
                 sl[h].admitted = 1;
                 rp->stats[sl[h].tier * 8 + F_ADMITTED]++;
                 rp->stats[sl[h].tier * 8 + F_QDELAY] += t - sl[h].tarr;
+                hist_add(rp, H_QDELAY, sl[h].tier, t - sl[h].tarr);
             }
         }
     }
@@ -821,7 +850,8 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
         rp->freeb = (int64_t *)calloc(x->I, sizeof(int64_t));
         rp->mig = (mig_t *)calloc(x->I, sizeof(mig_t));
         rp->drain = (uint8_t *)calloc(x->I, 1);
-        if (!rp->slot || !rp->freeb || !rp->mig || !rp->drain) { *err = -2; or_destroy(x); return NULL; }
+        rp->hist = calloc(2, sizeof(*rp->hist));
+        if (!rp->slot || !rp->freeb || !rp->mig || !rp->drain || !rp->hist) { *err = -2; or_destroy(x); return NULL; }
         for (uint32_t i = 0; i < x->I; ++i) { rp->freeb[i] = cfg->kv_blocks; rp->mig[i].dst = -1; }
     }
     *err = 0;
@@ -834,7 +864,7 @@ void or_destroy(or_ctx *x)
     if (x->rep)
         for (uint32_t r = 0; r < x->r_count; ++r) {
             free(x->rep[r].slot); free(x->rep[r].freeb); free(x->rep[r].mig); free(x->rep[r].arr);
-            free(x->rep[r].drain);
+            free(x->rep[r].drain); free(x->rep[r].hist);
         }
     free(x->rep);
     if (x->tier_tab) for (uint32_t g = 0; g < x->cfg.n_groups; ++g) free(x->tier_tab[g].q);
@@ -1004,3 +1034,23 @@ int or_autoscale(const or_ctx *x, uint32_t r, int64_t *sum)
 {
     return autoscale_signal(x, &x->rep[r], sum);
 }
+
+/* latency histograms of local replicas [r0, r0 + nr): out[r][which][tier][bin],
+ * which 0 = queue delay, 1 = end-to-end; or_hist_set restores them */
+int or_hist_get(const or_ctx *x, uint32_t r0, uint32_t nr, uint32_t *out)
+{
+    if (r0 > x->r_count || nr > x->r_count - r0) return -1;
+    const size_t per = 2 * OR_MAX_TIERS * OR_HBINS;
+    for (uint32_t r = 0; r < nr; ++r) memcpy(out + r * per, x->rep[r0 + r].hist, per * sizeof(uint32_t));
+    return 0;
+}
+
+int or_hist_set(or_ctx *x, uint32_t r0, uint32_t nr, const uint32_t *in)
+{
+    if (r0 > x->r_count || nr > x->r_count - r0) return -1;
+    const size_t per = 2 * OR_MAX_TIERS * OR_HBINS;
+    for (uint32_t r = 0; r < nr; ++r) memcpy(x->rep[r0 + r].hist, in + r * per, per * sizeof(uint32_t));
+    return 0;
+}
+
+uint32_t or_hist_bin(uint64_t v) { return hist_bin(v); }

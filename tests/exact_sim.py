@@ -71,6 +71,9 @@ class ExactSim:
         self.drain = [0] * self.I
         self.next_seq = 0
         self.stats = [0] * NSTAT
+        # every request's (tier, queue delay) at its first admission and
+        # (tier, end-to-end time) at its finish, in ticks
+        self.latencies = ([], [])
         self.t = 0
 
     # -- helpers --------------------------------------------------------
@@ -158,6 +161,7 @@ class ExactSim:
                     self.free[i] += self.blocks(r.len)
                     st[r.tier * 8 + F_FINISHED] += 1
                     st[r.tier * 8 + F_E2E] += t - r.tarr
+                    self.latencies[1].append((r.tier, t - r.tarr))
                     if r.migrating:
                         aborted.add(i)
                     row[s] = None
@@ -183,6 +187,7 @@ class ExactSim:
                     r.admitted = 1
                     st[r.tier * 8 + F_ADMITTED] += 1
                     st[r.tier * 8 + F_QDELAY] += t - r.tarr
+                    self.latencies[0].append((r.tier, t - r.tarr))
         # C': auto-scaling signal
         sig, _ = self.autoscale()
         if sig < 0:

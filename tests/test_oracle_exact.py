@@ -39,6 +39,14 @@ def run_pair(cfg, ticks, drain_plan=None):
                 idx = np.nonzero(got[k] != want[k])[0][:8]
                 raise AssertionError("tick %d field %s differs at %s: oracle %s exact %s"
                                      % (t, k, idx, got[k][idx], want[k][idx]))
+    # latency histograms: the exact simulator's per-request latencies, binned
+    # with the oracle's bin function (itself pinned in test_oracle_pins.py)
+    want_h = np.zeros((2, oracle.MAX_TIERS, oracle.HBINS), np.uint32)
+    for m in (0, 1):
+        for tier, v in sim.latencies[m]:
+            want_h[m, tier, oracle.hist_bin(v)] += 1
+    got_h = oracle.hist_view(got["hist"], 1)[0]
+    assert np.array_equal(got_h, want_h), "latency histograms differ"
     return got["stats"].astype(np.int64)
 
 

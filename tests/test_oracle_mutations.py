@@ -58,6 +58,16 @@ MUTATIONS = {
                           "*num = 256 * ((int64_t)x->cfg.kv_blocks - phys - demand) - x->Hq[rp->group][0];")],
     # Section 3.6: scale-out at an average of exactly -0.5
     "scale_out_inclusive": [("if (acc < -half) return -1;", "if (acc <= -half) return -1;")],
+    # latency histograms: sub-ranges of a quarter octave instead of an eighth
+    "hist_quarter_octave": [("uint64_t sub = (v >> (e - 3)) - 8;  /* 0..7 */",
+                             "uint64_t sub = ((v >> (e - 2)) - 4) * 2;  /* 0..7 */")],
+    # latency histograms: queue delay counted again after every re-admission
+    "hist_qdelay_every_admission": [
+        ("                hist_add(rp, H_QDELAY, sl[h].tier, t - sl[h].tarr);\n            }",
+         "            }\n            hist_add(rp, H_QDELAY, sl[h].tier, t - sl[h].tarr);")],
+    # latency histograms: end-to-end time measured to the tick before the last token
+    "hist_e2e_early": [("hist_add(rp, H_E2E, sl[s].tier, t - sl[s].tarr);",
+                        "hist_add(rp, H_E2E, sl[s].tier, t - 1 - sl[s].tarr);")],
 }
 
 
@@ -76,6 +86,7 @@ def test_mutation_is_caught(name, tmp_path):
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_drain_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_hist_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_exact.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, "mutation %s survived every pin:\n%s" % (name, r.stdout[-2000:])
