@@ -46,9 +46,11 @@
 extern "C" {
 #endif
 
-#define MTS_ABI_VERSION 2
+#define MTS_ABI_VERSION 3
 #define MTS_MAX_TIERS 10
 #define MTS_NSTAT 96
+/* Latency histogram bins per (metric, tier); see mts_state_view.hist */
+#define MTS_HIST_BINS 240
 
 enum {
     MTS_OK = 0,
@@ -149,7 +151,19 @@ typedef struct mts_stats_t {
  *   mig[nr*I*4]   per source instance: dst (-1 none), src slot, dst slot, blocks copied
  *   next_seq[nr], stats[nr*MTS_NSTAT]
  *   drain[nr*I]   1 if the instance is draining (see mts_set_draining)
- * Empty slots are all-zero. */
+ *   hist[nr*2*MTS_MAX_TIERS*MTS_HIST_BINS]
+ *                 per-tier latency histograms in ticks (the per-tier latency
+ *                 distributions of Section 5.1), index
+ *                 ((r * 2 + metric) * MTS_MAX_TIERS + tier) * MTS_HIST_BINS + bin;
+ *                 metric 0 = queue delay (arrival to first admission, counted
+ *                 when admitted), 1 = end-to-end (arrival to the tick of the
+ *                 last token, counted at finish).  Bin of a value v: v for
+ *                 v < 16; otherwise, with 2^e <= v < 2^(e+1),
+ *                 16 + 8 (e - 4) + floor(v / 2^(e-3)) - 8 (eight equal
+ *                 sub-ranges per octave; at most 239)
+ * Empty slots are all-zero.  Export skips every NULL array.  Import needs
+ * every array but drain and hist; a NULL drain clears the flags, a NULL hist
+ * empties the histograms. */
 typedef struct mts_state_view {
     uint8_t* meta;
     uint32_t* lr;
@@ -160,6 +174,7 @@ typedef struct mts_state_view {
     uint32_t* next_seq;
     uint64_t* stats;
     uint8_t* drain;
+    uint32_t* hist;
 } mts_state_view;
 
 typedef struct mts_ctx* mts_handle;

@@ -125,6 +125,7 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.freeb = o;    o = up256(o + size_t(R) * I * 4);
     L.mig = o;      o = up256(o + size_t(R) * I * 16);
     L.drain = o;    o = up256(o + size_t(R) * I);
+    L.hist = o;     o = up256(o + size_t(R) * kHistPerReplica * 4);
     L.next_seq = o; o = up256(o + size_t(R) * 4);
     L.stats = o;    o = up256(o + size_t(R) * MTS_NSTAT * 8);
     L.digest = o;   o = up256(o + size_t(R) * 8);
@@ -182,6 +183,7 @@ Params make_params(const mts_ctx* h)
     p.freeb = reinterpret_cast<int32_t*>(d + L.freeb);
     p.mig = reinterpret_cast<int32_t*>(d + L.mig);
     p.drain = reinterpret_cast<uint8_t*>(d + L.drain);
+    p.hist = reinterpret_cast<uint32_t*>(d + L.hist);
     p.next_seq = reinterpret_cast<uint32_t*>(d + L.next_seq);
     p.stats = reinterpret_cast<unsigned long long*>(d + L.stats);
     p.digest = reinterpret_cast<unsigned long long*>(d + L.digest);
@@ -466,6 +468,7 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     get(v->next_seq, L.next_seq + size_t(r0) * 4, size_t(nr) * 4);
     get(v->stats, L.stats + size_t(r0) * MTS_NSTAT * 8, size_t(nr) * MTS_NSTAT * 8);
     get(v->drain, L.drain + size_t(r0) * I, size_t(nr) * I);
+    get(v->hist, L.hist + size_t(r0) * kHistPerReplica * 4, size_t(nr) * kHistPerReplica * 4);
     return hip_rc(e);
 }
 
@@ -528,6 +531,12 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     } else {
         const std::vector<uint8_t> none(size_t(nr) * I, 0);
         put(L.drain + size_t(r0) * I, none.data(), none.size());
+    }
+    const size_t hn = size_t(nr) * kHistPerReplica * 4;
+    if (v->hist) {
+        put(L.hist + size_t(r0) * kHistPerReplica * 4, v->hist, hn);
+    } else if (e == hipSuccess && hn) {
+        e = hipMemset(h->dev + L.hist + size_t(r0) * kHistPerReplica * 4, 0, hn);
     }
     return hip_rc(e);
 }

@@ -30,6 +30,9 @@ constexpr int kArrived = 0, kRejected = 1, kDispatched = 2, kAdmittedCnt = 3, kF
 constexpr int kMigQueued = 80, kMigStarted = 81, kMigCommitted = 82, kMigAborted = 83,
               kRunSlotTicks = 84, kWaitSlotTicks = 85, kInvariant = 86, kTicks = 87,
               kScaleOut = 88, kScaleIn = 89, kDrainFallback = 90;
+// latency histograms: queue delay and end-to-end, per tier
+constexpr int kHistQdelay = 0, kHistE2e = 1;
+constexpr size_t kHistPerReplica = size_t(2) * MTS_MAX_TIERS * MTS_HIST_BINS;
 
 struct Table {
     uint32_t base = 0;
@@ -51,6 +54,7 @@ struct Layout {
     size_t count_g, prompt_g, output_g;                                 // guide tables
     size_t meta, hot, seq, tarr;                                        // [R][I][S]
     size_t freeb, mig, drain;                                           // [R][I], [R][I][4], [R][I] u8
+    size_t hist;                                                        // [R][2][10][MTS_HIST_BINS] u32
     size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
     size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
     size_t wheel;                                                       // [R][wsz][wcap]
@@ -87,6 +91,7 @@ struct Params {
     int32_t* freeb;
     int32_t* mig;
     uint8_t* drain;
+    uint32_t* hist;
     uint32_t* next_seq;
     unsigned long long* stats;
     unsigned long long* digest;

@@ -96,8 +96,9 @@ struct Ctx {
     int* mig;                  // [I][4] dst, src slot, dst slot, copied
     unsigned* wc;              // [wsz / 2] entries filed per wheel bucket, two u16 per word
     unsigned* wov;             // [wsz / 32] bucket overflowed since its last visit
-    // HBM: timing wheel of this replica, slot arrays
+    // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
+    uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
     uint32_t wmask, wcap;
     uint32_t* hot;
     uint8_t* meta;
@@ -266,6 +267,20 @@ __device__ __forceinline__ void tier_inc(const Ctx& C, int i, int tier)
 }
 
 __device__ __forceinline__ void stat(const Ctx& C, int idx, unsigned long long v) { atomicAdd(&C.stats[idx], v); }
+
+// Latency histograms in ticks: a value below 16 has its own bin; a larger
+// value v with 2^e <= v < 2^(e+1) falls into one of eight sub-ranges of
+// width 2^(e-3), bin 16 + 8 (e - 4) + (v >> (e - 3)) - 8.
+__device__ __forceinline__ uint32_t hist_bin(uint32_t v)
+{
+    if (v < 16u) return v;
+    const uint32_t e = 31u - uint32_t(__builtin_clz(v));
+    return 8u * e - 24u + (v >> (e - 3u));
+}
+__device__ __forceinline__ void hist_add(const Ctx& C, int metric, int tier, uint32_t v)
+{
+    atomicAdd(&C.hist[(metric * kTiers + tier) * MTS_HIST_BINS + hist_bin(v)], 1u);
+}
 
 // lowest empty slot of instance i (one exists); uniform
 __device__ inline int lowest_empty(const Ctx& C, int i, int lane)
@@ -463,7 +478,9 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
             const uint32_t m = C.meta[b + s];
             const int tier = int((m >> 2) & 15u);
             stat(C, tier * 8 + kFinished, 1);
-            stat(C, tier * 8 + kE2e, t - C.tarr[b + s]);
+            const uint32_t e2e = t - C.tarr[b + s];
+            stat(C, tier * 8 + kE2e, e2e);
+            hist_add(C, kHistE2e, tier, e2e);
             c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
             if (m & kMigrating) ab = true;
@@ -543,6 +560,7 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
             const int tier = int((m >> 2) & 15u);
             stat(C, tier * 8 + kFinished, 1);
             stat(C, tier * 8 + kE2e, t - ta);
+            hist_add(C, kHistE2e, tier, t - ta);
             c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
             if (m & kMigrating) atomicOr(&C.flags[i], kFlagAbort);
@@ -648,6 +666,7 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
         if (!(meta & kAdmitted)) {
             stat(C, tier * 8 + kAdmittedCnt, 1);
             stat(C, tier * 8 + kQdelay, t - ta);
+            hist_add(C, kHistQdelay, tier, t - ta);
         }
         c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
         tier_inc(C, i, tier);
@@ -691,6 +710,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         const size_t rb = size_t(r) * I * S;
         C.hot = P.hot + rb; C.meta = P.meta + rb; C.seq = P.seq + rb; C.tarr = P.tarr + rb;
         C.wheel = P.wheel + size_t(r) * wsz * P.wcap;
+        C.hist = P.hist + size_t(r) * kHistPerReplica;
 
         // ---------------- prologue: derived per-instance state ----------------
         for (int j = lane; j < kNstat; j += 64) C.stats[j] = P.stats[size_t(r) * kNstat + j];
@@ -860,6 +880,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             if (!(m & kAdmitted)) {
                                 stat(C, tier * 8 + kAdmittedCnt, 1);
                                 stat(C, tier * 8 + kQdelay, t - C.hta[i]);
+                                hist_add(C, kHistQdelay, tier, t - C.hta[i]);
                             }
                             C.freeb[i] -= dem;
                             C.held[i] += dem;
@@ -1291,6 +1312,7 @@ __global__ void k_init(Params P)
         P.mig[4 * j] = -1; P.mig[4 * j + 1] = 0; P.mig[4 * j + 2] = 0; P.mig[4 * j + 3] = 0;
         P.drain[j] = 0;
     }
+    for (size_t j = t0; j < size_t(P.R) * kHistPerReplica; j += stride) P.hist[j] = 0;
     for (size_t j = t0; j < size_t(P.R) * kNstat; j += stride) P.stats[j] = 0;
     for (size_t j = t0; j < P.R; j += stride) { P.next_seq[j] = 0; P.digest[j] = 0; }
 }

@@ -12,9 +12,10 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libmts.so")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 MAX_TIERS = 10
 NSTAT = 96
+HIST_BINS = 240  # latency histogram bins per (metric, tier)
 
 TIER_KINDS = {"uniform": 0, "gauss": 1, "geometric": 2, "explicit": 3}
 ARRIVAL_KINDS = {"poisson": 0, "gamma_poisson": 1}
@@ -71,7 +72,7 @@ class mts_stats_t(ctypes.Structure):
 
 class mts_state_view(ctypes.Structure):
     _fields_ = [(k, ctypes.c_void_p) for k in
-                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")]
+                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist")]
 
 
 EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest",
@@ -194,7 +195,7 @@ def _stream_handle(stream):
 class Scheduler:
     """R replicas of a workload on one GPU, advanced by ``step``."""
 
-    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")
+    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist")
 
     def __init__(self, cfg, device="cuda", stream=None):
         import torch
@@ -282,7 +283,8 @@ class Scheduler:
                     seq=np.zeros(nr * IS, np.uint32), tarr=np.zeros(nr * IS, np.uint32),
                     free=np.zeros(nr * self.I, np.int32), mig=np.zeros(nr * self.I * 4, np.int32),
                     next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
-                    drain=np.zeros(nr * self.I, np.uint8))
+                    drain=np.zeros(nr * self.I, np.uint8),
+                    hist=np.zeros(nr * 2 * MAX_TIERS * HIST_BINS, np.uint32))
 
     def set_draining(self, flags, r0=0, nr=None):
         """flags: 0/1 per (replica, instance) of replicas [r0, r0 + nr)."""
@@ -299,10 +301,30 @@ class Scheduler:
         _check("mts_export_state", load_library().mts_export_state(self._h, r0, nr, ctypes.byref(v)))
         return a
 
+    def histograms(self, r0=0, nr=None):
+        """Latency histograms of replicas [r0, r0 + nr) as
+        [replica][metric (0 queue delay, 1 end-to-end)][tier][bin] (u32)."""
+        nr = self.R - r0 if nr is None else nr
+        h = np.zeros(nr * 2 * MAX_TIERS * HIST_BINS, np.uint32)
+        v = mts_state_view(*([None] * (len(self._ORDER) - 1) + [h.ctypes.data]))
+        _check("mts_export_state", load_library().mts_export_state(self._h, r0, nr, ctypes.byref(v)))
+        return h.reshape(nr, 2, MAX_TIERS, HIST_BINS)
+
+    def replica_stats(self, r0=0, nr=None):
+        """Per-replica counters of replicas [r0, r0 + nr) as [replica][MTS_NSTAT] (u64)."""
+        nr = self.R - r0 if nr is None else nr
+        st = np.zeros(nr * NSTAT, np.uint64)
+        ptrs = [None] * len(self._ORDER)
+        ptrs[self._ORDER.index("stats")] = st.ctypes.data
+        v = mts_state_view(*ptrs)
+        _check("mts_export_state", load_library().mts_export_state(self._h, r0, nr, ctypes.byref(v)))
+        return st.reshape(nr, NSTAT)
+
     def import_state(self, a, r0=0, nr=None):
+        """Overwrite replicas [r0, r0 + nr); a missing "drain" or "hist" clears them."""
         nr = len(a["next_seq"]) if nr is None else nr
-        b = {k: np.ascontiguousarray(a[k], dtype=v.dtype) for k, v in self._arrays(nr).items()}
-        v = mts_state_view(*[b[k].ctypes.data for k in self._ORDER])
+        b = {k: np.ascontiguousarray(a[k], dtype=v.dtype) for k, v in self._arrays(nr).items() if k in a}
+        v = mts_state_view(*[b[k].ctypes.data if k in b else None for k in self._ORDER])
         _check("mts_import_state", load_library().mts_import_state(self._h, r0, nr, ctypes.byref(v)))
 
     def table(self, which, g=0):

@@ -306,3 +306,43 @@ def test_draining_flags_are_validated():
     with pytest.raises(MtsError) as e:
         g.set_draining(np.array([0, 2, 0, 0], np.uint8))
     assert e.value.code == -1
+
+
+# ---------------------------------------------------------------------------
+# per-tier latency histograms (Section 5.1) and the differentiation study
+# ---------------------------------------------------------------------------
+def test_histogram_export_matches_full_export():
+    cfg = scaled("enterprise", replicas_per_group=8)
+    g = Scheduler(cfg)
+    g.step(500)
+    full = g.export()
+    h = g.histograms(2, 5)
+    assert np.array_equal(h.ravel(), full["hist"].reshape(g.R, -1)[2:7].ravel())
+    st = g.replica_stats()
+    assert np.array_equal(st.ravel(), full["stats"])
+    # bins add up to the admitted / finished counters per tier
+    hh = g.histograms().astype(np.int64)
+    s = st.astype(np.int64)
+    for p in range(4):
+        assert np.array_equal(hh[:, 0, p].sum(axis=1), s[:, p * 8 + 3])
+        assert np.array_equal(hh[:, 1, p].sum(axis=1), s[:, p * 8 + 4])
+    assert hh[:, 1].sum() > 0
+
+
+def test_differentiation_study_small_run_matches_oracle():
+    from paper_2608_16336_amd import study
+    cfg = study.sweep_cfg(30.0, 1, 500)
+    g = Scheduler(cfg)
+    g.step(500)
+    torch.cuda.synchronize()
+    for r in (0, 13, 29):  # K = 1 uniform, K = 5 gauss, K = 10 enterprise
+        o = oracle.Oracle(cfg, r, 1)
+        o.step(500)
+        assert_same(g.export(r, 1), o.export(), "study replica %d" % r)
+        o.close()
+    g.close()
+    _, rows = study.run(30.0, 1, 500)
+    assert len(rows) == 3 * sum(range(1, 11))
+    k1 = [x for x in rows if x["K"] == 1]
+    assert len(k1) == 3 and all(x["tier"] == 0 for x in k1)
+    assert sum(x["admitted"] for x in rows) > 0
