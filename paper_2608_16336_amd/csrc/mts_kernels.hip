@@ -36,7 +36,6 @@ constexpr int kTiers = MTS_MAX_TIERS;
 constexpr unsigned long long kNone = ~0ull;
 constexpr uint32_t kWaitW = 1u << 30, kRunW = 2u << 30, kInbW = 3u << 30;
 constexpr uint32_t kFin = 0x3FFFu;
-constexpr uint32_t kInf = 0xFFFFFFFFu;
 constexpr int kNoHol = -1, kHolUnknown = -2, kHolPending = -3;
 constexpr int kFlagAbort = 1, kFlagBusy = 2;
 
@@ -47,10 +46,12 @@ __device__ __forceinline__ uint32_t wmid(uint32_t v) { return (v >> 16) & kFin; 
 // ---------------------------------------------------------------------------
 // LDS of one wave (one replica)
 // ---------------------------------------------------------------------------
-constexpr int kInts = 19;
+constexpr int kInts = 20;
+// placements of the previous tick's dispatch kept in LDS (at most one wave's worth)
+constexpr int kLast = 64;
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, wc, wov, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, wc, wov, total;
 };
 
 __host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
@@ -74,6 +75,7 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     L.ints = o;  o += IM * kInts * 4;
     L.tcnt = o;  o += IM * kTiers / 2 * 4;
     L.mig = o;   o += IM * 16;
+    L.last = o;  o += kLast * 12 + 8;
     L.occ = o;   o += I * W * 8;
     L.res = o;   o += ((I * RB + 1) / 2) * 4;
     L.wc = o;    o += (wsz / 2) * 4;
@@ -90,6 +92,10 @@ struct Ctx {
     double* fd;                // [I] freeness num / den (exact order for S <= 2048)
     int *freeb, *B, *live, *nwait, *hols, *hold, *num, *den, *held, *inb, *tmask, *flags, *gtmp, *order, *pend;
     int* drn;                  // [I] draining (infinite virtual-usage sentinel)
+    int* frs;                  // [I] 1: every waiting request was placed by the previous tick's dispatch
+    unsigned *lw, *lsl, *lsq;  // [kLast] previous tick's placements in dispatch order: slot word,
+                               // instance << 16 | tier << 12 | slot, seq
+    int* lastn;                // number of those placements
     unsigned *hwd, *hmt, *hta; // [I] head of line: slot word, meta, arrival tick
     unsigned* res;             // [I][RB] running requests per growth residue (u16 pairs)
     unsigned* tcnt;            // [I][10] running requests per tier (u16 pairs)
@@ -134,12 +140,17 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.order = p; p += IM;
     C.pend = p; p += IM;
     C.drn = p; p += IM;
+    C.frs = p; p += IM;
     C.hwd = reinterpret_cast<unsigned*>(p); p += IM;
     C.hmt = reinterpret_cast<unsigned*>(p); p += IM;
     C.hta = reinterpret_cast<unsigned*>(p); p += IM;
     C.res = reinterpret_cast<unsigned*>(base + Y.res);
     C.tcnt = reinterpret_cast<unsigned*>(base + Y.tcnt);
     C.mig = reinterpret_cast<int*>(base + Y.mig);
+    C.lw = reinterpret_cast<unsigned*>(base + Y.last);
+    C.lsl = C.lw + kLast;
+    C.lsq = C.lsl + kLast;
+    C.lastn = reinterpret_cast<int*>(C.lsq + kLast);
     C.wc = reinterpret_cast<unsigned*>(base + Y.wc);
     C.wov = reinterpret_cast<unsigned*>(base + Y.wov);
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
@@ -355,6 +366,26 @@ __device__ __forceinline__ void wheel_put(const Ctx& C, uint32_t fin, int i, int
     }
 }
 
+// A running request that leaves its slot before its finish tick (preempted,
+// or moved out by a committed migration) loses its wheel entry: the entry is
+// overwritten with a tombstone, so every entry of the wheel names a distinct
+// running request.  A bucket that overflowed is rebuilt from the slots at its
+// visit and needs nothing here.  Uniform: the whole wave calls it.
+constexpr uint32_t kTomb = 0xFFFFFFFFu;
+__device__ inline void wheel_erase(const Ctx& C, uint32_t fin, int i, int s, int lane)
+{
+    const uint32_t b = fin & C.wmask;
+    if ((C.wov[b >> 5] >> (b & 31u)) & 1u) return;
+    const uint32_t n = (C.wc[b >> 1] >> ((b & 1u) * 16u)) & 0xFFFFu;
+    uint32_t* ent = C.wheel + size_t(b) * C.wcap;
+    const uint32_t key = (uint32_t(i) << 16) | uint32_t(s);
+    for (uint32_t e0 = 0; e0 < n; e0 += 64) {
+        const bool hit = e0 + lane < n && ent[e0 + lane] == key;
+        if (hit) ent[e0 + lane] = kTomb;
+        if (ballot(hit)) break;
+    }
+}
+
 // head of line of instance i from its slots: smallest (tier, seq) waiting
 __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
 {
@@ -417,11 +448,12 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
         const int vs = rl(bs, ffs64(ballot(bk == mx)));
         const int owner = vs & 63;
         int vb = 0, vg = 0, vt = 0, vr = 0, vm = 0;
-        uint32_t vw = 0, vmeta = 0, vta = 0;
+        uint32_t vw = 0, vmeta = 0, vta = 0, vfin = 0;
         if (lane == owner) {
             const uint32_t v = C.hot[b + vs];
             const uint32_t lenf = wlo(v), fin = fin_of(v, t);
             const uint32_t remb = fin - t + 1u, lenb = lenf - remb;
+            vfin = fin;
             vw = kWaitW | (remb << 16) | lenb;
             C.hot[b + vs] = vw;
             const uint32_t m = C.meta[b + vs];
@@ -436,12 +468,15 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
         }
         vb = rl(vb, owner); vg = rl(vg, owner); vt = rl(vt, owner); vr = rl(vr, owner); vm = rl(vm, owner);
         vw = rlu(vw, owner); vmeta = rlu(vmeta, owner); vta = rlu(vta, owner);
+        vfin = rlu(vfin, owner);
+        wheel_erase(C, vfin, i, vs, lane);
         fr += vb;
         G -= vg;
         if (lane == 0) {
             C.held[i] -= vb;
             C.B[i] -= 1;
             C.nwait[i] += 1;
+            C.frs[i] = 0;
             c16_dec(C.res, i * C.RB + vr);
             tier_dec(C, i, vt);
             stat(C, vt * 8 + kPreempted, 1);
@@ -538,19 +573,10 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
         uint32_t v = 0, m = 0, ta = 0;
         if (valid) { v = C.hot[idx]; m = C.meta[idx]; ta = C.tarr[idx]; }
         const uint32_t fin = fin_of(v, t);
-        bool f = valid && wst(v) == 2u && fin == t;
-        bool k = valid && wst(v) == 2u && fin != t && (fin & C.wmask) == bk;
-        // a slot listed twice in this batch is handled once
-        bool first = false;
-        for (unsigned long long pend = ballot(f || k); pend;) {
-            const int l = ffs64(pend);
-            const uint32_t ev = rlu(e, l);
-            const unsigned long long same = ballot((f || k) && e == ev);
-            if (lane == l) first = true;
-            pend &= ~same;
-        }
-        f = f && first;
-        k = k && first;
+        // entries name distinct running requests (wheel_erase); a tombstone
+        // or an entry whose slot changed since is dropped
+        const bool f = valid && wst(v) == 2u && fin == t;
+        const bool k = valid && wst(v) == 2u && fin != t && (fin & C.wmask) == bk;
         const unsigned long long km = ballot(k);
         if (k) ent[kept + __popcll(km & lanemask_lt())] = e;
         kept += __popcll(km);
@@ -592,6 +618,54 @@ __device__ __forceinline__ void tier_stat(const Ctx& C, int tier, bool f, int fi
         const int c = __popcll(fm & upto & ~((1ull << start) - 1ull));
         if (c) stat(C, tier * 8 + field, c);
     }
+}
+
+// Admits the longest prefix of w ranked waiting requests of instance i (lane
+// r holds the request of rank r: key, slot word, meta, arrival tick, slot)
+// whose summed demand fits the free blocks, and makes the next one the head
+// of line (Section 3.1: the local queue is served in priority order while
+// the head fits; the result equals admitting the head of line one request at
+// a time).
+__device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, int w, unsigned long long key,
+                                    uint32_t word, uint32_t meta, uint32_t ta, int slot)
+{
+    const size_t b = size_t(i) * C.S;
+    const int dem = lane < w ? blocks_of(wlo(word), C.shift) : 0;
+    const int pre = wscan(dem, lane);
+    const int fr = C.freeb[i];
+    const bool adm = lane < w && pre <= fr && uint32_t(slot) < C.S;
+    const int na = __popcll(ballot(adm));
+    if (adm) {
+        const uint32_t len = wlo(word), rem = wmid(word);
+        const uint32_t fin = t + rem;
+        const size_t hb = b + slot;
+        C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
+        C.meta[hb] = uint8_t((meta & ~3u) | kRunning | kAdmitted);
+        const int tier = int((meta >> 2) & 15u);
+        if (!(meta & kAdmitted)) {
+            stat(C, tier * 8 + kAdmittedCnt, 1);
+            stat(C, tier * 8 + kQdelay, t - ta);
+            hist_add(C, kHistQdelay, tier, t - ta);
+        }
+        c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
+        tier_inc(C, i, tier);
+        wheel_put(C, fin, i, slot);
+    }
+    const int used = na > 0 ? rl(pre, na - 1) : 0;
+    const int hs = rl(slot, na < w ? na : 0);
+    const unsigned long long hk = rl64(key, na < w ? na : 0);
+    const uint32_t hw = rlu(word, na < w ? na : 0), hm = rlu(meta, na < w ? na : 0),
+                   ht = rlu(ta, na < w ? na : 0);
+    if (lane == 0) {
+        C.freeb[i] -= used;
+        C.held[i] += used;
+        C.B[i] += na;
+        C.nwait[i] -= na;
+        if (w != C.nwait[i] + na) stat(C, kInvariant, 1);
+        if (na < w) set_hol(C, i, hs, hk, hw, hm, ht);
+        else clear_hol(C, i);
+    }
+    wave_sync();
 }
 
 // Admission of instance i when its head of line fits and 2..64 requests wait
@@ -651,42 +725,34 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
     ta = uint32_t(__builtin_amdgcn_ds_permute(ad, int(ta)));
     slot = __builtin_amdgcn_ds_permute(ad, slot);
     key = (static_cast<unsigned long long>(k_hi) << 32) | k_lo;
-    const int dem = lane < w ? blocks_of(wlo(word), C.shift) : 0;
-    const int pre = wscan(dem, lane);
-    const int fr = C.freeb[i];
-    const bool adm = lane < w && pre <= fr && uint32_t(slot) < C.S;
-    const int na = __popcll(ballot(adm));
-    if (adm) {
-        const uint32_t len = wlo(word), rem = wmid(word);
-        const uint32_t fin = t + rem;
-        const size_t hb = b + slot;
-        C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
-        C.meta[hb] = uint8_t((meta & ~3u) | kRunning | kAdmitted);
-        const int tier = int((meta >> 2) & 15u);
-        if (!(meta & kAdmitted)) {
-            stat(C, tier * 8 + kAdmittedCnt, 1);
-            stat(C, tier * 8 + kQdelay, t - ta);
-            hist_add(C, kHistQdelay, tier, t - ta);
-        }
-        c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
-        tier_inc(C, i, tier);
-        wheel_put(C, fin, i, slot);
+    admit_ranked(C, i, t, lane, w, key, word, meta, ta, slot);
+}
+
+// Admission of instance i whose waiting requests all arrived in the previous
+// tick (kept in LDS by the dispatch): they are listed in dispatch order,
+// which is (tier, seq) order, so no HBM read and no ranking is needed.
+__device__ inline void admit_fresh(const Ctx& C, int i, uint32_t t, int lane)
+{
+    const int n = *C.lastn;
+    const bool mine = lane < n && (C.lsl[lane] >> 16) == uint32_t(i);
+    const unsigned long long mm = ballot(mine);
+    const int w = __popcll(mm);
+    // lane r receives the list index of the r-th request of i
+    const int dest = mine ? __popcll(mm & lanemask_lt()) : w + __popcll(~mm & lanemask_lt());
+    const int idx = __builtin_amdgcn_ds_permute(dest * 4, lane);
+    unsigned long long key = kNone;
+    uint32_t word = 0, meta = 0, ta = 0;
+    int slot = 0;
+    if (lane < w) {
+        const uint32_t e = C.lsl[idx];
+        const uint32_t tier = (e >> 12) & 15u;
+        word = C.lw[idx];
+        meta = kWaiting | (tier << 2);
+        ta = t - 1u;
+        slot = int(e & 0xFFFu);
+        key = (static_cast<unsigned long long>(tier) << 32) | C.lsq[idx];
     }
-    const int used = na > 0 ? rl(pre, na - 1) : 0;
-    const int hs = rl(slot, na < w ? na : 0);
-    const unsigned long long hk = rl64(key, na < w ? na : 0);
-    const uint32_t hw = rlu(word, na < w ? na : 0), hm = rlu(meta, na < w ? na : 0),
-                   ht = rlu(ta, na < w ? na : 0);
-    if (lane == 0) {
-        C.freeb[i] -= used;
-        C.held[i] += used;
-        C.B[i] += na;
-        C.nwait[i] -= na;
-        if (w != C.nwait[i] + na) stat(C, kInvariant, 1);
-        if (na < w) set_hol(C, i, hs, hk, hw, hm, ht);
-        else clear_hol(C, i);
-    }
-    wave_sync();
+    admit_ranked(C, i, t, lane, w, key, word, meta, ta, slot);
 }
 
 // ---------------------------------------------------------------------------
@@ -721,8 +787,10 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             C.inb[i] = 0;
             C.flags[i] = 0;
             C.tmask[i] = 0;
+            C.frs[i] = 0;
         }
         for (uint32_t b = lane; b < wsz / 2; b += 64) C.wc[b] = 0;
+        if (lane == 0) *C.lastn = 0;
         for (uint32_t b = lane; b < (I * C.RB + 1) / 2; b += 64) C.res[b] = 0;
         for (uint32_t b = lane; b < (I * kTiers + 1) / 2; b += 64) C.tcnt[b] = 0;
         for (uint32_t b = lane; b < (wsz + 31) / 32; b += 64) C.wov[b] = 0;
@@ -856,15 +924,16 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         rescan_hol(C, 64 * j + ffs64(m), lane);
                 }
                 bool any = false;
-                unsigned long long bat[IPL];
+                unsigned long long bat[IPL], frm[IPL];
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
                     const uint32_t i = lane + 64 * j;
-                    bool batch = false;
+                    bool batch = false, fresh = false;
                     if (i < I && C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]) {
                         const int nw = C.nwait[i];
                         if (nw >= 2 && nw <= 64) {
-                            batch = true;
+                            fresh = C.frs[i] != 0;
+                            batch = !fresh;
                         } else {
                             // the only waiting request, or a queue longer than a wave:
                             // admit the head of line alone
@@ -894,11 +963,14 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         }
                     }
                     bat[j] = ballot(batch);
+                    frm[j] = ballot(fresh);
                 }
                 wave_sync();
 #pragma unroll
-                for (int j = 0; j < IPL; ++j)
+                for (int j = 0; j < IPL; ++j) {
+                    for (unsigned long long m = frm[j]; m; m &= m - 1) admit_fresh(C, 64 * j + ffs64(m), t, lane);
                     for (unsigned long long m = bat[j]; m; m &= m - 1) admit_batch(C, 64 * j + ffs64(m), t, lane);
+                }
                 if (!ballot(any)) break;
             }
             // auto-scaling signal (Section 3.6): the cluster average of the
@@ -909,10 +981,16 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             for (uint32_t i = lane; i < I; i += 64) {
                 set_f(C, int(i));
                 if (C.freeb[i] < 0 || C.freeb[i] + C.held[i] + C.inb[i] != int(C.M)) stat(C, kInvariant, 1);
+                // floor(x 2^20 / den): x 2^20 is exact in a double (|x| < 2^22) and
+                // the correctly rounded quotient never crosses an integer (the
+                // quotient sits at least 1/den >= 2^-11 from one, more than half
+                // an ulp below 2^42); the integer residual check keeps it exact
                 const long long a = static_cast<long long>(C.freeb[i] - C.hold[i]) * 1048576ll;
                 const long long d = C.den[i];
-                long long q = a / d;
-                if (q * d != a && a < 0) q -= 1;
+                long long q = static_cast<long long>(floor(double(a) / double(d)));
+                const long long rr = a - q * d;
+                if (rr < 0) q -= 1;
+                else if (rr >= d) q += 1;
                 fsum += q;
             }
             fsum = static_cast<long long>(wsum64(static_cast<unsigned long long>(fsum)));
@@ -924,6 +1002,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             wave_sync();
 
             // ===================== D: tier-ordered dispatch =====================
+            // an instance with an empty queue now holds, after this dispatch, only
+            // this tick's arrivals; they are recorded in LDS when they fit one wave
+            for (uint32_t i = lane; i < I; i += 64) C.frs[i] = C.nwait[i] == 0 && n <= uint32_t(kLast);
+            if (lane == 0) *C.lastn = 0;
+            wave_sync();
             if (n > 0) {
                 for (uint32_t k0 = 0; k0 < n; k0 += 64) {
                     const unsigned long long a = k0 == 0 ? a0 : (k0 + lane < n ? rec[k0 + lane] : 0);
@@ -1085,6 +1168,16 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         }
                     }
                     wave_sync();
+                    if (n <= uint32_t(kLast)) {
+                        const unsigned long long pm = ballot(tgt >= 0);
+                        if (tgt >= 0) {
+                            const int q = __popcll(pm & lanemask_lt());
+                            C.lw[q] = kWaitW | (uint32_t((a >> 16) & 0xFFFFu) << 16) | uint32_t(a & 0xFFFFu);
+                            C.lsl[q] = (uint32_t(tgt) << 16) | (uint32_t(tier) << 12) | uint32_t(s);
+                            C.lsq[q] = seq0 + unsigned(a >> 36);
+                        }
+                        if (lane == 0) *C.lastn = __popcll(pm);
+                    }
                     if (tgt >= 0) {
                         atomicOr(&C.occ[tgt * W + (s >> 6)], 1ull << (s & 63));
                         const size_t sb = size_t(tgt) * S + s;
@@ -1115,6 +1208,9 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             }
 
             // ===================== E1: staged copies =====================
+            // a commit leaves the source slot: its wheel entry (source slot in
+            // gtmp, finish tick in pend) is erased after the loop
+            for (uint32_t i = lane; i < I; i += 64) C.gtmp[i] = -1;
             for (uint32_t i = lane; i < I; i += 64) {
                 int* m = &C.mig[4 * i];
                 const int d = m[0];
@@ -1162,11 +1258,22 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     tier_dec(C, int(i), tier);
                     tier_inc(C, d, tier);
                     wheel_put(C, fin, d, m[2]);
+                    C.gtmp[i] = m[1];
+                    C.pend[i] = int(fin);
                     m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
                     stat(C, kMigCommitted, 1);
                     set_f(C, int(i));
                 }
                 set_f(C, d);
+            }
+            wave_sync();
+#pragma unroll
+            for (int j = 0; j < IPL; ++j) {
+                const uint32_t i0 = lane + 64 * j;
+                for (unsigned long long m = ballot(i0 < I && C.gtmp[i0] >= 0); m; m &= m - 1) {
+                    const int ii = 64 * j + ffs64(m);
+                    wheel_erase(C, uint32_t(C.pend[ii]), ii, C.gtmp[ii], lane);
+                }
             }
             wave_sync();
 
@@ -1227,6 +1334,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                 C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
                                 C.live[src] -= 1; C.nwait[src] -= 1;
                                 C.live[dst] += 1; C.nwait[dst] += 1;
+                                C.frs[src] = 0; C.frs[dst] = 0;
                                 const unsigned long long key = C.holk[src];
                                 if (C.hols[dst] == kNoHol || key < C.holk[dst]) set_hol(C, dst, ds, key, hw, hm, ht);
                                 if (C.nwait[src] == 0) clear_hol(C, src);
