@@ -540,10 +540,56 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
     wave_sync();
 }
 
-// Requests that emit their last token at tick t.  The bucket t mod wsz lists
-// every running request with fin = t (mod wsz): those with fin = t finish,
-// those with a later fin stay in the bucket (compacted in place), entries of
-// slots whose request has left are dropped.
+// One batch of up to 64 entries of bucket t mod wsz (lanes with inb set),
+// each with its slot's word, meta and arrival tick: entries with fin = t
+// finish, those with a later fin stay in the bucket (compacted in place from
+// position kept on; returns the new kept count), tombstones and entries whose
+// slot changed since are dropped.
+__device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint32_t* ent, uint32_t kept, bool inb,
+                                        uint32_t e, uint32_t v, uint32_t m, uint32_t ta)
+{
+    const uint32_t bk = t & C.wmask;
+    const int i = int(e >> 16), s = int(e & 0xFFFFu);
+    const bool valid = inb && uint32_t(i) < C.I && uint32_t(s) < C.S;
+    if (!valid) v = 0;
+    const uint32_t fin = fin_of(v, t);
+    // entries name distinct running requests (wheel_erase)
+    const bool f = valid && wst(v) == 2u && fin == t;
+    const bool k = valid && wst(v) == 2u && fin != t && (fin & C.wmask) == bk;
+    const unsigned long long km = ballot(k);
+    if (k) ent[kept + __popcll(km & lanemask_lt())] = e;
+    kept += __popcll(km);
+    if (f) {
+        const size_t idx = size_t(i) * C.S + s;
+        const uint32_t lenf = wlo(v);
+        const int bl = blocks_of(lenf, C.shift);
+        const int tier = int((m >> 2) & 15u);
+        stat(C, tier * 8 + kFinished, 1);
+        stat(C, tier * 8 + kE2e, t - ta);
+        hist_add(C, kHistE2e, tier, t - ta);
+        c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
+        tier_dec(C, i, tier);
+        if (m & kMigrating) atomicOr(&C.flags[i], kFlagAbort);
+        atomicAnd(&C.occ[i * C.W + (s >> 6)], ~(1ull << (s & 63)));
+        atomicAdd(&C.freeb[i], bl);
+        atomicSub(&C.held[i], bl);
+        atomicSub(&C.B[i], 1);
+        atomicSub(&C.live[i], 1);
+        C.hot[idx] = 0; C.meta[idx] = 0; C.seq[idx] = 0; C.tarr[idx] = 0;
+    }
+    wave_sync();
+    return kept;
+}
+
+__device__ __forceinline__ void wheel_set_count(const Ctx& C, uint32_t b, uint32_t n, int lane)
+{
+    const uint32_t sh = (b & 1u) * 16u;
+    if (lane == 0) C.wc[b >> 1] = (C.wc[b >> 1] & ~(0xFFFFu << sh)) | (n << sh);
+    wave_sync();
+}
+
+// Requests that emit their last token at tick t: the bucket t mod wsz lists
+// every running request with fin = t (mod wsz).
 __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
 {
     const uint32_t bk = t & C.wmask;
@@ -566,41 +612,16 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
     uint32_t* ent = C.wheel + size_t(bk) * C.wcap;
     uint32_t kept = 0;
     for (uint32_t e0 = 0; e0 < n; e0 += 64) {
-        const uint32_t e = e0 + lane < n ? ent[e0 + lane] : 0u;
+        const bool inb = e0 + lane < n;
+        const uint32_t e = inb ? ent[e0 + lane] : 0u;
         const int i = int(e >> 16), s = int(e & 0xFFFFu);
-        const bool valid = e0 + lane < n && uint32_t(i) < C.I && uint32_t(s) < C.S;
+        const bool valid = inb && uint32_t(i) < C.I && uint32_t(s) < C.S;
         const size_t idx = size_t(i) * C.S + s;
         uint32_t v = 0, m = 0, ta = 0;
         if (valid) { v = C.hot[idx]; m = C.meta[idx]; ta = C.tarr[idx]; }
-        const uint32_t fin = fin_of(v, t);
-        // entries name distinct running requests (wheel_erase); a tombstone
-        // or an entry whose slot changed since is dropped
-        const bool f = valid && wst(v) == 2u && fin == t;
-        const bool k = valid && wst(v) == 2u && fin != t && (fin & C.wmask) == bk;
-        const unsigned long long km = ballot(k);
-        if (k) ent[kept + __popcll(km & lanemask_lt())] = e;
-        kept += __popcll(km);
-        if (f) {
-            const uint32_t lenf = wlo(v);
-            const int bl = blocks_of(lenf, C.shift);
-            const int tier = int((m >> 2) & 15u);
-            stat(C, tier * 8 + kFinished, 1);
-            stat(C, tier * 8 + kE2e, t - ta);
-            hist_add(C, kHistE2e, tier, t - ta);
-            c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
-            tier_dec(C, i, tier);
-            if (m & kMigrating) atomicOr(&C.flags[i], kFlagAbort);
-            atomicAnd(&C.occ[i * C.W + (s >> 6)], ~(1ull << (s & 63)));
-            atomicAdd(&C.freeb[i], bl);
-            atomicSub(&C.held[i], bl);
-            atomicSub(&C.B[i], 1);
-            atomicSub(&C.live[i], 1);
-            C.hot[idx] = 0; C.meta[idx] = 0; C.seq[idx] = 0; C.tarr[idx] = 0;
-        }
-        wave_sync();
+        kept = finish_batch(C, t, lane, ent, kept, inb, e, v, m, ta);
     }
-    if (lane == 0) C.wc[bk >> 1] = (C.wc[bk >> 1] & ~(0xFFFFu << sh)) | (kept << sh);
-    wave_sync();
+    wheel_set_count(C, bk, kept, lane);
 }
 
 // Adds to stats[tier * 8 + field], for every tier, the number of lanes with f
@@ -861,6 +882,13 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         // the tick's count are never used
         const uint32_t lim = P.arr_cap < 64u ? P.arr_cap : 64u;
         uint32_t n_nx = cnts[0];
+        // the next tick's finish visit, loaded ahead: the entries of its bucket
+        // right after this tick's visit (pf_n of them; kNoPf: none), their
+        // slots' word, meta and arrival tick at the end of this tick.  It is
+        // used when the bucket still holds exactly pf_n entries and no
+        // preemption touched a slot in between; otherwise the visit loads again.
+        constexpr uint32_t kNoPf = 0xFFFFFFFFu;
+        uint32_t pf_n = kNoPf, pf_e = 0, pf_v = 0, pf_m = 0, pf_a = 0;
         unsigned long long a_nx = uint32_t(lane) < lim ? recs[lane] : 0ull;
         for (uint32_t tl = 0; tl < nt; ++tl) {
             const uint32_t t = t0u + tl;
@@ -883,16 +911,36 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 pre[j] = ballot(np);
             }
             wave_sync();
+            bool preempting = false;
 #pragma unroll
-            for (int j = 0; j < IPL; ++j)
+            for (int j = 0; j < IPL; ++j) {
+                preempting = preempting || pre[j] != 0;
                 for (unsigned long long m = pre[j]; m; m &= m - 1) preempt(C, 64 * j + ffs64(m), t, lane);
+            }
             for (uint32_t i = lane; i < I; i += 64) {
                 const int G = C.gtmp[i];
                 C.freeb[i] -= G;
                 C.held[i] += G;
             }
             wave_sync();
-            finish_tick(C, t, lane);
+            {
+                const uint32_t bk = t & C.wmask;
+                const uint32_t nb = (C.wc[bk >> 1] >> ((bk & 1u) * 16u)) & 0xFFFFu;
+                const bool ov = (C.wov[bk >> 5] >> (bk & 31u)) & 1u;
+                if (pf_n != kNoPf && !preempting && !ov && nb == pf_n) {
+                    uint32_t* ent = C.wheel + size_t(bk) * C.wcap;
+                    const uint32_t kept = finish_batch(C, t, lane, ent, 0, uint32_t(lane) < pf_n, pf_e, pf_v, pf_m, pf_a);
+                    wheel_set_count(C, bk, kept, lane);
+                } else {
+                    finish_tick(C, t, lane);
+                }
+                // entries of the next tick's bucket
+                const uint32_t b1 = (t + 1u) & C.wmask;
+                const uint32_t n1 = (C.wc[b1 >> 1] >> ((b1 & 1u) * 16u)) & 0xFFFFu;
+                const bool ov1 = (C.wov[b1 >> 5] >> (b1 & 31u)) & 1u;
+                pf_n = !ov1 && n1 <= 64u && b1 != bk ? n1 : kNoPf;
+                pf_e = pf_n != kNoPf && uint32_t(lane) < pf_n ? C.wheel[size_t(b1) * C.wcap + lane] : 0u;
+            }
             bool any_abort = false;
             for (uint32_t i = lane; i < I; i += 64) any_abort |= (C.flags[i] & kFlagAbort) != 0;
             // ===================== A2: release reservations of aborted migrations =====================
@@ -1382,6 +1430,15 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             }
 
             // ===================== end of tick =====================
+            // slots of the next tick's prefetched wheel entries
+            if (pf_n != kNoPf) {
+                const uint32_t pi = pf_e >> 16, ps = pf_e & 0xFFFFu;
+                const bool ok = uint32_t(lane) < pf_n && pi < I && ps < S;
+                const size_t idx = size_t(pi) * S + ps;
+                pf_v = ok ? C.hot[idx] : 0u;
+                pf_m = ok ? C.meta[idx] : 0u;
+                pf_a = ok ? C.tarr[idx] : 0u;
+            }
             for (uint32_t i = lane; i < I; i += 64) {
                 run_acc += unsigned(C.B[i]);
                 wait_acc += unsigned(C.nwait[i]);
