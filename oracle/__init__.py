@@ -35,6 +35,7 @@ _TIER_KIND = {"uniform": 0, "gauss": 1, "geometric": 2, "explicit": 3}
 _ARR_KIND = {"poisson": 0, "gamma_poisson": 1}
 _PROMPT_KIND = {"uniform_int": 0, "lognormal": 1}
 _OUT_KIND = {"geometric": 0, "pareto": 1}
+_POLICY = {"llumnix": 0, "infaas": 1}
 
 
 def build(force=True):
@@ -72,7 +73,10 @@ class _Cfg(ctypes.Structure):
                 ("out_min", ctypes.c_uint32), ("out_cap", ctypes.c_uint32),
                 ("seed", ctypes.c_uint64), ("replica_id_base", ctypes.c_uint64),
                 ("n_groups", ctypes.c_uint32), ("pad2", ctypes.c_uint32),
-                ("groups", ctypes.POINTER(_Group))]
+                ("groups", ctypes.POINTER(_Group)),
+                ("policy", ctypes.c_uint32), ("ewma_shift", ctypes.c_uint32),
+                ("alpha", ctypes.c_int32), ("beta", ctypes.c_int32), ("gamma_w", ctypes.c_int32),
+                ("pen_over", ctypes.c_uint32), ("pen_intf", ctypes.c_uint32), ("pad3", ctypes.c_uint32)]
 
 
 _lib = None
@@ -118,6 +122,10 @@ def lib():
         L.or_hist_set.argtypes = [vp, u32, u32, vp]
         L.or_hist_bin.restype = u32
         L.or_hist_bin.argtypes = [u64]
+        L.or_svc_get.restype = ctypes.c_int
+        L.or_svc_get.argtypes = [vp, u32, u32, vp]
+        L.or_svc_set.restype = ctypes.c_int
+        L.or_svc_set.argtypes = [vp, u32, u32, vp]
         _lib = L
     return _lib
 
@@ -182,6 +190,12 @@ def make_cfg(cfg):
     c.replica_id_base = cfg["replica_id_base"]
     c.n_groups = len(cfg["groups"])
     c.groups = groups
+    d = cfg.get("dispatch", {"policy": "llumnix"})
+    c.policy = _POLICY[d["policy"]]
+    if d["policy"] == "infaas":
+        c.alpha, c.beta, c.gamma_w = d["alpha"], d["beta"], d["gamma"]
+        c.pen_over, c.pen_intf = d["pen_overloaded"], d["pen_interfered"]
+        c.ewma_shift = d["ewma_shift"]
     return c, groups
 
 
@@ -235,7 +249,8 @@ class Oracle:
                     free=np.zeros(nr * self.I, np.int32), mig=np.zeros(nr * self.I * 4, np.int32),
                     next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
                     drain=np.zeros(nr * self.I, np.uint8),
-                    hist=np.zeros(nr * 2 * MAX_TIERS * HBINS, np.uint32))
+                    hist=np.zeros(nr * 2 * MAX_TIERS * HBINS, np.uint32),
+                    svc=np.zeros(nr * self.I, np.int64))
 
     _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")
 
@@ -245,7 +260,7 @@ class Oracle:
             nr = self.r_count - r0
         a = self._arrays(nr)
         rc = lib().or_export(self._h, r0, nr, *[_ptr(a[k]) for k in self._ORDER])
-        if rc or lib().or_hist_get(self._h, r0, nr, _ptr(a["hist"])):
+        if rc or lib().or_hist_get(self._h, r0, nr, _ptr(a["hist"])) or lib().or_svc_get(self._h, r0, nr, _ptr(a["svc"])):
             raise OracleError("export range")
         return a
 
@@ -253,10 +268,11 @@ class Oracle:
         if nr is None:
             nr = len(a["next_seq"])
         b = {k: np.ascontiguousarray(a[k], dtype=v.dtype) if k in a else v for k, v in self._arrays(nr).items()}
-        if "hist" not in a:
-            b["hist"][:] = 0
+        for k in ("hist", "svc"):
+            if k not in a:
+                b[k][:] = 0
         rc = lib().or_import(self._h, r0, nr, *[_ptr(b[k]) for k in self._ORDER])
-        if rc or lib().or_hist_set(self._h, r0, nr, _ptr(b["hist"])):
+        if rc or lib().or_hist_set(self._h, r0, nr, _ptr(b["hist"])) or lib().or_svc_set(self._h, r0, nr, _ptr(b["svc"])):
             raise OracleError("import range")
 
     def digests(self):

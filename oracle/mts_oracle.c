@@ -32,6 +32,16 @@
  * log-linear histogram: values 0..15 have a bin each; a larger value v with
  * 2^e <= v < 2^(e+1) falls into one of eight equal sub-ranges of that
  * octave, bin 16 + 8 (e - 4) + (floor(v / 2^(e-3)) - 8), up to bin 239.
+ * INFaaS-style dispatch (Section 3.7), the paper's comparison policy, as an
+ * alternative global scheduler: each arrival goes to the instance with the
+ * smallest cost alpha * q + beta * s + gamma * penalty, where q is the
+ * instance's queue depth (waiting requests, updated after every placement),
+ * s an exponentially weighted moving average of the end-to-end time of the
+ * requests that finished on it (updated once per tick, after admission,
+ * from that tick's finishes), and penalty the state penalty: OVERLOADED when
+ * its head of line does not fit its free blocks after admission, else
+ * INTERFERED when it preempted a request in this tick, else ACTIVE (0).  It
+ * keeps no freeness for dispatch and never migrates.
  * Auto-scaling (Section 3.6): every tick, after admission, the cluster
  * average of the normal-priority freeness F_normal (Eq. 1 without headroom)
  * is compared with the scale-out (-0.5) and scale-in (1.5) thresholds; the
@@ -97,7 +107,13 @@ typedef struct {
     uint64_t seed, replica_id_base;
     uint32_t n_groups, pad2;
     const or_group *groups;
+    /* global policy: 0 Llumnix freeness, 1 INFaaS cost */
+    uint32_t policy, ewma_shift;
+    int32_t alpha, beta, gamma_w;
+    uint32_t pen_over, pen_intf, pad3;
 } or_cfg;
+
+enum { POLICY_LLUMNIX = 0, POLICY_INFAAS = 1 };
 
 typedef struct {
     uint8_t st, tier, admitted, migrating;
@@ -119,6 +135,10 @@ typedef struct {
     int64_t *freeb;   /* [I] free KV blocks */
     mig_t *mig;       /* [I] */
     uint8_t *drain;   /* [I] 1: the instance is draining */
+    int64_t *svc;     /* [I] INFaaS service-time estimate, 1/256 tick */
+    uint64_t *fsum;   /* [I] end-to-end ticks of this tick's finishes */
+    uint32_t *fcnt;   /* [I] number of this tick's finishes */
+    uint8_t *intf;    /* [I] preempted a request in this tick */
     uint32_t next_seq;
     uint64_t stats[OR_NSTAT];
     uint32_t (*hist)[OR_MAX_TIERS][OR_HBINS];  /* [2]: queue delay, end-to-end */
@@ -482,6 +502,7 @@ static void phase_decode(or_ctx *x, replica_t *rp, uint64_t t, uint8_t *abort_pe
             if (sl[v].len % blk == 0) grow--;
             sl[v].st = ST_WAITING;
             rp->stats[sl[v].tier * 8 + F_PREEMPTED]++;
+            rp->intf[i] = 1;
         }
         rp->freeb[i] -= grow;
         for (uint32_t s = 0; s < x->S; ++s) {
@@ -493,6 +514,8 @@ static void phase_decode(or_ctx *x, replica_t *rp, uint64_t t, uint8_t *abort_pe
                 rp->stats[sl[s].tier * 8 + F_FINISHED]++;
                 rp->stats[sl[s].tier * 8 + F_E2E] += t - sl[s].tarr;
                 hist_add(rp, H_E2E, sl[s].tier, t - sl[s].tarr);
+                rp->fsum[i] += t - sl[s].tarr;
+                rp->fcnt[i] += 1;
                 if (sl[s].migrating) abort_pending[i] = 1;
                 clear_slot(&sl[s]);
             }
@@ -538,6 +561,50 @@ static void phase_admit(or_ctx *x, replica_t *rp, uint64_t t)
     }
 }
 
+/* floor(v / 2^k) */
+static int64_t floor_shift(int64_t v, uint32_t k)
+{
+    int64_t d = (int64_t)1 << k;
+    return floor_div(v, d);
+}
+
+/* INFaaS service-time estimate: once per tick, from the mean end-to-end
+ * time of the requests that finished on the instance in this tick,
+ * s += (256 * sum / count - s) / 2^shift, both divisions rounded down. */
+static void infaas_update_estimates(const or_ctx *x, replica_t *rp)
+{
+    for (uint32_t i = 0; i < x->I; ++i) {
+        if (rp->fcnt[i] == 0) continue;
+        int64_t mean = (int64_t)((rp->fsum[i] * 256) / rp->fcnt[i]);
+        rp->svc[i] += floor_shift(mean - rp->svc[i], x->cfg.ewma_shift);
+    }
+}
+
+/* the INFaaS state penalty of instance i in ticks: OVERLOADED (head of line
+ * does not fit the free blocks) before INTERFERED (preempted this tick) */
+static int64_t infaas_penalty(const or_ctx *x, replica_t *rp, uint32_t i)
+{
+    int h = head_of_line(x, rp, i);
+    if (h >= 0 && (int64_t)blocks(x, inst_slots(x, rp, i)[h].len) > rp->freeb[i]) return x->cfg.pen_over;
+    if (rp->intf[i]) return x->cfg.pen_intf;
+    return 0;
+}
+
+static int64_t waiting_count(const or_ctx *x, replica_t *rp, uint32_t i)
+{
+    slot_t *sl = inst_slots(x, rp, i);
+    int64_t q = 0;
+    for (uint32_t s = 0; s < x->S; ++s) q += sl[s].st == ST_WAITING;
+    return q;
+}
+
+/* cost in 1/256 tick: alpha * q + beta * s + gamma * penalty */
+static int64_t infaas_cost(const or_ctx *x, replica_t *rp, uint32_t i, int64_t pen)
+{
+    return (int64_t)x->cfg.alpha * waiting_count(x, rp, i) * 256 + (int64_t)x->cfg.beta * rp->svc[i] +
+           (int64_t)x->cfg.gamma_w * pen * 256;
+}
+
 /* ------------------------------------------------------------------ */
 /* Phase D: sample this tick's arrivals, dispatch in tier order        */
 /* ------------------------------------------------------------------ */
@@ -568,7 +635,11 @@ static void phase_dispatch(or_ctx *x, replica_t *rp, uint64_t t)
     int64_t *num = (int64_t *)malloc(x->I * sizeof(int64_t));
     int64_t *den = (int64_t *)malloc(x->I * sizeof(int64_t));
     int64_t *nempty = (int64_t *)malloc(x->I * sizeof(int64_t));
+    int64_t *pen = (int64_t *)malloc(x->I * sizeof(int64_t));
+    const int infaas = x->cfg.policy == POLICY_INFAAS;
     for (uint32_t i = 0; i < x->I; ++i) {
+        /* INFaaS states are taken once per tick, before dispatch */
+        pen[i] = infaas ? infaas_penalty(x, rp, i) : 0;
         freeness(x, rp, i, &num[i], &den[i]);
         nempty[i] = 0;
         slot_t *sl = inst_slots(x, rp, i);
@@ -579,21 +650,35 @@ static void phase_dispatch(or_ctx *x, replica_t *rp, uint64_t t)
         for (uint32_t k = 0; k < n; ++k) {
             const uint32_t *a = rp->arr + 3 * (size_t)k;
             if (a[0] != p) continue;
-            /* argmax F over the instances with a free slot; a draining
-             * instance's F is minus infinity */
             int best = -1, fallback = 0;
-            for (uint32_t i = 0; i < x->I; ++i) {
-                if (nempty[i] == 0 || rp->drain[i]) continue;
-                if (best < 0 || f_greater(num[i], den[i], num[best], den[best])) best = (int)i;
-            }
-            if (best < 0) {
-                /* every instance that can take the request is draining: the
-                 * least loaded of them, by freeness without the sentinel */
-                for (uint32_t j = 0; j < x->I; ++j) {
-                    if (nempty[j] == 0) continue;
-                    if (best < 0 || f_greater(num[j], den[j], num[best], den[best])) best = (int)j;
+            if (infaas) {
+                /* argmin cost over the non-draining instances with a free
+                 * slot, else over every instance with a free slot */
+                for (int pass = 0; pass < 2 && best < 0; ++pass) {
+                    int64_t bc = 0;
+                    for (uint32_t i = 0; i < x->I; ++i) {
+                        if (nempty[i] == 0 || (pass == 0 && rp->drain[i])) continue;
+                        int64_t c = infaas_cost(x, rp, i, pen[i]);
+                        if (best < 0 || c < bc) { best = (int)i; bc = c; }
+                    }
+                    fallback = pass == 1 && best >= 0;
                 }
-                fallback = best >= 0;
+            } else {
+                /* argmax F over the instances with a free slot; a draining
+                 * instance's F is minus infinity */
+                for (uint32_t i = 0; i < x->I; ++i) {
+                    if (nempty[i] == 0 || rp->drain[i]) continue;
+                    if (best < 0 || f_greater(num[i], den[i], num[best], den[best])) best = (int)i;
+                }
+                if (best < 0) {
+                    /* every instance that can take the request is draining: the
+                     * least loaded of them, by freeness without the sentinel */
+                    for (uint32_t j = 0; j < x->I; ++j) {
+                        if (nempty[j] == 0) continue;
+                        if (best < 0 || f_greater(num[j], den[j], num[best], den[best])) best = (int)j;
+                    }
+                    fallback = best >= 0;
+                }
             }
             if (best < 0) { rp->stats[p * 8 + F_REJECTED]++; continue; }
             if (fallback) rp->stats[S_DRAIN_FALLBACK]++;
@@ -606,7 +691,7 @@ static void phase_dispatch(or_ctx *x, replica_t *rp, uint64_t t)
             freeness(x, rp, (uint32_t)best, &num[best], &den[best]);
         }
     }
-    free(num); free(den); free(nempty);
+    free(num); free(den); free(nempty); free(pen);
 }
 
 /* ------------------------------------------------------------------ */
@@ -657,7 +742,7 @@ static void phase_migrate(or_ctx *x, replica_t *rp, uint64_t t)
      * its head-of-line queued request if it has one (moved at once, no KV
      * state), else its lowest-priority running request with the smallest
      * KV footprint, which starts a staged copy. */
-    if (t % x->cfg.mig_interval != 0) return;
+    if (t % x->cfg.mig_interval != 0 || x->cfg.policy == POLICY_INFAAS) return;
     uint32_t I = x->I, n = 0;
     uint32_t *L = (uint32_t *)malloc(I * sizeof(uint32_t));
     int64_t *num = (int64_t *)malloc(I * sizeof(int64_t));
@@ -774,9 +859,13 @@ static uint64_t check_invariants(const or_ctx *x, replica_t *rp)
 static void tick_replica(or_ctx *x, replica_t *rp, uint64_t t, uint8_t *abort_pending)
 {
     memset(abort_pending, 0, x->I);
+    memset(rp->fsum, 0, x->I * sizeof(uint64_t));
+    memset(rp->fcnt, 0, x->I * sizeof(uint32_t));
+    memset(rp->intf, 0, x->I);
     phase_decode(x, rp, t, abort_pending);
     phase_release(x, rp, abort_pending);
     phase_admit(x, rp, t);
+    if (x->cfg.policy == POLICY_INFAAS) infaas_update_estimates(x, rp);
     if (x->check) rp->stats[S_INVARIANT] += check_invariants(x, rp);
     int64_t fsum;
     int sig = autoscale_signal(x, rp, &fsum);
@@ -806,6 +895,7 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
     if (!cfg || cfg->n_groups == 0 || !cfg->groups) return NULL;
     if (cfg->n_instances == 0 || cfg->n_instances > 256 || cfg->slots == 0) return NULL;
     if (cfg->block_tokens == 0 || cfg->kv_blocks == 0 || cfg->mig_interval == 0 || cfg->theta_den <= 0) return NULL;
+    if (cfg->policy > POLICY_INFAAS || cfg->ewma_shift > 16) return NULL;
     uint32_t R = 0;
     for (uint32_t g = 0; g < cfg->n_groups; ++g) {
         if (cfg->groups[g].K == 0 || cfg->groups[g].K > OR_MAX_TIERS) return NULL;
@@ -851,7 +941,13 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
         rp->mig = (mig_t *)calloc(x->I, sizeof(mig_t));
         rp->drain = (uint8_t *)calloc(x->I, 1);
         rp->hist = calloc(2, sizeof(*rp->hist));
-        if (!rp->slot || !rp->freeb || !rp->mig || !rp->drain || !rp->hist) { *err = -2; or_destroy(x); return NULL; }
+        rp->svc = (int64_t *)calloc(x->I, sizeof(int64_t));
+        rp->fsum = (uint64_t *)calloc(x->I, sizeof(uint64_t));
+        rp->fcnt = (uint32_t *)calloc(x->I, sizeof(uint32_t));
+        rp->intf = (uint8_t *)calloc(x->I, 1);
+        if (!rp->slot || !rp->freeb || !rp->mig || !rp->drain || !rp->hist || !rp->svc || !rp->fsum || !rp->fcnt || !rp->intf) {
+            *err = -2; or_destroy(x); return NULL;
+        }
         for (uint32_t i = 0; i < x->I; ++i) { rp->freeb[i] = cfg->kv_blocks; rp->mig[i].dst = -1; }
     }
     *err = 0;
@@ -865,6 +961,7 @@ void or_destroy(or_ctx *x)
         for (uint32_t r = 0; r < x->r_count; ++r) {
             free(x->rep[r].slot); free(x->rep[r].freeb); free(x->rep[r].mig); free(x->rep[r].arr);
             free(x->rep[r].drain); free(x->rep[r].hist);
+            free(x->rep[r].svc); free(x->rep[r].fsum); free(x->rep[r].fcnt); free(x->rep[r].intf);
         }
     free(x->rep);
     if (x->tier_tab) for (uint32_t g = 0; g < x->cfg.n_groups; ++g) free(x->tier_tab[g].q);
@@ -1054,3 +1151,19 @@ int or_hist_set(or_ctx *x, uint32_t r0, uint32_t nr, const uint32_t *in)
 }
 
 uint32_t or_hist_bin(uint64_t v) { return hist_bin(v); }
+
+/* INFaaS service-time estimates of local replicas [r0, r0 + nr), [r][I] in
+ * 1/256 tick; or_svc_set restores them */
+int or_svc_get(const or_ctx *x, uint32_t r0, uint32_t nr, int64_t *out)
+{
+    if (r0 > x->r_count || nr > x->r_count - r0) return -1;
+    for (uint32_t r = 0; r < nr; ++r) memcpy(out + (size_t)r * x->I, x->rep[r0 + r].svc, x->I * sizeof(int64_t));
+    return 0;
+}
+
+int or_svc_set(or_ctx *x, uint32_t r0, uint32_t nr, const int64_t *in)
+{
+    if (r0 > x->r_count || nr > x->r_count - r0) return -1;
+    for (uint32_t r = 0; r < nr; ++r) memcpy(x->rep[r0 + r].svc, in + (size_t)r * x->I, x->I * sizeof(int64_t));
+    return 0;
+}

@@ -18,7 +18,15 @@ Draining (Sections 3.4, 3.5) is modelled literally: a draining instance's
 full freeness is ``-inf`` (the infinite-usage sentinel), dispatch takes the
 argmax over the non-draining instances with room and, only when there is
 none, the least loaded draining one; pairing sorts draining instances first
-and never uses one as a destination.  The auto-scaling signal (Section 3.6)
+and never uses one as a destination.  The INFaaS-style policy (Section 3.7) is written out literally too: the
+cost alpha * q + beta * s + gamma * penalty of every candidate instance, its
+queue depth q counted from the request list, its state penalty from the head
+of line against the free blocks (OVERLOADED) or this tick's preemptions
+(INTERFERED), the service-time estimate s as a moving average of the per-tick
+mean end-to-end time (1/256 tick, floors as the policy defines them), the
+minimum by exhaustive search, and no migration at all.
+
+The auto-scaling signal (Section 3.6)
 averages F_normal -- Eq. 1 with no headroom at all -- in fixed point with
 floor(F * 2^20) per instance.
 """
@@ -74,6 +82,10 @@ class ExactSim:
         # every request's (tier, queue delay) at its first admission and
         # (tier, end-to-end time) at its finish, in ticks
         self.latencies = ([], [])
+        d = cfg.get("dispatch", {"policy": "llumnix"})
+        self.infaas = d["policy"] == "infaas"
+        self.dsp = d
+        self.svc = [0] * self.I  # INFaaS service-time estimate, 1/256 tick
         self.t = 0
 
     # -- helpers --------------------------------------------------------
@@ -138,6 +150,8 @@ class ExactSim:
         t = self.t
         st = self.stats
         aborted = set()
+        finished = [[] for _ in range(self.I)]  # end-to-end ticks of this tick's finishes
+        interfered = set()
         # A: decode, growth, preemption, finish
         for i in range(self.I):
             row = self.slots[i]
@@ -153,6 +167,7 @@ class ExactSim:
                     need -= 1
                 rv.st = WAITING
                 st[rv.tier * 8 + F_PREEMPTED] += 1
+                interfered.add(i)
             self.free[i] -= need
             for s, r in self.requests(i, RUNNING):
                 r.len += 1
@@ -162,6 +177,7 @@ class ExactSim:
                     st[r.tier * 8 + F_FINISHED] += 1
                     st[r.tier * 8 + F_E2E] += t - r.tarr
                     self.latencies[1].append((r.tier, t - r.tarr))
+                    finished[i].append(t - r.tarr)
                     if r.migrating:
                         aborted.add(i)
                     row[s] = None
@@ -188,6 +204,21 @@ class ExactSim:
                     st[r.tier * 8 + F_ADMITTED] += 1
                     st[r.tier * 8 + F_QDELAY] += t - r.tarr
                     self.latencies[0].append((r.tier, t - r.tarr))
+        # INFaaS: estimates from this tick's finishes, states after admission
+        if self.infaas:
+            for i in range(self.I):
+                if finished[i]:
+                    mean = 256 * sum(finished[i]) // len(finished[i])
+                    self.svc[i] += (mean - self.svc[i]) // 2 ** self.dsp["ewma_shift"]
+            penalty = {}
+            for i in range(self.I):
+                h = self.hol(i)
+                if h is not None and self.blocks(self.slots[i][h].len) > self.free[i]:
+                    penalty[i] = self.dsp["pen_overloaded"]
+                elif i in interfered:
+                    penalty[i] = self.dsp["pen_interfered"]
+                else:
+                    penalty[i] = 0
         # C': auto-scaling signal
         sig, _ = self.autoscale()
         if sig < 0:
@@ -210,9 +241,16 @@ class ExactSim:
             if not cands:
                 cands = room  # all draining: the least loaded one
                 st[DRAIN_FALLBACK] += 1
-            F = {i: self.freeness(i) for i in cands}
-            best = max(F.values())
-            i = min(j for j in cands if F[j] == best)
+            if self.infaas:
+                d = self.dsp
+                cost = {j: d["alpha"] * 256 * len(self.requests(j, WAITING)) + d["beta"] * self.svc[j]
+                        + d["gamma"] * 256 * penalty[j] for j in cands}
+                low = min(cost.values())
+                i = min(j for j in cands if cost[j] == low)
+            else:
+                F = {i: self.freeness(i) for i in cands}
+                best = max(F.values())
+                i = min(j for j in cands if F[j] == best)
             self.slots[i][self.lowest_empty(i)] = Request(WAITING, tier, prompt, out, seq0 + k, t)
             st[tier * 8 + F_DISPATCHED] += 1
         # E1: staged copies
@@ -241,8 +279,8 @@ class ExactSim:
                 self.free[i] += b
                 st[MIG_COMMITTED] += 1
                 self.mig[i] = None
-        # E2: pairing
-        if t % self.cfg["mig_interval"] == 0:
+        # E2: pairing (INFaaS never migrates)
+        if t % self.cfg["mig_interval"] == 0 and not self.infaas:
             busy = set()
             for i, m in enumerate(self.mig):
                 if m is not None:
@@ -307,4 +345,5 @@ class ExactSim:
         return dict(meta=meta, lr=lr, seq=seq, tarr=tarr,
                     free=np.array(self.free, np.int32), mig=mig,
                     next_seq=np.array([self.next_seq], np.uint32),
-                    stats=np.array(self.stats, np.uint64), drain=np.array(self.drain, np.uint8))
+                    stats=np.array(self.stats, np.uint64), drain=np.array(self.drain, np.uint8),
+                    svc=np.array(self.svc, np.int64))

@@ -68,6 +68,21 @@ MUTATIONS = {
     # latency histograms: end-to-end time measured to the tick before the last token
     "hist_e2e_early": [("hist_add(rp, H_E2E, sl[s].tier, t - sl[s].tarr);",
                         "hist_add(rp, H_E2E, sl[s].tier, t - 1 - sl[s].tarr);")],
+    # INFaaS: largest instead of smallest cost
+    "infaas_argmax": [("if (best < 0 || c < bc) { best = (int)i; bc = c; }",
+                       "if (best < 0 || c > bc) { best = (int)i; bc = c; }")],
+    # INFaaS: ties go to the highest index
+    "infaas_tie_high": [("if (best < 0 || c < bc) { best = (int)i; bc = c; }",
+                         "if (best < 0 || c <= bc) { best = (int)i; bc = c; }")],
+    # INFaaS: migration left on
+    "infaas_migrates": [("if (t % x->cfg.mig_interval != 0 || x->cfg.policy == POLICY_INFAAS) return;",
+                         "if (t % x->cfg.mig_interval != 0) return;")],
+    # INFaaS: moving average rounded toward zero instead of down
+    "infaas_ewma_trunc": [("rp->svc[i] += floor_shift(mean - rp->svc[i], x->cfg.ewma_shift);",
+                           "rp->svc[i] += (mean - rp->svc[i]) / ((int64_t)1 << x->cfg.ewma_shift);")],
+    # INFaaS: INTERFERED takes precedence over OVERLOADED
+    "infaas_state_order": [("    if (h >= 0 && (int64_t)blocks(x, inst_slots(x, rp, i)[h].len) > rp->freeb[i]) return x->cfg.pen_over;\n    if (rp->intf[i]) return x->cfg.pen_intf;",
+                            "    if (rp->intf[i]) return x->cfg.pen_intf;\n    if (h >= 0 && (int64_t)blocks(x, inst_slots(x, rp, i)[h].len) > rp->freeb[i]) return x->cfg.pen_over;")],
 }
 
 
@@ -87,6 +102,7 @@ def test_mutation_is_caught(name, tmp_path):
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_drain_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_hist_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_infaas_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_exact.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, "mutation %s survived every pin:\n%s" % (name, r.stdout[-2000:])
