@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define MTS_ABI_VERSION 3
+#define MTS_ABI_VERSION 4
 #define MTS_MAX_TIERS 10
 #define MTS_NSTAT 96
 /* Latency histogram bins per (metric, tier); see mts_state_view.hist */
@@ -114,7 +114,30 @@ typedef struct mts_cfg {
     uint32_t n_groups;           /* >= 1 */
     uint32_t reserved2;          /* must be 0 */
     const mts_group* groups;     /* n_groups entries, copied by mts_create */
+    /* Global dispatch policy.  MTS_POLICY_LLUMNIX (0): tier-ordered dispatch
+     * to the largest freeness and migration (Sections 3.4, 3.5).
+     * MTS_POLICY_INFAAS (1), the paper's comparison scheduler (Section 3.7):
+     * each arrival goes to the instance with the smallest
+     *   cost = alpha * q + beta * s + gamma * penalty      (1/256 tick)
+     * with q the instance's waiting requests (updated after every placement,
+     * weighted as 256 each), s its service-time estimate in 1/256 tick and
+     * penalty in ticks (weighted as 256 each): pen_overloaded when its head of
+     * line does not fit its free blocks after admission, else pen_interfered
+     * when it preempted a request in this tick, else 0; ties go to the lowest
+     * index; no migration starts.  s is updated once per tick after
+     * admission from that tick's finishes on the instance:
+     *   s += floor((floor(256 * sum / count) - s) / 2^infaas_ewma_shift)
+     * with sum the end-to-end ticks of the count requests that finished. */
+    uint32_t dispatch_policy;    /* MTS_POLICY_* */
+    uint32_t infaas_ewma_shift;  /* 0..16 */
+    int32_t infaas_alpha;        /* 0..65536 */
+    int32_t infaas_beta;         /* 0..1024 */
+    int32_t infaas_gamma;        /* 0..65536 */
+    uint32_t infaas_pen_overloaded, infaas_pen_interfered; /* ticks, 0..2^20 */
+    uint32_t reserved3;          /* must be 0 */
 } mts_cfg;
+
+enum { MTS_POLICY_LLUMNIX = 0, MTS_POLICY_INFAAS = 1 };
 
 /* Counters summed over all replicas (mts_stats) or per replica
  * (mts_export_state).  Index layout of the raw arrays: per_tier[p][f] is
@@ -161,9 +184,12 @@ typedef struct mts_stats_t {
  *                 v < 16; otherwise, with 2^e <= v < 2^(e+1),
  *                 16 + 8 (e - 4) + floor(v / 2^(e-3)) - 8 (eight equal
  *                 sub-ranges per octave; at most 239)
+ *   svc[nr*I]     INFaaS service-time estimate s of each instance, 1/256 tick
+ *                 (0 under MTS_POLICY_LLUMNIX)
  * Empty slots are all-zero.  Export skips every NULL array.  Import needs
- * every array but drain and hist; a NULL drain clears the flags, a NULL hist
- * empties the histograms. */
+ * every array but drain, hist and svc; a NULL drain clears the flags, a NULL
+ * hist empties the histograms, a NULL svc zeroes the estimates; an estimate
+ * outside 0..2^40 is MTS_EINVAL. */
 typedef struct mts_state_view {
     uint8_t* meta;
     uint32_t* lr;
@@ -175,6 +201,7 @@ typedef struct mts_state_view {
     uint64_t* stats;
     uint8_t* drain;
     uint32_t* hist;
+    int64_t* svc;
 } mts_state_view;
 
 typedef struct mts_ctx* mts_handle;

@@ -126,6 +126,7 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.mig = o;      o = up256(o + size_t(R) * I * 16);
     L.drain = o;    o = up256(o + size_t(R) * I);
     L.hist = o;     o = up256(o + size_t(R) * kHistPerReplica * 4);
+    L.svc = o;      o = up256(o + size_t(R) * I * 8);
     L.next_seq = o; o = up256(o + size_t(R) * 4);
     L.stats = o;    o = up256(o + size_t(R) * MTS_NSTAT * 8);
     L.digest = o;   o = up256(o + size_t(R) * 8);
@@ -165,6 +166,13 @@ Params make_params(const mts_ctx* h)
     p.wcap = h->wcap;
     p.seed = c.seed;
     p.id_base = c.replica_id_base;
+    p.policy = c.dispatch_policy;
+    p.ewma_shift = c.infaas_ewma_shift;
+    p.alpha256 = static_cast<long long>(c.infaas_alpha) * 256;
+    p.beta = c.infaas_beta;
+    p.gamma256 = static_cast<long long>(c.infaas_gamma) * 256;
+    p.pen_over = c.infaas_pen_overloaded;
+    p.pen_intf = c.infaas_pen_interfered;
     const Layout& L = h->lay;
     p.tier_q = reinterpret_cast<const uint32_t*>(d + L.tier_q);
     p.hq = reinterpret_cast<const int32_t*>(d + L.hq);
@@ -184,6 +192,7 @@ Params make_params(const mts_ctx* h)
     p.mig = reinterpret_cast<int32_t*>(d + L.mig);
     p.drain = reinterpret_cast<uint8_t*>(d + L.drain);
     p.hist = reinterpret_cast<uint32_t*>(d + L.hist);
+    p.svc = reinterpret_cast<long long*>(d + L.svc);
     p.next_seq = reinterpret_cast<uint32_t*>(d + L.next_seq);
     p.stats = reinterpret_cast<unsigned long long*>(d + L.stats);
     p.digest = reinterpret_cast<unsigned long long*>(d + L.digest);
@@ -281,7 +290,7 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
         delete x;
         return MTS_EDEVICE;
     }
-    if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
+    if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
 
     // tables and per-replica group index
     const uint32_t G = x->cfg.n_groups;
@@ -469,6 +478,7 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     get(v->stats, L.stats + size_t(r0) * MTS_NSTAT * 8, size_t(nr) * MTS_NSTAT * 8);
     get(v->drain, L.drain + size_t(r0) * I, size_t(nr) * I);
     get(v->hist, L.hist + size_t(r0) * kHistPerReplica * 4, size_t(nr) * kHistPerReplica * 4);
+    get(v->svc, L.svc + size_t(r0) * I * 8, size_t(nr) * I * 8);
     return hip_rc(e);
 }
 
@@ -511,6 +521,8 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
             const int32_t f = v->free[size_t(r) * I + i];
             if (f < -int32_t(h->cfg.kv_blocks) || f > int32_t(h->cfg.kv_blocks)) return MTS_EINVAL;
             if (v->drain && v->drain[size_t(r) * I + i] > 1) return MTS_EINVAL;
+            if (v->svc && (v->svc[size_t(r) * I + i] < 0 || v->svc[size_t(r) * I + i] > (int64_t(1) << 40)))
+                return MTS_EINVAL;
         }
     }
     const Layout& L = h->lay;
@@ -537,6 +549,12 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
         put(L.hist + size_t(r0) * kHistPerReplica * 4, v->hist, hn);
     } else if (e == hipSuccess && hn) {
         e = hipMemset(h->dev + L.hist + size_t(r0) * kHistPerReplica * 4, 0, hn);
+    }
+    const size_t sn = size_t(nr) * I * 8;
+    if (v->svc) {
+        put(L.svc + size_t(r0) * I * 8, v->svc, sn);
+    } else if (e == hipSuccess && sn) {
+        e = hipMemset(h->dev + L.svc + size_t(r0) * I * 8, 0, sn);
     }
     return hip_rc(e);
 }

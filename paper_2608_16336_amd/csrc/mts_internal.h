@@ -55,6 +55,7 @@ struct Layout {
     size_t meta, hot, seq, tarr;                                        // [R][I][S]
     size_t freeb, mig, drain;                                           // [R][I], [R][I][4], [R][I] u8
     size_t hist;                                                        // [R][2][10][MTS_HIST_BINS] u32
+    size_t svc;                                                         // [R][I] i64 INFaaS estimate
     size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
     size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
     size_t wheel;                                                       // [R][wsz][wcap]
@@ -74,6 +75,9 @@ struct Params {
     uint32_t arr_group;            // lanes per tick in the arrival kernel (16, 32 or 64)
     uint32_t wsz, wcap;            // finish wheel: buckets (power of two), entries per bucket
     uint64_t seed, id_base;
+    uint32_t policy, ewma_shift;   // MTS_POLICY_*, INFaaS moving-average shift
+    long long alpha256, beta, gamma256;  // INFaaS weights (alpha and gamma times 256)
+    uint32_t pen_over, pen_intf;   // INFaaS state penalties in ticks
     const uint32_t* tier_q;        // [group][MTS_MAX_TIERS]
     const int32_t* hq;             // [group][MTS_MAX_TIERS]
     const uint32_t* group_K32;     // [group] tier count
@@ -92,6 +96,7 @@ struct Params {
     int32_t* mig;
     uint8_t* drain;
     uint32_t* hist;
+    long long* svc;
     uint32_t* next_seq;
     unsigned long long* stats;
     unsigned long long* digest;
@@ -101,7 +106,7 @@ struct Params {
 };
 
 // LDS bytes of one wave (one replica) of the step kernel
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz);
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy);
 
 // kernel launches (mts_kernels.hip, mts_arrivals.hip); return hipError_t as int
 int launch_init(const Params& p, hipStream_t stream);

@@ -37,7 +37,7 @@ constexpr unsigned long long kNone = ~0ull;
 constexpr uint32_t kWaitW = 1u << 30, kRunW = 2u << 30, kInbW = 3u << 30;
 constexpr uint32_t kFin = 0x3FFFu;
 constexpr int kNoHol = -1, kHolUnknown = -2, kHolPending = -3;
-constexpr int kFlagAbort = 1, kFlagBusy = 2;
+constexpr int kFlagAbort = 1, kFlagBusy = 2, kFlagIntf = 4;
 
 __device__ __forceinline__ uint32_t wst(uint32_t v) { return v >> 30; }
 __device__ __forceinline__ uint32_t wlo(uint32_t v) { return v & 0xFFFFu; }
@@ -51,7 +51,7 @@ constexpr int kInts = 20;
 constexpr int kLast = 64;
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, wc, wov, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, wc, wov, inf, total;
 };
 
 __host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
@@ -65,7 +65,8 @@ __host__ __device__ constexpr uint32_t imax_for(uint32_t I)
     return I <= 16 ? 16 : I <= 32 ? 32 : I <= 64 ? 64 : I <= 128 ? 128 : 256;
 }
 
-__host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_t W, uint32_t RB, uint32_t wsz)
+__host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_t W, uint32_t RB, uint32_t wsz,
+                                                uint32_t policy)
 {
     LdsLayout L;
     uint32_t o = 0;
@@ -80,6 +81,10 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     L.res = o;   o += ((I * RB + 1) / 2) * 4;
     L.wc = o;    o += (wsz / 2) * 4;
     L.wov = o;   o += ((wsz + 31) / 32) * 4;
+    // INFaaS only: per instance this tick's finished end-to-end sum (u64), the
+    // service-time estimate (i64), the finish count and the state penalty
+    o = al8(o);
+    L.inf = o;   o += policy == MTS_POLICY_INFAAS ? IM * 24 : 0;
     L.total = al8(o);
     return L;
 }
@@ -102,6 +107,10 @@ struct Ctx {
     int* mig;                  // [I][4] dst, src slot, dst slot, copied
     unsigned* wc;              // [wsz / 2] entries filed per wheel bucket, two u16 per word
     unsigned* wov;             // [wsz / 32] bucket overflowed since its last visit
+    // INFaaS policy only (null otherwise), per instance
+    unsigned long long* fsum;  // [I] end-to-end ticks of this tick's finishes
+    long long* svc;            // [I] service-time estimate, 1/256 tick
+    int *fcnt, *pen;           // [I] this tick's finishes; state penalty in ticks
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -114,10 +123,10 @@ struct Ctx {
     int hq[kTiers];
 };
 
-template <int IM>
+template <int IM, bool INF>
 __device__ inline Ctx carve(char* base, const Params& P)
 {
-    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz);
+    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz, P.policy);
     Ctx C;
     C.stats = reinterpret_cast<unsigned long long*>(base + Y.stats);
     C.occ = reinterpret_cast<unsigned long long*>(base + Y.occ);
@@ -153,6 +162,14 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.lastn = reinterpret_cast<int*>(C.lsq + kLast);
     C.wc = reinterpret_cast<unsigned*>(base + Y.wc);
     C.wov = reinterpret_cast<unsigned*>(base + Y.wov);
+    if (INF) {
+        C.fsum = reinterpret_cast<unsigned long long*>(base + Y.inf);
+        C.svc = reinterpret_cast<long long*>(base + Y.inf + IM * 8);
+        C.fcnt = reinterpret_cast<int*>(base + Y.inf + IM * 16);
+        C.pen = C.fcnt + IM;
+    } else {
+        C.fsum = nullptr; C.svc = nullptr; C.fcnt = nullptr; C.pen = nullptr;
+    }
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
@@ -291,6 +308,15 @@ __device__ __forceinline__ uint32_t hist_bin(uint32_t v)
 __device__ __forceinline__ void hist_add(const Ctx& C, int metric, int tier, uint32_t v)
 {
     atomicAdd(&C.hist[(metric * kTiers + tier) * MTS_HIST_BINS + hist_bin(v)], 1u);
+}
+
+// INFaaS cost of instance i in 1/256 tick with extra queued requests:
+// alpha q + beta s + gamma penalty, q = waiting + extra.  Below 2^51 by the
+// configuration limits, so exact as a double.
+__device__ __forceinline__ double infaas_cost(const Ctx& C, const Params& P, int i, int extra)
+{
+    const long long c = P.alpha256 * (C.nwait[i] + extra) + P.beta * C.svc[i] + P.gamma256 * C.pen[i];
+    return double(c);
 }
 
 // lowest empty slot of instance i (one exists); uniform
@@ -477,6 +503,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             C.B[i] -= 1;
             C.nwait[i] += 1;
             C.frs[i] = 0;
+            C.flags[i] |= kFlagIntf;
             c16_dec(C.res, i * C.RB + vr);
             tier_dec(C, i, vt);
             stat(C, vt * 8 + kPreempted, 1);
@@ -516,6 +543,7 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
             const uint32_t e2e = t - C.tarr[b + s];
             stat(C, tier * 8 + kE2e, e2e);
             hist_add(C, kHistE2e, tier, e2e);
+            if (C.fsum) { atomicAdd(&C.fsum[i], static_cast<unsigned long long>(e2e)); atomicAdd(&C.fcnt[i], 1); }
             c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
             if (m & kMigrating) ab = true;
@@ -567,6 +595,7 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
         stat(C, tier * 8 + kFinished, 1);
         stat(C, tier * 8 + kE2e, t - ta);
         hist_add(C, kHistE2e, tier, t - ta);
+        if (C.fsum) { atomicAdd(&C.fsum[i], static_cast<unsigned long long>(t - ta)); atomicAdd(&C.fcnt[i], 1); }
         c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
         tier_dec(C, i, tier);
         if (m & kMigrating) atomicOr(&C.flags[i], kFlagAbort);
@@ -779,15 +808,16 @@ __device__ inline void admit_fresh(const Ctx& C, int i, uint32_t t, int lane)
 // ---------------------------------------------------------------------------
 // k_step
 // ---------------------------------------------------------------------------
-template <int IM>
+template <int IM, bool INF>
 __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigned long long t0, uint32_t nt)
 {
     constexpr int IPL = (IM + 63) / 64;
     extern __shared__ __align__(16) char lds_raw[];
-    Ctx C = carve<IM>(lds_raw, P);
+    Ctx C = carve<IM, INF>(lds_raw, P);
     const int lane = lane_id();
     const uint32_t I = P.I, S = P.S, W = P.W;
     const uint32_t wsz = P.wsz;
+    constexpr bool infaas = INF;  // the global policy: INFaaS cost, else Llumnix freeness
 
     for (uint32_t r = blockIdx.x; r < P.R; r += gridDim.x) {
         const uint32_t g = P.group_of[r];
@@ -809,6 +839,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             C.flags[i] = 0;
             C.tmask[i] = 0;
             C.frs[i] = 0;
+            if (C.svc) C.svc[i] = P.svc[size_t(r) * I + i];
         }
         for (uint32_t b = lane; b < wsz / 2; b += 64) C.wc[b] = 0;
         if (lane == 0) *C.lastn = 0;
@@ -907,6 +938,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     const int G = int(c16_get(C.res, i * C.RB + cres));
                     C.gtmp[i] = G;
                     np = G > C.freeb[i];
+                    if (C.flags[i] & kFlagIntf) C.flags[i] &= ~kFlagIntf;
+                    if (C.fsum) { C.fsum[i] = 0; C.fcnt[i] = 0; }
                 }
                 pre[j] = ballot(np);
             }
@@ -1042,6 +1075,25 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 fsum += q;
             }
             fsum = static_cast<long long>(wsum64(static_cast<unsigned long long>(fsum)));
+            if (C.svc) {
+                // INFaaS: service-time estimate from this tick's finishes, then
+                // the state penalty (OVERLOADED before INTERFERED before ACTIVE)
+                for (uint32_t i = lane; i < I; i += 64) {
+                    const int c = C.fcnt[i];
+                    if (c > 0) {
+                        // floor(256 sum / c): sum < 2^43, so 256 sum is exact in a
+                        // double; the residual corrects the rounded quotient
+                        const long long num = static_cast<long long>(C.fsum[i] * 256ull);
+                        long long mean = static_cast<long long>(floor(double(num) / double(c)));
+                        const long long rr = num - mean * c;
+                        if (rr < 0) mean -= 1;
+                        else if (rr >= c) mean += 1;
+                        C.svc[i] += (mean - C.svc[i]) >> P.ewma_shift;  // arithmetic shift: floor
+                    }
+                    C.pen[i] = C.hols[i] >= 0 && C.hold[i] > C.freeb[i] ? int(P.pen_over)
+                             : (C.flags[i] & kFlagIntf) ? int(P.pen_intf) : 0;
+                }
+            }
             if (lane == 0) {
                 const long long half = static_cast<long long>(I) << 19;
                 if (fsum < -half) stat(C, kScaleOut, 1);
@@ -1086,7 +1138,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         hs_r[j] = hs;
                         hk_r[j] = C.hols[i] == kNoHol ? kNone : C.holk[i];
                         drn_r[j] = C.drn[i];
-                        key[j] = live_r[j] < int(S) && !drn_r[j] ? C.fd[i] : -__builtin_inf();
+                        key[j] = live_r[j] < int(S) && !drn_r[j] ? (infaas ? -infaas_cost(C, P, int(i), 0) : C.fd[i])
+                                                                 : -__builtin_inf();
                     } else {
                         live_r[j] = int(S); fr_r[j] = 0; den_r[j] = 1; dem_r[j] = 0; hs_r[j] = 0; hk_r[j] = 0;
                         drn_r[j] = 0;
@@ -1116,7 +1169,9 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
 #pragma unroll
                                 for (int j = 0; j < IPL; ++j) {
                                     const uint32_t i = lane + 64 * j;
-                                    key[j] = i < I && live_r[j] < int(S) && drn_r[j] ? C.fd[i] : -__builtin_inf();
+                                    key[j] = i < I && live_r[j] < int(S) && drn_r[j]
+                                                 ? (infaas ? -infaas_cost(C, P, int(i), nadd[j]) : C.fd[i])
+                                                 : -__builtin_inf();
                                 }
                                 lb = key[0];
 #pragma unroll
@@ -1144,7 +1199,9 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         // so does the argmax for the following arrivals, none of which can
                         // become the head of line (keys increase along the arrival order):
                         // they all go to cur until its slots run out.
-                        const int m = becomes ? 1 : min(int(cn - k), int(S) - lv);
+                        // (under INFaaS every placement raises cur's cost by alpha)
+                        const bool step1 = becomes || (infaas && P.alpha256 > 0);
+                        const int m = step1 ? 1 : min(int(cn - k), int(S) - lv);
                         const int nl = lv + m;
                         if (lane == lc) {
 #pragma unroll
@@ -1157,13 +1214,14 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                     pend_r[j] = int(k0 + k);
                                     dem_r[j] = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
                                     const int num = 256 * (fr_r[j] - dem_r[j]) - hs_r[j];
-                                    key[j] = double(num) / double(den_r[j]);
+                                    if (!infaas) key[j] = double(num) / double(den_r[j]);
                                 }
+                                if (infaas) key[j] -= double(P.alpha256) * double(m);
                                 if (nl >= int(S)) key[j] = -__builtin_inf();
                             }
                         }
                         if (lane >= int(k) && lane < int(k) + m) tgt = cur;
-                        if (becomes || nl >= int(S)) cur = -1;
+                        if (step1 || nl >= int(S)) cur = -1;
                         if (drain_mode) nfall += m;
                         k += uint32_t(m);
                     }
@@ -1326,7 +1384,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             wave_sync();
 
             // ===================== E2: pairing on interval ticks =====================
-            if (t % P.mig_interval == 0) {
+            if (!infaas && t % P.mig_interval == 0) {
                 bool neg = false;
                 for (uint32_t i = lane; i < I; i += 64) neg |= C.num[i] < 0 || C.drn[i];
                 if (ballot(neg)) {
@@ -1456,6 +1514,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         for (int j = lane; j < kNstat; j += 64) P.stats[size_t(r) * kNstat + j] = C.stats[j];
         for (uint32_t i = lane; i < I; i += 64) {
             P.freeb[size_t(r) * I + i] = C.freeb[i];
+            if (C.svc) P.svc[size_t(r) * I + i] = C.svc[i];
             for (int k = 0; k < 4; ++k) P.mig[(size_t(r) * I + i) * 4 + k] = C.mig[4 * i + k];
         }
         if (lane == 0) P.next_seq[r] = next_seq;
@@ -1478,6 +1537,7 @@ __global__ void k_init(Params P)
         P.drain[j] = 0;
     }
     for (size_t j = t0; j < size_t(P.R) * kHistPerReplica; j += stride) P.hist[j] = 0;
+    for (size_t j = t0; j < size_t(P.R) * P.I; j += stride) P.svc[j] = 0;
     for (size_t j = t0; j < size_t(P.R) * kNstat; j += stride) P.stats[j] = 0;
     for (size_t j = t0; j < P.R; j += stride) { P.next_seq[j] = 0; P.digest[j] = 0; }
 }
@@ -1556,9 +1616,9 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t 
 
 }  // namespace
 
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz)
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy)
 {
-    return lds_layout(imax_for(I), I, S / 64, RB, wsz).total;
+    return lds_layout(imax_for(I), I, S / 64, RB, wsz, policy).total;
 }
 
 int launch_init(const Params& p, hipStream_t stream)
@@ -1570,20 +1630,38 @@ int launch_init(const Params& p, hipStream_t stream)
 
 namespace {
 
+template <bool INF>
+const void* step_fn_t(uint32_t I)
+{
+    switch (imax_for(I)) {
+    case 16: return reinterpret_cast<const void*>(&k_step<16, INF>);
+    case 32: return reinterpret_cast<const void*>(&k_step<32, INF>);
+    case 64: return reinterpret_cast<const void*>(&k_step<64, INF>);
+    case 128: return reinterpret_cast<const void*>(&k_step<128, INF>);
+    default: return reinterpret_cast<const void*>(&k_step<256, INF>);
+    }
+}
+
 const void* step_fn(const Params& p)
 {
+    return p.policy == MTS_POLICY_INFAAS ? step_fn_t<true>(p.I) : step_fn_t<false>(p.I);
+}
+
+template <bool INF>
+void launch_step_t(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, size_t lds, hipStream_t stream)
+{
     switch (imax_for(p.I)) {
-    case 16: return reinterpret_cast<const void*>(&k_step<16>);
-    case 32: return reinterpret_cast<const void*>(&k_step<32>);
-    case 64: return reinterpret_cast<const void*>(&k_step<64>);
-    case 128: return reinterpret_cast<const void*>(&k_step<128>);
-    default: return reinterpret_cast<const void*>(&k_step<256>);
+    case 16: hipLaunchKernelGGL((k_step<16, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 32: hipLaunchKernelGGL((k_step<32, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 64: hipLaunchKernelGGL((k_step<64, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 128: hipLaunchKernelGGL((k_step<128, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    default: hipLaunchKernelGGL((k_step<256, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
     }
 }
 
 size_t step_lds(const Params& p)
 {
-    const size_t lds = lds_bytes(p.I, p.S, p.RB, p.wsz);
+    const size_t lds = lds_bytes(p.I, p.S, p.RB, p.wsz, p.policy);
     if (lds > 64 * 1024) {
         // raise the dynamic LDS limit; a real failure shows up at the launch
         (void)hipFuncSetAttribute(step_fn(p), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
@@ -1608,13 +1686,8 @@ int step_blocks_per_cu(const Params& p)
 int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream)
 {
     const size_t lds = step_lds(p);
-    switch (imax_for(p.I)) {
-    case 16: hipLaunchKernelGGL(k_step<16>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 32: hipLaunchKernelGGL(k_step<32>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 64: hipLaunchKernelGGL(k_step<64>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 128: hipLaunchKernelGGL(k_step<128>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    default: hipLaunchKernelGGL(k_step<256>, dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    }
+    if (p.policy == MTS_POLICY_INFAAS) launch_step_t<true>(p, t0, nt, blocks, lds, stream);
+    else launch_step_t<false>(p, t0, nt, blocks, lds, stream);
     return int(hipGetLastError());
 }
 

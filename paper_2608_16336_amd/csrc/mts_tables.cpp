@@ -126,7 +126,12 @@ bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
 
 int validate(const mts_cfg& c)
 {
-    if (c.abi_version != MTS_ABI_VERSION || c.reserved != 0 || c.reserved2 != 0) return MTS_EINVAL;
+    if (c.abi_version != MTS_ABI_VERSION || c.reserved != 0 || c.reserved2 != 0 || c.reserved3 != 0) return MTS_EINVAL;
+    if (c.dispatch_policy > MTS_POLICY_INFAAS || c.infaas_ewma_shift > 16) return MTS_EINVAL;
+    if (c.infaas_alpha < 0 || c.infaas_alpha > 65536 || c.infaas_beta < 0 || c.infaas_beta > 1024 ||
+        c.infaas_gamma < 0 || c.infaas_gamma > 65536)
+        return MTS_EINVAL;
+    if (c.infaas_pen_overloaded > (1u << 20) || c.infaas_pen_interfered > (1u << 20)) return MTS_EINVAL;
     if (c.n_instances < 1 || c.n_instances > kMaxInstances) return MTS_EINVAL;
     if (c.slots_per_instance < 64 || c.slots_per_instance > kMaxSlots || c.slots_per_instance % 64) return MTS_EINVAL;
     if (c.kv_blocks < 1 || c.kv_blocks > kMaxBlocks) return MTS_EINVAL;

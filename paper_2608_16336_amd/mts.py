@@ -12,12 +12,13 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libmts.so")
 
-ABI_VERSION = 3
+ABI_VERSION = 4
 MAX_TIERS = 10
 NSTAT = 96
 HIST_BINS = 240  # latency histogram bins per (metric, tier)
 
 TIER_KINDS = {"uniform": 0, "gauss": 1, "geometric": 2, "explicit": 3}
+POLICIES = {"llumnix": 0, "infaas": 1}
 ARRIVAL_KINDS = {"poisson": 0, "gamma_poisson": 1}
 PROMPT_KINDS = {"uniform_int": 0, "lognormal": 1}
 OUTPUT_KINDS = {"geometric": 0, "pareto": 1}
@@ -56,7 +57,11 @@ class mts_cfg(ctypes.Structure):
                 ("output_min", ctypes.c_uint32), ("output_cap", ctypes.c_uint32),
                 ("seed", ctypes.c_uint64), ("replica_id_base", ctypes.c_uint64),
                 ("n_groups", ctypes.c_uint32), ("reserved2", ctypes.c_uint32),
-                ("groups", ctypes.POINTER(mts_group))]
+                ("groups", ctypes.POINTER(mts_group)),
+                ("dispatch_policy", ctypes.c_uint32), ("infaas_ewma_shift", ctypes.c_uint32),
+                ("infaas_alpha", ctypes.c_int32), ("infaas_beta", ctypes.c_int32), ("infaas_gamma", ctypes.c_int32),
+                ("infaas_pen_overloaded", ctypes.c_uint32), ("infaas_pen_interfered", ctypes.c_uint32),
+                ("reserved3", ctypes.c_uint32)]
 
 
 class mts_stats_t(ctypes.Structure):
@@ -72,7 +77,7 @@ class mts_stats_t(ctypes.Structure):
 
 class mts_state_view(ctypes.Structure):
     _fields_ = [(k, ctypes.c_void_p) for k in
-                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist")]
+                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist", "svc")]
 
 
 EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest",
@@ -175,6 +180,12 @@ def make_cfg(cfg):
     c.replica_id_base = cfg["replica_id_base"]
     c.n_groups = len(cfg["groups"])
     c.groups = groups
+    d = cfg.get("dispatch", {"policy": "llumnix"})
+    c.dispatch_policy = POLICIES[d["policy"]]
+    if d["policy"] == "infaas":
+        c.infaas_alpha, c.infaas_beta, c.infaas_gamma = d["alpha"], d["beta"], d["gamma"]
+        c.infaas_pen_overloaded, c.infaas_pen_interfered = d["pen_overloaded"], d["pen_interfered"]
+        c.infaas_ewma_shift = d["ewma_shift"]
     return c, groups
 
 
@@ -195,7 +206,7 @@ def _stream_handle(stream):
 class Scheduler:
     """R replicas of a workload on one GPU, advanced by ``step``."""
 
-    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist")
+    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist", "svc")
 
     def __init__(self, cfg, device="cuda", stream=None):
         import torch
@@ -284,7 +295,8 @@ class Scheduler:
                     free=np.zeros(nr * self.I, np.int32), mig=np.zeros(nr * self.I * 4, np.int32),
                     next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
                     drain=np.zeros(nr * self.I, np.uint8),
-                    hist=np.zeros(nr * 2 * MAX_TIERS * HIST_BINS, np.uint32))
+                    hist=np.zeros(nr * 2 * MAX_TIERS * HIST_BINS, np.uint32),
+                    svc=np.zeros(nr * self.I, np.int64))
 
     def set_draining(self, flags, r0=0, nr=None):
         """flags: 0/1 per (replica, instance) of replicas [r0, r0 + nr)."""
@@ -306,7 +318,9 @@ class Scheduler:
         [replica][metric (0 queue delay, 1 end-to-end)][tier][bin] (u32)."""
         nr = self.R - r0 if nr is None else nr
         h = np.zeros(nr * 2 * MAX_TIERS * HIST_BINS, np.uint32)
-        v = mts_state_view(*([None] * (len(self._ORDER) - 1) + [h.ctypes.data]))
+        ptrs = [None] * len(self._ORDER)
+        ptrs[self._ORDER.index("hist")] = h.ctypes.data
+        v = mts_state_view(*ptrs)
         _check("mts_export_state", load_library().mts_export_state(self._h, r0, nr, ctypes.byref(v)))
         return h.reshape(nr, 2, MAX_TIERS, HIST_BINS)
 

@@ -346,3 +346,72 @@ def test_differentiation_study_small_run_matches_oracle():
     k1 = [x for x in rows if x["K"] == 1]
     assert len(k1) == 3 and all(x["tier"] == 0 for x in k1)
     assert sum(x["admitted"] for x in rows) > 0
+
+
+# ---------------------------------------------------------------------------
+# INFaaS-style cost dispatch (Section 3.7), the alternative global policy
+# ---------------------------------------------------------------------------
+INFAAS = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512, pen_interfered=128, ewma_shift=4)
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_infaas_clusters(case):
+    from test_oracle_exact import _random_cfg as rc, _random_drain_plan
+    rng = random.Random(7000 + case)
+    cfg = rc(rng)
+    cfg["dispatch"] = dict(policy="infaas", alpha=rng.choice([0, 1, 64, 300]), beta=rng.choice([0, 1, 3]),
+                           gamma=rng.choice([0, 1, 5]), pen_overloaded=rng.choice([0, 40, 512]),
+                           pen_interfered=rng.choice([0, 20, 128]), ewma_shift=rng.choice([0, 2, 4, 16]))
+    cfg["groups"][0]["n_replicas"] = 3
+    if case % 2:
+        g = run_plan_both(cfg, 250, _random_drain_plan(rng, cfg["n_instances"], 250))
+    else:
+        g = run_both(cfg, 250)
+    s = g.stats()["raw"]
+    assert s[80:84].sum() == 0 and s[86] == 0
+
+
+@pytest.mark.parametrize("name,rpg,ticks", [
+    ("tiny", 1, 1000),
+    ("enterprise", 8, 600),
+    ("gauss10", 8, 600),
+    ("sweep", 1, 300),
+    ("wide", 1, 100),
+])
+def test_infaas_presets_reduced(name, rpg, ticks):
+    cfg = scaled(name, replicas_per_group=rpg)
+    cfg["dispatch"] = dict(INFAAS)
+    g = Scheduler(cfg)
+    g.step(ticks)
+    o = oracle.Oracle(cfg)
+    o.step(ticks)
+    assert_same(g.export(), o.export(), name)
+    assert np.array_equal(g.digests(), o.digests())
+    s = g.stats()["raw"]
+    assert s[86] == 0 and s[80:84].sum() == 0
+    assert np.any(g.export()["svc"] > 0)
+
+
+def test_infaas_export_import_resumes_exactly():
+    cfg = scaled("enterprise", replicas_per_group=4)
+    cfg["dispatch"] = dict(INFAAS)
+    a = Scheduler(cfg)
+    a.step(300)
+    st = a.export()
+    b = Scheduler(cfg)
+    b.import_state(st)
+    b.tick = a.tick
+    a.step(200)
+    b.step(200)
+    assert_same(b.export(), a.export(), "resumed")
+
+
+def test_infaas_estimate_is_validated():
+    cfg = preset("tiny")
+    cfg["dispatch"] = dict(INFAAS)
+    g = Scheduler(cfg)
+    st = g.export()
+    st["svc"][1] = -5
+    with pytest.raises(MtsError) as e:
+        g.import_state(st)
+    assert e.value.code == -1
