@@ -90,6 +90,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0,
                     help="MiB copied device-to-device once before timing (counter calibration)")
+    ap.add_argument("--policy", choices=("llumnix", "infaas"), default="llumnix",
+                    help="global dispatch policy (infaas: cost-based dispatch without migration)")
+    ap.add_argument("--drain-instances", type=int, default=0,
+                    help="mark the first n instances of every replica draining after the first timed step")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -103,6 +107,9 @@ def main():
     from workloads import preset
 
     cfg = preset(args.workload)
+    if args.policy == "infaas":
+        cfg["dispatch"] = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512,
+                               pen_interfered=128, ewma_shift=4)
     R = sum(g["n_replicas"] for g in cfg["groups"])
     T, K, W = args.ticks_per_step, args.steps, args.warmup
     torch.cuda.set_device(0)
@@ -134,6 +141,11 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(K):
+        if k == 1 and args.drain_instances:
+            # host decision between steps (synchronous, inside the timed region)
+            flags = np.zeros((R, cfg["n_instances"]), np.uint8)
+            flags[:, :args.drain_instances] = 1
+            sch.set_draining(flags)
         sch.step(T, stream=stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -150,7 +162,8 @@ def main():
     b_alg = algorithmic_bytes(cfg, R, T * K, d)
     avg_launch_s = step_ms / 1e3 / launches
     achieved = b_alg / launches / avg_launch_s / 1e9
-    traffic = MEASURED_TRAFFIC.get(kernel_source_hash()) if (args.workload, T) == ("sweep", 1000) else None
+    default_run = (args.workload, T, args.policy, args.drain_instances) == ("sweep", 1000, "llumnix", 0)
+    traffic = MEASURED_TRAFFIC.get(kernel_source_hash()) if default_run else None
 
     out = {
         "metric": "replica-ticks/s and request-slot updates/s at 1 MI355X; % of HBM roofline",
@@ -168,6 +181,7 @@ def main():
         "config": {"workload": cfg["name"], "replicas": R, "instances": cfg["n_instances"],
                    "slots_per_instance": cfg["slots_per_instance"], "ticks_per_step": T,
                    "ticks_timed": T * K, "parallelism": "replicas across workgroups",
+                   "policy": args.policy, "draining_instances": args.drain_instances,
                    "blocks": sch.launch()[1], "threads_per_block": 64},
         "slot_updates_per_s": value * slots,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -49,9 +49,11 @@ __device__ __forceinline__ uint32_t wmid(uint32_t v) { return (v >> 16) & kFin; 
 constexpr int kInts = 20;
 // placements of the previous tick's dispatch kept in LDS (at most one wave's worth)
 constexpr int kLast = 64;
+// requests preempted in the current tick, listed for the prefetched finish visit
+constexpr int kVic = 16;
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, wc, wov, inf, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, total;
 };
 
 __host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
@@ -77,6 +79,7 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     L.tcnt = o;  o += IM * kTiers / 2 * 4;
     L.mig = o;   o += IM * 16;
     L.last = o;  o += kLast * 12 + 8;
+    L.vic = o;   o += kVic * 4 + 8;
     L.occ = o;   o += I * W * 8;
     L.res = o;   o += ((I * RB + 1) / 2) * 4;
     L.wc = o;    o += (wsz / 2) * 4;
@@ -101,6 +104,8 @@ struct Ctx {
     unsigned *lw, *lsl, *lsq;  // [kLast] previous tick's placements in dispatch order: slot word,
                                // instance << 16 | tier << 12 | slot, seq
     int* lastn;                // number of those placements
+    unsigned* vic;             // [kVic] instance << 16 | slot of this tick's preemption victims
+    int* nvic;                 // their number (kVic + 1: more than the list holds)
     unsigned *hwd, *hmt, *hta; // [I] head of line: slot word, meta, arrival tick
     unsigned* res;             // [I][RB] running requests per growth residue (u16 pairs)
     unsigned* tcnt;            // [I][10] running requests per tier (u16 pairs)
@@ -160,6 +165,8 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.lsl = C.lw + kLast;
     C.lsq = C.lsl + kLast;
     C.lastn = reinterpret_cast<int*>(C.lsq + kLast);
+    C.vic = reinterpret_cast<unsigned*>(base + Y.vic);
+    C.nvic = reinterpret_cast<int*>(C.vic + kVic);
     C.wc = reinterpret_cast<unsigned*>(base + Y.wc);
     C.wov = reinterpret_cast<unsigned*>(base + Y.wov);
     if (INF) {
@@ -504,6 +511,9 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             C.nwait[i] += 1;
             C.frs[i] = 0;
             C.flags[i] |= kFlagIntf;
+            const int nv = *C.nvic;
+            if (nv < kVic) C.vic[nv] = (uint32_t(i) << 16) | uint32_t(vs);
+            *C.nvic = nv < kVic ? nv + 1 : kVic + 1;
             c16_dec(C.res, i * C.RB + vr);
             tier_dec(C, i, vt);
             stat(C, vt * 8 + kPreempted, 1);
@@ -943,12 +953,23 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 }
                 pre[j] = ballot(np);
             }
+            if (lane == 0) *C.nvic = 0;
             wave_sync();
             bool preempting = false;
 #pragma unroll
             for (int j = 0; j < IPL; ++j) {
                 preempting = preempting || pre[j] != 0;
                 for (unsigned long long m = pre[j]; m; m &= m - 1) preempt(C, 64 * j + ffs64(m), t, lane);
+            }
+            // a preempted request is waiting now: its prefetched entry is dropped
+            // (its wheel entry was erased); more victims than the list holds
+            // make the visit load again
+            bool pf_lost = false;
+            if (preempting) {
+                const int nv = *C.nvic;
+                pf_lost = nv > kVic;
+                for (int v = 0; v < nv && v < kVic; ++v)
+                    if (pf_e == C.vic[v]) pf_e = kTomb;
             }
             for (uint32_t i = lane; i < I; i += 64) {
                 const int G = C.gtmp[i];
@@ -960,7 +981,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 const uint32_t bk = t & C.wmask;
                 const uint32_t nb = (C.wc[bk >> 1] >> ((bk & 1u) * 16u)) & 0xFFFFu;
                 const bool ov = (C.wov[bk >> 5] >> (bk & 31u)) & 1u;
-                if (pf_n != kNoPf && !preempting && !ov && nb == pf_n) {
+                if (pf_n != kNoPf && !pf_lost && !ov && nb == pf_n) {
                     uint32_t* ent = C.wheel + size_t(bk) * C.wcap;
                     const uint32_t kept = finish_batch(C, t, lane, ent, 0, uint32_t(lane) < pf_n, pf_e, pf_v, pf_m, pf_a);
                     wheel_set_count(C, bk, kept, lane);
@@ -1431,10 +1452,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         const int h = C.hols[src];
                         if (h >= 0) {
                             if (lane == 0) {
+                                // the head of line's fields are cached in LDS
                                 const size_t hb = size_t(src) * S + h;
-                                const uint32_t hw = C.hot[hb], hm = C.meta[hb], ht = C.tarr[hb];
+                                const uint32_t hw = C.hwd[src], hm = C.hmt[src], ht = C.hta[src];
                                 C.hot[dsb] = hw; C.meta[dsb] = uint8_t(hm);
-                                C.seq[dsb] = C.seq[hb]; C.tarr[dsb] = ht;
+                                C.seq[dsb] = uint32_t(C.holk[src]); C.tarr[dsb] = ht;
                                 C.hot[hb] = 0; C.meta[hb] = 0; C.seq[hb] = 0; C.tarr[hb] = 0;
                                 C.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
                                 C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);

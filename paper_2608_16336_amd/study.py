@@ -52,21 +52,27 @@ def percentile(counts, q):
     return float(bin_edges()[1][min(b, HIST_BINS - 1)])
 
 
-def sweep_cfg(arrival_mean, replicas_per_group, ticks):
+INFAAS = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512, pen_interfered=128, ewma_shift=4)
+
+
+def sweep_cfg(arrival_mean, replicas_per_group, ticks, policy="llumnix"):
     from workloads import preset
     cfg = preset("sweep")
+    if policy == "infaas":
+        cfg["dispatch"] = dict(INFAAS)
     cfg["arrival"] = dict(kind="poisson", mean=float(arrival_mean))
     for g in cfg["groups"]:
         g["n_replicas"] = replicas_per_group
     cfg["ticks"] = ticks
-    cfg["name"] = "differentiation study: sweep groups x %d, Poisson %g/tick" % (replicas_per_group, arrival_mean)
+    cfg["name"] = "differentiation study: sweep groups x %d, Poisson %g/tick, %s dispatch" % (
+        replicas_per_group, arrival_mean, policy)
     return cfg
 
 
-def run(arrival_mean=24.0, replicas_per_group=128, ticks=4000, device="cuda"):
+def run(arrival_mean=24.0, replicas_per_group=128, ticks=4000, device="cuda", policy="llumnix"):
     """Run the sweep and return one row per (tier mix, K, tier)."""
     import torch
-    cfg = sweep_cfg(arrival_mean, replicas_per_group, ticks)
+    cfg = sweep_cfg(arrival_mean, replicas_per_group, ticks, policy)
     g = Scheduler(cfg, device=device)
     g.step(ticks)
     torch.cuda.synchronize()
@@ -115,9 +121,10 @@ def main(argv=None):
     ap.add_argument("--arrival-mean", type=float, default=24.0)
     ap.add_argument("--replicas-per-group", type=int, default=128)
     ap.add_argument("--ticks", type=int, default=4000)
+    ap.add_argument("--policy", choices=("llumnix", "infaas"), default="llumnix")
     ap.add_argument("--json", help="also write the rows to this file")
     a = ap.parse_args(argv)
-    cfg, rows = run(a.arrival_mean, a.replicas_per_group, a.ticks)
+    cfg, rows = run(a.arrival_mean, a.replicas_per_group, a.ticks, policy=a.policy)
     print("# %s, %d ticks\n" % (cfg["name"], a.ticks))
     print(markdown(rows))
     if a.json:
