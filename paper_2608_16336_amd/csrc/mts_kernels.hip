@@ -326,17 +326,6 @@ __device__ __forceinline__ double infaas_cost(const Ctx& C, const Params& P, int
     return double(c);
 }
 
-// lowest empty slot of instance i (one exists); uniform
-__device__ inline int lowest_empty(const Ctx& C, int i, int lane)
-{
-    const unsigned long long w = lane < int(C.W) ? C.occ[i * C.W + lane] : kNone;
-    const unsigned long long fm = ballot(w != kNone);
-    if (fm == 0) return -1;
-    const int c0 = ffs64(fm);
-    const unsigned long long w0 = rl64(w, c0);
-    return c0 * 64 + ffs64(~w0);
-}
-
 // number of 64-slot chunks of instance i up to its highest non-empty one; uniform
 __device__ __forceinline__ int live_chunks(const Ctx& C, int i, int lane)
 {
@@ -1432,78 +1421,100 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     }
                     const int n2 = wsum(mine);
                     wave_sync();
-                    for (int k = 0; k < int(P.mig_max_pairs) && k < n2 - 1 - k; ++k) {
-                        const int src = C.order[k], dst = C.order[n2 - 1 - k];
-                        // a draining destination: every instance left is draining
-                        if (C.drn[dst]) break;
-                        if (!C.drn[src]) {
-                            // (a draining source is overloaded and any destination is
-                            // more than theta freer)
-                            if (C.num[src] >= 0) break;
-                            const long long lhs = (long long)P.theta_den *
-                                ((long long)C.num[dst] * C.den[src] - (long long)C.num[src] * C.den[dst]);
-                            const long long rhs = (long long)P.theta_num * 256 * C.den[src] * C.den[dst];
-                            if (lhs < rhs) break;
-                        }
-                        if (C.live[dst] >= int(S)) continue;
-                        const int ds = lowest_empty(C, dst, lane);
-                        if (ds < 0) continue;
-                        const size_t dsb = size_t(dst) * S + ds;
-                        const int h = C.hols[src];
-                        if (h >= 0) {
-                            if (lane == 0) {
-                                // the head of line's fields are cached in LDS
-                                const size_t hb = size_t(src) * S + h;
-                                const uint32_t hw = C.hwd[src], hm = C.hmt[src], ht = C.hta[src];
-                                C.hot[dsb] = hw; C.meta[dsb] = uint8_t(hm);
-                                C.seq[dsb] = uint32_t(C.holk[src]); C.tarr[dsb] = ht;
-                                C.hot[hb] = 0; C.meta[hb] = 0; C.seq[hb] = 0; C.tarr[hb] = 0;
-                                C.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
-                                C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
-                                C.live[src] -= 1; C.nwait[src] -= 1;
-                                C.live[dst] += 1; C.nwait[dst] += 1;
-                                C.frs[src] = 0; C.frs[dst] = 0;
-                                const unsigned long long key = C.holk[src];
-                                if (C.hols[dst] == kNoHol || key < C.holk[dst]) set_hol(C, dst, ds, key, hw, hm, ht);
-                                if (C.nwait[src] == 0) clear_hol(C, src);
-                                else C.hols[src] = kHolUnknown;
-                                stat(C, kMigQueued, 1);
-                            }
-                            wave_sync();
-                            continue;
-                        }
-                        // running candidate: largest tier, then fewest blocks, then newest
-                        const size_t sbase = size_t(src) * S;
-                        const int nch = live_chunks(C, src, lane);
-                        unsigned long long bk = 0;
-                        int bs = 0;
-                        for (int c = 0; c < nch; ++c) {
-                            const int s = c * 64 + lane;
-                            const uint32_t v = C.hot[sbase + s];
-                            const uint32_t m = C.meta[sbase + s];
-                            if (wst(v) == 2u && !(m & kMigrating)) {
-                                const uint32_t fin = fin_of(v, t);
-                                const unsigned long long kk =
-                                    (static_cast<unsigned long long>(((m >> 2) & 15u) + 1u) << 48) |
-                                    (static_cast<unsigned long long>(65535 - blocks_of(wlo(v) - (fin - t), C.shift)) << 32) |
-                                    C.seq[sbase + s];
-                                if (kk > bk) { bk = kk; bs = s; }
+                    // Pairs (L[k], L[n2 - 1 - k]) use disjoint instances and one
+                    // snapshot of F, so the stopping pair is found for all pairs at
+                    // once (lane k tests pair k), the queued moves of the pairs
+                    // before it run in parallel, and only the staged copies, which
+                    // scan a source's slots with the whole wave, go one at a time.
+                    const int npairs = min(int(P.mig_max_pairs), n2 / 2);
+                    for (int k0 = 0; k0 < npairs; k0 += 64) {
+                        const int k = k0 + lane;
+                        const bool in = k < npairs;
+                        const int src = in ? C.order[k] : 0, dst = in ? C.order[n2 - 1 - k] : 0;
+                        bool stop = false;
+                        if (in) {
+                            if (C.drn[dst]) {
+                                // a draining destination: every instance left is draining
+                                stop = true;
+                            } else if (!C.drn[src]) {
+                                // (a draining source is overloaded and any destination is
+                                // more than theta freer)
+                                const long long lhs = (long long)P.theta_den *
+                                    ((long long)C.num[dst] * C.den[src] - (long long)C.num[src] * C.den[dst]);
+                                const long long rhs = (long long)P.theta_num * 256 * C.den[src] * C.den[dst];
+                                stop = C.num[src] >= 0 || lhs < rhs;
                             }
                         }
-                        const unsigned long long mx = wmax64(bk);
-                        if (mx == 0) continue;
-                        const int cs = rl(bs, ffs64(ballot(bk == mx)));
-                        if (lane == 0) {
-                            C.hot[dsb] = kInbW;
-                            C.meta[dsb] = uint8_t(kInbound);
+                        const unsigned long long sm = ballot(stop);
+                        const int kstop = sm ? ffs64(sm) : 64;
+                        // the destination's lowest empty slot; a full one skips its pair
+                        int ds = -1;
+                        if (in && lane < kstop && C.live[dst] < int(S)) {
+                            for (uint32_t w = 0; w < W; ++w) {
+                                const unsigned long long word = C.occ[dst * W + w];
+                                if (word != kNone) { ds = int(w) * 64 + ffs64(~word); break; }
+                            }
+                        }
+                        const bool act = ds >= 0;
+                        const int h = act ? C.hols[src] : kNoHol;
+                        if (act && h >= 0) {
+                            // queued move of the source's head of line (fields cached in LDS)
+                            const size_t dsb = size_t(dst) * S + ds, hb = size_t(src) * S + h;
+                            const uint32_t hw = C.hwd[src], hm = C.hmt[src], ht = C.hta[src];
+                            const unsigned long long key = C.holk[src];
+                            C.hot[dsb] = hw; C.meta[dsb] = uint8_t(hm);
+                            C.seq[dsb] = uint32_t(key); C.tarr[dsb] = ht;
+                            C.hot[hb] = 0; C.meta[hb] = 0; C.seq[hb] = 0; C.tarr[hb] = 0;
+                            C.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
                             C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
-                            C.live[dst] += 1;
-                            C.meta[sbase + cs] = uint8_t(C.meta[sbase + cs] | kMigrating);
-                            int* m = &C.mig[4 * src];
-                            m[0] = dst; m[1] = cs; m[2] = ds; m[3] = 0;
-                            stat(C, kMigStarted, 1);
+                            C.live[src] -= 1; C.nwait[src] -= 1;
+                            C.live[dst] += 1; C.nwait[dst] += 1;
+                            C.frs[src] = 0; C.frs[dst] = 0;
+                            if (C.hols[dst] == kNoHol || key < C.holk[dst]) set_hol(C, dst, ds, key, hw, hm, ht);
+                            if (C.nwait[src] == 0) clear_hol(C, src);
+                            else C.hols[src] = kHolUnknown;
+                            stat(C, kMigQueued, 1);
                         }
                         wave_sync();
+                        // staged copies: running candidate of largest tier, then fewest
+                        // blocks, then newest
+                        for (unsigned long long pm = ballot(act && h < 0); pm; pm &= pm - 1) {
+                            const int l = ffs64(pm);
+                            const int psrc = rl(src, l), pdst = rl(dst, l), pds = rl(ds, l);
+                            const size_t sbase = size_t(psrc) * S;
+                            const int nch = live_chunks(C, psrc, lane);
+                            unsigned long long bk = 0;
+                            int bs = 0;
+                            for (int c = 0; c < nch; ++c) {
+                                const int s = c * 64 + lane;
+                                const uint32_t v = C.hot[sbase + s];
+                                const uint32_t m = C.meta[sbase + s];
+                                if (wst(v) == 2u && !(m & kMigrating)) {
+                                    const uint32_t fin = fin_of(v, t);
+                                    const unsigned long long kk =
+                                        (static_cast<unsigned long long>(((m >> 2) & 15u) + 1u) << 48) |
+                                        (static_cast<unsigned long long>(65535 - blocks_of(wlo(v) - (fin - t), C.shift)) << 32) |
+                                        C.seq[sbase + s];
+                                    if (kk > bk) { bk = kk; bs = s; }
+                                }
+                            }
+                            const unsigned long long mx = wmax64(bk);
+                            if (mx == 0) continue;  // nothing to move (an empty draining source)
+                            const int cs = rl(bs, ffs64(ballot(bk == mx)));
+                            if (lane == 0) {
+                                const size_t dsb = size_t(pdst) * S + pds;
+                                C.hot[dsb] = kInbW;
+                                C.meta[dsb] = uint8_t(kInbound);
+                                C.occ[pdst * W + (pds >> 6)] |= 1ull << (pds & 63);
+                                C.live[pdst] += 1;
+                                C.meta[sbase + cs] = uint8_t(C.meta[sbase + cs] | kMigrating);
+                                int* m = &C.mig[4 * psrc];
+                                m[0] = pdst; m[1] = cs; m[2] = pds; m[3] = 0;
+                                stat(C, kMigStarted, 1);
+                            }
+                            wave_sync();
+                        }
+                        if (sm) break;
                     }
                 }
                 wave_sync();
