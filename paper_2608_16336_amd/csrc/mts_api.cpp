@@ -26,6 +26,7 @@ struct mts_ctx {
     uint32_t wsz = 0, wcap = 0;        // finish wheel: buckets, entries per bucket
     uint32_t arr_group = 64;           // lanes per tick in the arrival kernel
     uint32_t blocks = 0;               // step-kernel blocks (one wave each); 0 = automatic
+    uint32_t qdepth = 0;               // queue-cache entries per instance (chosen at create)
     int device = 0;
     hipStream_t last = nullptr;
     std::vector<uint16_t> group_of;
@@ -173,6 +174,7 @@ Params make_params(const mts_ctx* h)
     p.gamma256 = static_cast<long long>(c.infaas_gamma) * 256;
     p.pen_over = c.infaas_pen_overloaded;
     p.pen_intf = c.infaas_pen_interfered;
+    p.qdepth = h->qdepth;
     const Layout& L = h->lay;
     p.tier_q = reinterpret_cast<const uint32_t*>(d + L.tier_q);
     p.hq = reinterpret_cast<const int32_t*>(d + L.hq);
@@ -290,7 +292,21 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
         delete x;
         return MTS_EDEVICE;
     }
-    if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
+    if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, 0) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
+    // queue cache depth: the deepest of 7, 3, 1 that keeps the step kernel's
+    // blocks per CU (the cache only saves rescans; a lost block per CU costs
+    // more: with no spare room per CU the dispatcher cannot place every
+    // block at once)
+    {
+        Params p = make_params(x);
+        p.qdepth = 0;
+        const int base = step_blocks_per_cu(p);
+        for (uint32_t d : {7u, 3u, 1u}) {
+            p.qdepth = d;
+            if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, d) > size_t(max_lds)) continue;
+            if (step_blocks_per_cu(p) >= base) { x->qdepth = d; break; }
+        }
+    }
 
     // tables and per-replica group index
     const uint32_t G = x->cfg.n_groups;
@@ -354,6 +370,27 @@ int auto_blocks(mts_handle h, const Params& p, uint32_t* blocks)
 }
 
 }  // namespace
+
+int mts_set_queue_cache(mts_handle h, uint32_t depth)
+{
+    if (!h || depth > 15) return MTS_EINVAL;
+    int max_lds = 0;
+    if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) != hipSuccess)
+        return MTS_EDEVICE;
+    if (lds_bytes(h->I, h->S, h->cfg.block_tokens, h->wsz, h->cfg.dispatch_policy, depth) > size_t(max_lds))
+        return MTS_EINVAL;
+    hipError_t e = hipStreamSynchronize(h->last);
+    if (e != hipSuccess) return MTS_EDEVICE;
+    h->qdepth = depth;
+    return MTS_OK;
+}
+
+int mts_get_queue_cache(mts_handle h, uint32_t* depth)
+{
+    if (!h || !depth) return MTS_EINVAL;
+    *depth = h->qdepth;
+    return MTS_OK;
+}
 
 int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks)
 {

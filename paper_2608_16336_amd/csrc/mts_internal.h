@@ -78,6 +78,7 @@ struct Params {
     uint32_t policy, ewma_shift;   // MTS_POLICY_*, INFaaS moving-average shift
     long long alpha256, beta, gamma256;  // INFaaS weights (alpha and gamma times 256)
     uint32_t pen_over, pen_intf;   // INFaaS state penalties in ticks
+    uint32_t qdepth;               // queue-cache entries behind each head of line (LDS)
     const uint32_t* tier_q;        // [group][MTS_MAX_TIERS]
     const int32_t* hq;             // [group][MTS_MAX_TIERS]
     const uint32_t* group_K32;     // [group] tier count
@@ -106,7 +107,7 @@ struct Params {
 };
 
 // LDS bytes of one wave (one replica) of the step kernel
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy);
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy, uint32_t qdepth);
 
 // kernel launches (mts_kernels.hip, mts_arrivals.hip); return hipError_t as int
 int launch_init(const Params& p, hipStream_t stream);

@@ -53,7 +53,7 @@ constexpr int kLast = 64;
 constexpr int kVic = 16;
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, total;
 };
 
 __host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
@@ -68,7 +68,7 @@ __host__ __device__ constexpr uint32_t imax_for(uint32_t I)
 }
 
 __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_t W, uint32_t RB, uint32_t wsz,
-                                                uint32_t policy)
+                                                uint32_t policy, uint32_t qdepth)
 {
     LdsLayout L;
     uint32_t o = 0;
@@ -88,6 +88,11 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     // service-time estimate (i64), the finish count and the state penalty
     o = al8(o);
     L.inf = o;   o += policy == MTS_POLICY_INFAAS ? IM * 24 : 0;
+    // queue cache: per instance the qdepth waiting requests after the head of
+    // line, in (tier, seq) order, 16 bytes each, and their number
+    o = (o + 15u) & ~15u;
+    L.qt = o;    o += IM * qdepth * 16;
+    L.qn = o;    o += qdepth ? IM * 4 : 0;
     L.total = al8(o);
     return L;
 }
@@ -116,6 +121,11 @@ struct Ctx {
     unsigned long long* fsum;  // [I] end-to-end ticks of this tick's finishes
     long long* svc;            // [I] service-time estimate, 1/256 tick
     int *fcnt, *pen;           // [I] this tick's finishes; state penalty in ticks
+    // queue cache behind the head of line (td entries per instance; td = 0: none):
+    // entry {seq, slot word, arrival tick, slot | tier << 12 | admitted << 16}
+    uint4* qt;                 // [I][td]
+    int* qn;                   // [I] cached entries
+    int td;
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -131,7 +141,7 @@ struct Ctx {
 template <int IM, bool INF>
 __device__ inline Ctx carve(char* base, const Params& P)
 {
-    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz, P.policy);
+    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz, P.policy, P.qdepth);
     Ctx C;
     C.stats = reinterpret_cast<unsigned long long*>(base + Y.stats);
     C.occ = reinterpret_cast<unsigned long long*>(base + Y.occ);
@@ -169,6 +179,9 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.nvic = reinterpret_cast<int*>(C.vic + kVic);
     C.wc = reinterpret_cast<unsigned*>(base + Y.wc);
     C.wov = reinterpret_cast<unsigned*>(base + Y.wov);
+    C.td = int(P.qdepth);
+    C.qt = reinterpret_cast<uint4*>(base + Y.qt);
+    C.qn = reinterpret_cast<int*>(base + Y.qn);
     if (INF) {
         C.fsum = reinterpret_cast<unsigned long long*>(base + Y.inf);
         C.svc = reinterpret_cast<long long*>(base + Y.inf + IM * 8);
@@ -364,6 +377,7 @@ __device__ __forceinline__ int wscan(int x, int lane)
 __device__ __forceinline__ void clear_hol(const Ctx& C, int i)
 {
     C.hols[i] = kNoHol; C.holk[i] = kNone; C.hold[i] = 0;
+    if (C.td) C.qn[i] = 0;
 }
 
 __device__ __forceinline__ void set_hol(const Ctx& C, int i, int slot, unsigned long long key, uint32_t word,
@@ -371,6 +385,65 @@ __device__ __forceinline__ void set_hol(const Ctx& C, int i, int slot, unsigned 
 {
     C.hols[i] = slot; C.holk[i] = key; C.hold[i] = blocks_of(wlo(word), C.shift);
     C.hwd[i] = word; C.hmt[i] = meta; C.hta[i] = tarr;
+}
+
+// Queue cache.  Invariant: the head of line and the qn[i] cached entries are
+// the qn[i] + 1 smallest (tier, seq) keys among instance i's waiting
+// requests, in order.  The functions below are per lane (lane-private
+// instance i) and keep it: popping the head promotes the first cached entry
+// (or leaves the head unknown, to be found by a rescan), a new waiting
+// request becomes the head or enters the cache at its place when it is
+// smaller than the last cached entry.
+__device__ __forceinline__ uint4 qc_pack(unsigned long long key, int slot, uint32_t word, uint32_t meta, uint32_t tarr)
+{
+    return make_uint4(uint32_t(key), word, tarr,
+                      uint32_t(slot) | (uint32_t(key >> 32) << 12) | (((meta >> 6) & 1u) << 16));
+}
+__device__ __forceinline__ unsigned long long qc_key(uint4 e)
+{
+    return (static_cast<unsigned long long>((e.w >> 12) & 15u) << 32) | e.x;
+}
+// insert e at position p of instance i's cache (the last entry drops out when full)
+__device__ inline void qc_insert_at(const Ctx& C, int i, int p, uint4 e)
+{
+    uint4* q = C.qt + i * C.td;
+    const int n = C.qn[i];
+    const int last = n < C.td ? n : C.td - 1;
+    for (int k = last; k > p; --k) q[k] = q[k - 1];
+    q[p] = e;
+    C.qn[i] = n < C.td ? n + 1 : C.td;
+}
+// the head of line of i left the queue (admitted or moved)
+__device__ inline void hol_pop(const Ctx& C, int i)
+{
+    if (C.nwait[i] == 0) { clear_hol(C, i); return; }
+    const int n = C.td ? C.qn[i] : 0;
+    if (n == 0) { C.hols[i] = kHolUnknown; return; }
+    uint4* q = C.qt + i * C.td;
+    const uint4 e = q[0];
+    const uint32_t tier = (e.w >> 12) & 15u;
+    set_hol(C, i, int(e.w & 0xFFFu), qc_key(e), e.y, kWaiting | (tier << 2) | (((e.w >> 16) & 1u) << 6), e.z);
+    for (int k = 1; k < n; ++k) q[k - 1] = q[k];
+    C.qn[i] = n - 1;
+}
+// a new waiting request of i (nwait already counts it)
+__device__ inline void hol_insert(const Ctx& C, int i, unsigned long long key, int slot, uint32_t word, uint32_t meta,
+                                  uint32_t tarr)
+{
+    const int h = C.hols[i];
+    if (h == kHolUnknown) return;
+    if (h == kNoHol) { set_hol(C, i, slot, key, word, meta, tarr); if (C.td) C.qn[i] = 0; return; }
+    if (key < C.holk[i]) {
+        if (C.td) qc_insert_at(C, i, 0, qc_pack(C.holk[i], h, C.hwd[i], C.hmt[i], C.hta[i]));
+        set_hol(C, i, slot, key, word, meta, tarr);
+        return;
+    }
+    if (!C.td) return;
+    const uint4* q = C.qt + i * C.td;
+    const int n = C.qn[i];
+    int p = 0;
+    while (p < n && qc_key(q[p]) < key) ++p;
+    if (p < n) qc_insert_at(C, i, p, qc_pack(key, slot, word, meta, tarr));
 }
 
 // file a running request under its finish tick
@@ -408,14 +481,19 @@ __device__ inline void wheel_erase(const Ctx& C, uint32_t fin, int i, int s, int
     }
 }
 
-// head of line of instance i from its slots: smallest (tier, seq) waiting
+// Head of line of instance i from its slots, and behind it as many of the
+// next smallest (tier, seq) waiting requests as the queue cache holds.  Each
+// lane keeps the two smallest keys of its slots; the wave then takes the
+// minimum over the lanes' first keys round by round (the winner moves its
+// second key up), and stops when the winner had more waiting slots than the
+// two it kept (its next key is unknown).  A second read fetches the fields
+// of the requests taken.
 __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
 {
     const size_t b = size_t(i) * C.S;
     const int nch = live_chunks(C, i, lane);
-    unsigned long long bk = kNone;
-    int bs = 0;
-    uint32_t bv = 0, bm = 0;
+    unsigned long long k1 = kNone, k2 = kNone;
+    int s1 = 0, s2 = 0, cnt = 0;
     for (int c0 = 0; c0 < nch; c0 += 4) {
         uint32_t v[4], m[4], q[4];
 #pragma unroll
@@ -428,22 +506,42 @@ __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             if (wst(v[g]) != 1u) continue;
+            ++cnt;
             const unsigned long long k = (static_cast<unsigned long long>((m[g] >> 2) & 15u) << 32) | q[g];
-            if (k < bk) { bk = k; bs = (c0 + g) * 64 + lane; bv = v[g]; bm = m[g]; }
+            const int sl = (c0 + g) * 64 + lane;
+            if (k < k1) { k2 = k1; s2 = s1; k1 = k; s1 = sl; }
+            else if (k < k2) { k2 = k; s2 = sl; }
         }
     }
-    const unsigned long long mn = wmin64(bk);
-    if (mn == kNone) {
+    unsigned long long myk = kNone;
+    int mys = 0, got = 0, taken = 0;
+    for (int r = 0; r <= C.td; ++r) {
+        const unsigned long long mn = wmin64(k1);
+        if (mn == kNone) break;
+        const int wl = ffs64(ballot(k1 == mn));
+        const int sl = rl(s1, wl);
+        if (lane == r) { myk = mn; mys = sl; }
+        got = r + 1;
+        bool unknown = false;
+        if (lane == wl) {
+            k1 = k2; s1 = s2; k2 = kNone;
+            ++taken;
+            unknown = taken >= 2 && cnt > 2;
+        }
+        if (ballot(unknown)) break;
+    }
+    if (got == 0) {
         if (lane == 0) clear_hol(C, i);
         wave_sync();
         return;
     }
-    const int wl = ffs64(ballot(bk == mn));
-    uint32_t ta = lane == wl ? C.tarr[b + bs] : 0u;
-    const int h = rl(bs, wl);
-    const uint32_t word = rlu(bv, wl), meta = rlu(bm, wl);
-    ta = rlu(ta, wl);
-    if (lane == 0) set_hol(C, i, h, mn, word, meta, ta);
+    uint32_t w = 0, mt = 0, ta = 0;
+    if (lane < got) { w = C.hot[b + mys]; mt = C.meta[b + mys]; ta = C.tarr[b + mys]; }
+    if (lane == 0) {
+        set_hol(C, i, mys, myk, w, mt, ta);
+        if (C.td) C.qn[i] = got - 1;
+    }
+    if (lane >= 1 && lane < got) C.qt[i * C.td + lane - 1] = qc_pack(myk, mys, w, mt, ta);
     wave_sync();
 }
 
@@ -508,8 +606,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             stat(C, vt * 8 + kPreempted, 1);
             if (vm) C.flags[i] |= kFlagAbort;
             const unsigned long long key = (static_cast<unsigned long long>(vt) << 32) | static_cast<unsigned>(mx);
-            if (C.hols[i] != kHolUnknown && (C.hols[i] == kNoHol || key < C.holk[i]))
-                set_hol(C, i, vs, key, vw, vmeta, vta);
+            hol_insert(C, i, key, vs, vw, vmeta, vta);
         }
         wave_sync();
     }
@@ -713,7 +810,11 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
         if (w != C.nwait[i] + na) stat(C, kInvariant, 1);
         if (na < w) set_hol(C, i, hs, hk, hw, hm, ht);
         else clear_hol(C, i);
+        if (C.td && na < w) C.qn[i] = min(w - na - 1, C.td);
     }
+    // every waiting request is in the ranked list: the ones after the new head fill the cache
+    if (C.td && lane > na && lane < w && lane - na - 1 < C.td)
+        C.qt[i * C.td + lane - na - 1] = qc_pack(key, slot, word, meta, ta);
     wave_sync();
 }
 
@@ -838,6 +939,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             C.flags[i] = 0;
             C.tmask[i] = 0;
             C.frs[i] = 0;
+            if (C.td) C.qn[i] = 0;
             if (C.svc) C.svc[i] = P.svc[size_t(r) * I + i];
         }
         for (uint32_t b = lane; b < wsz / 2; b += 64) C.wc[b] = 0;
@@ -1049,8 +1151,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
                             tier_inc(C, int(i), tier);
                             wheel_put(C, fin, int(i), h);
-                            if (C.nwait[i] == 0) clear_hol(C, int(i));
-                            else C.hols[i] = kHolUnknown;
+                            hol_pop(C, int(i));
                         }
                     }
                     bat[j] = ballot(batch);
@@ -1242,6 +1343,16 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         if (i >= I) continue;
                         C.live[i] = live_r[j];
                         C.nwait[i] += nadd[j];
+                        if (C.td && nadd[j] > 0) {
+                            // queue cache: an arrival that became the head of line pushes
+                            // the old head to the front of the cache; other arrivals may
+                            // fall between cached entries, so the cache is emptied
+                            if (nadd[j] > (pend_r[j] >= 0 ? 1 : 0)) {
+                                C.qn[i] = 0;
+                            } else if (C.hols[i] >= 0) {
+                                qc_insert_at(C, int(i), 0, qc_pack(C.holk[i], C.hols[i], C.hwd[i], C.hmt[i], C.hta[i]));
+                            }
+                        }
                         nadd[j] = 0;
                         if (pend_r[j] >= 0) {
                             C.hols[i] = kHolPending;
@@ -1470,9 +1581,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             C.live[src] -= 1; C.nwait[src] -= 1;
                             C.live[dst] += 1; C.nwait[dst] += 1;
                             C.frs[src] = 0; C.frs[dst] = 0;
-                            if (C.hols[dst] == kNoHol || key < C.holk[dst]) set_hol(C, dst, ds, key, hw, hm, ht);
-                            if (C.nwait[src] == 0) clear_hol(C, src);
-                            else C.hols[src] = kHolUnknown;
+                            hol_insert(C, dst, key, ds, hw, hm, ht);
+                            hol_pop(C, src);
                             stat(C, kMigQueued, 1);
                         }
                         wave_sync();
@@ -1649,9 +1759,9 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t 
 
 }  // namespace
 
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy)
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy, uint32_t qdepth)
 {
-    return lds_layout(imax_for(I), I, S / 64, RB, wsz, policy).total;
+    return lds_layout(imax_for(I), I, S / 64, RB, wsz, policy, qdepth).total;
 }
 
 int launch_init(const Params& p, hipStream_t stream)
@@ -1694,7 +1804,7 @@ void launch_step_t(const Params& p, unsigned long long t0, uint32_t nt, uint32_t
 
 size_t step_lds(const Params& p)
 {
-    const size_t lds = lds_bytes(p.I, p.S, p.RB, p.wsz, p.policy);
+    const size_t lds = lds_bytes(p.I, p.S, p.RB, p.wsz, p.policy, p.qdepth);
     if (lds > 64 * 1024) {
         // raise the dynamic LDS limit; a real failure shows up at the launch
         (void)hipFuncSetAttribute(step_fn(p), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));

@@ -83,7 +83,8 @@ class mts_state_view(ctypes.Structure):
 EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest",
             "mts_export_state", "mts_import_state", "mts_get_table", "mts_get_headroom",
             "mts_tick", "mts_set_tick", "mts_set_launch", "mts_get_launch", "mts_set_timing",
-            "mts_get_timing", "mts_set_draining", "mts_destroy", "mts_strerror")
+            "mts_get_timing", "mts_set_draining", "mts_set_queue_cache", "mts_get_queue_cache",
+            "mts_destroy", "mts_strerror")
 
 _lib = None
 
@@ -115,6 +116,8 @@ def load_library(path=LIB_PATH):
     L.mts_get_launch.argtypes = [vp, ctypes.POINTER(u32), ctypes.POINTER(u32)]
     L.mts_set_timing.argtypes = [vp, ci]
     L.mts_set_draining.argtypes = [vp, u32, u32, vp]
+    L.mts_set_queue_cache.argtypes = [vp, u32]
+    L.mts_get_queue_cache.argtypes = [vp, ctypes.POINTER(u32)]
     L.mts_get_timing.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                  ctypes.POINTER(u32)]
     L.mts_destroy.argtypes = [vp]
@@ -123,7 +126,8 @@ def load_library(path=LIB_PATH):
     L.mts_strerror.restype = ctypes.c_char_p
     for f in ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest", "mts_export_state",
               "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch", "mts_get_launch",
-              "mts_set_timing", "mts_get_timing", "mts_set_draining"):
+              "mts_set_timing", "mts_get_timing", "mts_set_draining", "mts_set_queue_cache",
+              "mts_get_queue_cache"):
         getattr(L, f).restype = ci
     _lib = L
     return L
@@ -297,6 +301,17 @@ class Scheduler:
                     drain=np.zeros(nr * self.I, np.uint8),
                     hist=np.zeros(nr * 2 * MAX_TIERS * HIST_BINS, np.uint32),
                     svc=np.zeros(nr * self.I, np.int64))
+
+    @property
+    def queue_cache(self):
+        """Queue-cache entries per instance behind the head of line (LDS)."""
+        d = ctypes.c_uint32(0)
+        _check("mts_get_queue_cache", load_library().mts_get_queue_cache(self._h, ctypes.byref(d)))
+        return d.value
+
+    @queue_cache.setter
+    def queue_cache(self, depth):
+        _check("mts_set_queue_cache", load_library().mts_set_queue_cache(self._h, depth))
 
     def set_draining(self, flags, r0=0, nr=None):
         """flags: 0/1 per (replica, instance) of replicas [r0, r0 + nr)."""

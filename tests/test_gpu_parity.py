@@ -415,3 +415,35 @@ def test_infaas_estimate_is_validated():
     with pytest.raises(MtsError) as e:
         g.import_state(st)
     assert e.value.code == -1
+
+
+# ---------------------------------------------------------------------------
+# queue cache (the waiting requests behind each head of line, kept in LDS):
+# a performance setting that must never change a result
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("depth", [0, 1, 3, 7, 15])
+def test_queue_cache_depth_does_not_change_results(depth):
+    cfg = scaled("gauss10", replicas_per_group=6)
+    g = Scheduler(cfg)
+    g.queue_cache = depth
+    assert g.queue_cache == depth
+    g.step(700)
+    o = oracle.Oracle(cfg)
+    o.step(700)
+    assert_same(g.export(), o.export(), "gauss10 depth %d" % depth)
+    for case in (3, 8, 14):
+        c = _random_cfg(case)
+        c["groups"][0]["n_replicas"] = 2
+        h = Scheduler(c)
+        h.queue_cache = depth
+        h.step(250)
+        o = oracle.Oracle(c)
+        o.step(250)
+        assert_same(h.export(), o.export(), "random %d depth %d" % (case, depth))
+
+
+def test_queue_cache_depth_is_validated():
+    g = Scheduler(preset("tiny"))
+    assert 0 <= g.queue_cache <= 7
+    with pytest.raises(MtsError):
+        g.queue_cache = 16
