@@ -1124,34 +1124,40 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     bool batch = false, fresh = false;
                     if (i < I && C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]) {
                         const int nw = C.nwait[i];
-                        if (nw >= 2 && nw <= 64) {
-                            fresh = C.frs[i] != 0;
-                            batch = !fresh;
+                        const bool cached = C.td && C.qn[i] > 0;
+                        if (nw >= 2 && nw <= 64 && C.frs[i]) {
+                            fresh = true;
+                        } else if (nw >= 2 && nw <= 64 && !cached) {
+                            batch = true;
                         } else {
-                            // the only waiting request, or a queue longer than a wave:
-                            // admit the head of line alone
-                            any = any || nw > 1;
-                            const int h = C.hols[i], dem = C.hold[i];
-                            const uint32_t w = C.hwd[i], m = C.hmt[i];
-                            const uint32_t len = wlo(w), rem = wmid(w);
-                            const uint32_t fin = t + rem;
-                            const size_t hb = size_t(i) * S + h;
-                            C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
-                            C.meta[hb] = uint8_t((m & ~3u) | kRunning | kAdmitted);
-                            const int tier = int((m >> 2) & 15u);
-                            if (!(m & kAdmitted)) {
-                                stat(C, tier * 8 + kAdmittedCnt, 1);
-                                stat(C, tier * 8 + kQdelay, t - C.hta[i]);
-                                hist_add(C, kHistQdelay, tier, t - C.hta[i]);
-                            }
-                            C.freeb[i] -= dem;
-                            C.held[i] += dem;
-                            C.B[i] += 1;
-                            C.nwait[i] -= 1;
-                            c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
-                            tier_inc(C, int(i), tier);
-                            wheel_put(C, fin, int(i), h);
-                            hol_pop(C, int(i));
+                            // the only waiting request, a queue longer than a wave or one
+                            // whose next requests are cached: admit heads of line one at a
+                            // time while they fit and are known
+                            do {
+                                const int h = C.hols[i], dem = C.hold[i];
+                                const uint32_t w = C.hwd[i], m = C.hmt[i];
+                                const uint32_t len = wlo(w), rem = wmid(w);
+                                const uint32_t fin = t + rem;
+                                const size_t hb = size_t(i) * S + h;
+                                C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
+                                C.meta[hb] = uint8_t((m & ~3u) | kRunning | kAdmitted);
+                                const int tier = int((m >> 2) & 15u);
+                                if (!(m & kAdmitted)) {
+                                    stat(C, tier * 8 + kAdmittedCnt, 1);
+                                    stat(C, tier * 8 + kQdelay, t - C.hta[i]);
+                                    hist_add(C, kHistQdelay, tier, t - C.hta[i]);
+                                }
+                                C.freeb[i] -= dem;
+                                C.held[i] += dem;
+                                C.B[i] += 1;
+                                C.nwait[i] -= 1;
+                                c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
+                                tier_inc(C, int(i), tier);
+                                wheel_put(C, fin, int(i), h);
+                                hol_pop(C, int(i));
+                            } while (C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]);
+                            // an unknown head of line is found by the next round's rescan
+                            any = any || C.hols[i] == kHolUnknown;
                         }
                     }
                     bat[j] = ballot(batch);
@@ -1516,21 +1522,41 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         if (d >= 0) { atomicOr(&C.flags[i], kFlagBusy); atomicOr(&C.flags[d], kFlagBusy); }
                     }
                     wave_sync();
-                    int mine = 0;
-                    for (uint32_t i = lane; i < I; i += 64) {
-                        if (C.flags[i] & kFlagBusy) continue;
-                        ++mine;
-                        // a draining instance's F is minus infinity (sentinel)
-                        const double fi = C.drn[i] ? -__builtin_inf() : C.fd[i];
-                        int rank = 0;
-                        for (uint32_t j = 0; j < I; ++j) {
-                            if (C.flags[j] & kFlagBusy) continue;
-                            const double fj = C.drn[j] ? -__builtin_inf() : C.fd[j];
-                            rank += (fj < fi || (fj == fi && j < i)) ? 1 : 0;
-                        }
-                        C.order[rank] = int(i);
+                    // rank the instances not in a migration by (F, index): F as an
+                    // order-preserving 64-bit key (a draining instance's F is minus
+                    // infinity), compared with every other lane's key through readlane
+                    unsigned long long fk[IPL];
+                    unsigned long long avm[IPL];
+                    int n2 = 0;
+#pragma unroll
+                    for (int j = 0; j < IPL; ++j) {
+                        const uint32_t i = lane + 64 * j;
+                        const bool av = i < I && !(C.flags[i] & kFlagBusy);
+                        const double f = i < I && C.drn[i] ? -__builtin_inf() : (i < I ? C.fd[i] : 0.0);
+                        const unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(f));
+                        fk[j] = (bits >> 63) ? ~bits : bits | (1ull << 63);
+                        avm[j] = ballot(av);
+                        n2 += __popcll(avm[j]);
                     }
-                    const int n2 = wsum(mine);
+                    int rk[IPL];
+#pragma unroll
+                    for (int j = 0; j < IPL; ++j) rk[j] = 0;
+#pragma unroll
+                    for (int jj = 0; jj < IPL; ++jj) {
+                        for (unsigned long long mm = avm[jj]; mm; mm &= mm - 1) {
+                            const int l = ffs64(mm);
+                            const unsigned long long kl = rl64(fk[jj], l);
+                            const int il = 64 * jj + l;
+#pragma unroll
+                            for (int j = 0; j < IPL; ++j) {
+                                const int i = lane + 64 * j;
+                                rk[j] += (kl < fk[j] || (kl == fk[j] && il < i)) ? 1 : 0;
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < IPL; ++j)
+                        if ((avm[j] >> lane) & 1ull) C.order[rk[j]] = lane + 64 * j;
                     wave_sync();
                     // Pairs (L[k], L[n2 - 1 - k]) use disjoint instances and one
                     // snapshot of F, so the stopping pair is found for all pairs at
