@@ -92,7 +92,7 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     // line, in (tier, seq) order, 16 bytes each, and their number
     o = (o + 15u) & ~15u;
     L.qt = o;    o += IM * qdepth * 16;
-    L.qn = o;    o += qdepth ? IM * 4 : 0;
+    L.qn = o;    o += qdepth ? IM * 8 : 0;
     L.total = al8(o);
     return L;
 }
@@ -123,8 +123,9 @@ struct Ctx {
     int *fcnt, *pen;           // [I] this tick's finishes; state penalty in ticks
     // queue cache behind the head of line (td entries per instance; td = 0: none):
     // entry {seq, slot word, arrival tick, slot | tier << 12 | admitted << 16}
-    uint4* qt;                 // [I][td]
+    uint4* qt;                 // [I][td] a ring: entry k at (qh + k) mod td
     int* qn;                   // [I] cached entries
+    int* qh;                   // [I] ring position of the first entry
     int td;
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
@@ -182,6 +183,7 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.td = int(P.qdepth);
     C.qt = reinterpret_cast<uint4*>(base + Y.qt);
     C.qn = reinterpret_cast<int*>(base + Y.qn);
+    C.qh = C.qn + IM;
     if (INF) {
         C.fsum = reinterpret_cast<unsigned long long*>(base + Y.inf);
         C.svc = reinterpret_cast<long long*>(base + Y.inf + IM * 8);
@@ -403,15 +405,27 @@ __device__ __forceinline__ unsigned long long qc_key(uint4 e)
 {
     return (static_cast<unsigned long long>((e.w >> 12) & 15u) << 32) | e.x;
 }
+__device__ __forceinline__ int qc_at(const Ctx& C, int i, int k)
+{
+    const int x = C.qh[i] + k;
+    return i * C.td + (x >= C.td ? x - C.td : x);
+}
 // insert e at position p of instance i's cache (the last entry drops out when full)
 __device__ inline void qc_insert_at(const Ctx& C, int i, int p, uint4 e)
 {
-    uint4* q = C.qt + i * C.td;
     const int n = C.qn[i];
+    if (p == 0) {
+        // in front: the ring start moves back (over the last entry when full)
+        const int h = C.qh[i];
+        C.qh[i] = h == 0 ? C.td - 1 : h - 1;
+        C.qt[qc_at(C, i, 0)] = e;
+        C.qn[i] = n < C.td ? n + 1 : C.td;
+        return;
+    }
     const int last = n < C.td ? n : C.td - 1;
-    for (int k = last; k > p; --k) q[k] = q[k - 1];
-    q[p] = e;
-    C.qn[i] = n < C.td ? n + 1 : C.td;
+    for (int k = last; k > p; --k) C.qt[qc_at(C, i, k)] = C.qt[qc_at(C, i, k - 1)];
+    C.qt[qc_at(C, i, p)] = e;
+    C.qn[i] = last + 1;
 }
 // the head of line of i left the queue (admitted or moved)
 __device__ inline void hol_pop(const Ctx& C, int i)
@@ -419,11 +433,11 @@ __device__ inline void hol_pop(const Ctx& C, int i)
     if (C.nwait[i] == 0) { clear_hol(C, i); return; }
     const int n = C.td ? C.qn[i] : 0;
     if (n == 0) { C.hols[i] = kHolUnknown; return; }
-    uint4* q = C.qt + i * C.td;
-    const uint4 e = q[0];
+    const uint4 e = C.qt[qc_at(C, i, 0)];
     const uint32_t tier = (e.w >> 12) & 15u;
     set_hol(C, i, int(e.w & 0xFFFu), qc_key(e), e.y, kWaiting | (tier << 2) | (((e.w >> 16) & 1u) << 6), e.z);
-    for (int k = 1; k < n; ++k) q[k - 1] = q[k];
+    const int h = C.qh[i] + 1;
+    C.qh[i] = h == C.td ? 0 : h;
     C.qn[i] = n - 1;
 }
 // a new waiting request of i (nwait already counts it)
@@ -439,10 +453,9 @@ __device__ inline void hol_insert(const Ctx& C, int i, unsigned long long key, i
         return;
     }
     if (!C.td) return;
-    const uint4* q = C.qt + i * C.td;
     const int n = C.qn[i];
     int p = 0;
-    while (p < n && qc_key(q[p]) < key) ++p;
+    while (p < n && qc_key(C.qt[qc_at(C, i, p)]) < key) ++p;
     if (p < n) qc_insert_at(C, i, p, qc_pack(key, slot, word, meta, tarr));
 }
 
@@ -487,24 +500,26 @@ __device__ inline void wheel_erase(const Ctx& C, uint32_t fin, int i, int s, int
 // minimum over the lanes' first keys round by round (the winner moves its
 // second key up), and stops when the winner had more waiting slots than the
 // two it kept (its next key is unknown).  A second read fetches the fields
-// of the requests taken.
+// of the requests taken.  GR chunks of 64 slots are read per memory round
+// trip (more for the large instances of the kernels with registers to spare).
+template <int GR>
 __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
 {
     const size_t b = size_t(i) * C.S;
     const int nch = live_chunks(C, i, lane);
     unsigned long long k1 = kNone, k2 = kNone;
     int s1 = 0, s2 = 0, cnt = 0;
-    for (int c0 = 0; c0 < nch; c0 += 4) {
-        uint32_t v[4], m[4], q[4];
+    for (int c0 = 0; c0 < nch; c0 += GR) {
+        uint32_t v[GR], m[GR], q[GR];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int g = 0; g < GR; ++g) {
             const bool in = c0 + g < nch;
             v[g] = in ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
             m[g] = in ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
             q[g] = in ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
         }
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int g = 0; g < GR; ++g) {
             if (wst(v[g]) != 1u) continue;
             ++cnt;
             const unsigned long long k = (static_cast<unsigned long long>((m[g] >> 2) & 15u) << 32) | q[g];
@@ -539,7 +554,7 @@ __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
     if (lane < got) { w = C.hot[b + mys]; mt = C.meta[b + mys]; ta = C.tarr[b + mys]; }
     if (lane == 0) {
         set_hol(C, i, mys, myk, w, mt, ta);
-        if (C.td) C.qn[i] = got - 1;
+        if (C.td) { C.qn[i] = got - 1; C.qh[i] = 0; }
     }
     if (lane >= 1 && lane < got) C.qt[i * C.td + lane - 1] = qc_pack(myk, mys, w, mt, ta);
     wave_sync();
@@ -810,7 +825,7 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
         if (w != C.nwait[i] + na) stat(C, kInvariant, 1);
         if (na < w) set_hol(C, i, hs, hk, hw, hm, ht);
         else clear_hol(C, i);
-        if (C.td && na < w) C.qn[i] = min(w - na - 1, C.td);
+        if (C.td && na < w) { C.qn[i] = min(w - na - 1, C.td); C.qh[i] = 0; }
     }
     // every waiting request is in the ranked list: the ones after the new head fill the cache
     if (C.td && lane > na && lane < w && lane - na - 1 < C.td)
@@ -939,7 +954,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             C.flags[i] = 0;
             C.tmask[i] = 0;
             C.frs[i] = 0;
-            if (C.td) C.qn[i] = 0;
+            if (C.td) { C.qn[i] = 0; C.qh[i] = 0; }
             if (C.svc) C.svc[i] = P.svc[size_t(r) * I + i];
         }
         for (uint32_t b = lane; b < wsz / 2; b += 64) C.wc[b] = 0;
@@ -1114,7 +1129,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 for (int j = 0; j < IPL; ++j) {
                     const uint32_t i = lane + 64 * j;
                     for (unsigned long long m = ballot(i < I && C.hols[i] == kHolUnknown); m; m &= m - 1)
-                        rescan_hol(C, 64 * j + ffs64(m), lane);
+                        rescan_hol<(IM >= 128 ? 16 : 4)>(C, 64 * j + ffs64(m), lane);
                 }
                 bool any = false;
                 unsigned long long bat[IPL], frm[IPL];
@@ -1235,8 +1250,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 // per-instance dispatch state in registers: lane l, register j <-> instance 64 j + l
                 // key: F of the instances that can take an arrival (minus infinity
                 // for a full instance and, in the first mode, for a draining one)
+                // (an arrival that becomes an instance's head of line updates its
+                // demand, num and F in LDS at once: only that instance's lane
+                // touches them until the write-back)
                 double key[IPL];
-                int live_r[IPL], fr_r[IPL], hs_r[IPL], den_r[IPL], dem_r[IPL], nadd[IPL], pend_r[IPL], drn_r[IPL];
+                int live_r[IPL], nadd[IPL], pend_r[IPL];
                 unsigned long long hk_r[IPL];
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
@@ -1245,21 +1263,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     pend_r[j] = -1;
                     if (i < I) {
                         live_r[j] = C.live[i];
-                        fr_r[j] = C.freeb[i];
-                        den_r[j] = C.den[i];
-                        dem_r[j] = C.hold[i];
-                        int hs = 0;
-                        const int tm = C.tmask[i];
-#pragma unroll
-                        for (int p = 0; p < kTiers; ++p) hs += (tm >> p) & 1 ? C.hq[p] : 0;
-                        hs_r[j] = hs;
                         hk_r[j] = C.hols[i] == kNoHol ? kNone : C.holk[i];
-                        drn_r[j] = C.drn[i];
-                        key[j] = live_r[j] < int(S) && !drn_r[j] ? (infaas ? -infaas_cost(C, P, int(i), 0) : C.fd[i])
+                        key[j] = live_r[j] < int(S) && !C.drn[i] ? (infaas ? -infaas_cost(C, P, int(i), 0) : C.fd[i])
                                                                  : -__builtin_inf();
                     } else {
-                        live_r[j] = int(S); fr_r[j] = 0; den_r[j] = 1; dem_r[j] = 0; hs_r[j] = 0; hk_r[j] = 0;
-                        drn_r[j] = 0;
+                        live_r[j] = int(S); hk_r[j] = 0;
                         key[j] = -__builtin_inf();
                     }
                 }
@@ -1286,7 +1294,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
 #pragma unroll
                                 for (int j = 0; j < IPL; ++j) {
                                     const uint32_t i = lane + 64 * j;
-                                    key[j] = i < I && live_r[j] < int(S) && drn_r[j]
+                                    key[j] = i < I && live_r[j] < int(S) && C.drn[i]
                                                  ? (infaas ? -infaas_cost(C, P, int(i), nadd[j]) : C.fd[i])
                                                  : -__builtin_inf();
                                 }
@@ -1329,9 +1337,15 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                 if (becomes) {
                                     hk_r[j] = hk;
                                     pend_r[j] = int(k0 + k);
-                                    dem_r[j] = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
-                                    const int num = 256 * (fr_r[j] - dem_r[j]) - hs_r[j];
-                                    if (!infaas) key[j] = double(num) / double(den_r[j]);
+                                    // Eq. 1-2: F moves by the change of head-of-line demand
+                                    const int ii = lc + 64 * j;
+                                    const int dem = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
+                                    const int num = C.num[ii] - 256 * (dem - C.hold[ii]);
+                                    const double f = double(num) / double(C.den[ii]);
+                                    C.hold[ii] = dem;
+                                    C.num[ii] = num;
+                                    C.fd[ii] = f;
+                                    if (!infaas) key[j] = f;
                                 }
                                 if (infaas) key[j] -= double(P.alpha256) * double(m);
                                 if (nl >= int(S)) key[j] = -__builtin_inf();
@@ -1364,10 +1378,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             C.hols[i] = kHolPending;
                             C.pend[i] = pend_r[j];
                             C.holk[i] = hk_r[j];
-                            C.hold[i] = dem_r[j];
-                            const int num = 256 * (fr_r[j] - dem_r[j]) - hs_r[j];
-                            C.num[i] = num;
-                            C.fd[i] = double(num) / double(den_r[j]);
                             pend_r[j] = -1;
                         }
                     }
