@@ -76,7 +76,7 @@ class _Cfg(ctypes.Structure):
                 ("groups", ctypes.POINTER(_Group)),
                 ("policy", ctypes.c_uint32), ("ewma_shift", ctypes.c_uint32),
                 ("alpha", ctypes.c_int32), ("beta", ctypes.c_int32), ("gamma_w", ctypes.c_int32),
-                ("pen_over", ctypes.c_uint32), ("pen_intf", ctypes.c_uint32), ("pad3", ctypes.c_uint32)]
+                ("pen_over", ctypes.c_uint32), ("pen_intf", ctypes.c_uint32), ("tier_blind", ctypes.c_uint32)]
 
 
 _lib = None
@@ -192,6 +192,7 @@ def make_cfg(cfg):
     c.groups = groups
     d = cfg.get("dispatch", {"policy": "llumnix"})
     c.policy = _POLICY[d["policy"]]
+    c.tier_blind = 1 if cfg.get("tier_blind") else 0
     if d["policy"] == "infaas":
         c.alpha, c.beta, c.gamma_w = d["alpha"], d["beta"], d["gamma"]
         c.pen_over, c.pen_intf = d["pen_overloaded"], d["pen_interfered"]

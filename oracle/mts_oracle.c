@@ -42,6 +42,13 @@
  * its head of line does not fit its free blocks after admission, else
  * INTERFERED when it preempted a request in this tick, else ACTIVE (0).  It
  * keeps no freeness for dispatch and never migrates.
+ * Tier-blind scheduling (the priority-blind vLLM local scheduler the paper
+ * pairs with INFaaS, Section 5.3): when set, tiers no longer order anything
+ * -- arrivals are dispatched in arrival order, each instance's queue is
+ * served first come first served, preemption takes the newest running
+ * request and the migration candidate is chosen by size and age alone --
+ * while tiers still label requests in the counters and histograms and still
+ * enter the headroom of Eq. 4.
  * Auto-scaling (Section 3.6): every tick, after admission, the cluster
  * average of the normal-priority freeness F_normal (Eq. 1 without headroom)
  * is compared with the scale-out (-0.5) and scale-in (1.5) thresholds; the
@@ -110,7 +117,8 @@ typedef struct {
     /* global policy: 0 Llumnix freeness, 1 INFaaS cost */
     uint32_t policy, ewma_shift;
     int32_t alpha, beta, gamma_w;
-    uint32_t pen_over, pen_intf, pad3;
+    uint32_t pen_over, pen_intf;
+    uint32_t tier_blind;         /* 1: tiers order nothing (priority-blind local scheduler) */
 } or_cfg;
 
 enum { POLICY_LLUMNIX = 0, POLICY_INFAAS = 1 };
@@ -360,13 +368,18 @@ static int lowest_empty(const or_ctx *x, replica_t *rp, uint32_t i)
 }
 
 /* head of line: the waiting request with the smallest (tier, seq) */
+/* the rank a tier gives in every ordering: the tier itself, or 0 for all
+ * when scheduling is tier-blind */
+static uint32_t prio(const or_ctx *x, uint32_t tier) { return x->cfg.tier_blind ? 0 : tier; }
+
 static int head_of_line(const or_ctx *x, replica_t *rp, uint32_t i)
 {
     slot_t *sl = inst_slots(x, rp, i);
     int h = -1;
     for (uint32_t s = 0; s < x->S; ++s) {
         if (sl[s].st != ST_WAITING) continue;
-        if (h < 0 || sl[s].tier < sl[h].tier || (sl[s].tier == sl[h].tier && sl[s].seq < sl[h].seq)) h = (int)s;
+        uint32_t ps = prio(x, sl[s].tier);
+        if (h < 0 || ps < prio(x, sl[h].tier) || (ps == prio(x, sl[h].tier) && sl[s].seq < sl[h].seq)) h = (int)s;
     }
     return h;
 }
@@ -494,7 +507,9 @@ static void phase_decode(or_ctx *x, replica_t *rp, uint64_t t, uint8_t *abort_pe
             int v = -1;
             for (uint32_t s = 0; s < x->S; ++s) {
                 if (sl[s].st != ST_RUNNING) continue;
-                if (v < 0 || sl[s].tier > sl[v].tier || (sl[s].tier == sl[v].tier && sl[s].seq > sl[v].seq)) v = (int)s;
+                if (v < 0) { v = (int)s; continue; }
+                uint32_t ps = prio(x, sl[s].tier), pv = prio(x, sl[v].tier);
+                if (ps > pv || (ps == pv && sl[s].seq > sl[v].seq)) v = (int)s;
             }
             if (v < 0) break;  /* only reachable from an inconsistent imported state */
             if (sl[v].migrating) { sl[v].migrating = 0; abort_pending[i] = 1; }
@@ -645,11 +660,12 @@ static void phase_dispatch(or_ctx *x, replica_t *rp, uint64_t t)
         slot_t *sl = inst_slots(x, rp, i);
         for (uint32_t s = 0; s < x->S; ++s) nempty[i] += sl[s].st == ST_EMPTY;
     }
-    /* strict tier order (tier 0 first), FCFS within a tier */
-    for (uint32_t p = 0; p < K; ++p) {
+    /* strict tier order (tier 0 first), FCFS within a tier; arrival order
+     * when tier-blind */
+    for (uint32_t p = 0; p < (x->cfg.tier_blind ? 1 : K); ++p) {
         for (uint32_t k = 0; k < n; ++k) {
             const uint32_t *a = rp->arr + 3 * (size_t)k;
-            if (a[0] != p) continue;
+            if (prio(x, a[0]) != p) continue;
             int best = -1, fallback = 0;
             if (infaas) {
                 /* argmin cost over the non-draining instances with a free
@@ -680,14 +696,14 @@ static void phase_dispatch(or_ctx *x, replica_t *rp, uint64_t t)
                     fallback = best >= 0;
                 }
             }
-            if (best < 0) { rp->stats[p * 8 + F_REJECTED]++; continue; }
+            if (best < 0) { rp->stats[a[0] * 8 + F_REJECTED]++; continue; }
             if (fallback) rp->stats[S_DRAIN_FALLBACK]++;
             int s = lowest_empty(x, rp, (uint32_t)best);
             slot_t *sl = &inst_slots(x, rp, (uint32_t)best)[s];
-            sl->st = ST_WAITING; sl->tier = (uint8_t)p; sl->admitted = 0; sl->migrating = 0;
+            sl->st = ST_WAITING; sl->tier = (uint8_t)a[0]; sl->admitted = 0; sl->migrating = 0;
             sl->len = a[1]; sl->rem = a[2]; sl->seq = seq0 + k; sl->tarr = (uint32_t)t;
             nempty[best]--;
-            rp->stats[p * 8 + F_DISPATCHED]++;
+            rp->stats[a[0] * 8 + F_DISPATCHED]++;
             freeness(x, rp, (uint32_t)best, &num[best], &den[best]);
         }
     }
@@ -794,8 +810,8 @@ static void phase_migrate(or_ctx *x, replica_t *rp, uint64_t t)
                 if (sl[s].st != ST_RUNNING || sl[s].migrating) continue;
                 if (c < 0) { c = (int)s; continue; }
                 uint32_t bs = blocks(x, sl[s].len), bc = blocks(x, sl[c].len);
-                if (sl[s].tier > sl[c].tier ||
-                    (sl[s].tier == sl[c].tier && (bs < bc || (bs == bc && sl[s].seq > sl[c].seq))))
+                uint32_t ps = prio(x, sl[s].tier), pc = prio(x, sl[c].tier);
+                if (ps > pc || (ps == pc && (bs < bc || (bs == bc && sl[s].seq > sl[c].seq))))
                     c = (int)s;
             }
             /* nothing to move: only a draining source can be empty; its pair
@@ -895,7 +911,7 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
     if (!cfg || cfg->n_groups == 0 || !cfg->groups) return NULL;
     if (cfg->n_instances == 0 || cfg->n_instances > 256 || cfg->slots == 0) return NULL;
     if (cfg->block_tokens == 0 || cfg->kv_blocks == 0 || cfg->mig_interval == 0 || cfg->theta_den <= 0) return NULL;
-    if (cfg->policy > POLICY_INFAAS || cfg->ewma_shift > 16) return NULL;
+    if (cfg->policy > POLICY_INFAAS || cfg->ewma_shift > 16 || cfg->tier_blind > 1) return NULL;
     uint32_t R = 0;
     for (uint32_t g = 0; g < cfg->n_groups; ++g) {
         if (cfg->groups[g].K == 0 || cfg->groups[g].K > OR_MAX_TIERS) return NULL;

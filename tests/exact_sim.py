@@ -26,6 +26,11 @@ of line against the free blocks (OVERLOADED) or this tick's preemptions
 mean end-to-end time (1/256 tick, floors as the policy defines them), the
 minimum by exhaustive search, and no migration at all.
 
+Tier-blind scheduling (the priority-blind local scheduler of the paper's
+INFaaS baseline, Section 5.3) replaces the tier by a constant in every
+ordering -- dispatch order, queue order, preemption victim, migration
+candidate -- and nowhere else.
+
 The auto-scaling signal (Section 3.6)
 averages F_normal -- Eq. 1 with no headroom at all -- in fixed point with
 floor(F * 2^20) per instance.
@@ -86,6 +91,7 @@ class ExactSim:
         self.infaas = d["policy"] == "infaas"
         self.dsp = d
         self.svc = [0] * self.I  # INFaaS service-time estimate, 1/256 tick
+        self.blind = bool(cfg.get("tier_blind"))
         self.t = 0
 
     # -- helpers --------------------------------------------------------
@@ -95,9 +101,13 @@ class ExactSim:
     def requests(self, i, st):
         return [(s, r) for s, r in enumerate(self.slots[i]) if r is not None and r.st == st]
 
+    def rank(self, tier):
+        """What a tier counts for in an ordering."""
+        return 0 if self.blind else tier
+
     def hol(self, i):
         w = self.requests(i, WAITING)
-        return min(w, key=lambda sr: (sr[1].tier, sr[1].seq))[0] if w else None
+        return min(w, key=lambda sr: (self.rank(sr[1].tier), sr[1].seq))[0] if w else None
 
     def lowest_empty(self, i):
         for s, r in enumerate(self.slots[i]):
@@ -158,7 +168,7 @@ class ExactSim:
             need = sum(1 for _, r in self.requests(i, RUNNING) if r.len % self.blk == 0)
             while need > self.free[i]:
                 run = self.requests(i, RUNNING)
-                v, rv = max(run, key=lambda sr: (sr[1].tier, sr[1].seq))
+                v, rv = max(run, key=lambda sr: (self.rank(sr[1].tier), sr[1].seq))
                 if rv.migrating:
                     rv.migrating = 0
                     aborted.add(i)
@@ -230,7 +240,7 @@ class ExactSim:
         self.next_seq += len(arrivals)
         for tier, _, _ in arrivals:
             st[tier * 8 + F_ARRIVED] += 1
-        order = sorted(range(len(arrivals)), key=lambda k: (arrivals[k][0], k))
+        order = sorted(range(len(arrivals)), key=lambda k: (self.rank(arrivals[k][0]), k))
         for k in order:
             tier, prompt, out = arrivals[k]
             room = [i for i in range(self.I) if self.lowest_empty(i) is not None]
@@ -310,7 +320,7 @@ class ExactSim:
                     run = [(s, r) for s, r in self.requests(src, RUNNING) if not r.migrating]
                     if not run:  # an empty draining source: nothing to move
                         continue
-                    c, rc = max(run, key=lambda sr: (sr[1].tier, -self.blocks(sr[1].len), sr[1].seq))
+                    c, rc = max(run, key=lambda sr: (self.rank(sr[1].tier), -self.blocks(sr[1].len), sr[1].seq))
                     self.slots[dst][ds] = Request(INBOUND, 0, 0, 0, 0, 0)
                     rc.migrating = 1
                     self.mig[src] = [dst, c, ds, 0]

@@ -141,3 +141,71 @@ def test_random_infaas_clusters(case):
     plan = _random_drain_plan(rng, c["n_instances"], 250) if case % 2 else None
     s = run_pair(c, 250, plan)
     assert s[86] == 0 and s[80:84].sum() == 0
+
+
+# ---------------------------------------------------------------------------
+# tier-blind scheduling: the priority-blind local scheduler of the paper's
+# INFaaS baseline (Section 5.3)
+# ---------------------------------------------------------------------------
+def _strip_tiers(a):
+    """State with the tier label removed from every slot's meta."""
+    b = dict(a)
+    b["meta"] = a["meta"] & np.uint8(~(15 << 2) & 0xFF)
+    return b
+
+
+@pytest.mark.parametrize("mix", ["uniform", "gauss", "explicit"])
+def test_tier_blind_infaas_is_the_single_tier_system(mix):
+    # INFaaS never looks at tiers and a tier-blind local scheduler does not
+    # either, so K tiers behave like one: same slots, same request order,
+    # same estimates; the per-tier counters add up to the single tier's
+    c = preset("tiny")
+    c["arrival"] = dict(kind="poisson", mean=3.0)
+    c["dispatch"] = dict(INFAAS)
+    c["tier_blind"] = 1
+    tiers = dict(kind=mix)
+    if mix == "gauss":
+        tiers.update(mu=1.5, sigma=1.0)
+    if mix == "explicit":
+        tiers.update(probs=[0.1, 0.2, 0.3, 0.4])
+    c["groups"] = [dict(n_replicas=1, K=4, tiers=tiers)]
+    one = dict(c)
+    one["groups"] = [dict(n_replicas=1, K=1, tiers=dict(kind="uniform"))]
+    a, b = oracle.Oracle(c), oracle.Oracle(one)
+    a.step(800)
+    b.step(800)
+    sa, sb = a.export(), b.export()
+    for k in ("lr", "seq", "tarr", "free", "mig", "next_seq", "svc"):
+        assert np.array_equal(sa[k], sb[k]), k
+    assert np.array_equal(_strip_tiers(sa)["meta"], sb["meta"])
+    per_a = sa["stats"][:80].reshape(10, 8).astype(np.int64).sum(axis=0)
+    per_b = sb["stats"][:80].reshape(10, 8).astype(np.int64)[0]
+    assert np.array_equal(per_a, per_b)
+    assert np.array_equal(sa["stats"][80:], sb["stats"][80:])
+    assert len(set(int(v) for v in (sa["meta"][(sa["meta"] & 3) != 0] >> 2) & 15)) > 1
+
+
+def test_tier_aware_infaas_is_not_the_single_tier_system():
+    # the same run with the priority-ordered local queue differs
+    c = preset("tiny")
+    c["arrival"] = dict(kind="poisson", mean=3.0)
+    c["dispatch"] = dict(INFAAS)
+    c["groups"] = [dict(n_replicas=1, K=4, tiers=dict(kind="uniform"))]
+    one = dict(c)
+    one["groups"] = [dict(n_replicas=1, K=1, tiers=dict(kind="uniform"))]
+    a, b = oracle.Oracle(c), oracle.Oracle(one)
+    a.step(800)
+    b.step(800)
+    assert not np.array_equal(a.export()["seq"], b.export()["seq"])
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_random_tier_blind_clusters(case):
+    rng = random.Random(9000 + case)
+    c = _random_cfg(rng)
+    c["tier_blind"] = 1
+    if case % 2:
+        c["dispatch"] = dict(INFAAS)
+    plan = _random_drain_plan(rng, c["n_instances"], 250) if case % 3 == 0 else None
+    s = run_pair(c, 250, plan)
+    assert s[86] == 0

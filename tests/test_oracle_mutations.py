@@ -80,6 +80,13 @@ MUTATIONS = {
     # INFaaS: moving average rounded toward zero instead of down
     "infaas_ewma_trunc": [("rp->svc[i] += floor_shift(mean - rp->svc[i], x->cfg.ewma_shift);",
                            "rp->svc[i] += (mean - rp->svc[i]) / ((int64_t)1 << x->cfg.ewma_shift);")],
+    # tier-blind scheduling that still orders queues by tier
+    "blind_ignored": [("static uint32_t prio(const or_ctx *x, uint32_t tier) { return x->cfg.tier_blind ? 0 : tier; }",
+                       "static uint32_t prio(const or_ctx *x, uint32_t tier) { (void)x; return tier; }")],
+    # tier-blind scheduling that still dispatches tier 0 first
+    "blind_dispatch_tier_order": [("    for (uint32_t p = 0; p < (x->cfg.tier_blind ? 1 : K); ++p) {",
+                                   "    for (uint32_t p = 0; p < K; ++p) {"),
+                                  ("            if (prio(x, a[0]) != p) continue;", "            if (a[0] != p) continue;")],
     # INFaaS: INTERFERED takes precedence over OVERLOADED
     "infaas_state_order": [("    if (h >= 0 && (int64_t)blocks(x, inst_slots(x, rp, i)[h].len) > rp->freeb[i]) return x->cfg.pen_over;\n    if (rp->intf[i]) return x->cfg.pen_intf;",
                             "    if (rp->intf[i]) return x->cfg.pen_intf;\n    if (h >= 0 && (int64_t)blocks(x, inst_slots(x, rp, i)[h].len) > rp->freeb[i]) return x->cfg.pen_over;")],
