@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define MTS_ABI_VERSION 4
+#define MTS_ABI_VERSION 5
 #define MTS_MAX_TIERS 10
 #define MTS_NSTAT 96
 /* Latency histogram bins per (metric, tier); see mts_state_view.hist */
@@ -134,7 +134,13 @@ typedef struct mts_cfg {
     int32_t infaas_beta;         /* 0..1024 */
     int32_t infaas_gamma;        /* 0..65536 */
     uint32_t infaas_pen_overloaded, infaas_pen_interfered; /* ticks, 0..2^20 */
-    uint32_t reserved3;          /* must be 0 */
+    /* 1: tier-blind scheduling, the priority-blind local scheduler the paper
+     * pairs with INFaaS (Section 5.3): arrivals are dispatched in arrival
+     * order, queues are served first come first served, preemption takes the
+     * newest running request and the migration candidate ignores tiers.
+     * Tiers still label the counters and histograms and still enter Eq. 4's
+     * headroom.  0: tier order everywhere (Sections 3.1, 3.4). */
+    uint32_t tier_blind;
 } mts_cfg;
 
 enum { MTS_POLICY_LLUMNIX = 0, MTS_POLICY_INFAAS = 1 };

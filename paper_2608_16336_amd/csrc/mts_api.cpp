@@ -175,6 +175,7 @@ Params make_params(const mts_ctx* h)
     p.pen_over = c.infaas_pen_overloaded;
     p.pen_intf = c.infaas_pen_interfered;
     p.qdepth = h->qdepth;
+    p.blind = c.tier_blind;
     const Layout& L = h->lay;
     p.tier_q = reinterpret_cast<const uint32_t*>(d + L.tier_q);
     p.hq = reinterpret_cast<const int32_t*>(d + L.hq);

@@ -10,7 +10,8 @@
 //
 // Output per (replica, tick): the count, and the arrivals as records
 // prompt | out << 16 | tier << 32 | k << 36 sorted by tier, arrival order
-// within a tier (Section 3.4: the pending queue is served tier 0 first).
+// within a tier (Section 3.4: the pending queue is served tier 0 first); in
+// arrival order when scheduling is tier-blind.
 //
 // A wave serves 64 / G ticks, G lanes each: the group's last lane draws the
 // tick's count while the other G - 1 lanes draw the first G - 1 arrivals in
@@ -116,6 +117,7 @@ __device__ void arrivals_wave(const Params& P, uint32_t r, uint32_t tl, unsigned
             tier = 0;
 #pragma unroll
             for (int j = 0; j < kTiers - 1; ++j) tier += (j < K - 1 && tq[j] <= ut) ? 1 : 0;
+            if (P.blind) tier = 0;  // sorted by rank: arrival order when tier-blind
         }
 #pragma unroll
         for (int p = 0; p < kTiers; ++p)
@@ -131,11 +133,12 @@ __device__ void arrivals_wave(const Params& P, uint32_t r, uint32_t tl, unsigned
         Draw d{~0u, 0};
         if (k < n) d = draw_arrival(P, t, gid, k, tq, K);
         int pos = 0;
+        const uint32_t rk = P.blind && d.tier != ~0u ? 0u : d.tier;
 #pragma unroll
         for (int p = 0; p < kTiers; ++p) {
             if (p >= K) continue;
-            const unsigned long long b = ballot(d.tier == uint32_t(p));
-            if (d.tier == uint32_t(p)) pos = off[p] + __popcll(b & lanemask_lt());
+            const unsigned long long b = ballot(rk == uint32_t(p));
+            if (rk == uint32_t(p)) pos = off[p] + __popcll(b & lanemask_lt());
             off[p] += __popcll(b);
         }
         if (k < n) out[pos] = d.rec;
@@ -173,10 +176,11 @@ __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t
     const bool mine = live && fast && q < n;
     const unsigned long long gm = G == 64 ? ~0ull : ((1ull << G) - 1ull) << gb;
     int pos = 0, off = 0;
+    const uint32_t rk = P.blind ? 0u : d.tier;  // sorted by rank: arrival order when tier-blind
 #pragma unroll
     for (int p = 0; p < kTiers; ++p) {
-        const unsigned long long b = ballot(mine && d.tier == uint32_t(p)) & gm;
-        if (mine && d.tier == uint32_t(p)) pos = off + __popcll(b & lanemask_lt());
+        const unsigned long long b = ballot(mine && rk == uint32_t(p)) & gm;
+        if (mine && rk == uint32_t(p)) pos = off + __popcll(b & lanemask_lt());
         off += __popcll(b);
     }
     if (mine) P.arr_rec[(size_t(r) * P.chunk + tl) * P.arr_cap + pos] = d.rec;

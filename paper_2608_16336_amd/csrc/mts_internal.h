@@ -79,6 +79,7 @@ struct Params {
     long long alpha256, beta, gamma256;  // INFaaS weights (alpha and gamma times 256)
     uint32_t pen_over, pen_intf;   // INFaaS state penalties in ticks
     uint32_t qdepth;               // queue-cache entries behind each head of line (LDS)
+    uint32_t blind;                // 1: tiers order nothing (tier-blind scheduling)
     const uint32_t* tier_q;        // [group][MTS_MAX_TIERS]
     const int32_t* hq;             // [group][MTS_MAX_TIERS]
     const uint32_t* group_K32;     // [group] tier count

@@ -127,6 +127,7 @@ struct Ctx {
     int* qn;                   // [I] cached entries
     int* qh;                   // [I] ring position of the first entry
     int td;
+    uint32_t blind;            // 1: tiers order nothing (tier-blind scheduling)
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -181,6 +182,7 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.wc = reinterpret_cast<unsigned*>(base + Y.wc);
     C.wov = reinterpret_cast<unsigned*>(base + Y.wov);
     C.td = int(P.qdepth);
+    C.blind = P.blind;
     C.qt = reinterpret_cast<uint4*>(base + Y.qt);
     C.qn = reinterpret_cast<int*>(base + Y.qn);
     C.qh = C.qn + IM;
@@ -396,14 +398,21 @@ __device__ __forceinline__ void set_hol(const Ctx& C, int i, int slot, unsigned 
 // (or leaves the head unknown, to be found by a rescan), a new waiting
 // request becomes the head or enters the cache at its place when it is
 // smaller than the last cached entry.
+// the rank a tier gives in every ordering (queue, preemption, migration
+// candidate): the tier itself, or 0 for all when scheduling is tier-blind
+__device__ __forceinline__ unsigned long long rank_of(const Ctx& C, uint32_t tier)
+{
+    return C.blind ? 0ull : static_cast<unsigned long long>(tier);
+}
+
 __device__ __forceinline__ uint4 qc_pack(unsigned long long key, int slot, uint32_t word, uint32_t meta, uint32_t tarr)
 {
     return make_uint4(uint32_t(key), word, tarr,
-                      uint32_t(slot) | (uint32_t(key >> 32) << 12) | (((meta >> 6) & 1u) << 16));
+                      uint32_t(slot) | (((meta >> 2) & 15u) << 12) | (((meta >> 6) & 1u) << 16));
 }
-__device__ __forceinline__ unsigned long long qc_key(uint4 e)
+__device__ __forceinline__ unsigned long long qc_key(const Ctx& C, uint4 e)
 {
-    return (static_cast<unsigned long long>((e.w >> 12) & 15u) << 32) | e.x;
+    return (rank_of(C, (e.w >> 12) & 15u) << 32) | e.x;
 }
 __device__ __forceinline__ int qc_at(const Ctx& C, int i, int k)
 {
@@ -435,7 +444,7 @@ __device__ inline void hol_pop(const Ctx& C, int i)
     if (n == 0) { C.hols[i] = kHolUnknown; return; }
     const uint4 e = C.qt[qc_at(C, i, 0)];
     const uint32_t tier = (e.w >> 12) & 15u;
-    set_hol(C, i, int(e.w & 0xFFFu), qc_key(e), e.y, kWaiting | (tier << 2) | (((e.w >> 16) & 1u) << 6), e.z);
+    set_hol(C, i, int(e.w & 0xFFFu), qc_key(C, e), e.y, kWaiting | (tier << 2) | (((e.w >> 16) & 1u) << 6), e.z);
     const int h = C.qh[i] + 1;
     C.qh[i] = h == C.td ? 0 : h;
     C.qn[i] = n - 1;
@@ -455,7 +464,7 @@ __device__ inline void hol_insert(const Ctx& C, int i, unsigned long long key, i
     if (!C.td) return;
     const int n = C.qn[i];
     int p = 0;
-    while (p < n && qc_key(C.qt[qc_at(C, i, p)]) < key) ++p;
+    while (p < n && qc_key(C, C.qt[qc_at(C, i, p)]) < key) ++p;
     if (p < n) qc_insert_at(C, i, p, qc_pack(key, slot, word, meta, tarr));
 }
 
@@ -522,7 +531,7 @@ __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
         for (int g = 0; g < GR; ++g) {
             if (wst(v[g]) != 1u) continue;
             ++cnt;
-            const unsigned long long k = (static_cast<unsigned long long>((m[g] >> 2) & 15u) << 32) | q[g];
+            const unsigned long long k = (rank_of(C, (m[g] >> 2) & 15u) << 32) | q[g];
             const int sl = (c0 + g) * 64 + lane;
             if (k < k1) { k2 = k1; s2 = s1; k1 = k; s1 = sl; }
             else if (k < k2) { k2 = k; s2 = sl; }
@@ -574,7 +583,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             const int s = c * 64 + lane;
             const uint32_t v = C.hot[b + s];
             if (wst(v) == 2u) {
-                const unsigned long long k = (static_cast<unsigned long long>(((C.meta[b + s] >> 2) & 15u) + 1u) << 32) | C.seq[b + s];
+                const unsigned long long k = ((rank_of(C, (C.meta[b + s] >> 2) & 15u) + 1ull) << 32) | C.seq[b + s];
                 if (k > bk) { bk = k; bs = s; }
             }
         }
@@ -620,7 +629,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             tier_dec(C, i, vt);
             stat(C, vt * 8 + kPreempted, 1);
             if (vm) C.flags[i] |= kFlagAbort;
-            const unsigned long long key = (static_cast<unsigned long long>(vt) << 32) | static_cast<unsigned>(mx);
+            const unsigned long long key = (rank_of(C, uint32_t(vt)) << 32) | static_cast<unsigned>(mx);
             hol_insert(C, i, key, vs, vw, vmeta, vta);
         }
         wave_sync();
@@ -766,9 +775,17 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
 
 // Adds to stats[tier * 8 + field], for every tier, the number of lanes with f
 // set among the lanes of that tier.  The lanes' tiers are non-decreasing
-// (arrivals are sorted by tier); lanes that hold no arrival carry tier 15.
+// (arrivals are sorted by tier) unless scheduling is tier-blind; lanes that
+// hold no arrival carry tier 15.
 __device__ __forceinline__ void tier_stat(const Ctx& C, int tier, bool f, int field, int lane)
 {
+    if (C.blind) {
+        for (int p = 0; p < int(C.K); ++p) {
+            const int c = __popcll(ballot(f && tier == p));
+            if (lane == 0 && c) stat(C, p * 8 + field, c);
+        }
+        return;
+    }
     const int tn = __shfl_down(tier, 1);
     const bool last = lane == 63 || tn != tier;
     const unsigned long long bm = ballot(last), fm = ballot(f);
@@ -870,7 +887,7 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
                            pa = __shfl(a[g], src);
             if (take) {
                 word = pv; meta = pm; ta = pa;
-                key = (static_cast<unsigned long long>((pm >> 2) & 15u) << 32) | pq;
+                key = (rank_of(C, (pm >> 2) & 15u) << 32) | pq;
                 slot = (c0 + g) * 64 + src;
             }
             w += cnt;
@@ -915,7 +932,7 @@ __device__ inline void admit_fresh(const Ctx& C, int i, uint32_t t, int lane)
         meta = kWaiting | (tier << 2);
         ta = t - 1u;
         slot = int(e & 0xFFFu);
-        key = (static_cast<unsigned long long>(tier) << 32) | C.lsq[idx];
+        key = (rank_of(C, tier) << 32) | C.lsq[idx];
     }
     admit_ranked(C, i, t, lane, w, key, word, meta, ta, slot);
 }
@@ -993,7 +1010,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     wheel_put(C, fin, int(i), s);
                 } else if (st == 1u) {
                     const uint32_t m = C.meta[b + s];
-                    const unsigned long long k = (static_cast<unsigned long long>((m >> 2) & 15u) << 32) | C.seq[b + s];
+                    const unsigned long long k = (rank_of(C, (m >> 2) & 15u) << 32) | C.seq[b + s];
                     if (k < bk) { bk = k; bs = s; bv = v; bm = m; }
                 }
             }
@@ -1317,7 +1334,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         for (int j = 0; j < IPL; ++j)
                             if (j == jc) { lv = rl(live_r[j], lc); hkc = rl64(hk_r[j], lc); }
                         const unsigned long long ak = rl64(a, int(k));
-                        const unsigned long long hk = ((ak >> 32) & 15u) << 32 | (seq0 + unsigned(ak >> 36));
+                        const unsigned long long hk = rank_of(C, uint32_t(ak >> 32) & 15u) << 32 | (seq0 + unsigned(ak >> 36));
                         const bool becomes = hk < hkc;
                         // Arrival k goes to cur.  If it becomes cur's head of line, F of cur
                         // changes and the argmax is taken again.  Otherwise F stays, and
@@ -1638,7 +1655,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                 if (wst(v) == 2u && !(m & kMigrating)) {
                                     const uint32_t fin = fin_of(v, t);
                                     const unsigned long long kk =
-                                        (static_cast<unsigned long long>(((m >> 2) & 15u) + 1u) << 48) |
+                                        ((rank_of(C, (m >> 2) & 15u) + 1ull) << 48) |
                                         (static_cast<unsigned long long>(65535 - blocks_of(wlo(v) - (fin - t), C.shift)) << 32) |
                                         C.seq[sbase + s];
                                     if (kk > bk) { bk = kk; bs = s; }

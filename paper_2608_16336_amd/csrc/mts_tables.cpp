@@ -126,7 +126,7 @@ bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
 
 int validate(const mts_cfg& c)
 {
-    if (c.abi_version != MTS_ABI_VERSION || c.reserved != 0 || c.reserved2 != 0 || c.reserved3 != 0) return MTS_EINVAL;
+    if (c.abi_version != MTS_ABI_VERSION || c.reserved != 0 || c.reserved2 != 0 || c.tier_blind > 1) return MTS_EINVAL;
     if (c.dispatch_policy > MTS_POLICY_INFAAS || c.infaas_ewma_shift > 16) return MTS_EINVAL;
     if (c.infaas_alpha < 0 || c.infaas_alpha > 65536 || c.infaas_beta < 0 || c.infaas_beta > 1024 ||
         c.infaas_gamma < 0 || c.infaas_gamma > 65536)

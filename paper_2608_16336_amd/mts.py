@@ -12,7 +12,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libmts.so")
 
-ABI_VERSION = 4
+ABI_VERSION = 5
 MAX_TIERS = 10
 NSTAT = 96
 HIST_BINS = 240  # latency histogram bins per (metric, tier)
@@ -61,7 +61,7 @@ class mts_cfg(ctypes.Structure):
                 ("dispatch_policy", ctypes.c_uint32), ("infaas_ewma_shift", ctypes.c_uint32),
                 ("infaas_alpha", ctypes.c_int32), ("infaas_beta", ctypes.c_int32), ("infaas_gamma", ctypes.c_int32),
                 ("infaas_pen_overloaded", ctypes.c_uint32), ("infaas_pen_interfered", ctypes.c_uint32),
-                ("reserved3", ctypes.c_uint32)]
+                ("tier_blind", ctypes.c_uint32)]
 
 
 class mts_stats_t(ctypes.Structure):
@@ -186,6 +186,7 @@ def make_cfg(cfg):
     c.groups = groups
     d = cfg.get("dispatch", {"policy": "llumnix"})
     c.dispatch_policy = POLICIES[d["policy"]]
+    c.tier_blind = 1 if cfg.get("tier_blind") else 0
     if d["policy"] == "infaas":
         c.infaas_alpha, c.infaas_beta, c.infaas_gamma = d["alpha"], d["beta"], d["gamma"]
         c.infaas_pen_overloaded, c.infaas_pen_interfered = d["pen_overloaded"], d["pen_interfered"]

@@ -447,3 +447,41 @@ def test_queue_cache_depth_is_validated():
     assert 0 <= g.queue_cache <= 7
     with pytest.raises(MtsError):
         g.queue_cache = 16
+
+
+# ---------------------------------------------------------------------------
+# tier-blind scheduling (the priority-blind local scheduler of the paper's
+# INFaaS baseline, Section 5.3)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("case", range(10))
+def test_random_tier_blind_clusters(case):
+    from test_oracle_exact import _random_cfg as rc, _random_drain_plan
+    rng = random.Random(9000 + case)
+    cfg = rc(rng)
+    cfg["tier_blind"] = 1
+    if case % 2:
+        cfg["dispatch"] = dict(INFAAS)
+    cfg["groups"][0]["n_replicas"] = 3
+    if case % 3 == 0:
+        run_plan_both(cfg, 250, _random_drain_plan(rng, cfg["n_instances"], 250))
+    else:
+        run_both(cfg, 250)
+
+
+@pytest.mark.parametrize("name,rpg,ticks,policy", [
+    ("enterprise", 6, 600, "infaas"),
+    ("gauss10", 6, 600, "infaas"),
+    ("sweep", 1, 300, "llumnix"),
+    ("wide", 1, 80, "infaas"),
+])
+def test_tier_blind_presets_reduced(name, rpg, ticks, policy):
+    cfg = scaled(name, replicas_per_group=rpg)
+    cfg["tier_blind"] = 1
+    if policy == "infaas":
+        cfg["dispatch"] = dict(INFAAS)
+    g = Scheduler(cfg)
+    g.step(ticks)
+    o = oracle.Oracle(cfg)
+    o.step(ticks)
+    assert_same(g.export(), o.export(), name)
+    assert g.stats()["raw"][86] == 0
