@@ -92,6 +92,8 @@ def main():
                     help="MiB copied device-to-device once before timing (counter calibration)")
     ap.add_argument("--policy", choices=("llumnix", "infaas"), default="llumnix",
                     help="global dispatch policy (infaas: cost-based dispatch without migration)")
+    ap.add_argument("--tier-blind", action="store_true",
+                    help="first-come-first-served queues and arrival-order dispatch")
     ap.add_argument("--drain-instances", type=int, default=0,
                     help="mark the first n instances of every replica draining after the first timed step")
     args = ap.parse_args()
@@ -110,6 +112,8 @@ def main():
     if args.policy == "infaas":
         cfg["dispatch"] = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512,
                                pen_interfered=128, ewma_shift=4)
+    if args.tier_blind:
+        cfg["tier_blind"] = 1
     R = sum(g["n_replicas"] for g in cfg["groups"])
     T, K, W = args.ticks_per_step, args.steps, args.warmup
     torch.cuda.set_device(0)
@@ -162,7 +166,7 @@ def main():
     b_alg = algorithmic_bytes(cfg, R, T * K, d)
     avg_launch_s = step_ms / 1e3 / launches
     achieved = b_alg / launches / avg_launch_s / 1e9
-    default_run = (args.workload, T, args.policy, args.drain_instances) == ("sweep", 1000, "llumnix", 0)
+    default_run = (args.workload, T, args.policy, args.drain_instances, args.tier_blind) == ("sweep", 1000, "llumnix", 0, False)
     traffic = MEASURED_TRAFFIC.get(kernel_source_hash()) if default_run else None
 
     out = {
@@ -181,7 +185,7 @@ def main():
         "config": {"workload": cfg["name"], "replicas": R, "instances": cfg["n_instances"],
                    "slots_per_instance": cfg["slots_per_instance"], "ticks_per_step": T,
                    "ticks_timed": T * K, "parallelism": "replicas across workgroups",
-                   "policy": args.policy, "draining_instances": args.drain_instances,
+                   "policy": args.policy, "tier_blind": args.tier_blind, "draining_instances": args.drain_instances,
                    "blocks": sch.launch()[1], "threads_per_block": 64},
         "slot_updates_per_s": value * slots,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

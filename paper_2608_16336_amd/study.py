@@ -55,24 +55,27 @@ def percentile(counts, q):
 INFAAS = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512, pen_interfered=128, ewma_shift=4)
 
 
-def sweep_cfg(arrival_mean, replicas_per_group, ticks, policy="llumnix"):
+def sweep_cfg(arrival_mean, replicas_per_group, ticks, policy="llumnix", tier_blind=False):
     from workloads import preset
     cfg = preset("sweep")
     if policy == "infaas":
         cfg["dispatch"] = dict(INFAAS)
+    if tier_blind:
+        cfg["tier_blind"] = 1
     cfg["arrival"] = dict(kind="poisson", mean=float(arrival_mean))
     for g in cfg["groups"]:
         g["n_replicas"] = replicas_per_group
     cfg["ticks"] = ticks
-    cfg["name"] = "differentiation study: sweep groups x %d, Poisson %g/tick, %s dispatch" % (
-        replicas_per_group, arrival_mean, policy)
+    cfg["name"] = "differentiation study: sweep groups x %d, Poisson %g/tick, %s dispatch%s" % (
+        replicas_per_group, arrival_mean, policy, ", tier-blind queues" if tier_blind else "")
     return cfg
 
 
-def run(arrival_mean=24.0, replicas_per_group=128, ticks=4000, device="cuda", policy="llumnix"):
+def run(arrival_mean=24.0, replicas_per_group=128, ticks=4000, device="cuda", policy="llumnix",
+        tier_blind=False):
     """Run the sweep and return one row per (tier mix, K, tier)."""
     import torch
-    cfg = sweep_cfg(arrival_mean, replicas_per_group, ticks, policy)
+    cfg = sweep_cfg(arrival_mean, replicas_per_group, ticks, policy, tier_blind)
     g = Scheduler(cfg, device=device)
     g.step(ticks)
     torch.cuda.synchronize()
@@ -122,9 +125,11 @@ def main(argv=None):
     ap.add_argument("--replicas-per-group", type=int, default=128)
     ap.add_argument("--ticks", type=int, default=4000)
     ap.add_argument("--policy", choices=("llumnix", "infaas"), default="llumnix")
+    ap.add_argument("--tier-blind", action="store_true",
+                    help="first-come-first-served queues and arrival-order dispatch (the paper's INFaaS+vLLM baseline)")
     ap.add_argument("--json", help="also write the rows to this file")
     a = ap.parse_args(argv)
-    cfg, rows = run(a.arrival_mean, a.replicas_per_group, a.ticks, policy=a.policy)
+    cfg, rows = run(a.arrival_mean, a.replicas_per_group, a.ticks, policy=a.policy, tier_blind=a.tier_blind)
     print("# %s, %d ticks\n" % (cfg["name"], a.ticks))
     print(markdown(rows))
     if a.json:
