@@ -25,13 +25,13 @@ MUTATIONS = {
     "dispatch_tie": [("if (best < 0 || f_greater(num[i], den[i], num[best], den[best])) best = (int)i;",
                       "if (best < 0 || !f_greater(num[best], den[best], num[i], den[i])) best = (int)i;")],
     # Section 3.4: lowest tier first instead of tier 0 first
-    "dispatch_order": [("for (uint32_t p = 0; p < K; ++p) {\n        for (uint32_t k = 0; k < n; ++k) {",
-                        "for (uint32_t p = K; p-- > 0;) {\n        for (uint32_t k = 0; k < n; ++k) {")],
+    "dispatch_order": [("for (uint32_t p = 0; p < (x->cfg.tier_blind ? 1 : K); ++p) {\n        for (uint32_t k = 0; k < n; ++k) {",
+                        "for (uint32_t p = (x->cfg.tier_blind ? 1 : K); p-- > 0;) {\n        for (uint32_t k = 0; k < n; ++k) {")],
     # Eq. 3 reading: the lowest tier keeps its headroom
     "lowest_tier_headroom": [("if (c->zero_lowest) out[K - 1] = 0;", "")],
     # preemption takes the oldest instead of the newest request of the worst tier
-    "preempt_order": [("(sl[s].tier == sl[v].tier && sl[s].seq > sl[v].seq)) v = (int)s;",
-                       "(sl[s].tier == sl[v].tier && sl[s].seq < sl[v].seq)) v = (int)s;")],
+    "preempt_order": [("if (ps > pv || (ps == pv && sl[s].seq > sl[v].seq)) v = (int)s;",
+                       "if (ps > pv || (ps == pv && sl[s].seq < sl[v].seq)) v = (int)s;")],
     # KV growth one token late
     "growth_off_by_one": [("if (sl[s].st == ST_RUNNING && sl[s].len % blk == 0) grow++;",
                            "if (sl[s].st == ST_RUNNING && (sl[s].len + 1) % blk == 0) grow++;")],
