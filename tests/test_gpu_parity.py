@@ -485,3 +485,76 @@ def test_tier_blind_presets_reduced(name, rpg, ticks, policy):
     o.step(ticks)
     assert_same(g.export(), o.export(), name)
     assert g.stats()["raw"][86] == 0
+
+
+# ---------------------------------------------------------------------------
+# wider random clusters: several 64-slot chunks per instance, every knob
+# ---------------------------------------------------------------------------
+def _wide_random_cfg(rng):
+    I = rng.choice([2, 3, 5, 8, 16, 33])
+    S = rng.choice([128, 192, 256, 512, 1024])
+    K = rng.randint(1, 10)
+    blk = rng.choice([1, 2, 16, 64])
+    M = rng.choice([64, 300, 2048, 8192])
+    kind = rng.choice(["uniform", "gauss", "geometric", "explicit"])
+    tiers = dict(kind=kind)
+    if kind == "gauss":
+        tiers.update(mu=(K - 1) / 2, sigma=max(K / 4, 0.3))
+    elif kind == "geometric":
+        tiers.update(r=0.5)
+    elif kind == "explicit":
+        w = [rng.choice([0.0, 0.2, 1.0]) + (0.05 if j == 0 else 0.0) for j in range(K)]
+        tiers.update(probs=[v / sum(w) for v in w])
+    c = preset("tiny")
+    c.update(
+        n_instances=I, slots_per_instance=S, kv_blocks=M, block_tokens=blk,
+        headroom_base=rng.choice([0.0, 0.2, 0.7]) * M, headroom_decay=rng.choice([0.4, 0.8]),
+        zero_lowest_tier=rng.choice([0, 1]), mig_interval=rng.choice([1, 2, 5]),
+        mig_stage_blocks=rng.choice([1, 8, 64]), mig_max_pairs=rng.randint(0, I // 2),
+        theta_num=rng.choice([0, 3, 40]), theta_den=10,
+        arrival=rng.choice([dict(kind="poisson", mean=rng.choice([1.0, 6.0, 30.0])),
+                            dict(kind="gamma_poisson", mean=rng.choice([5.0, 40.0]), cv=2.0)]),
+        prompt=rng.choice([dict(kind="uniform_int", lo=1, hi=rng.choice([100, 2000])),
+                           dict(kind="lognormal", mu=5.0, sigma=1.0, lo=8, hi=6000)]),
+        output=rng.choice([dict(kind="geometric", mean=rng.choice([20.0, 150.0])),
+                           dict(kind="pareto", alpha=1.5, min=4, cap=3000)]),
+        groups=[dict(n_replicas=2, K=K, tiers=tiers)],
+        seed=rng.randrange(2**63), replica_id_base=rng.randrange(1000))
+    c["mig_max_pairs"] = min(c["mig_max_pairs"], I // 2)
+    if rng.random() < 0.3:
+        c["dispatch"] = dict(policy="infaas", alpha=rng.choice([0, 64]), beta=rng.choice([0, 1]), gamma=1,
+                             pen_overloaded=256, pen_interfered=64, ewma_shift=rng.choice([0, 4]))
+    if rng.random() < 0.25:
+        c["tier_blind"] = 1
+    return c
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_wide_random_clusters(case):
+    from test_oracle_exact import _random_drain_plan
+    rng = random.Random(11000 + case)
+    cfg = _wide_random_cfg(rng)
+    depth = rng.choice([None, 0, 3, 15])
+    plan = _random_drain_plan(rng, cfg["n_instances"], 200) if rng.random() < 0.4 else {}
+    g = Scheduler(cfg)
+    if depth is not None:
+        g.queue_cache = depth
+    orc = [oracle.Oracle(cfg, r, 1) for r in range(g.R)]
+    flags = np.zeros((g.R, cfg["n_instances"]), np.uint8)
+    t = 0
+    for stop in sorted([k for k in plan if k < 200]) + [200]:
+        if stop > t:
+            g.step(stop - t)
+            for o in orc:
+                o.step(stop - t)
+            t = stop
+        if stop in plan:
+            for i, on in plan[stop]:
+                flags[:, i] = 1 if on else 0
+                for o in orc:
+                    o.set_drain(0, i, on)
+            g.set_draining(flags)
+    for r, o in enumerate(orc):
+        assert_same(g.export(r, 1), o.export(), "case %d replica %d" % (case, r))
+        assert np.array_equal(g.digests(r, 1), o.digests())
+    assert g.stats()["raw"][86] == 0
