@@ -109,7 +109,7 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     const size_t I = c.n_instances, S = c.slots_per_instance;
     const size_t N = size_t(R) * I * S;
     size_t o = 0;
-    L.tier_q = o;   o = up256(o + size_t(c.n_groups) * MTS_MAX_TIERS * 4);
+    L.tier_q = o;   o = up256(o + size_t(c.n_groups) * MTS_MAX_TIERS * 8);
     L.hq = o;       o = up256(o + size_t(c.n_groups) * MTS_MAX_TIERS * 4);
     L.group_K = o;  o = up256(o + size_t(c.n_groups) * 4);
     L.count_q = o;  o = up256(o + T.count.q.size() * 4);
@@ -177,7 +177,7 @@ Params make_params(const mts_ctx* h)
     p.qdepth = h->qdepth;
     p.blind = c.tier_blind;
     const Layout& L = h->lay;
-    p.tier_q = reinterpret_cast<const uint32_t*>(d + L.tier_q);
+    p.tier_q = reinterpret_cast<const unsigned long long*>(d + L.tier_q);
     p.hq = reinterpret_cast<const int32_t*>(d + L.hq);
     p.group_K32 = reinterpret_cast<const uint32_t*>(d + L.group_K);
     p.count_q = reinterpret_cast<const uint32_t*>(d + L.count_q);
@@ -311,14 +311,21 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
 
     // tables and per-replica group index
     const uint32_t G = x->cfg.n_groups;
-    std::vector<uint32_t> tier(size_t(G) * MTS_MAX_TIERS, 0);
+    // tier tables keep 64-bit entries: a tier of probability 0 at the top
+    // makes an earlier entry exactly 2^32
+    std::vector<uint64_t> tier(size_t(G) * MTS_MAX_TIERS, 0);
     for (uint32_t g = 0; g < G; ++g) {
         const Table& t = x->tables.tier[g];
-        for (size_t j = 0; j + 1 < t.q.size(); ++j) tier[size_t(g) * MTS_MAX_TIERS + j] = uint32_t(t.q[j]);
+        for (size_t j = 0; j + 1 < t.q.size(); ++j) tier[size_t(g) * MTS_MAX_TIERS + j] = t.q[j];
         x->group_K.push_back(x->groups[g].K);
     }
     for (uint32_t g = 0; g < G; ++g)
         for (uint32_t k = 0; k < x->groups[g].n_replicas; ++k) x->group_of.push_back(uint16_t(g));
+    // the count, prompt and output tables end where the CDF reaches 1, so
+    // every entry but their last fits 32 bits; checked, as the sampler relies on it
+    for (const Table* t : {&x->tables.count, &x->tables.prompt, &x->tables.output})
+        for (size_t j = 0; j + 1 < t->q.size(); ++j)
+            if (t->q[j] > 0xFFFFFFFFull) { delete x; return MTS_EINVAL; }
     const std::vector<uint32_t> cq = device_table(x->tables.count, 1), pq = device_table(x->tables.prompt, 1),
                                 oq = device_table(x->tables.output, 1);
     const Layout& L = x->lay;
@@ -326,7 +333,7 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
     auto up = [&](size_t off, const void* src, size_t n) {
         if (e == hipSuccess && n) e = hipMemcpyAsync(x->dev + off, src, n, hipMemcpyHostToDevice, stream);
     };
-    up(L.tier_q, tier.data(), tier.size() * 4);
+    up(L.tier_q, tier.data(), tier.size() * 8);
     up(L.hq, x->tables.hq.data(), x->tables.hq.size() * 4);
     up(L.group_K, x->group_K.data(), x->group_K.size() * 4);
     up(L.count_q, cq.data(), cq.size() * 4);

@@ -66,7 +66,7 @@ struct Draw {
 
 // tier, prompt and output length of arrival k from its Philox output x
 __device__ __forceinline__ Draw arrival_of(const Params& P, const unsigned long long x[4], uint32_t k,
-                                           const uint32_t* tq, int K)
+                                           const unsigned long long* tq, int K)
 {
     const uint32_t ut = uint32_t(x[0]);
     uint32_t tier = 0;
@@ -82,7 +82,7 @@ __device__ __forceinline__ Draw arrival_of(const Params& P, const unsigned long 
 }
 
 __device__ __forceinline__ Draw draw_arrival(const Params& P, unsigned long long t, unsigned long long gid, uint32_t k,
-                                             const uint32_t* tq, int K)
+                                             const unsigned long long* tq, int K)
 {
     unsigned long long y[4] = {t, k, 1, 0};
     philox4x64_10(y, P.seed, gid);
@@ -96,7 +96,7 @@ __device__ void arrivals_wave(const Params& P, uint32_t r, uint32_t tl, unsigned
     const unsigned long long gid = P.id_base + r;
     const uint32_t g = P.group_of[r];
     const int K = int(P.group_K32[g]);
-    const uint32_t* tq = P.tier_q + size_t(g) * kTiers;
+    const unsigned long long* tq = P.tier_q + size_t(g) * kTiers;
     unsigned long long x[4] = {t, 0, 0, 0};
     philox4x64_10(x, P.seed, gid);
     const uint32_t n = P.count_base + sample(P.count_q, P.count_g, P.count_gs, uint32_t(x[0]));
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t
     const unsigned long long gid = P.id_base + r;
     const uint32_t g = P.group_of[r];
     const int K = int(P.group_K32[g]);
-    const uint32_t* tq = P.tier_q + size_t(g) * kTiers;
+    const unsigned long long* tq = P.tier_q + size_t(g) * kTiers;
     // one Philox pass: the count on the group's last lane, arrival q elsewhere
     const bool cl = q == G - 1u;
     unsigned long long x[4] = {t, cl ? 0ull : q, cl ? 0ull : 1ull, 0};

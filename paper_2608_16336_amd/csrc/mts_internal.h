@@ -80,7 +80,7 @@ struct Params {
     uint32_t pen_over, pen_intf;   // INFaaS state penalties in ticks
     uint32_t qdepth;               // queue-cache entries behind each head of line (LDS)
     uint32_t blind;                // 1: tiers order nothing (tier-blind scheduling)
-    const uint32_t* tier_q;        // [group][MTS_MAX_TIERS]
+    const unsigned long long* tier_q;  // [group][MTS_MAX_TIERS] floor(2^32 CDF), up to 2^32
     const int32_t* hq;             // [group][MTS_MAX_TIERS]
     const uint32_t* group_K32;     // [group] tier count
     const uint32_t* count_q;

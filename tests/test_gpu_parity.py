@@ -558,3 +558,16 @@ def test_wide_random_clusters(case):
         assert_same(g.export(r, 1), o.export(), "case %d replica %d" % (case, r))
         assert np.array_equal(g.digests(r, 1), o.digests())
     assert g.stats()["raw"][86] == 0
+
+
+@pytest.mark.parametrize("probs", [[0.4, 0.0, 0.6], [0.5, 0.5, 0.0], [0.0, 0.3, 0.7, 0.0], [0.2, 0.3, 0.5, 0.0, 0.0]])
+def test_zero_probability_tiers(probs):
+    # a tier of probability 0 makes a cumulative table entry exactly 2^32;
+    # no request may ever carry such a tier
+    cfg = preset("tiny")
+    cfg["groups"] = [dict(n_replicas=3, K=len(probs), tiers=dict(kind="explicit", probs=probs))]
+    g = run_both(cfg, 300)
+    s = g.stats()["raw"]
+    for p, w in enumerate(probs):
+        if w == 0.0:
+            assert s[p * 8] == 0
