@@ -225,8 +225,10 @@ int mts_state_bytes(const mts_cfg* cfg, size_t* bytes);
 int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stream, mts_handle* out);
 
 /* Enqueue n_ticks ticks of every replica on stream and return after the
- * launch (asynchronous).  n_ticks = 0 is a no-op.  MTS_ERANGE if the tick or
- * sequence counters could overflow 32 bits. */
+ * launch (asynchronous).  n_ticks = 0 is a no-op.  MTS_ERANGE if the tick
+ * would pass 2^32 - 2^16, or a replica's sequence counter could pass 2^32
+ * (the library bounds it by the largest imported counter plus the ticks
+ * stepped since, times the most arrivals one tick can hold). */
 int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream);
 
 /* Synchronise with the last stream used on h, sum the per-replica counters

@@ -22,6 +22,7 @@ struct mts_ctx {
     uint32_t R = 0, I = 0, S = 0;
     uint64_t tick = 0;
     uint32_t arr_cap = 0;              // arrival records per (replica, tick)
+    uint64_t seq_bound = 0;            // no replica's sequence counter exceeds this
     uint32_t chunk = 0;                // ticks per arrival batch
     uint32_t wsz = 0, wcap = 0;        // finish wheel: buckets, entries per bucket
     uint32_t arr_group = 64;           // lanes per tick in the arrival kernel
@@ -411,10 +412,11 @@ int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
 {
     if (!h) return MTS_EINVAL;
     if (n_ticks == 0) return MTS_OK;
-    // ticks are 32-bit on the device and the sequence counter grows by at
+    // ticks are 32-bit on the device and the sequence counters grow by at
     // most arr_cap - 1 per tick
     const uint64_t end = h->tick + n_ticks;
-    if (end > 0xFFFF0000ull || end * uint64_t(h->arr_cap) > 0xFFFFFFFFull) return MTS_ERANGE;
+    const uint64_t seq_end = h->seq_bound + n_ticks * uint64_t(h->arr_cap);
+    if (end > 0xFFFF0000ull || seq_end > 0xFFFFFFFFull) return MTS_ERANGE;
     const Params p = make_params(h);
     uint32_t blocks = 0;
     const int rc = auto_blocks(h, p, &blocks);
@@ -434,6 +436,7 @@ int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
         if (h->timing && hipEventRecord(e[2], stream) != hipSuccess) return MTS_EDEVICE;
     }
     h->tick = end;
+    h->seq_bound = seq_end;
     h->last = stream;
     return MTS_OK;
 }
@@ -582,6 +585,7 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     put(L.freeb + size_t(r0) * I * 4, v->free, size_t(nr) * I * 4);
     put(L.mig + size_t(r0) * I * 16, v->mig, size_t(nr) * I * 16);
     put(L.next_seq + size_t(r0) * 4, v->next_seq, size_t(nr) * 4);
+    for (uint32_t r = 0; r < nr; ++r) h->seq_bound = std::max<uint64_t>(h->seq_bound, v->next_seq[r]);
     put(L.stats + size_t(r0) * MTS_NSTAT * 8, v->stats, size_t(nr) * MTS_NSTAT * 8);
     if (v->drain) {
         put(L.drain + size_t(r0) * I, v->drain, size_t(nr) * I);

@@ -571,3 +571,49 @@ def test_zero_probability_tiers(probs):
     for p, w in enumerate(probs):
         if w == 0.0:
             assert s[p * 8] == 0
+
+
+# ---------------------------------------------------------------------------
+# clock wrap of the running word's finish field (14 bits), limits, groups
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("t0", [16300, 32700, 65500, (1 << 31) - 150, (1 << 32) - (1 << 16) - 700])
+def test_runs_across_finish_field_wraps(t0):
+    cfg = preset("tiny")
+    cfg["output"] = dict(kind="pareto", alpha=1.2, min=50, cap=16000)
+    cfg["groups"][0]["n_replicas"] = 2
+    g = Scheduler(cfg)
+    g.tick = t0
+    o = oracle.Oracle(cfg)
+    o.tick = t0
+    for n in (120, 250, 230):
+        g.step(n)
+        o.step(n)
+        assert_same(g.export(), o.export(), "t0 %d" % t0)
+    assert g.stats()["raw"][86] == 0
+
+
+def test_extreme_lengths_and_tiny_kv():
+    cfg = preset("tiny")
+    cfg.update(kv_blocks=3, block_tokens=64)
+    cfg["prompt"] = dict(kind="uniform_int", lo=1, hi=49000)
+    cfg["output"] = dict(kind="pareto", alpha=0.8, min=1, cap=16383)
+    cfg["groups"][0]["n_replicas"] = 2
+    run_both(cfg, 400)
+    cfg = preset("tiny")
+    cfg.update(kv_blocks=1, block_tokens=1)
+    cfg["prompt"] = dict(kind="uniform_int", lo=1, hi=1)
+    cfg["output"] = dict(kind="geometric", mean=3.0)
+    cfg["groups"][0]["n_replicas"] = 2
+    run_both(cfg, 300)
+
+
+def test_several_groups_with_different_tier_counts():
+    cfg = preset("tiny")
+    cfg.update(n_instances=6, slots_per_instance=128, kv_blocks=512, mig_max_pairs=3)
+    cfg["arrival"] = dict(kind="poisson", mean=4.0)
+    cfg["groups"] = [dict(n_replicas=2, K=1, tiers=dict(kind="uniform")),
+                     dict(n_replicas=1, K=10, tiers=dict(kind="gauss", mu=4.5, sigma=0.05)),
+                     dict(n_replicas=2, K=7, tiers=dict(kind="geometric", r=0.2)),
+                     dict(n_replicas=1, K=3, tiers=dict(kind="explicit", probs=[0.0, 0.0, 1.0]))]
+    g = run_both(cfg, 400)
+    assert g.stats()["raw"][86] == 0
