@@ -115,3 +115,26 @@ def test_full_sweep_with_draining_instances():
         assert np.array_equal(g.digests(r, 1), o.digests())
         o.close()
     g.close()
+
+
+@pytest.mark.parametrize("name,ticks,picks", [
+    ("enterprise", 5000, [0, 517, 1023]),
+    ("gauss10", 10000, [0, 4095]),
+    ("sweep", 10000, [5, 1930, 3839]),
+])
+def test_full_length_runs_sampled(name, ticks, picks):
+    # the workloads' whole runs, as the bench times them, in launches of 1000 ticks
+    cfg = preset(name)
+    g = Scheduler(cfg)
+    for _ in range(ticks // 1000):
+        g.step(1000)
+    torch.cuda.synchronize()
+    s = g.stats()
+    assert s["raw"][86] == 0 and s["raw"][87] == g.R * ticks
+    for r in picks:
+        o = oracle.Oracle(cfg, r, 1, check=False)
+        o.step(ticks)
+        assert_same(g.export(r, 1), o.export(), "%s replica %d after %d ticks" % (name, r, ticks))
+        assert np.array_equal(g.digests(r, 1), o.digests())
+        o.close()
+    g.close()
