@@ -25,7 +25,6 @@ struct mts_ctx {
     uint64_t seq_bound = 0;            // no replica's sequence counter exceeds this
     uint32_t chunk = 0;                // ticks per arrival batch
     uint32_t wsz = 0, wcap = 0;        // finish wheel: buckets, entries per bucket
-    uint32_t arr_group = 64;           // lanes per tick in the arrival kernel
     uint32_t blocks = 0;               // step-kernel blocks (one wave each); 0 = automatic
     uint32_t qdepth = 0;               // queue-cache entries per instance (chosen at create)
     int device = 0;
@@ -163,7 +162,6 @@ Params make_params(const mts_ctx* h)
     p.output_gs = guide_shift(h->tables.output);
     p.chunk = h->chunk;
     p.arr_cap = h->arr_cap;
-    p.arr_group = h->arr_group;
     p.wsz = h->wsz;
     p.wcap = h->wcap;
     p.seed = c.seed;
@@ -206,19 +204,6 @@ Params make_params(const mts_ctx* h)
     return p;
 }
 
-// Lanes per tick in the arrival kernel: the smallest of 16, 32, 64 such that
-// a tick has at least that many arrivals with probability below 2^-10 (such
-// ticks are drawn again by a whole wave).
-uint32_t arrival_group(const Table& count)
-{
-    for (uint32_t G : {16u, 32u}) {
-        if (G - 1 < count.base) continue;
-        const size_t j = G - 1 - count.base;  // P(n <= G - 1) = q[j] / 2^32
-        if (j + 1 >= count.q.size() || (uint64_t(1) << 32) - count.q[j] < (uint64_t(1) << 22)) return G;
-    }
-    return 64;
-}
-
 // u32 device image of a table: its first n-1 entries (the last, 2^32, is implicit)
 std::vector<uint32_t> device_table(const Table& t, size_t pad_to = 0)
 {
@@ -245,7 +230,6 @@ int prepare(const mts_cfg* cfg, mts_ctx& x)
     x.arr_cap = uint32_t(x.tables.count.base + x.tables.count.q.size());
     x.chunk = chunk_for(x.R, x.arr_cap);
     wheel_size(x.cfg, x.tables, x.wsz, x.wcap);
-    x.arr_group = arrival_group(x.tables.count);
     x.lay = make_layout(x.cfg, x.tables, x.R, x.chunk, x.arr_cap, x.wsz, x.wcap);
     return MTS_OK;
 }

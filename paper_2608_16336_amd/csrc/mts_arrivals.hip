@@ -12,11 +12,6 @@
 // prompt | out << 16 | tier << 32 | k << 36 sorted by tier, arrival order
 // within a tier (Section 3.4: the pending queue is served tier 0 first); in
 // arrival order when scheduling is tier-blind.
-//
-// A wave serves 64 / G ticks, G lanes each: the group's last lane draws the
-// tick's count while the other G - 1 lanes draw the first G - 1 arrivals in
-// the same Philox pass.  The rare tick with G or more arrivals is redrawn by
-// the whole wave.
 #include <hip/hip_runtime.h>
 
 #include "mts_internal.h"
@@ -145,49 +140,106 @@ __device__ void arrivals_wave(const Params& P, uint32_t r, uint32_t tl, unsigned
     }
 }
 
-template <int G>
-__global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t0, uint32_t nt)
+// Ticks with fewer than kDense arrivals go through the dense path; a wave
+// stages at most kCap of their records in LDS at a time.
+constexpr uint32_t kDense = 64;
+constexpr uint32_t kCap = 512;
+constexpr int kWavesPerBlock = 4;
+
+// A wave serves 64 consecutive (replica, tick) items.  Lane l draws the count
+// of item l; an inclusive wave scan lays the items' arrivals end to end, and
+// the lanes then draw that flat list 64 arrivals at a time, every lane busy.
+// The list is cut into segments of whole ticks that fit kCap; a segment is
+// drawn into LDS, then each arrival counts the arrivals of its tick that sort
+// before it (tier, then arrival order; arrival order alone when tier-blind)
+// and writes its record at that rank.  Items with kDense or more arrivals are
+// drawn afterwards by the whole wave, one at a time.
+__global__ __launch_bounds__(64 * kWavesPerBlock) void k_arrivals(Params P, unsigned long long t0, uint32_t nt)
 {
-    constexpr uint32_t kTicksPerWave = 64 / G;
+    __shared__ unsigned long long stage[kWavesPerBlock][kCap];
+    __shared__ uint8_t owner[kWavesPerBlock][kCap];
     const int lane = lane_id();
-    const uint32_t q = uint32_t(lane) & (G - 1u), gb = uint32_t(lane) & ~(G - 1u);
-    const uint32_t wv = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const uint32_t w = threadIdx.x >> 6;
+    const uint32_t wv = blockIdx.x * kWavesPerBlock + w;
     const uint32_t items = P.R * nt;
-    if (wv * kTicksPerWave >= items) return;
-    const uint32_t item = wv * kTicksPerWave + uint32_t(lane) / G;
+    if (wv * 64u >= items) return;
+    unsigned long long* L = stage[w];
+    const uint32_t* L32 = reinterpret_cast<const uint32_t*>(L);
+    uint8_t* own = owner[w];
+    const uint32_t item = wv * 64u + uint32_t(lane);
     const bool live = item < items;
     const uint32_t r = live ? item / nt : 0, tl = live ? item % nt : 0;
-    const unsigned long long t = t0 + tl;
-    const unsigned long long gid = P.id_base + r;
     const uint32_t g = P.group_of[r];
     const int K = int(P.group_K32[g]);
-    const unsigned long long* tq = P.tier_q + size_t(g) * kTiers;
-    // one Philox pass: the count on the group's last lane, arrival q elsewhere
-    const bool cl = q == G - 1u;
-    unsigned long long x[4] = {t, cl ? 0ull : q, cl ? 0ull : 1ull, 0};
-    philox4x64_10(x, P.seed, gid);
+    unsigned long long x[4] = {t0 + tl, 0, 0, 0};
+    philox4x64_10(x, P.seed, P.id_base + r);
     uint32_t n = 0;
-    Draw d{~0u, 0};
-    if (cl) n = P.count_base + sample(P.count_q, P.count_g, P.count_gs, uint32_t(x[0]));
-    else d = arrival_of(P, x, q, tq, K);
-    n = uint32_t(__shfl(int(n), int(gb + G - 1u)));
-    const bool fast = n < G;  // every arrival of the tick was drawn
-    if (live && cl) P.arr_cnt[size_t(r) * P.chunk + tl] = n;
-    const bool mine = live && fast && q < n;
-    const unsigned long long gm = G == 64 ? ~0ull : ((1ull << G) - 1ull) << gb;
-    int pos = 0, off = 0;
-    const uint32_t rk = P.blind ? 0u : d.tier;  // sorted by rank: arrival order when tier-blind
-#pragma unroll
-    for (int p = 0; p < kTiers; ++p) {
-        const unsigned long long b = ballot(mine && rk == uint32_t(p)) & gm;
-        if (mine && rk == uint32_t(p)) pos = off + __popcll(b & lanemask_lt());
-        off += __popcll(b);
+    if (live) {
+        n = P.count_base + sample(P.count_q, P.count_g, P.count_gs, uint32_t(x[0]));
+        P.arr_cnt[size_t(r) * P.chunk + tl] = n;
     }
-    if (mine) P.arr_rec[(size_t(r) * P.chunk + tl) * P.arr_cap + pos] = d.rec;
-    // ticks with G or more arrivals: the whole wave draws them again
-    for (unsigned long long ov = ballot(live && cl && !fast); ov; ov &= ov - 1) {
+    const uint32_t nd = n < kDense ? n : 0;
+    uint32_t e = nd;  // inclusive scan: the item's arrivals are [e - nd, e) of the flat list
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t v = uint32_t(__shfl_up(int(e), d));
+        if (lane >= d) e += v;
+    }
+    const uint32_t s = e - nd;
+    const uint32_t total = rlu(e, 63);
+    for (uint32_t base = 0; base < total;) {
+        // the segment: every item whose arrivals end by base + kCap (a prefix of
+        // the lanes, never empty since no dense item holds kCap arrivals)
+        const unsigned long long fit = ballot(e <= base + kCap);
+        const uint32_t end = rlu(e, 63 - __clzll(static_cast<long long>(fit)));
+        for (uint32_t f0 = base; f0 < end; f0 += 64) {
+            const uint32_t f = f0 + uint32_t(lane);
+            const uint32_t fc = f < end ? f : end - 1;
+            // owner: the last lane whose arrivals start at or before fc
+            int i = 0;
+            uint32_t si = 0;
+#pragma unroll
+            for (int step = 32; step; step >>= 1) {
+                const uint32_t v = uint32_t(__shfl(int(s), i + step));
+                if (v <= fc) { i += step; si = v; }
+            }
+            const uint32_t ri = uint32_t(__shfl(int(r), i)), ti = uint32_t(__shfl(int(tl), i));
+            const uint32_t gi = uint32_t(__shfl(int(g), i));
+            const int Ki = __shfl(K, i);
+            if (f < end) {
+                const Draw d = draw_arrival(P, t0 + ti, P.id_base + ri, f - si, P.tier_q + size_t(gi) * kTiers, Ki);
+                L[f - base] = d.rec;
+                own[f - base] = uint8_t(i);
+            }
+        }
+        wave_sync();
+        for (uint32_t f0 = base; f0 < end; f0 += 64) {
+            const uint32_t f = f0 + uint32_t(lane);
+            const uint32_t j = (f < end ? f : end - 1) - base;
+            const int i = own[j];
+            const uint32_t si = uint32_t(__shfl(int(s), i)) - base, ni = uint32_t(__shfl(int(nd), i));
+            const uint32_t ri = uint32_t(__shfl(int(r), i)), ti = uint32_t(__shfl(int(tl), i));
+            if (f < end) {
+                // high word of a record: tier | k << 4; (tier, k) order is key order
+                const uint32_t hw = L32[2 * j + 1];
+                uint32_t pos = j - si;
+                if (!P.blind) {
+                    const uint32_t key = (hw & 15u) << 6 | (hw >> 4);
+                    pos = 0;
+                    for (uint32_t m = si; m < si + ni; ++m) {
+                        const uint32_t hm = L32[2 * m + 1];
+                        pos += ((hm & 15u) << 6 | (hm >> 4)) < key ? 1u : 0u;
+                    }
+                }
+                P.arr_rec[(size_t(ri) * P.chunk + ti) * P.arr_cap + pos] = L[j];
+            }
+        }
+        wave_sync();
+        base = end;
+    }
+    for (unsigned long long ov = ballot(live && n >= kDense); ov; ov &= ov - 1) {
         const int l = ffs64(ov);
-        arrivals_wave(P, uint32_t(rl(int(r), l)), uint32_t(rl(int(tl), l)), t0, lane);
+        arrivals_wave(P, rlu(r, l), rlu(tl, l), t0, lane);
     }
 }
 
@@ -195,15 +247,9 @@ __global__ __launch_bounds__(256) void k_arrivals(Params P, unsigned long long t
 
 int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStream_t stream)
 {
-    const uint32_t items = p.R * nt;
-    const uint32_t tpw = 64 / p.arr_group;
-    const uint32_t waves = (items + tpw - 1) / tpw;
-    const dim3 grid((waves + 3) / 4), block(256);
-    switch (p.arr_group) {
-    case 16: hipLaunchKernelGGL(k_arrivals<16>, grid, block, 0, stream, p, t0, nt); break;
-    case 32: hipLaunchKernelGGL(k_arrivals<32>, grid, block, 0, stream, p, t0, nt); break;
-    default: hipLaunchKernelGGL(k_arrivals<64>, grid, block, 0, stream, p, t0, nt); break;
-    }
+    const uint32_t waves = (p.R * nt + 63) / 64;
+    const dim3 grid((waves + kWavesPerBlock - 1) / kWavesPerBlock), block(64 * kWavesPerBlock);
+    hipLaunchKernelGGL(k_arrivals, grid, block, 0, stream, p, t0, nt);
     return int(hipGetLastError());
 }
 

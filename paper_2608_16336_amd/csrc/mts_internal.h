@@ -72,7 +72,6 @@ struct Params {
     uint32_t count_base, prompt_base, output_base;
     uint32_t count_gs, prompt_gs, output_gs;  // guide shift: bucket = u >> shift
     uint32_t chunk, arr_cap;       // ticks per arrival batch, records per tick
-    uint32_t arr_group;            // lanes per tick in the arrival kernel (16, 32 or 64)
     uint32_t wsz, wcap;            // finish wheel: buckets (power of two), entries per bucket
     uint64_t seed, id_base;
     uint32_t policy, ewma_shift;   // MTS_POLICY_*, INFaaS moving-average shift

@@ -205,15 +205,6 @@ __device__ inline Ctx carve(char* base, const Params& P)
 
 using namespace wave;
 
-// Lanes of the wave exchange values through LDS and HBM: every write by a
-// subset of lanes that other lanes read later is followed by this point, so
-// that no later load is moved above it and every later load sees the write.
-__device__ __forceinline__ void wave_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-}
-
 __device__ __forceinline__ int wsum(int x)
 {
 #pragma unroll

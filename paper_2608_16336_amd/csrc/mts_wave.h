@@ -20,5 +20,14 @@ __device__ __forceinline__ unsigned long long rl64(unsigned long long v, int l)
     return (static_cast<unsigned long long>(hi) << 32) | lo;
 }
 
+// Lanes of the wave exchange values through LDS and HBM: every write by a
+// subset of lanes that other lanes read later is followed by this point, so
+// that no later load is moved above it and every later load sees the write.
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+}
+
 }  // namespace wave
 }  // namespace mts

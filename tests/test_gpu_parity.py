@@ -617,3 +617,33 @@ def test_several_groups_with_different_tier_counts():
                      dict(n_replicas=1, K=3, tiers=dict(kind="explicit", probs=[0.0, 0.0, 1.0]))]
     g = run_both(cfg, 400)
     assert g.stats()["raw"][86] == 0
+
+
+# ---------------------------------------------------------------------------
+# arrival sampling: counts across the dense path's limits, bursts, tier order
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("arrival,K,blind", [
+    (dict(kind="poisson", mean=7.9), 10, 0),        # about 506 arrivals per 64 ticks: segments cut near the LDS stage size
+    (dict(kind="poisson", mean=60.0), 10, 0),       # a third of the ticks hold 64 or more arrivals
+    (dict(kind="poisson", mean=60.0), 6, 1),
+    (dict(kind="gamma_poisson", mean=10.0, cv=3.0), 7, 0),   # mostly empty ticks and rare large bursts
+    (dict(kind="gamma_poisson", mean=150.0, cv=0.3), 3, 0),  # every tick above the dense limit
+    (dict(kind="poisson", mean=0.3), 4, 0),
+])
+def test_arrival_bursts_and_tier_order(arrival, K, blind):
+    cfg = preset("tiny")
+    cfg.update(n_instances=3, slots_per_instance=64, kv_blocks=1024, mig_max_pairs=1, arrival=arrival,
+               tier_blind=blind)
+    cfg["groups"] = [dict(n_replicas=3, K=K, tiers=dict(kind="gauss", mu=(K - 1) / 2, sigma=K / 3)),
+                     dict(n_replicas=2, K=K, tiers=dict(kind="uniform"))]
+    g = Scheduler(cfg)
+    orc = [oracle.Oracle(cfg, r, 1) for r in range(g.R)]
+    for n in (37, 150, 64):   # chunks that do not fill whole waves: waves straddle replicas
+        g.step(n)
+        for o in orc:
+            o.step(n)
+    for r, o in enumerate(orc):
+        assert_same(g.export(r, 1), o.export(), "replica %d" % r)
+        assert np.array_equal(g.digests(r, 1), o.digests())
+    s = g.stats()["raw"]
+    assert sum(int(s[p * 8]) for p in range(K)) > 0
