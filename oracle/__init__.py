@@ -76,7 +76,11 @@ class _Cfg(ctypes.Structure):
                 ("groups", ctypes.POINTER(_Group)),
                 ("policy", ctypes.c_uint32), ("ewma_shift", ctypes.c_uint32),
                 ("alpha", ctypes.c_int32), ("beta", ctypes.c_int32), ("gamma_w", ctypes.c_int32),
-                ("pen_over", ctypes.c_uint32), ("pen_intf", ctypes.c_uint32), ("tier_blind", ctypes.c_uint32)]
+                ("pen_over", ctypes.c_uint32), ("pen_intf", ctypes.c_uint32), ("tier_blind", ctypes.c_uint32),
+                ("adapt_epoch", ctypes.c_uint32), ("adapt_up", ctypes.c_uint32), ("adapt_down", ctypes.c_uint32),
+                ("adapt_max", ctypes.c_uint32), ("adapt_margin", ctypes.c_uint32),
+                ("adapt_slo", ctypes.c_uint32 * MAX_TIERS),
+                ("promote_period", ctypes.c_uint32), ("promote_age", ctypes.c_uint32 * MAX_TIERS)]
 
 
 _lib = None
@@ -126,6 +130,10 @@ def lib():
         L.or_svc_get.argtypes = [vp, u32, u32, vp]
         L.or_svc_set.restype = ctypes.c_int
         L.or_svc_set.argtypes = [vp, u32, u32, vp]
+        L.or_adapt_get.restype = ctypes.c_int
+        L.or_adapt_get.argtypes = [vp, u32, u32, vp, vp]
+        L.or_adapt_set.restype = ctypes.c_int
+        L.or_adapt_set.argtypes = [vp, u32, u32, vp, vp]
         _lib = L
     return _lib
 
@@ -197,6 +205,18 @@ def make_cfg(cfg):
         c.alpha, c.beta, c.gamma_w = d["alpha"], d["beta"], d["gamma"]
         c.pen_over, c.pen_intf = d["pen_overloaded"], d["pen_interfered"]
         c.ewma_shift = d["ewma_shift"]
+    ad = cfg.get("adaptive")
+    if ad:
+        c.adapt_epoch, c.adapt_up, c.adapt_down = ad["epoch"], ad["step_up"], ad["step_down"]
+        c.adapt_max, c.adapt_margin = ad["max"], ad["margin"]
+        slo = list(ad["slo"])
+        for p in range(MAX_TIERS):
+            c.adapt_slo[p] = slo[min(p, len(slo) - 1)]
+    pr = cfg.get("promotion")
+    if pr:
+        c.promote_period = pr["period"]
+        for p, v in enumerate(pr["age"]):
+            c.promote_age[p] = v
     return c, groups
 
 
@@ -251,7 +271,8 @@ class Oracle:
                     next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
                     drain=np.zeros(nr * self.I, np.uint8),
                     hist=np.zeros(nr * 2 * MAX_TIERS * HBINS, np.uint32),
-                    svc=np.zeros(nr * self.I, np.int64))
+                    svc=np.zeros(nr * self.I, np.int64),
+                    hq=np.zeros(nr * MAX_TIERS, np.int32), hq_snap=np.zeros(nr * 2 * MAX_TIERS, np.uint64))
 
     _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain")
 
@@ -262,6 +283,8 @@ class Oracle:
         a = self._arrays(nr)
         rc = lib().or_export(self._h, r0, nr, *[_ptr(a[k]) for k in self._ORDER])
         if rc or lib().or_hist_get(self._h, r0, nr, _ptr(a["hist"])) or lib().or_svc_get(self._h, r0, nr, _ptr(a["svc"])):
+            raise OracleError("export range")
+        if lib().or_adapt_get(self._h, r0, nr, _ptr(a["hq"]), _ptr(a["hq_snap"])):
             raise OracleError("export range")
         return a
 
@@ -275,6 +298,11 @@ class Oracle:
         rc = lib().or_import(self._h, r0, nr, *[_ptr(b[k]) for k in self._ORDER])
         if rc or lib().or_hist_set(self._h, r0, nr, _ptr(b["hist"])) or lib().or_svc_set(self._h, r0, nr, _ptr(b["svc"])):
             raise OracleError("import range")
+        # adaptive headroom state: a missing array takes its default (Eq. 3's
+        # table; the current counters as the last update's)
+        if lib().or_adapt_set(self._h, r0, nr, _ptr(b["hq"]) if "hq" in a else None,
+                              _ptr(b["hq_snap"]) if "hq_snap" in a else None):
+            raise OracleError("import: adaptive headroom state out of range")
 
     def digests(self):
         out = np.zeros(self.r_count, np.uint64)

@@ -53,6 +53,15 @@
  * average of the normal-priority freeness F_normal (Eq. 1 without headroom)
  * is compared with the scale-out (-0.5) and scale-in (1.5) thresholds; the
  * ticks that signal either are counted.
+ * Adaptive headroom and multilevel-feedback promotion (Section 6.5, future
+ * work the paper leaves unspecified; the readings below are this oracle's):
+ *   - every adapt_epoch ticks each tier's headroom H_p moves up by a step
+ *     when the mean queue delay of the tier's requests first admitted since
+ *     the previous update exceeds the tier's target, down by a step when that
+ *     mean is at most a margin fraction of the target (the headroom went
+ *     unused), within [0, adapt_max];
+ *   - every promote_period ticks each waiting request of tier p >= 1 whose
+ *     age since arrival has reached the tier's quota moves up to tier p - 1.
  * Every quantity is an integer.  The headroom H_p is quantised to 1/256 block
  * and freeness values are compared by exact 64-bit cross-multiplication.
  *
@@ -119,6 +128,12 @@ typedef struct {
     int32_t alpha, beta, gamma_w;
     uint32_t pen_over, pen_intf;
     uint32_t tier_blind;         /* 1: tiers order nothing (priority-blind local scheduler) */
+    /* adaptive headroom: 0 epoch keeps Eq. 3's static table */
+    uint32_t adapt_epoch, adapt_up, adapt_down, adapt_max, adapt_margin;
+    uint32_t adapt_slo[OR_MAX_TIERS];     /* mean queue-delay target per tier, ticks */
+    /* promotion: 0 period promotes nothing; promote_age[p] = 0 never promotes tier p */
+    uint32_t promote_period;
+    uint32_t promote_age[OR_MAX_TIERS];
 } or_cfg;
 
 enum { POLICY_LLUMNIX = 0, POLICY_INFAAS = 1 };
@@ -148,6 +163,9 @@ typedef struct {
     uint32_t *fcnt;   /* [I] number of this tick's finishes */
     uint8_t *intf;    /* [I] preempted a request in this tick */
     uint32_t next_seq;
+    int32_t hq[OR_MAX_TIERS];           /* headroom H_p in 1/256 block (Eq. 3, then adapted) */
+    uint64_t snap_adm[OR_MAX_TIERS];    /* admitted / queue-delay counters at the last update */
+    uint64_t snap_qd[OR_MAX_TIERS];
     uint64_t stats[OR_NSTAT];
     uint32_t (*hist)[OR_MAX_TIERS][OR_HBINS];  /* [2]: queue delay, end-to-end */
     uint32_t n_arr, cap_arr;
@@ -411,7 +429,7 @@ static void freeness(const or_ctx *x, replica_t *rp, uint32_t i, int64_t *num, i
     int64_t demand = h >= 0 ? blocks(x, sl[h].len) : 0;
     int64_t v256 = 256 * (phys + demand);
     for (int p = 0; p < OR_MAX_TIERS; ++p)
-        if (present[p]) v256 += x->Hq[rp->group][p];
+        if (present[p]) v256 += rp->hq[p];
     *num = 256 * (int64_t)x->cfg.kv_blocks - v256;
     *den = running > 0 ? running : 1;
 }
@@ -872,8 +890,57 @@ static uint64_t check_invariants(const or_ctx *x, replica_t *rp)
     return bad;
 }
 
+/* ------------------------------------------------------------------ */
+/* Section 6.5 extensions, at the start of a tick                      */
+/* ------------------------------------------------------------------ */
+/* Adaptive headroom: at a tick t with t mod adapt_epoch = 0, tier p (every
+ * tier but the lowest when zero_lowest is set) takes the a requests of tier p
+ * first admitted since the previous update, with summed queue delay d:
+ *   d > slo_p * a                     the mean delay misses the target:
+ *                                     H_p = min(H_p + adapt_up, adapt_max)
+ *   256 d <= adapt_margin * slo_p * a the target is met with margin, the
+ *                                     headroom sat unused:
+ *                                     H_p = max(H_p - adapt_down, 0)
+ * and H_p stays otherwise, also when a = 0. */
+static void adapt_headroom(const or_ctx *x, replica_t *rp, uint64_t t)
+{
+    const or_cfg *c = &x->cfg;
+    if (c->adapt_epoch == 0 || t % c->adapt_epoch != 0) return;
+    const uint32_t K = x->groups[rp->group].K;
+    for (uint32_t p = 0; p < K; ++p) {
+        const uint64_t adm = rp->stats[p * 8 + F_ADMITTED], qd = rp->stats[p * 8 + F_QDELAY];
+        const unsigned __int128 a = adm - rp->snap_adm[p], d = qd - rp->snap_qd[p];
+        rp->snap_adm[p] = adm;
+        rp->snap_qd[p] = qd;
+        if ((c->zero_lowest && p == K - 1) || a == 0) continue;
+        const unsigned __int128 slo = c->adapt_slo[p];
+        int64_t h = rp->hq[p];
+        if (d > slo * a) h = h + c->adapt_up > c->adapt_max ? c->adapt_max : h + c->adapt_up;
+        else if (256 * d <= c->adapt_margin * slo * a) h = h < c->adapt_down ? 0 : h - c->adapt_down;
+        rp->hq[p] = (int32_t)h;
+    }
+}
+
+/* Multilevel-feedback promotion: at a tick t with t mod promote_period = 0,
+ * every waiting request of tier p >= 1 whose age t - tarr has reached
+ * promote_age[p] (> 0) moves to tier p - 1; later counters and histograms
+ * label it with the tier it holds then. */
+static void promote_waiting(const or_ctx *x, replica_t *rp, uint64_t t)
+{
+    const or_cfg *c = &x->cfg;
+    if (c->promote_period == 0 || t % c->promote_period != 0) return;
+    for (size_t s = 0; s < (size_t)x->I * x->S; ++s) {
+        slot_t *sl = &rp->slot[s];
+        if (sl->st != ST_WAITING || sl->tier == 0) continue;
+        const uint32_t age = (uint32_t)t - sl->tarr;
+        if (c->promote_age[sl->tier] != 0 && age >= c->promote_age[sl->tier]) sl->tier -= 1;
+    }
+}
+
 static void tick_replica(or_ctx *x, replica_t *rp, uint64_t t, uint8_t *abort_pending)
 {
+    promote_waiting(x, rp, t);
+    adapt_headroom(x, rp, t);
     memset(abort_pending, 0, x->I);
     memset(rp->fsum, 0, x->I * sizeof(uint64_t));
     memset(rp->fcnt, 0, x->I * sizeof(uint32_t));
@@ -912,6 +979,7 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
     if (cfg->n_instances == 0 || cfg->n_instances > 256 || cfg->slots == 0) return NULL;
     if (cfg->block_tokens == 0 || cfg->kv_blocks == 0 || cfg->mig_interval == 0 || cfg->theta_den <= 0) return NULL;
     if (cfg->policy > POLICY_INFAAS || cfg->ewma_shift > 16 || cfg->tier_blind > 1) return NULL;
+    if (cfg->adapt_margin > 256 || cfg->adapt_max > (1u << 29) / OR_MAX_TIERS) return NULL;
     uint32_t R = 0;
     for (uint32_t g = 0; g < cfg->n_groups; ++g) {
         if (cfg->groups[g].K == 0 || cfg->groups[g].K > OR_MAX_TIERS) return NULL;
@@ -934,6 +1002,14 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
     for (uint32_t g = 0; g < cfg->n_groups && !rc; ++g) {
         build_headroom(cfg, cfg->groups[g].K, x->Hq[g]);
         rc = build_tier_table(&cfg->groups[g], &x->tier_tab[g]);
+    }
+    if (!rc && cfg->adapt_epoch) {
+        if (cfg->adapt_epoch > (1u << 16)) rc = -1;
+        for (uint32_t p = 0; p < OR_MAX_TIERS && !rc; ++p)
+            if (cfg->adapt_slo[p] == 0 || cfg->adapt_slo[p] > (1u << 20)) rc = -1;
+        for (uint32_t g = 0; g < cfg->n_groups && !rc; ++g)
+            for (uint32_t p = 0; p < OR_MAX_TIERS; ++p)
+                if ((uint32_t)x->Hq[g][p] > cfg->adapt_max) rc = -1;
     }
     if (!rc) rc = build_count_table(cfg, &x->count_tab);
     if (!rc) rc = build_prompt_table(cfg, &x->prompt_tab);
@@ -965,6 +1041,7 @@ or_ctx *or_create(const or_cfg *cfg, uint32_t r_begin, uint32_t r_count, int che
             *err = -2; or_destroy(x); return NULL;
         }
         for (uint32_t i = 0; i < x->I; ++i) { rp->freeb[i] = cfg->kv_blocks; rp->mig[i].dst = -1; }
+        memcpy(rp->hq, x->Hq[g], sizeof(rp->hq));
     }
     *err = 0;
     return x;
@@ -1181,5 +1258,55 @@ int or_svc_set(or_ctx *x, uint32_t r0, uint32_t nr, const int64_t *in)
 {
     if (r0 > x->r_count || nr > x->r_count - r0) return -1;
     for (uint32_t r = 0; r < nr; ++r) memcpy(x->rep[r0 + r].svc, in + (size_t)r * x->I, x->I * sizeof(int64_t));
+    return 0;
+}
+
+/* adaptive headroom state of replicas [r0, r0+nr): hq[nr][10] in 1/256
+ * block; snap[nr][2][10] the admitted and queue-delay counters at the last
+ * update.  With a static headroom (adapt_epoch 0) or_adapt_set ignores both
+ * arrays and restores Eq. 3's table with zero counters; otherwise hq NULL
+ * restores Eq. 3's table, snap NULL takes the current counters, and an H_p
+ * outside [0, adapt_max], for a tier >= K or for the lowest tier when
+ * zero_lowest is set, other than 0, is rejected (-1, nothing changed). */
+int or_adapt_get(const or_ctx *x, uint32_t r0, uint32_t nr, int32_t *hq, uint64_t *snap)
+{
+    if (r0 > x->r_count || nr > x->r_count - r0) return -1;
+    for (uint32_t r = 0; r < nr; ++r) {
+        const replica_t *rp = &x->rep[r0 + r];
+        memcpy(hq + (size_t)r * OR_MAX_TIERS, rp->hq, sizeof(rp->hq));
+        memcpy(snap + (size_t)r * 2 * OR_MAX_TIERS, rp->snap_adm, sizeof(rp->snap_adm));
+        memcpy(snap + (size_t)r * 2 * OR_MAX_TIERS + OR_MAX_TIERS, rp->snap_qd, sizeof(rp->snap_qd));
+    }
+    return 0;
+}
+
+int or_adapt_set(or_ctx *x, uint32_t r0, uint32_t nr, const int32_t *hq, const uint64_t *snap)
+{
+    if (r0 > x->r_count || nr > x->r_count - r0) return -1;
+    const or_cfg *c = &x->cfg;
+    for (uint32_t r = 0; r < nr; ++r) {
+        replica_t *rp = &x->rep[r0 + r];
+        const uint32_t K = x->groups[rp->group].K;
+        if (c->adapt_epoch && hq)
+            for (uint32_t p = 0; p < OR_MAX_TIERS; ++p) {
+                const int32_t v = hq[(size_t)r * OR_MAX_TIERS + p];
+                if (v < 0 || (uint32_t)v > c->adapt_max || (p >= K && v != 0) || (c->zero_lowest && p == K - 1 && v != 0))
+                    return -1;
+            }
+    }
+    for (uint32_t r = 0; r < nr; ++r) {
+        replica_t *rp = &x->rep[r0 + r];
+        if (c->adapt_epoch && hq) memcpy(rp->hq, hq + (size_t)r * OR_MAX_TIERS, sizeof(rp->hq));
+        else memcpy(rp->hq, x->Hq[rp->group], sizeof(rp->hq));
+        for (int p = 0; p < OR_MAX_TIERS; ++p) {
+            if (c->adapt_epoch && snap) {
+                rp->snap_adm[p] = snap[(size_t)r * 2 * OR_MAX_TIERS + p];
+                rp->snap_qd[p] = snap[(size_t)r * 2 * OR_MAX_TIERS + OR_MAX_TIERS + p];
+            } else {
+                rp->snap_adm[p] = c->adapt_epoch ? rp->stats[p * 8 + F_ADMITTED] : 0;
+                rp->snap_qd[p] = c->adapt_epoch ? rp->stats[p * 8 + F_QDELAY] : 0;
+            }
+        }
+    }
     return 0;
 }

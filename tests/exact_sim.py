@@ -31,6 +31,13 @@ INFaaS baseline, Section 5.3) replaces the tier by a constant in every
 ordering -- dispatch order, queue order, preemption victim, migration
 candidate -- and nowhere else.
 
+Adaptive headroom and multilevel-feedback promotion (Section 6.5, future
+work; the readings are the library's) are written from the request list: the
+headroom update at an epoch boundary takes the queue delays of the requests
+first admitted since the previous boundary from the per-request latency log
+and compares their exact mean with the tier's target; promotion walks the
+waiting requests and compares each one's age with its tier's quota.
+
 The auto-scaling signal (Section 3.6)
 averages F_normal -- Eq. 1 with no headroom at all -- in fixed point with
 floor(F * 2^20) per instance.
@@ -75,8 +82,11 @@ class ExactSim:
         self.I, self.S = cfg["n_instances"], cfg["slots_per_instance"]
         self.M, self.blk = cfg["kv_blocks"], cfg["block_tokens"]
         self.K = K
-        self.H = [Fraction(h, 256) for h in exact_headroom(
-            cfg["headroom_base"], cfg["headroom_decay"], K, cfg["zero_lowest_tier"])]
+        self.Hint = exact_headroom(cfg["headroom_base"], cfg["headroom_decay"], K, cfg["zero_lowest_tier"])
+        self.H = [Fraction(h, 256) for h in self.Hint]
+        self.adapt = cfg.get("adaptive") or {}
+        self.promo = cfg.get("promotion") or {}
+        self.epoch_mark = 0  # first entry of the latency log since the last headroom update
         self.theta = Fraction(cfg["theta_num"], cfg["theta_den"])
         self.slots = [[None] * self.S for _ in range(self.I)]
         self.free = [self.M] * self.I
@@ -156,9 +166,45 @@ class ExactSim:
         return 0, total
 
     # -- the tick ---------------------------------------------------------
+    def promote(self, t):
+        period = self.promo.get("period", 0)
+        if not period or t % period:
+            return
+        age = list(self.promo["age"]) + [0] * 10
+        for i in range(self.I):
+            for _, r in self.requests(i, WAITING):
+                if r.tier >= 1 and age[r.tier] and t - r.tarr >= age[r.tier]:
+                    r.tier -= 1
+
+    def adapt_headroom(self, t):
+        epoch = self.adapt.get("epoch", 0)
+        if not epoch or t % epoch:
+            return
+        fresh = self.latencies[0][self.epoch_mark:]
+        self.epoch_mark = len(self.latencies[0])
+        ad = self.adapt
+        slo = list(ad["slo"])
+        for p in range(self.K):
+            if self.cfg["zero_lowest_tier"] and p == self.K - 1:
+                continue
+            lat = [v for tier, v in fresh if tier == p]
+            if not lat:
+                continue
+            mean = Fraction(sum(lat), len(lat))
+            target = slo[min(p, len(slo) - 1)]
+            h = self.Hint[p]
+            if mean > target:
+                h = min(h + ad["step_up"], ad["max"])
+            elif mean <= Fraction(ad["margin"] * target, 256):
+                h = max(h - ad["step_down"], 0)
+            self.Hint[p] = h
+            self.H[p] = Fraction(h, 256)
+
     def tick(self, arrivals):
         t = self.t
         st = self.stats
+        self.promote(t)
+        self.adapt_headroom(t)
         aborted = set()
         finished = [[] for _ in range(self.I)]  # end-to-end ticks of this tick's finishes
         interfered = set()
@@ -356,4 +402,5 @@ class ExactSim:
                     free=np.array(self.free, np.int32), mig=mig,
                     next_seq=np.array([self.next_seq], np.uint32),
                     stats=np.array(self.stats, np.uint64), drain=np.array(self.drain, np.uint8),
-                    svc=np.array(self.svc, np.int64))
+                    svc=np.array(self.svc, np.int64),
+                    hq=np.array(self.Hint + [0] * (10 - self.K), np.int32))

@@ -17,8 +17,8 @@ SRC = os.path.join(ROOT, "oracle", "mts_oracle.c")
 MUTATIONS = {
     # Eq. 4: headroom charged per running request instead of once per tier
     "headroom_per_request": [("present[sl[s].tier] = 1;", "present[sl[s].tier] += 1;"),
-                             ("if (present[p]) v256 += x->Hq[rp->group][p];",
-                              "v256 += present[p] * x->Hq[rp->group][p];")],
+                             ("if (present[p]) v256 += rp->hq[p];",
+                              "v256 += present[p] * rp->hq[p];")],
     # Eq. 2: head-of-line demand with the wrong sign
     "hol_sign": [("int64_t v256 = 256 * (phys + demand);", "int64_t v256 = 256 * (phys - demand);")],
     # Section 3.4: ties in F go to the highest index
@@ -90,6 +90,26 @@ MUTATIONS = {
     # INFaaS: INTERFERED takes precedence over OVERLOADED
     "infaas_state_order": [("    if (h >= 0 && (int64_t)blocks(x, inst_slots(x, rp, i)[h].len) > rp->freeb[i]) return x->cfg.pen_over;\n    if (rp->intf[i]) return x->cfg.pen_intf;",
                             "    if (rp->intf[i]) return x->cfg.pen_intf;\n    if (h >= 0 && (int64_t)blocks(x, inst_slots(x, rp, i)[h].len) > rp->freeb[i]) return x->cfg.pen_over;")],
+    # Section 6.5 promotion: strict instead of non-strict quota
+    "promote_strict_age": [("if (c->promote_age[sl->tier] != 0 && age >= c->promote_age[sl->tier]) sl->tier -= 1;",
+                            "if (c->promote_age[sl->tier] != 0 && age > c->promote_age[sl->tier]) sl->tier -= 1;")],
+    # Section 6.5 promotion: two tiers per pass
+    "promote_two_tiers": [("age >= c->promote_age[sl->tier]) sl->tier -= 1;",
+                           "age >= c->promote_age[sl->tier]) sl->tier = sl->tier >= 2 ? sl->tier - 2 : 0;")],
+    # Section 6.5 promotion: running requests promoted too
+    "promote_running": [("if (sl->st != ST_WAITING || sl->tier == 0) continue;",
+                         "if (sl->st == ST_EMPTY || sl->tier == 0) continue;")],
+    # Section 6.5 adaptive headroom: a mean exactly on target counts as a miss
+    "adapt_miss_inclusive": [("if (d > slo * a) h =", "if (d >= slo * a) h =")],
+    # Section 6.5 adaptive headroom: the two steps swapped
+    "adapt_steps_swapped": [("h = h + c->adapt_up > c->adapt_max ? c->adapt_max : h + c->adapt_up;",
+                             "h = h + c->adapt_down > c->adapt_max ? c->adapt_max : h + c->adapt_down;"),
+                            ("h = h < c->adapt_down ? 0 : h - c->adapt_down;",
+                             "h = h < c->adapt_up ? 0 : h - c->adapt_up;")],
+    # Section 6.5 adaptive headroom: the lowest tier adapts under zero_lowest
+    "adapt_lowest_tier": [("if ((c->zero_lowest && p == K - 1) || a == 0) continue;", "if (a == 0) continue;")],
+    # Section 6.5 adaptive headroom: counters never re-based (cumulative means)
+    "adapt_cumulative": [("        rp->snap_adm[p] = adm;\n        rp->snap_qd[p] = qd;\n", "")],
 }
 
 
@@ -110,6 +130,7 @@ def test_mutation_is_caught(name, tmp_path):
                         os.path.join(ROOT, "tests", "test_oracle_drain_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_hist_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_infaas_pins.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_exact.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_exact.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_adaptive_pins.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, "mutation %s survived every pin:\n%s" % (name, r.stdout[-2000:])
