@@ -26,6 +26,9 @@
  *      high-F destinations while the gap is at least theta; each source
  *      moves its head-of-line queued request, else starts a staged copy of
  *      its lowest-priority, smallest running request (Section 3.5, Fig. 4)
+ * Optional, at the start of a tick (Section 6.5 future work, see mts_cfg):
+ *   the headroom of each tier adapts to its observed queue delay, and
+ *   waiting requests that waited past their tier's quota are promoted.
  * All scheduler state and arithmetic is integer; headroom is fixed point at
  * 1/256 block and freeness values are compared exactly.
  *
@@ -46,7 +49,7 @@
 extern "C" {
 #endif
 
-#define MTS_ABI_VERSION 5
+#define MTS_ABI_VERSION 6
 #define MTS_MAX_TIERS 10
 #define MTS_NSTAT 96
 /* Latency histogram bins per (metric, tier); see mts_state_view.hist */
@@ -141,6 +144,35 @@ typedef struct mts_cfg {
      * Tiers still label the counters and histograms and still enter Eq. 4's
      * headroom.  0: tier order everywhere (Sections 3.1, 3.4). */
     uint32_t tier_blind;
+    /* Adaptive headroom (Section 6.5 names it as future work and leaves the
+     * controller open; this is the library's reading).  adapt_epoch = 0
+     * keeps Eq. 3's static table.  Otherwise each replica carries its own
+     * table, starting from Eq. 3's, and at the start of every tick t with
+     * t % adapt_epoch == 0 each tier p < K (but the lowest when
+     * zero_lowest_tier is set) takes the a requests of tier p first admitted
+     * since the previous update and their summed queue delay d (ticks):
+     *   d > adapt_slo[p] * a                 the mean misses the target:
+     *        H_p = min(H_p + adapt_up, adapt_max)
+     *   256 d <= adapt_margin * adapt_slo[p] * a
+     *                                        met with margin, the headroom
+     *                                        sat unused: H_p = max(H_p - adapt_down, 0)
+     * and H_p stays otherwise, also when a = 0.  H_p, adapt_up, adapt_down
+     * and adapt_max are in 1/256 block; exact for any counter values. */
+    uint32_t adapt_epoch;        /* 0..65536 ticks */
+    uint32_t adapt_up, adapt_down;/* any */
+    uint32_t adapt_max;          /* >= every static H_p, <= 2^29 / MTS_MAX_TIERS */
+    uint32_t adapt_margin;       /* 0..256 (fraction of the target in 1/256) */
+    uint32_t adapt_slo[MTS_MAX_TIERS]; /* mean queue-delay target per tier, 1..2^20 ticks (epoch > 0) */
+    /* Multilevel-feedback promotion (Section 6.5 future work; the library's
+     * reading).  promote_period = 0 promotes nothing.  Otherwise at the start
+     * of every tick t with t % promote_period == 0 each waiting request of
+     * tier p >= 1 whose age t - tarr (mod 2^32) is at least promote_age[p]
+     * moves to tier p - 1 (one tier per pass; promote_age[p] = 0: tier p is
+     * never promoted; promote_age[0] is ignored).  A promoted request keeps
+     * its new tier: admission, preemption, finish, the queue order, Eq. 4's
+     * tier mask, the counters and the histograms all see the tier it holds. */
+    uint32_t promote_period;
+    uint32_t promote_age[MTS_MAX_TIERS];
 } mts_cfg;
 
 enum { MTS_POLICY_LLUMNIX = 0, MTS_POLICY_INFAAS = 1 };
@@ -192,10 +224,21 @@ typedef struct mts_stats_t {
  *                 sub-ranges per octave; at most 239)
  *   svc[nr*I]     INFaaS service-time estimate s of each instance, 1/256 tick
  *                 (0 under MTS_POLICY_LLUMNIX)
+ *   hq[nr*MTS_MAX_TIERS]
+ *                 headroom H_p in 1/256 block the replica uses now (Eq. 3's
+ *                 table unless the headroom adapts; 0 for p >= K)
+ *   hq_snap[nr*2*MTS_MAX_TIERS]
+ *                 adaptive headroom: the per-tier admitted (first 10) and
+ *                 queue-delay-sum (next 10) counters at the last update
+ *                 (zeros when the headroom is static)
  * Empty slots are all-zero.  Export skips every NULL array.  Import needs
- * every array but drain, hist and svc; a NULL drain clears the flags, a NULL
- * hist empties the histograms, a NULL svc zeroes the estimates; an estimate
- * outside 0..2^40 is MTS_EINVAL. */
+ * every array but drain, hist, svc, hq and hq_snap; a NULL drain clears the
+ * flags, a NULL hist empties the histograms, a NULL svc zeroes the
+ * estimates; an estimate outside 0..2^40 is MTS_EINVAL.  With a static
+ * headroom hq and hq_snap are ignored.  With an adaptive one a NULL hq
+ * restores Eq. 3's table, a NULL hq_snap takes the imported counters, and an
+ * H_p outside 0..adapt_max, or other than 0 for p >= K or for the lowest
+ * tier under zero_lowest_tier, is MTS_EINVAL. */
 typedef struct mts_state_view {
     uint8_t* meta;
     uint32_t* lr;
@@ -208,6 +251,8 @@ typedef struct mts_state_view {
     uint8_t* drain;
     uint32_t* hist;
     int64_t* svc;
+    int32_t* hq;
+    uint64_t* hq_snap;
 } mts_state_view;
 
 typedef struct mts_ctx* mts_handle;

@@ -128,6 +128,10 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.drain = o;    o = up256(o + size_t(R) * I);
     L.hist = o;     o = up256(o + size_t(R) * kHistPerReplica * 4);
     L.svc = o;      o = up256(o + size_t(R) * I * 8);
+    L.ext = o;      o = up256(o + 2 * MTS_MAX_TIERS * 4);
+    const bool adapt = c.adapt_epoch != 0;
+    L.hqr = o;      o = up256(o + (adapt ? size_t(R) * MTS_MAX_TIERS * 4 : 0));
+    L.hsnap = o;    o = up256(o + (adapt ? size_t(R) * 2 * MTS_MAX_TIERS * 8 : 0));
     L.next_seq = o; o = up256(o + size_t(R) * 4);
     L.stats = o;    o = up256(o + size_t(R) * MTS_NSTAT * 8);
     L.digest = o;   o = up256(o + size_t(R) * 8);
@@ -175,7 +179,17 @@ Params make_params(const mts_ctx* h)
     p.pen_intf = c.infaas_pen_interfered;
     p.qdepth = h->qdepth;
     p.blind = c.tier_blind;
+    p.zero_lowest = c.zero_lowest_tier;
+    p.adapt_epoch = c.adapt_epoch;
+    p.adapt_up = c.adapt_up;
+    p.adapt_down = c.adapt_down;
+    p.adapt_max = c.adapt_max;
+    p.adapt_margin = c.adapt_margin;
+    p.promo_period = c.promote_period;
     const Layout& L = h->lay;
+    p.ext = reinterpret_cast<const uint32_t*>(d + L.ext);
+    p.hqr = c.adapt_epoch ? reinterpret_cast<int32_t*>(d + L.hqr) : nullptr;
+    p.hsnap = c.adapt_epoch ? reinterpret_cast<unsigned long long*>(d + L.hsnap) : nullptr;
     p.tier_q = reinterpret_cast<const unsigned long long*>(d + L.tier_q);
     p.hq = reinterpret_cast<const int32_t*>(d + L.hq);
     p.group_K32 = reinterpret_cast<const uint32_t*>(d + L.group_K);
@@ -213,6 +227,9 @@ std::vector<uint32_t> device_table(const Table& t, size_t pad_to = 0)
 }
 
 int hip_rc(hipError_t e) { return e == hipSuccess ? MTS_OK : MTS_EDEVICE; }
+
+// the step kernel keeps adaptive-headroom or promotion state in LDS
+bool ext_state(const mts_cfg& c) { return c.adapt_epoch != 0 || c.promote_period != 0; }
 
 int prepare(const mts_cfg* cfg, mts_ctx& x)
 {
@@ -278,7 +295,7 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
         delete x;
         return MTS_EDEVICE;
     }
-    if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, 0) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
+    if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, 0, ext_state(x->cfg)) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
     // queue cache depth: the deepest of 7, 3, 1 that keeps the step kernel's
     // blocks per CU (the cache only saves rescans; a lost block per CU costs
     // more: with no spare room per CU the dispatcher cannot place every
@@ -289,7 +306,7 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
         const int base = step_blocks_per_cu(p);
         for (uint32_t d : {7u, 3u, 1u}) {
             p.qdepth = d;
-            if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, d) > size_t(max_lds)) continue;
+            if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, d, ext_state(x->cfg)) > size_t(max_lds)) continue;
             if (step_blocks_per_cu(p) >= base) { x->qdepth = d; break; }
         }
     }
@@ -330,6 +347,19 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
     up(L.prompt_g, pg.data(), pg.size() * 4);
     up(L.output_g, og.data(), og.size() * 4);
     up(L.group_of, x->group_of.data(), x->group_of.size() * 2);
+    uint32_t ext[2 * MTS_MAX_TIERS];
+    std::memcpy(ext, x->cfg.adapt_slo, sizeof(x->cfg.adapt_slo));
+    std::memcpy(ext + MTS_MAX_TIERS, x->cfg.promote_age, sizeof(x->cfg.promote_age));
+    up(L.ext, ext, sizeof(ext));
+    // adaptive headroom starts from each replica's group table
+    std::vector<int32_t> hqr;
+    if (x->cfg.adapt_epoch) {
+        hqr.resize(size_t(x->R) * MTS_MAX_TIERS);
+        for (uint32_t r = 0; r < x->R; ++r)
+            std::memcpy(&hqr[size_t(r) * MTS_MAX_TIERS], &x->tables.hq[size_t(x->group_of[r]) * MTS_MAX_TIERS],
+                        MTS_MAX_TIERS * 4);
+        up(L.hqr, hqr.data(), hqr.size() * 4);
+    }
     if (e == hipSuccess) e = hipStreamSynchronize(stream);  // host vectors go out of scope
     if (e != hipSuccess) { delete x; return MTS_EDEVICE; }
     const Params p = make_params(x);
@@ -370,7 +400,7 @@ int mts_set_queue_cache(mts_handle h, uint32_t depth)
     int max_lds = 0;
     if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device) != hipSuccess)
         return MTS_EDEVICE;
-    if (lds_bytes(h->I, h->S, h->cfg.block_tokens, h->wsz, h->cfg.dispatch_policy, depth) > size_t(max_lds))
+    if (lds_bytes(h->I, h->S, h->cfg.block_tokens, h->wsz, h->cfg.dispatch_policy, depth, ext_state(h->cfg)) > size_t(max_lds))
         return MTS_EINVAL;
     hipError_t e = hipStreamSynchronize(h->last);
     if (e != hipSuccess) return MTS_EDEVICE;
@@ -511,6 +541,16 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     get(v->drain, L.drain + size_t(r0) * I, size_t(nr) * I);
     get(v->hist, L.hist + size_t(r0) * kHistPerReplica * 4, size_t(nr) * kHistPerReplica * 4);
     get(v->svc, L.svc + size_t(r0) * I * 8, size_t(nr) * I * 8);
+    if (h->cfg.adapt_epoch) {
+        get(v->hq, L.hqr + size_t(r0) * MTS_MAX_TIERS * 4, size_t(nr) * MTS_MAX_TIERS * 4);
+        get(v->hq_snap, L.hsnap + size_t(r0) * 2 * MTS_MAX_TIERS * 8, size_t(nr) * 2 * MTS_MAX_TIERS * 8);
+    } else {
+        // static headroom: the group's table, no counters
+        for (uint32_t r = 0; r < nr && v->hq; ++r)
+            std::memcpy(v->hq + size_t(r) * MTS_MAX_TIERS, &h->tables.hq[size_t(h->group_of[r0 + r]) * MTS_MAX_TIERS],
+                        MTS_MAX_TIERS * 4);
+        if (v->hq_snap) std::memset(v->hq_snap, 0, size_t(nr) * 2 * MTS_MAX_TIERS * 8);
+    }
     return hip_rc(e);
 }
 
@@ -556,6 +596,13 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
             if (v->svc && (v->svc[size_t(r) * I + i] < 0 || v->svc[size_t(r) * I + i] > (int64_t(1) << 40)))
                 return MTS_EINVAL;
         }
+        if (h->cfg.adapt_epoch && v->hq)
+            for (uint32_t p = 0; p < MTS_MAX_TIERS; ++p) {
+                const int32_t x = v->hq[size_t(r) * MTS_MAX_TIERS + p];
+                if (x < 0 || uint32_t(x) > h->cfg.adapt_max || (p >= K && x != 0) ||
+                    (h->cfg.zero_lowest_tier && p == K - 1 && x != 0))
+                    return MTS_EINVAL;
+            }
     }
     const Layout& L = h->lay;
     hipError_t e = hipStreamSynchronize(h->last);
@@ -588,6 +635,22 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
         put(L.svc + size_t(r0) * I * 8, v->svc, sn);
     } else if (e == hipSuccess && sn) {
         e = hipMemset(h->dev + L.svc + size_t(r0) * I * 8, 0, sn);
+    }
+    if (h->cfg.adapt_epoch) {
+        // missing arrays: the group's Eq. 3 table; the imported counters as
+        // the last update's
+        std::vector<int32_t> hq(size_t(nr) * MTS_MAX_TIERS);
+        std::vector<uint64_t> snap(size_t(nr) * 2 * MTS_MAX_TIERS);
+        for (uint32_t r = 0; r < nr; ++r)
+            for (uint32_t p = 0; p < MTS_MAX_TIERS; ++p) {
+                const size_t k = size_t(r) * MTS_MAX_TIERS + p, k2 = size_t(r) * 2 * MTS_MAX_TIERS + p;
+                hq[k] = v->hq ? v->hq[k] : h->tables.hq[size_t(h->group_of[r0 + r]) * MTS_MAX_TIERS + p];
+                snap[k2] = v->hq_snap ? v->hq_snap[k2] : v->stats[size_t(r) * MTS_NSTAT + p * 8 + kAdmittedCnt];
+                snap[k2 + MTS_MAX_TIERS] = v->hq_snap ? v->hq_snap[k2 + MTS_MAX_TIERS]
+                                                      : v->stats[size_t(r) * MTS_NSTAT + p * 8 + kQdelay];
+            }
+        put(L.hqr + size_t(r0) * MTS_MAX_TIERS * 4, hq.data(), hq.size() * 4);
+        put(L.hsnap + size_t(r0) * 2 * MTS_MAX_TIERS * 8, snap.data(), snap.size() * 8);
     }
     return hip_rc(e);
 }

@@ -56,6 +56,8 @@ struct Layout {
     size_t freeb, mig, drain;                                           // [R][I], [R][I][4], [R][I] u8
     size_t hist;                                                        // [R][2][10][MTS_HIST_BINS] u32
     size_t svc;                                                         // [R][I] i64 INFaaS estimate
+    size_t ext;                                                         // u32 adapt_slo[10], promote_age[10]
+    size_t hqr, hsnap;                                                  // adaptive: [R][10] i32, [R][2][10] u64
     size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
     size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
     size_t wheel;                                                       // [R][wsz][wcap]
@@ -79,6 +81,13 @@ struct Params {
     uint32_t pen_over, pen_intf;   // INFaaS state penalties in ticks
     uint32_t qdepth;               // queue-cache entries behind each head of line (LDS)
     uint32_t blind;                // 1: tiers order nothing (tier-blind scheduling)
+    uint32_t zero_lowest;          // 1: the lowest tier carries no headroom
+    // adaptive headroom (epoch 0: static) and promotion (period 0: none)
+    uint32_t adapt_epoch, adapt_up, adapt_down, adapt_max, adapt_margin;
+    uint32_t promo_period;
+    const uint32_t* ext;           // adapt_slo[10], then promote_age[10]
+    int32_t* hqr;                  // [R][10] per-replica headroom (adaptive only)
+    unsigned long long* hsnap;     // [R][2][10] admitted / queue-delay counters at the last update
     const unsigned long long* tier_q;  // [group][MTS_MAX_TIERS] floor(2^32 CDF), up to 2^32
     const int32_t* hq;             // [group][MTS_MAX_TIERS]
     const uint32_t* group_K32;     // [group] tier count
@@ -107,7 +116,8 @@ struct Params {
 };
 
 // LDS bytes of one wave (one replica) of the step kernel
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy, uint32_t qdepth);
+// (ext: the adaptive-headroom or promotion state is kept in LDS)
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy, uint32_t qdepth, bool ext);
 
 // kernel launches (mts_kernels.hip, mts_arrivals.hip); return hipError_t as int
 int launch_init(const Params& p, hipStream_t stream);

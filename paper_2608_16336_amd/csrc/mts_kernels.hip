@@ -53,7 +53,7 @@ constexpr int kLast = 64;
 constexpr int kVic = 16;
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, ext, total;
 };
 
 __host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
@@ -68,7 +68,7 @@ __host__ __device__ constexpr uint32_t imax_for(uint32_t I)
 }
 
 __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_t W, uint32_t RB, uint32_t wsz,
-                                                uint32_t policy, uint32_t qdepth)
+                                                uint32_t policy, uint32_t qdepth, bool ext)
 {
     LdsLayout L;
     uint32_t o = 0;
@@ -93,6 +93,11 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     o = (o + 15u) & ~15u;
     L.qt = o;    o += IM * qdepth * 16;
     L.qn = o;    o += qdepth ? IM * 8 : 0;
+    // adaptive headroom / promotion: per tier the admitted and queue-delay
+    // counters at the last headroom update (u64 each), the headroom, the
+    // queue-delay target and the promotion quota
+    o = al8(o);
+    L.ext = o;   o += ext ? kTiers * 28 : 0;
     L.total = al8(o);
     return L;
 }
@@ -128,6 +133,11 @@ struct Ctx {
     int* qh;                   // [I] ring position of the first entry
     int td;
     uint32_t blind;            // 1: tiers order nothing (tier-blind scheduling)
+    // adaptive headroom and promotion (null when both are off), per tier
+    unsigned long long* asnap; // [2][10] admitted, queue-delay counters at the last update
+    int* ahq;                  // [10] headroom, 1/256 block
+    unsigned* aslo;            // [10] queue-delay target, ticks
+    unsigned* apage;           // [10] promotion quota, ticks (0: never)
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -143,7 +153,8 @@ struct Ctx {
 template <int IM, bool INF>
 __device__ inline Ctx carve(char* base, const Params& P)
 {
-    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz, P.policy, P.qdepth);
+    const bool ext = P.adapt_epoch != 0 || P.promo_period != 0;
+    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz, P.policy, P.qdepth, ext);
     Ctx C;
     C.stats = reinterpret_cast<unsigned long long*>(base + Y.stats);
     C.occ = reinterpret_cast<unsigned long long*>(base + Y.occ);
@@ -193,6 +204,14 @@ __device__ inline Ctx carve(char* base, const Params& P)
         C.pen = C.fcnt + IM;
     } else {
         C.fsum = nullptr; C.svc = nullptr; C.fcnt = nullptr; C.pen = nullptr;
+    }
+    if (ext) {
+        C.asnap = reinterpret_cast<unsigned long long*>(base + Y.ext);
+        C.ahq = reinterpret_cast<int*>(C.asnap + 2 * kTiers);
+        C.aslo = reinterpret_cast<unsigned*>(C.ahq + kTiers);
+        C.apage = C.aslo + kTiers;
+    } else {
+        C.asnap = nullptr; C.ahq = nullptr; C.aslo = nullptr; C.apage = nullptr;
     }
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
@@ -929,9 +948,72 @@ __device__ inline void admit_fresh(const Ctx& C, int i, uint32_t t, int lane)
 }
 
 // ---------------------------------------------------------------------------
+// Section 6.5 extensions, run at the start of a tick (uniform)
+// ---------------------------------------------------------------------------
+
+// Promotion pass: every waiting request of tier p >= 1 whose age t - tarr
+// has reached the tier's quota (non-zero) moves to tier p - 1.  An instance
+// whose queue changed order loses its cached head of line and queue cache
+// (found again by the admission rescan) and its list of fresh placements.
+__device__ inline void promote_waiting(const Ctx& C, uint32_t t, int lane)
+{
+    for (uint32_t i = 0; i < C.I; ++i) {
+        if (C.nwait[i] == 0) continue;
+        const size_t b = size_t(i) * C.S;
+        const int nch = live_chunks(C, i, lane);
+        bool any = false;
+        for (int c = 0; c < nch; ++c) {
+            const int s = c * 64 + lane;
+            if (wst(C.hot[b + s]) != 1u) continue;
+            const uint32_t m = C.meta[b + s], tier = (m >> 2) & 15u;
+            if (tier == 0) continue;
+            const uint32_t q = C.apage[tier];
+            if (q != 0 && t - C.tarr[b + s] >= q) {
+                C.meta[b + s] = uint8_t(m - 4u);  // tier field at bits 2..5
+                any = true;
+            }
+        }
+        if (ballot(any) != 0 && lane == 0) { C.hols[i] = kHolUnknown; C.frs[i] = 0; }
+    }
+    wave_sync();
+}
+
+// Adaptive headroom update: lane p < 10 handles tier p.  With a requests
+// first admitted since the last update and their summed queue delay d, the
+// headroom rises by a step when d > slo a, falls by a step when
+// 256 d <= margin slo a, both tests in exact 128-bit arithmetic.
+__device__ inline void adapt_headroom(const Ctx& C, const Params& P, int lane)
+{
+    if (lane < kTiers) {
+        const int p = lane;
+        const unsigned long long adm = C.stats[p * 8 + kAdmittedCnt], qd = C.stats[p * 8 + kQdelay];
+        const unsigned long long a = adm - C.asnap[p], d = qd - C.asnap[kTiers + p];
+        C.asnap[p] = adm;
+        C.asnap[kTiers + p] = qd;
+        if (p < int(C.K) && !(P.zero_lowest && p == int(C.K) - 1) && a != 0) {
+            const unsigned long long slo = C.aslo[p];
+            const unsigned long long xl = slo * a, xh = __umul64hi(slo, a);
+            const unsigned long long ms = slo * P.adapt_margin;  // < 2^29
+            const unsigned long long yl = ms * a, yh = __umul64hi(ms, a);
+            const unsigned long long dl = d << 8, dh = d >> 56;
+            long long h = C.ahq[p];
+            if (xh == 0 && d > xl) {
+                h += P.adapt_up;
+                if (h > static_cast<long long>(P.adapt_max)) h = P.adapt_max;
+            } else if (dh < yh || (dh == yh && dl <= yl)) {
+                h -= P.adapt_down;
+                if (h < 0) h = 0;
+            }
+            C.ahq[p] = int(h);
+        }
+    }
+    wave_sync();
+}
+
+// ---------------------------------------------------------------------------
 // k_step
 // ---------------------------------------------------------------------------
-template <int IM, bool INF>
+template <int IM, bool INF, bool EXT>
 __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigned long long t0, uint32_t nt)
 {
     constexpr int IPL = (IM + 63) / 64;
@@ -945,8 +1027,20 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
     for (uint32_t r = blockIdx.x; r < P.R; r += gridDim.x) {
         const uint32_t g = P.group_of[r];
         C.K = P.group_K32[g];
+        if (EXT) {
+            if (lane < kTiers) {
+                C.aslo[lane] = P.ext[lane];
+                C.apage[lane] = P.ext[kTiers + lane];
+                if (P.hqr) {
+                    C.ahq[lane] = P.hqr[size_t(r) * kTiers + lane];
+                    C.asnap[lane] = P.hsnap[size_t(r) * 2 * kTiers + lane];
+                    C.asnap[kTiers + lane] = P.hsnap[size_t(r) * 2 * kTiers + kTiers + lane];
+                }
+            }
+        }
+        const int32_t* hq = EXT && P.hqr ? P.hqr + size_t(r) * kTiers : P.hq + g * kTiers;
 #pragma unroll
-        for (int p = 0; p < kTiers; ++p) C.hq[p] = P.hq[g * kTiers + p];
+        for (int p = 0; p < kTiers; ++p) C.hq[p] = hq[p];
         const size_t rb = size_t(r) * I * S;
         C.hot = P.hot + rb; C.meta = P.meta + rb; C.seq = P.seq + rb; C.tarr = P.tarr + rb;
         C.wheel = P.wheel + size_t(r) * wsz * P.wcap;
@@ -1045,11 +1139,28 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         constexpr uint32_t kNoPf = 0xFFFFFFFFu;
         uint32_t pf_n = kNoPf, pf_e = 0, pf_v = 0, pf_m = 0, pf_a = 0;
         unsigned long long a_nx = uint32_t(lane) < lim ? recs[lane] : 0ull;
+        // ticks until the next promotion pass and headroom update
+        uint32_t pc = EXT && P.promo_period ? t0u % P.promo_period : 0u;
+        uint32_t ac = EXT && P.adapt_epoch ? t0u % P.adapt_epoch : 0u;
         for (uint32_t tl = 0; tl < nt; ++tl) {
             const uint32_t t = t0u + tl;
             const uint32_t n = n_nx;
             const unsigned long long* rec = recs + size_t(tl) * P.arr_cap;
             const unsigned long long a0 = a_nx;
+
+            // ============ Section 6.5: promotion, adaptive headroom ============
+            if (EXT && P.promo_period) {
+                if (pc == 0) promote_waiting(C, t, lane);
+                pc = pc + 1u == P.promo_period ? 0u : pc + 1u;
+            }
+            if (EXT && P.adapt_epoch) {
+                if (ac == 0) {
+                    adapt_headroom(C, P, lane);
+#pragma unroll
+                    for (int p = 0; p < kTiers; ++p) C.hq[p] = C.ahq[p];
+                }
+                ac = ac + 1u == P.adapt_epoch ? 0u : ac + 1u;
+            }
 
             // ===================== A: growth, preemption, finish =====================
             const uint32_t cres = (0u - t) & C.bmask;
@@ -1705,6 +1816,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             for (int k = 0; k < 4; ++k) P.mig[(size_t(r) * I + i) * 4 + k] = C.mig[4 * i + k];
         }
         if (lane == 0) P.next_seq[r] = next_seq;
+        if (EXT && P.hqr && lane < kTiers) {
+            P.hqr[size_t(r) * kTiers + lane] = C.ahq[lane];
+            P.hsnap[size_t(r) * 2 * kTiers + lane] = C.asnap[lane];
+            P.hsnap[size_t(r) * 2 * kTiers + kTiers + lane] = C.asnap[kTiers + lane];
+        }
         wave_sync();
     }
 }
@@ -1727,6 +1843,8 @@ __global__ void k_init(Params P)
     for (size_t j = t0; j < size_t(P.R) * P.I; j += stride) P.svc[j] = 0;
     for (size_t j = t0; j < size_t(P.R) * kNstat; j += stride) P.stats[j] = 0;
     for (size_t j = t0; j < P.R; j += stride) { P.next_seq[j] = 0; P.digest[j] = 0; }
+    if (P.hsnap)
+        for (size_t j = t0; j < size_t(P.R) * 2 * kTiers; j += stride) P.hsnap[j] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -1803,9 +1921,9 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t 
 
 }  // namespace
 
-size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy, uint32_t qdepth)
+size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t policy, uint32_t qdepth, bool ext)
 {
-    return lds_layout(imax_for(I), I, S / 64, RB, wsz, policy, qdepth).total;
+    return lds_layout(imax_for(I), I, S / 64, RB, wsz, policy, qdepth, ext).total;
 }
 
 int launch_init(const Params& p, hipStream_t stream)
@@ -1817,38 +1935,43 @@ int launch_init(const Params& p, hipStream_t stream)
 
 namespace {
 
-template <bool INF>
+template <bool INF, bool EXT>
 const void* step_fn_t(uint32_t I)
 {
     switch (imax_for(I)) {
-    case 16: return reinterpret_cast<const void*>(&k_step<16, INF>);
-    case 32: return reinterpret_cast<const void*>(&k_step<32, INF>);
-    case 64: return reinterpret_cast<const void*>(&k_step<64, INF>);
-    case 128: return reinterpret_cast<const void*>(&k_step<128, INF>);
-    default: return reinterpret_cast<const void*>(&k_step<256, INF>);
+    case 16: return reinterpret_cast<const void*>(&k_step<16, INF, EXT>);
+    case 32: return reinterpret_cast<const void*>(&k_step<32, INF, EXT>);
+    case 64: return reinterpret_cast<const void*>(&k_step<64, INF, EXT>);
+    case 128: return reinterpret_cast<const void*>(&k_step<128, INF, EXT>);
+    default: return reinterpret_cast<const void*>(&k_step<256, INF, EXT>);
     }
 }
 
+// the kernels with the adaptive-headroom / promotion code are separate
+// instantiations, so that the others carry none of its registers
+bool ext_on(const Params& p) { return p.adapt_epoch != 0 || p.promo_period != 0; }
+
 const void* step_fn(const Params& p)
 {
-    return p.policy == MTS_POLICY_INFAAS ? step_fn_t<true>(p.I) : step_fn_t<false>(p.I);
+    if (p.policy == MTS_POLICY_INFAAS) return ext_on(p) ? step_fn_t<true, true>(p.I) : step_fn_t<true, false>(p.I);
+    return ext_on(p) ? step_fn_t<false, true>(p.I) : step_fn_t<false, false>(p.I);
 }
 
-template <bool INF>
+template <bool INF, bool EXT>
 void launch_step_t(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, size_t lds, hipStream_t stream)
 {
     switch (imax_for(p.I)) {
-    case 16: hipLaunchKernelGGL((k_step<16, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 32: hipLaunchKernelGGL((k_step<32, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 64: hipLaunchKernelGGL((k_step<64, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 128: hipLaunchKernelGGL((k_step<128, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    default: hipLaunchKernelGGL((k_step<256, INF>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 16: hipLaunchKernelGGL((k_step<16, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 32: hipLaunchKernelGGL((k_step<32, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 64: hipLaunchKernelGGL((k_step<64, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 128: hipLaunchKernelGGL((k_step<128, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    default: hipLaunchKernelGGL((k_step<256, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
     }
 }
 
 size_t step_lds(const Params& p)
 {
-    const size_t lds = lds_bytes(p.I, p.S, p.RB, p.wsz, p.policy, p.qdepth);
+    const size_t lds = lds_bytes(p.I, p.S, p.RB, p.wsz, p.policy, p.qdepth, ext_on(p));
     if (lds > 64 * 1024) {
         // raise the dynamic LDS limit; a real failure shows up at the launch
         (void)hipFuncSetAttribute(step_fn(p), hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
@@ -1873,8 +1996,13 @@ int step_blocks_per_cu(const Params& p)
 int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream)
 {
     const size_t lds = step_lds(p);
-    if (p.policy == MTS_POLICY_INFAAS) launch_step_t<true>(p, t0, nt, blocks, lds, stream);
-    else launch_step_t<false>(p, t0, nt, blocks, lds, stream);
+    if (p.policy == MTS_POLICY_INFAAS) {
+        if (ext_on(p)) launch_step_t<true, true>(p, t0, nt, blocks, lds, stream);
+        else launch_step_t<true, false>(p, t0, nt, blocks, lds, stream);
+    } else {
+        if (ext_on(p)) launch_step_t<false, true>(p, t0, nt, blocks, lds, stream);
+        else launch_step_t<false, false>(p, t0, nt, blocks, lds, stream);
+    }
     return int(hipGetLastError());
 }
 

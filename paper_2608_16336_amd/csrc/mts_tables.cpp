@@ -132,6 +132,12 @@ int validate(const mts_cfg& c)
         c.infaas_gamma < 0 || c.infaas_gamma > 65536)
         return MTS_EINVAL;
     if (c.infaas_pen_overloaded > (1u << 20) || c.infaas_pen_interfered > (1u << 20)) return MTS_EINVAL;
+    // adaptive headroom: every H_p stays in [0, adapt_max], so the sum over
+    // tiers keeps the freeness numerators below 2^30 like the static table
+    if (c.adapt_margin > 256 || c.adapt_max > (1u << 29) / MTS_MAX_TIERS || c.adapt_epoch > (1u << 16)) return MTS_EINVAL;
+    if (c.adapt_epoch)
+        for (uint32_t p = 0; p < MTS_MAX_TIERS; ++p)
+            if (c.adapt_slo[p] < 1 || c.adapt_slo[p] > (1u << 20)) return MTS_EINVAL;
     if (c.n_instances < 1 || c.n_instances > kMaxInstances) return MTS_EINVAL;
     if (c.slots_per_instance < 64 || c.slots_per_instance > kMaxSlots || c.slots_per_instance % 64) return MTS_EINVAL;
     if (c.kv_blocks < 1 || c.kv_blocks > kMaxBlocks) return MTS_EINVAL;
@@ -195,6 +201,9 @@ int build_tables(const mts_cfg& c, Tables& T)
         int64_t hsum = 0;
         for (uint32_t p = 0; p < MTS_MAX_TIERS; ++p) hsum += T.hq[size_t(g) * MTS_MAX_TIERS + p];
         if (hsum > (int64_t(1) << 29)) return MTS_EINVAL;
+        if (c.adapt_epoch)
+            for (uint32_t p = 0; p < MTS_MAX_TIERS; ++p)
+                if (uint32_t(T.hq[size_t(g) * MTS_MAX_TIERS + p]) > c.adapt_max) return MTS_EINVAL;
         int rc = tier_table(c.groups[g], T.tier[g]);
         if (rc) return rc;
     }

@@ -12,7 +12,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libmts.so")
 
-ABI_VERSION = 5
+ABI_VERSION = 6
 MAX_TIERS = 10
 NSTAT = 96
 HIST_BINS = 240  # latency histogram bins per (metric, tier)
@@ -61,7 +61,11 @@ class mts_cfg(ctypes.Structure):
                 ("dispatch_policy", ctypes.c_uint32), ("infaas_ewma_shift", ctypes.c_uint32),
                 ("infaas_alpha", ctypes.c_int32), ("infaas_beta", ctypes.c_int32), ("infaas_gamma", ctypes.c_int32),
                 ("infaas_pen_overloaded", ctypes.c_uint32), ("infaas_pen_interfered", ctypes.c_uint32),
-                ("tier_blind", ctypes.c_uint32)]
+                ("tier_blind", ctypes.c_uint32),
+                ("adapt_epoch", ctypes.c_uint32), ("adapt_up", ctypes.c_uint32), ("adapt_down", ctypes.c_uint32),
+                ("adapt_max", ctypes.c_uint32), ("adapt_margin", ctypes.c_uint32),
+                ("adapt_slo", ctypes.c_uint32 * MAX_TIERS),
+                ("promote_period", ctypes.c_uint32), ("promote_age", ctypes.c_uint32 * MAX_TIERS)]
 
 
 class mts_stats_t(ctypes.Structure):
@@ -77,7 +81,8 @@ class mts_stats_t(ctypes.Structure):
 
 class mts_state_view(ctypes.Structure):
     _fields_ = [(k, ctypes.c_void_p) for k in
-                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist", "svc")]
+                ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist", "svc",
+                 "hq", "hq_snap")]
 
 
 EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest",
@@ -191,6 +196,22 @@ def make_cfg(cfg):
         c.infaas_alpha, c.infaas_beta, c.infaas_gamma = d["alpha"], d["beta"], d["gamma"]
         c.infaas_pen_overloaded, c.infaas_pen_interfered = d["pen_overloaded"], d["pen_interfered"]
         c.infaas_ewma_shift = d["ewma_shift"]
+    # Section 6.5 extensions: {"epoch", "step_up", "step_down", "max", "margin",
+    # "slo"} (headroom amounts in 1/256 block; slo lists per-tier targets in
+    # ticks, the last one repeated for the tiers it does not reach) and
+    # {"period", "age"} (per-tier quotas in ticks, missing tiers 0 = never)
+    ad = cfg.get("adaptive")
+    if ad:
+        c.adapt_epoch, c.adapt_up, c.adapt_down = ad["epoch"], ad["step_up"], ad["step_down"]
+        c.adapt_max, c.adapt_margin = ad["max"], ad["margin"]
+        slo = list(ad["slo"])
+        for p in range(MAX_TIERS):
+            c.adapt_slo[p] = slo[min(p, len(slo) - 1)]
+    pr = cfg.get("promotion")
+    if pr:
+        c.promote_period = pr["period"]
+        for p, v in enumerate(pr["age"]):
+            c.promote_age[p] = v
     return c, groups
 
 
@@ -211,7 +232,8 @@ def _stream_handle(stream):
 class Scheduler:
     """R replicas of a workload on one GPU, advanced by ``step``."""
 
-    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist", "svc")
+    _ORDER = ("meta", "lr", "seq", "tarr", "free", "mig", "next_seq", "stats", "drain", "hist", "svc", "hq",
+              "hq_snap")
 
     def __init__(self, cfg, device="cuda", stream=None):
         import torch
@@ -301,7 +323,8 @@ class Scheduler:
                     next_seq=np.zeros(nr, np.uint32), stats=np.zeros(nr * NSTAT, np.uint64),
                     drain=np.zeros(nr * self.I, np.uint8),
                     hist=np.zeros(nr * 2 * MAX_TIERS * HIST_BINS, np.uint32),
-                    svc=np.zeros(nr * self.I, np.int64))
+                    svc=np.zeros(nr * self.I, np.int64),
+                    hq=np.zeros(nr * MAX_TIERS, np.int32), hq_snap=np.zeros(nr * 2 * MAX_TIERS, np.uint64))
 
     @property
     def queue_cache(self):
@@ -351,7 +374,8 @@ class Scheduler:
         return st.reshape(nr, NSTAT)
 
     def import_state(self, a, r0=0, nr=None):
-        """Overwrite replicas [r0, r0 + nr); a missing "drain" or "hist" clears them."""
+        """Overwrite replicas [r0, r0 + nr); a missing "drain", "hist" or "svc"
+        clears it, a missing "hq" / "hq_snap" takes its default (mts.h)."""
         nr = len(a["next_seq"]) if nr is None else nr
         b = {k: np.ascontiguousarray(a[k], dtype=v.dtype) for k, v in self._arrays(nr).items() if k in a}
         v = mts_state_view(*[b[k].ctypes.data if k in b else None for k in self._ORDER])

@@ -647,3 +647,105 @@ def test_arrival_bursts_and_tier_order(arrival, K, blind):
         assert np.array_equal(g.digests(r, 1), o.digests())
     s = g.stats()["raw"]
     assert sum(int(s[p * 8]) for p in range(K)) > 0
+
+
+# ---------------------------------------------------------------------------
+# Section 6.5 extensions: adaptive headroom, promotion of waiting requests
+# ---------------------------------------------------------------------------
+def _with_extensions(rng, c):
+    K = max(g["K"] for g in c["groups"])
+    hmax = int(c["headroom_base"] * 256) + 1
+    c["adaptive"] = dict(epoch=rng.choice([1, 9, 64]), step_up=rng.choice([100, 4000, 60000]),
+                         step_down=rng.choice([0, 300, 9000]), max=max(hmax, rng.choice([256 * 64, 256 * c["kv_blocks"]])),
+                         margin=rng.choice([0, 100, 256]),
+                         slo=[rng.choice([1, 4, 30, 400]) for _ in range(rng.randint(1, 10))])
+    if rng.random() < 0.85:
+        c["promotion"] = dict(period=rng.choice([1, 4, 37]),
+                              age=[0] + [rng.choice([0, 2, 15, 90]) for _ in range(max(K - 1, 0))])
+    if rng.random() < 0.2:
+        del c["adaptive"]
+    return c
+
+
+def _compare(g, orc, what):
+    for r, o in enumerate(orc):
+        assert_same(g.export(r, 1), o.export(), "%s replica %d" % (what, r))
+        assert np.array_equal(g.digests(r, 1), o.digests())
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_clusters_with_adaptive_headroom_and_promotion(case):
+    rng = random.Random(13000 + case)
+    cfg = _with_extensions(rng, _wide_random_cfg(rng))
+    g = Scheduler(cfg)
+    depth = rng.choice([None, 0, 1, 7])
+    if depth is not None:
+        g.queue_cache = depth
+    orc = [oracle.Oracle(cfg, r, 1) for r in range(g.R)]
+    for n in (1, 70, 129):  # launches start on and off the update ticks
+        g.step(n)
+        for o in orc:
+            o.step(n)
+    _compare(g, orc, "case %d" % case)
+    assert g.stats()["raw"][86] == 0
+
+
+@pytest.mark.parametrize("name,rpg,ticks", [("gauss10", 3, 500), ("sweep", 1, 300), ("enterprise", 4, 400)])
+def test_extension_presets_reduced(name, rpg, ticks):
+    cfg = scaled(name, replicas_per_group=rpg)
+    K = max(gr["K"] for gr in cfg["groups"])
+    cfg["adaptive"] = dict(epoch=25, step_up=2048, step_down=512, max=256 * cfg["kv_blocks"] // 4, margin=128,
+                           slo=[2, 6, 15, 40, 100])
+    cfg["promotion"] = dict(period=5, age=[0] + [40 + 10 * p for p in range(1, K)])
+    g = run_both(cfg, ticks)
+    assert g.stats()["raw"][86] == 0
+
+
+@pytest.mark.parametrize("policy,blind", [("infaas", 0), ("llumnix", 1), ("infaas", 1)])
+def test_promotion_under_other_policies(policy, blind):
+    cfg = scaled("gauss10", replicas_per_group=2)
+    cfg["tier_blind"] = blind
+    if policy == "infaas":
+        cfg["dispatch"] = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512,
+                               pen_interfered=128, ewma_shift=4)
+    cfg["promotion"] = dict(period=3, age=[0] + [20] * 9)
+    cfg["adaptive"] = dict(epoch=10, step_up=1000, step_down=200, max=256 * 2048, margin=200, slo=[5, 50])
+    run_both(cfg, 400)
+
+
+def test_extension_state_export_import_resumes_exactly():
+    cfg = scaled("gauss10", replicas_per_group=3)
+    cfg["adaptive"] = dict(epoch=7, step_up=3000, step_down=700, max=256 * 4096, margin=180, slo=[3, 20])
+    cfg["promotion"] = dict(period=4, age=[0] + [25] * 9)
+    g = Scheduler(cfg)
+    g.step(213)
+    a = g.export()
+    assert (a["hq"].reshape(g.R, 10) != g.headroom(0)).any()  # the headroom moved
+    h = Scheduler(cfg)
+    h.tick = 213
+    h.import_state(a)
+    g.step(150)
+    h.step(150)
+    for k, v in g.export().items():
+        assert np.array_equal(v, h.export()[k]), k
+    # defaults for missing arrays (Eq. 3's table, the imported counters) match the oracle's
+    b = {k: v for k, v in a.items() if k not in ("hq", "hq_snap")}
+    h2 = Scheduler(cfg)
+    h2.tick = 213
+    h2.import_state(b)
+    o = oracle.Oracle(cfg)
+    o.tick = 213
+    o.import_state(b)
+    h2.step(90)
+    o.step(90)
+    assert_same(h2.export(), o.export(), "defaults")
+    # out-of-range headroom is rejected
+    bad = dict(a)
+    bad["hq"] = a["hq"].copy()
+    bad["hq"][3] = cfg["adaptive"]["max"] + 1
+    with pytest.raises(MtsError):
+        h2.import_state(bad)
+    bad["hq"] = a["hq"].copy()
+    bad["hq"][9] = 5  # the lowest of 10 tiers under zero_lowest_tier
+    with pytest.raises(MtsError):
+        h2.import_state(bad)

@@ -75,6 +75,13 @@ def _bad(**over):
     _bad(output=dict(kind="geometric", mean=0.5)),
     _bad(arrival=dict(kind="poisson", mean=0.0)),
     _bad(g_n_replicas=0),
+    # Section 6.5 extensions: the same limits the oracle enforces
+    _bad(adaptive=dict(epoch=10, step_up=1, step_down=1, max=256 * 600, margin=257, slo=[5])),
+    _bad(adaptive=dict(epoch=10, step_up=1, step_down=1, max=(1 << 29) // 10 + 1, margin=0, slo=[5])),
+    _bad(adaptive=dict(epoch=(1 << 16) + 1, step_up=1, step_down=1, max=256 * 600, margin=0, slo=[5])),
+    _bad(adaptive=dict(epoch=10, step_up=1, step_down=1, max=256 * 600, margin=0, slo=[0])),
+    _bad(adaptive=dict(epoch=10, step_up=1, step_down=1, max=256 * 600, margin=0, slo=[1 << 21])),
+    _bad(adaptive=dict(epoch=10, step_up=1, step_down=1, max=100, margin=0, slo=[5])),  # below Eq. 3's H_0
 ], ids=lambda c: "bad")
 def test_invalid_configs_are_rejected(cfg):
     with pytest.raises(mts.MtsError) as e:
@@ -94,3 +101,11 @@ def test_strerror():
     L = mts.load_library()
     assert L.mts_strerror(0) == b"ok"
     assert b"invalid" in L.mts_strerror(-1)
+
+
+def test_adaptive_limits_accept_what_the_oracle_accepts():
+    import oracle
+    c = _bad(adaptive=dict(epoch=1 << 16, step_up=2**32 - 1, step_down=2**32 - 1, max=(1 << 29) // 10,
+                           margin=256, slo=[1, 1 << 20]), promotion=dict(period=2**32 - 1, age=[2**32 - 1] * 10))
+    assert mts.mts_state_bytes(c) > 0
+    oracle.Oracle(c).close()
