@@ -94,6 +94,8 @@ def main():
                     help="global dispatch policy (infaas: cost-based dispatch without migration)")
     ap.add_argument("--tier-blind", action="store_true",
                     help="first-come-first-served queues and arrival-order dispatch")
+    ap.add_argument("--extensions", action="store_true",
+                    help="adaptive headroom and promotion of waiting requests at the workloads package's settings")
     ap.add_argument("--drain-instances", type=int, default=0,
                     help="mark the first n instances of every replica draining after the first timed step")
     args = ap.parse_args()
@@ -106,9 +108,11 @@ def main():
     import torch
 
     from paper_2608_16336_amd import Scheduler
-    from workloads import preset
+    from workloads import preset, with_extensions
 
     cfg = preset(args.workload)
+    if args.extensions:
+        cfg = with_extensions(cfg)
     if args.policy == "infaas":
         cfg["dispatch"] = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512,
                                pen_interfered=128, ewma_shift=4)
@@ -166,7 +170,8 @@ def main():
     b_alg = algorithmic_bytes(cfg, R, T * K, d)
     avg_launch_s = step_ms / 1e3 / launches
     achieved = b_alg / launches / avg_launch_s / 1e9
-    default_run = (args.workload, T, args.policy, args.drain_instances, args.tier_blind) == ("sweep", 1000, "llumnix", 0, False)
+    default_run = (args.workload, T, args.policy, args.drain_instances, args.tier_blind, args.extensions) == (
+        "sweep", 1000, "llumnix", 0, False, False)
     traffic = MEASURED_TRAFFIC.get(kernel_source_hash()) if default_run else None
 
     out = {
@@ -186,6 +191,7 @@ def main():
                    "slots_per_instance": cfg["slots_per_instance"], "ticks_per_step": T,
                    "ticks_timed": T * K, "parallelism": "replicas across workgroups",
                    "policy": args.policy, "tier_blind": args.tier_blind, "draining_instances": args.drain_instances,
+                   "adaptive_headroom_and_promotion": args.extensions,
                    "blocks": sch.launch()[1], "threads_per_block": 64},
         "slot_updates_per_s": value * slots,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -128,7 +128,7 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.drain = o;    o = up256(o + size_t(R) * I);
     L.hist = o;     o = up256(o + size_t(R) * kHistPerReplica * 4);
     L.svc = o;      o = up256(o + size_t(R) * I * 8);
-    L.ext = o;      o = up256(o + 2 * MTS_MAX_TIERS * 4);
+    L.ext = o;      o = up256(o + MTS_EXT_WORDS * 4);
     const bool adapt = c.adapt_epoch != 0;
     L.hqr = o;      o = up256(o + (adapt ? size_t(R) * MTS_MAX_TIERS * 4 : 0));
     L.hsnap = o;    o = up256(o + (adapt ? size_t(R) * 2 * MTS_MAX_TIERS * 8 : 0));
@@ -347,9 +347,25 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
     up(L.prompt_g, pg.data(), pg.size() * 4);
     up(L.output_g, og.data(), og.size() * 4);
     up(L.group_of, x->group_of.data(), x->group_of.size() * 2);
-    uint32_t ext[2 * MTS_MAX_TIERS];
-    std::memcpy(ext, x->cfg.adapt_slo, sizeof(x->cfg.adapt_slo));
-    std::memcpy(ext + MTS_MAX_TIERS, x->cfg.promote_age, sizeof(x->cfg.promote_age));
+    // extension table: per-tier targets and quotas, the smallest non-zero
+    // quota of tiers 1..9 (2^32 - 1: none), period, epoch, up, down, max,
+    // margin, zero_lowest_tier, then the device addresses of the per-replica
+    // headroom and snapshot arrays (0 when the headroom is static)
+    uint32_t ext[MTS_EXT_WORDS] = {0};
+    {
+        const mts_cfg& c = x->cfg;
+        std::memcpy(ext, c.adapt_slo, sizeof(c.adapt_slo));
+        std::memcpy(ext + MTS_MAX_TIERS, c.promote_age, sizeof(c.promote_age));
+        uint32_t qmin = 0xFFFFFFFFu;
+        for (uint32_t q = 1; q < MTS_MAX_TIERS; ++q)
+            if (c.promote_age[q] != 0 && c.promote_age[q] < qmin) qmin = c.promote_age[q];
+        const uint32_t words[8] = {qmin, c.promote_period, c.adapt_epoch, c.adapt_up, c.adapt_down, c.adapt_max,
+                                   c.adapt_margin, c.zero_lowest_tier};
+        std::memcpy(ext + 2 * MTS_MAX_TIERS, words, sizeof(words));
+        const uint64_t addr[2] = {c.adapt_epoch ? uint64_t(reinterpret_cast<uintptr_t>(x->dev + L.hqr)) : 0,
+                                  c.adapt_epoch ? uint64_t(reinterpret_cast<uintptr_t>(x->dev + L.hsnap)) : 0};
+        std::memcpy(ext + 28, addr, sizeof(addr));
+    }
     up(L.ext, ext, sizeof(ext));
     // adaptive headroom starts from each replica's group table
     std::vector<int32_t> hqr;

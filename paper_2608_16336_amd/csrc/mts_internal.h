@@ -19,6 +19,8 @@ constexpr uint32_t kMaxBlocks = 1u << 21;
 constexpr uint32_t kMaxGroups = 4096;
 constexpr uint64_t kMaxReplicas = 1u << 20;
 constexpr uint32_t kMaxTable = 1u << 17;
+// words of the device table of the Section 6.5 extensions
+#define MTS_EXT_WORDS 32
 
 // slot status and meta flags (canonical layout, see mts.h)
 constexpr uint32_t kEmpty = 0, kWaiting = 1, kRunning = 2, kInbound = 3;
@@ -85,7 +87,7 @@ struct Params {
     // adaptive headroom (epoch 0: static) and promotion (period 0: none)
     uint32_t adapt_epoch, adapt_up, adapt_down, adapt_max, adapt_margin;
     uint32_t promo_period;
-    const uint32_t* ext;           // adapt_slo[10], then promote_age[10]
+    const uint32_t* ext;           // extension table, MTS_EXT_WORDS u32 (mts_api.cpp builds it)
     int32_t* hqr;                  // [R][10] per-replica headroom (adaptive only)
     unsigned long long* hsnap;     // [R][2][10] admitted / queue-delay counters at the last update
     const unsigned long long* tier_q;  // [group][MTS_MAX_TIERS] floor(2^32 CDF), up to 2^32

@@ -51,6 +51,11 @@ constexpr int kInts = 20;
 constexpr int kLast = 64;
 // requests preempted in the current tick, listed for the prefetched finish visit
 constexpr int kVic = 16;
+// Section 6.5 extensions: words of the device table (u32; the addresses of
+// the per-replica headroom and snapshot arrays as u64 at the end)
+enum { kXSlo = 0, kXAge = 10, kXPromoMin = 20, kXPromoPeriod, kXAdaptEpoch, kXAdaptUp, kXAdaptDown, kXAdaptMax,
+       kXAdaptMargin, kXZeroLowest, kXHqr = 28, kXHsnap = 30, kXWords = 32 };
+static_assert(kXWords == MTS_EXT_WORDS, "extension table size");
 
 struct LdsLayout {
     uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, ext, total;
@@ -93,11 +98,12 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     o = (o + 15u) & ~15u;
     L.qt = o;    o += IM * qdepth * 16;
     L.qn = o;    o += qdepth ? IM * 8 : 0;
-    // adaptive headroom / promotion: per tier the admitted and queue-delay
-    // counters at the last headroom update (u64 each), the headroom, the
-    // queue-delay target and the promotion quota
+    // adaptive headroom / promotion: the ticks left to the next promotion
+    // pass and headroom update, and per instance a lower bound on the
+    // arrival ticks of its waiting requests (the rest of their state stays
+    // in HBM: it is touched only on pass and update ticks)
     o = al8(o);
-    L.ext = o;   o += ext ? kTiers * 28 : 0;
+    L.ext = o;   o += ext ? 8 + IM * 4 : 0;
     L.total = al8(o);
     return L;
 }
@@ -133,11 +139,9 @@ struct Ctx {
     int* qh;                   // [I] ring position of the first entry
     int td;
     uint32_t blind;            // 1: tiers order nothing (tier-blind scheduling)
-    // adaptive headroom and promotion (null when both are off), per tier
-    unsigned long long* asnap; // [2][10] admitted, queue-delay counters at the last update
-    int* ahq;                  // [10] headroom, 1/256 block
-    unsigned* aslo;            // [10] queue-delay target, ticks
-    unsigned* apage;           // [10] promotion quota, ticks (0: never)
+    // adaptive headroom and promotion (null when both are off): the LDS
+    // region read through the accessors below
+    unsigned char* ext;
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -150,11 +154,26 @@ struct Ctx {
     int hq[kTiers];
 };
 
-template <int IM, bool INF>
+// Section 6.5 extension state in LDS, at fixed offsets from C.ext: the
+// ticks left to the next promotion pass and headroom update, then per
+// instance a lower bound lb on the arrival ticks of its waiting requests
+// (0: unknown, the next pass reads the instance)
+__device__ __forceinline__ int* xleft(const Ctx& C) { return reinterpret_cast<int*>(C.ext); }
+__device__ __forceinline__ unsigned* wlb(const Ctx& C) { return reinterpret_cast<unsigned*>(C.ext + 8); }
+// addresses of the per-replica headroom and snapshot arrays (null: static headroom)
+__device__ __forceinline__ int32_t* ext_hqr(const Params& P)
+{
+    return reinterpret_cast<int32_t*>(reinterpret_cast<const unsigned long long*>(P.ext + kXHqr)[0]);
+}
+__device__ __forceinline__ unsigned long long* ext_hsnap(const Params& P)
+{
+    return reinterpret_cast<unsigned long long*>(reinterpret_cast<const unsigned long long*>(P.ext + kXHsnap)[0]);
+}
+
+template <int IM, bool INF, bool EXT>
 __device__ inline Ctx carve(char* base, const Params& P)
 {
-    const bool ext = P.adapt_epoch != 0 || P.promo_period != 0;
-    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz, P.policy, P.qdepth, ext);
+    const LdsLayout Y = lds_layout(IM, P.I, P.W, P.RB, P.wsz, P.policy, P.qdepth, EXT);
     Ctx C;
     C.stats = reinterpret_cast<unsigned long long*>(base + Y.stats);
     C.occ = reinterpret_cast<unsigned long long*>(base + Y.occ);
@@ -205,14 +224,7 @@ __device__ inline Ctx carve(char* base, const Params& P)
     } else {
         C.fsum = nullptr; C.svc = nullptr; C.fcnt = nullptr; C.pen = nullptr;
     }
-    if (ext) {
-        C.asnap = reinterpret_cast<unsigned long long*>(base + Y.ext);
-        C.ahq = reinterpret_cast<int*>(C.asnap + 2 * kTiers);
-        C.aslo = reinterpret_cast<unsigned*>(C.ahq + kTiers);
-        C.apage = C.aslo + kTiers;
-    } else {
-        C.asnap = nullptr; C.ahq = nullptr; C.aslo = nullptr; C.apage = nullptr;
-    }
+    C.ext = EXT ? reinterpret_cast<unsigned char*>(base + Y.ext) : nullptr;
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
@@ -242,6 +254,15 @@ __device__ __forceinline__ unsigned long long wmax64(unsigned long long x)
     for (int o = 32; o > 0; o >>= 1) {
         const unsigned long long y = __shfl_xor(x, o);
         x = y > x ? y : x;
+    }
+    return x;
+}
+__device__ __forceinline__ uint32_t wmin32(uint32_t x)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t y = uint32_t(__shfl_xor(int(x), o));
+        x = y < x ? y : x;
     }
     return x;
 }
@@ -641,6 +662,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             if (vm) C.flags[i] |= kFlagAbort;
             const unsigned long long key = (rank_of(C, uint32_t(vt)) << 32) | static_cast<unsigned>(mx);
             hol_insert(C, i, key, vs, vw, vmeta, vta);
+            if (C.ext) wlb(C)[i] = vta < wlb(C)[i] ? vta : wlb(C)[i];
         }
         wave_sync();
     }
@@ -953,58 +975,90 @@ __device__ inline void admit_fresh(const Ctx& C, int i, uint32_t t, int lane)
 
 // Promotion pass: every waiting request of tier p >= 1 whose age t - tarr
 // has reached the tier's quota (non-zero) moves to tier p - 1.  An instance
-// whose queue changed order loses its cached head of line and queue cache
-// (found again by the admission rescan) and its list of fresh placements.
-__device__ inline void promote_waiting(const Ctx& C, uint32_t t, int lane)
+// with a promoted request loses its list of fresh placements and its queue
+// cache; its head of line stays when it was not promoted and every promoted
+// key is still larger, else it is found again by the admission rescan.
+// lb <= the arrival tick of every waiting request of the instance, and every
+// such tick is at most t (requests start to wait at the current tick or
+// keep an older one): when t - lb is below the smallest quota no request can
+// be old enough and the instance is not read.  lb = 0 means unknown (a
+// launch starts so, as does an instance holding a request that arrived
+// after t, possible only after the clock was moved back).
+__device__ inline void promote_waiting(const Ctx& C, const Params& P, uint32_t t, int lane)
 {
+    const uint32_t qmin = P.ext[kXPromoMin];
     for (uint32_t i = 0; i < C.I; ++i) {
         if (C.nwait[i] == 0) continue;
+        const uint32_t lb = wlb(C)[i];
+        if (lb != 0 && t - lb < qmin) continue;
         const size_t b = size_t(i) * C.S;
         const int nch = live_chunks(C, i, lane);
-        bool any = false;
+        const int h = C.hols[i];
+        bool any = false, late = false, head = false;
+        uint32_t lo = 0xFFFFFFFFu;
+        unsigned long long kmin = kNone;
         for (int c = 0; c < nch; ++c) {
             const int s = c * 64 + lane;
             if (wst(C.hot[b + s]) != 1u) continue;
-            const uint32_t m = C.meta[b + s], tier = (m >> 2) & 15u;
+            const uint32_t m = C.meta[b + s], tier = (m >> 2) & 15u, ta = C.tarr[b + s];
+            lo = ta < lo ? ta : lo;
+            late = late || ta > t;
             if (tier == 0) continue;
-            const uint32_t q = C.apage[tier];
-            if (q != 0 && t - C.tarr[b + s] >= q) {
+            const uint32_t q = P.ext[kXAge + tier];
+            if (q != 0 && t - ta >= q) {
                 C.meta[b + s] = uint8_t(m - 4u);  // tier field at bits 2..5
                 any = true;
+                head = head || s == h;
+                const unsigned long long k = (rank_of(C, tier - 1u) << 32) | C.seq[b + s];
+                kmin = k < kmin ? k : kmin;
             }
         }
-        if (ballot(any) != 0 && lane == 0) { C.hols[i] = kHolUnknown; C.frs[i] = 0; }
+        lo = wmin32(lo);
+        kmin = wmin64(kmin);
+        const bool moved = ballot(any) != 0, unknown = ballot(late) != 0, hit = ballot(head) != 0;
+        if (lane == 0) {
+            wlb(C)[i] = unknown ? 0u : lo;
+            if (moved) {
+                C.frs[i] = 0;
+                if (hit || h < 0 || kmin < C.holk[i]) C.hols[i] = kHolUnknown;
+                else if (C.td) C.qn[i] = 0;
+            }
+        }
     }
     wave_sync();
 }
 
-// Adaptive headroom update: lane p < 10 handles tier p.  With a requests
-// first admitted since the last update and their summed queue delay d, the
+// Adaptive headroom update of replica r: lane p < 10 handles tier p, with
+// the headroom and the counter snapshots in HBM.  With a requests first
+// admitted since the last update and their summed queue delay d, the
 // headroom rises by a step when d > slo a, falls by a step when
 // 256 d <= margin slo a, both tests in exact 128-bit arithmetic.
-__device__ inline void adapt_headroom(const Ctx& C, const Params& P, int lane)
+__device__ inline void adapt_headroom(const Ctx& C, const Params& P, uint32_t r, int lane)
 {
     if (lane < kTiers) {
         const int p = lane;
+        int32_t* hq = ext_hqr(P) + size_t(r) * kTiers;
+        unsigned long long* snap = ext_hsnap(P) + size_t(r) * 2 * kTiers;
         const unsigned long long adm = C.stats[p * 8 + kAdmittedCnt], qd = C.stats[p * 8 + kQdelay];
-        const unsigned long long a = adm - C.asnap[p], d = qd - C.asnap[kTiers + p];
-        C.asnap[p] = adm;
-        C.asnap[kTiers + p] = qd;
-        if (p < int(C.K) && !(P.zero_lowest && p == int(C.K) - 1) && a != 0) {
-            const unsigned long long slo = C.aslo[p];
+        const unsigned long long a = adm - snap[p], d = qd - snap[kTiers + p];
+        snap[p] = adm;
+        snap[kTiers + p] = qd;
+        if (p < int(C.K) && !(P.ext[kXZeroLowest] && p == int(C.K) - 1) && a != 0) {
+            const unsigned long long slo = P.ext[kXSlo + p];
             const unsigned long long xl = slo * a, xh = __umul64hi(slo, a);
-            const unsigned long long ms = slo * P.adapt_margin;  // < 2^29
+            const unsigned long long ms = slo * P.ext[kXAdaptMargin];  // < 2^29
             const unsigned long long yl = ms * a, yh = __umul64hi(ms, a);
             const unsigned long long dl = d << 8, dh = d >> 56;
-            long long h = C.ahq[p];
+            long long h = hq[p];
             if (xh == 0 && d > xl) {
-                h += P.adapt_up;
-                if (h > static_cast<long long>(P.adapt_max)) h = P.adapt_max;
+                h += P.ext[kXAdaptUp];
+                const long long mx = P.ext[kXAdaptMax];
+                if (h > mx) h = mx;
             } else if (dh < yh || (dh == yh && dl <= yl)) {
-                h -= P.adapt_down;
+                h -= P.ext[kXAdaptDown];
                 if (h < 0) h = 0;
             }
-            C.ahq[p] = int(h);
+            hq[p] = int32_t(h);
         }
     }
     wave_sync();
@@ -1018,7 +1072,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
 {
     constexpr int IPL = (IM + 63) / 64;
     extern __shared__ __align__(16) char lds_raw[];
-    Ctx C = carve<IM, INF>(lds_raw, P);
+    Ctx C = carve<IM, INF, EXT>(lds_raw, P);
     const int lane = lane_id();
     const uint32_t I = P.I, S = P.S, W = P.W;
     const uint32_t wsz = P.wsz;
@@ -1027,18 +1081,19 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
     for (uint32_t r = blockIdx.x; r < P.R; r += gridDim.x) {
         const uint32_t g = P.group_of[r];
         C.K = P.group_K32[g];
+        const int32_t* hq = P.hq + g * kTiers;
         if (EXT) {
-            if (lane < kTiers) {
-                C.aslo[lane] = P.ext[lane];
-                C.apage[lane] = P.ext[kTiers + lane];
-                if (P.hqr) {
-                    C.ahq[lane] = P.hqr[size_t(r) * kTiers + lane];
-                    C.asnap[lane] = P.hsnap[size_t(r) * 2 * kTiers + lane];
-                    C.asnap[kTiers + lane] = P.hsnap[size_t(r) * 2 * kTiers + kTiers + lane];
-                }
+            // (the parameters are read from memory where they are used, so that
+            // none of them stays in registers through the tick loop)
+            const int32_t* hqr = ext_hqr(P);
+            if (hqr) hq = hqr + size_t(r) * kTiers;
+            if (lane == 0) {
+                const uint32_t t0u = uint32_t(t0), per = P.ext[kXPromoPeriod], ep = P.ext[kXAdaptEpoch];
+                xleft(C)[0] = per ? int(t0u % per) : 0;
+                xleft(C)[1] = ep ? int(t0u % ep) : 0;
             }
+            for (uint32_t i = lane; i < P.I; i += 64) wlb(C)[i] = 0u;  // unknown: the first pass reads them
         }
-        const int32_t* hq = EXT && P.hqr ? P.hqr + size_t(r) * kTiers : P.hq + g * kTiers;
 #pragma unroll
         for (int p = 0; p < kTiers; ++p) C.hq[p] = hq[p];
         const size_t rb = size_t(r) * I * S;
@@ -1139,9 +1194,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         constexpr uint32_t kNoPf = 0xFFFFFFFFu;
         uint32_t pf_n = kNoPf, pf_e = 0, pf_v = 0, pf_m = 0, pf_a = 0;
         unsigned long long a_nx = uint32_t(lane) < lim ? recs[lane] : 0ull;
-        // ticks until the next promotion pass and headroom update
-        uint32_t pc = EXT && P.promo_period ? t0u % P.promo_period : 0u;
-        uint32_t ac = EXT && P.adapt_epoch ? t0u % P.adapt_epoch : 0u;
         for (uint32_t tl = 0; tl < nt; ++tl) {
             const uint32_t t = t0u + tl;
             const uint32_t n = n_nx;
@@ -1149,17 +1201,22 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             const unsigned long long a0 = a_nx;
 
             // ============ Section 6.5: promotion, adaptive headroom ============
-            if (EXT && P.promo_period) {
-                if (pc == 0) promote_waiting(C, t, lane);
-                pc = pc + 1u == P.promo_period ? 0u : pc + 1u;
-            }
-            if (EXT && P.adapt_epoch) {
-                if (ac == 0) {
-                    adapt_headroom(C, P, lane);
+            // (the countdowns and parameters live in LDS: nothing of this stays
+            // in registers across the tick)
+            if (EXT) {
+                const int pl = xleft(C)[0], al = xleft(C)[1];
+                const int per = int(P.ext[kXPromoPeriod]), ep = int(P.ext[kXAdaptEpoch]);
+                if (per && pl == 0) promote_waiting(C, P, t, lane);
+                if (ep && al == 0) {
+                    adapt_headroom(C, P, r, lane);
+                    const int32_t* hq = ext_hqr(P) + size_t(r) * kTiers;
 #pragma unroll
-                    for (int p = 0; p < kTiers; ++p) C.hq[p] = C.ahq[p];
+                    for (int p = 0; p < kTiers; ++p) C.hq[p] = hq[p];
                 }
-                ac = ac + 1u == P.adapt_epoch ? 0u : ac + 1u;
+                if (lane == 0) {
+                    xleft(C)[0] = per && pl + 1 < per ? pl + 1 : 0;
+                    xleft(C)[1] = ep && al + 1 < ep ? al + 1 : 0;
+                }
             }
 
             // ===================== A: growth, preemption, finish =====================
@@ -1482,6 +1539,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         if (i >= I) continue;
                         C.live[i] = live_r[j];
                         C.nwait[i] += nadd[j];
+                        if (C.ext && nadd[j] > 0) wlb(C)[i] = t < wlb(C)[i] ? t : wlb(C)[i];
                         if (C.td && nadd[j] > 0) {
                             // queue cache: an arrival that became the head of line pushes
                             // the old head to the front of the cache; other arrivals may
@@ -1739,6 +1797,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             hol_insert(C, dst, key, ds, hw, hm, ht);
                             hol_pop(C, src);
                             stat(C, kMigQueued, 1);
+                            if (C.ext) wlb(C)[dst] = ht < wlb(C)[dst] ? ht : wlb(C)[dst];
                         }
                         wave_sync();
                         // staged copies: running candidate of largest tier, then fewest
@@ -1816,11 +1875,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             for (int k = 0; k < 4; ++k) P.mig[(size_t(r) * I + i) * 4 + k] = C.mig[4 * i + k];
         }
         if (lane == 0) P.next_seq[r] = next_seq;
-        if (EXT && P.hqr && lane < kTiers) {
-            P.hqr[size_t(r) * kTiers + lane] = C.ahq[lane];
-            P.hsnap[size_t(r) * 2 * kTiers + lane] = C.asnap[lane];
-            P.hsnap[size_t(r) * 2 * kTiers + kTiers + lane] = C.asnap[kTiers + lane];
-        }
         wave_sync();
     }
 }

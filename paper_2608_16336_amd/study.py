@@ -55,9 +55,11 @@ def percentile(counts, q):
 INFAAS = dict(policy="infaas", alpha=64, beta=1, gamma=1, pen_overloaded=512, pen_interfered=128, ewma_shift=4)
 
 
-def sweep_cfg(arrival_mean, replicas_per_group, ticks, policy="llumnix", tier_blind=False):
-    from workloads import preset
+def sweep_cfg(arrival_mean, replicas_per_group, ticks, policy="llumnix", tier_blind=False, extensions=()):
+    from workloads import preset, with_extensions
     cfg = preset("sweep")
+    if extensions:
+        cfg = with_extensions(cfg, adaptive="adaptive" in extensions, promotion="promotion" in extensions)
     if policy == "infaas":
         cfg["dispatch"] = dict(INFAAS)
     if tier_blind:
@@ -66,16 +68,18 @@ def sweep_cfg(arrival_mean, replicas_per_group, ticks, policy="llumnix", tier_bl
     for g in cfg["groups"]:
         g["n_replicas"] = replicas_per_group
     cfg["ticks"] = ticks
-    cfg["name"] = "differentiation study: sweep groups x %d, Poisson %g/tick, %s dispatch%s" % (
-        replicas_per_group, arrival_mean, policy, ", tier-blind queues" if tier_blind else "")
+    cfg["name"] = "differentiation study: sweep groups x %d, Poisson %g/tick, %s dispatch%s%s" % (
+        replicas_per_group, arrival_mean, policy, ", tier-blind queues" if tier_blind else "",
+        "".join(", " + label for key, label in (("adaptive", "adaptive headroom"), ("promotion", "promotion"))
+                if key in extensions))
     return cfg
 
 
 def run(arrival_mean=24.0, replicas_per_group=128, ticks=4000, device="cuda", policy="llumnix",
-        tier_blind=False):
+        tier_blind=False, extensions=()):
     """Run the sweep and return one row per (tier mix, K, tier)."""
     import torch
-    cfg = sweep_cfg(arrival_mean, replicas_per_group, ticks, policy, tier_blind)
+    cfg = sweep_cfg(arrival_mean, replicas_per_group, ticks, policy, tier_blind, extensions)
     g = Scheduler(cfg, device=device)
     g.step(ticks)
     torch.cuda.synchronize()
@@ -127,9 +131,13 @@ def main(argv=None):
     ap.add_argument("--policy", choices=("llumnix", "infaas"), default="llumnix")
     ap.add_argument("--tier-blind", action="store_true",
                     help="first-come-first-served queues and arrival-order dispatch (the paper's INFaaS+vLLM baseline)")
+    ap.add_argument("--adaptive", action="store_true", help="adaptive headroom (Section 6.5 extension)")
+    ap.add_argument("--promotion", action="store_true", help="promotion of long-waiting requests (Section 6.5 extension)")
     ap.add_argument("--json", help="also write the rows to this file")
     a = ap.parse_args(argv)
-    cfg, rows = run(a.arrival_mean, a.replicas_per_group, a.ticks, policy=a.policy, tier_blind=a.tier_blind)
+    ext = tuple(e for e in ("adaptive", "promotion") if getattr(a, e))
+    cfg, rows = run(a.arrival_mean, a.replicas_per_group, a.ticks, policy=a.policy, tier_blind=a.tier_blind,
+                    extensions=ext)
     print("# %s, %d ticks\n" % (cfg["name"], a.ticks))
     print(markdown(rows))
     if a.json:

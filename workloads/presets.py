@@ -113,6 +113,22 @@ def preset(name):
     return copy.deepcopy(PRESETS[name])
 
 
+def with_extensions(cfg, adaptive=True, promotion=True):
+    """The Section 6.5 extensions at the settings the benchmark and the study
+    use (a copy of cfg): headroom updated every 50 ticks, up 8 blocks when the
+    tier's mean queue delay since the last update exceeds 2^(p+1) ticks for
+    tier p, down 2 blocks when it stays at or below half of that, never above
+    a quarter of M; a promotion pass every 10 ticks with a quota of 50 p
+    ticks for tier p."""
+    d = copy.deepcopy(cfg)
+    if adaptive:
+        d["adaptive"] = dict(epoch=50, step_up=8 * 256, step_down=2 * 256, max=d["kv_blocks"] * 256 // 4,
+                             margin=128, slo=[2 << p for p in range(10)])
+    if promotion:
+        d["promotion"] = dict(period=10, age=[50 * p for p in range(10)])
+    return d
+
+
 def n_replicas(cfg):
     return sum(g["n_replicas"] for g in cfg["groups"])
 
