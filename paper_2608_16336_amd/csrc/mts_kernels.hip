@@ -1185,7 +1185,10 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         // the arrivals of the next tick are loaded one tick ahead; records past
         // the tick's count are never used
         const uint32_t lim = P.arr_cap < 64u ? P.arr_cap : 64u;
-        uint32_t n_nx = cnts[0];
+        // arrival counts 64 ticks at a time, lane l holding tick (tl & ~63) + l:
+        // a tick's count is a lane read of a register, so no tick waits for
+        // a load (and for the stores before it) to make its count uniform
+        uint32_t cnt64 = uint32_t(lane) < nt ? cnts[lane] : 0u;
         // the next tick's finish visit, loaded ahead: the entries of its bucket
         // right after this tick's visit (pf_n of them; kNoPf: none), their
         // slots' word, meta and arrival tick at the end of this tick.  It is
@@ -1196,7 +1199,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         unsigned long long a_nx = uint32_t(lane) < lim ? recs[lane] : 0ull;
         for (uint32_t tl = 0; tl < nt; ++tl) {
             const uint32_t t = t0u + tl;
-            const uint32_t n = n_nx;
+            const uint32_t n = rlu(cnt64, int(tl & 63u));
             const unsigned long long* rec = recs + size_t(tl) * P.arr_cap;
             const unsigned long long a0 = a_nx;
 
@@ -1623,8 +1626,12 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             }
 
             if (tl + 1 < nt) {
-                n_nx = cnts[tl + 1];
-                a_nx = uint32_t(lane) < lim ? rec[P.arr_cap + lane] : 0ull;
+                if (((tl + 1u) & 63u) == 0) {
+                    const uint32_t* cn = uniform_ptr(cnts + tl + 1u);
+                    cnt64 = tl + 1u + lane < nt ? cn[lane] : 0u;
+                }
+                const unsigned long long* rn = uniform_ptr(rec + P.arr_cap);
+                a_nx = uint32_t(lane) < lim ? rn[lane] : 0ull;
             }
 
             // ===================== E1: staged copies =====================

@@ -20,6 +20,18 @@ __device__ __forceinline__ unsigned long long rl64(unsigned long long v, int l)
     return (static_cast<unsigned long long>(hi) << 32) | lo;
 }
 
+// A wave-uniform pointer made opaque to the optimiser (its two halves go
+// through readfirstlane): addresses built on it stay a scalar base plus a
+// lane offset instead of becoming 64-bit per-lane induction variables
+template <typename T>
+__device__ __forceinline__ T* uniform_ptr(T* p)
+{
+    const unsigned long long v = reinterpret_cast<unsigned long long>(p);
+    const unsigned lo = unsigned(__builtin_amdgcn_readfirstlane(int(unsigned(v))));
+    const unsigned hi = unsigned(__builtin_amdgcn_readfirstlane(int(unsigned(v >> 32))));
+    return reinterpret_cast<T*>((static_cast<unsigned long long>(hi) << 32) | lo);
+}
+
 // Lanes of the wave exchange values through LDS and HBM: every write by a
 // subset of lanes that other lanes read later is followed by this point, so
 // that no later load is moved above it and every later load sees the write.
