@@ -236,44 +236,65 @@ __device__ inline Ctx carve(char* base, const Params& P)
 
 using namespace wave;
 
+// Wave reductions and scans through DPP lane moves and lane reads (no LDS
+// round trip): four row steps leave every lane of a 16-lane row with the
+// row's reduction (quad_perm 1,0,3,2; quad_perm 2,3,0,1; row_half_mirror;
+// row_mirror), the four rows are combined from lanes 0, 16, 32, 48.
+template <int kCtrl>
+__device__ __forceinline__ int dpp_row(int x)
+{
+    return __builtin_amdgcn_mov_dpp(x, kCtrl, 0xF, 0xF, false);
+}
+template <int kCtrl>
+__device__ __forceinline__ unsigned long long dpp_row64(unsigned long long x)
+{
+    const unsigned lo = unsigned(dpp_row<kCtrl>(int(unsigned(x))));
+    const unsigned hi = unsigned(dpp_row<kCtrl>(int(unsigned(x >> 32))));
+    return (static_cast<unsigned long long>(hi) << 32) | lo;
+}
 __device__ __forceinline__ int wsum(int x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return x;
+    x += dpp_row<0xB1>(x);
+    x += dpp_row<0x4E>(x);
+    x += dpp_row<0x141>(x);
+    x += dpp_row<0x140>(x);
+    return rl(x, 0) + rl(x, 16) + rl(x, 32) + rl(x, 48);
 }
 __device__ __forceinline__ unsigned long long wsum64(unsigned long long x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return x;
+    x += dpp_row64<0xB1>(x);
+    x += dpp_row64<0x4E>(x);
+    x += dpp_row64<0x141>(x);
+    x += dpp_row64<0x140>(x);
+    return rl64(x, 0) + rl64(x, 16) + rl64(x, 32) + rl64(x, 48);
 }
+template <typename T>
+__device__ __forceinline__ T tmax(T a, T b) { return a > b ? a : b; }
+template <typename T>
+__device__ __forceinline__ T tmin(T a, T b) { return a < b ? a : b; }
 __device__ __forceinline__ unsigned long long wmax64(unsigned long long x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const unsigned long long y = __shfl_xor(x, o);
-        x = y > x ? y : x;
-    }
-    return x;
-}
-__device__ __forceinline__ uint32_t wmin32(uint32_t x)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint32_t y = uint32_t(__shfl_xor(int(x), o));
-        x = y < x ? y : x;
-    }
-    return x;
+    x = tmax(x, dpp_row64<0xB1>(x));
+    x = tmax(x, dpp_row64<0x4E>(x));
+    x = tmax(x, dpp_row64<0x141>(x));
+    x = tmax(x, dpp_row64<0x140>(x));
+    return tmax(tmax(rl64(x, 0), rl64(x, 16)), tmax(rl64(x, 32), rl64(x, 48)));
 }
 __device__ __forceinline__ unsigned long long wmin64(unsigned long long x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const unsigned long long y = __shfl_xor(x, o);
-        x = y < x ? y : x;
-    }
-    return x;
+    x = tmin(x, dpp_row64<0xB1>(x));
+    x = tmin(x, dpp_row64<0x4E>(x));
+    x = tmin(x, dpp_row64<0x141>(x));
+    x = tmin(x, dpp_row64<0x140>(x));
+    return tmin(tmin(rl64(x, 0), rl64(x, 16)), tmin(rl64(x, 32), rl64(x, 48)));
+}
+__device__ __forceinline__ uint32_t wmin32(uint32_t x)
+{
+    x = tmin(x, uint32_t(dpp_row<0xB1>(int(x))));
+    x = tmin(x, uint32_t(dpp_row<0x4E>(int(x))));
+    x = tmin(x, uint32_t(dpp_row<0x141>(int(x))));
+    x = tmin(x, uint32_t(dpp_row<0x140>(int(x))));
+    return tmin(tmin(rlu(x, 0), rlu(x, 16)), tmin(rlu(x, 32), rlu(x, 48)));
 }
 
 // wave-wide max of a double through DPP lane moves; every lane gets the result
@@ -285,16 +306,28 @@ __device__ __forceinline__ double dpp_f64(double v)
     const int hi2 = __builtin_amdgcn_update_dpp(hi, hi, kCtrl, kRowMask, 0xF, false);
     return __hiloint2double(hi2, lo2);
 }
+// a lane move in which every lane reads a lane of its own row (no old value)
+template <int kCtrl>
+__device__ __forceinline__ double dpp_row_f64(double v)
+{
+    const int lo = __builtin_amdgcn_mov_dpp(__double2loint(v), kCtrl, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(v), kCtrl, 0xF, 0xF, false);
+    return __hiloint2double(hi, lo);
+}
+// Maximum over the first NL lanes (NL = 16, 32 or 64) for every lane; the
+// other lanes must not exceed it.  (The file is compiled without NaN
+// support: no operand needs quieting before v_max_f64.)
+template <int NL>
 __device__ __forceinline__ double wave_max_f64(double v)
 {
-    v = fmax(v, dpp_f64<0xB1, 0xF>(v));   // quad_perm 1,0,3,2
-    v = fmax(v, dpp_f64<0x4E, 0xF>(v));   // quad_perm 2,3,0,1
-    v = fmax(v, dpp_f64<0x141, 0xF>(v));  // row_half_mirror
-    v = fmax(v, dpp_f64<0x140, 0xF>(v));  // row_mirror
-    v = fmax(v, dpp_f64<0x142, 0xA>(v));  // row_bcast:15
-    v = fmax(v, dpp_f64<0x143, 0xC>(v));  // row_bcast:31
-    const int lo = __builtin_amdgcn_readlane(__double2loint(v), 63);
-    const int hi = __builtin_amdgcn_readlane(__double2hiint(v), 63);
+    v = fmax(v, dpp_row_f64<0xB1>(v));    // quad_perm 1,0,3,2
+    v = fmax(v, dpp_row_f64<0x4E>(v));    // quad_perm 2,3,0,1
+    v = fmax(v, dpp_row_f64<0x141>(v));   // row_half_mirror
+    v = fmax(v, dpp_row_f64<0x140>(v));   // row_mirror: every lane of a row holds its maximum
+    if (NL > 16) v = fmax(v, dpp_f64<0x142, 0xA>(v));  // row_bcast:15
+    if (NL > 32) v = fmax(v, dpp_f64<0x143, 0xC>(v));  // row_bcast:31
+    const int lo = __builtin_amdgcn_readlane(__double2loint(v), NL - 1);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(v), NL - 1);
     return __hiloint2double(hi, lo);
 }
 
@@ -394,14 +427,19 @@ __device__ __forceinline__ int kth_set_bit(unsigned long long m, int k)
     return pos;
 }
 
-// inclusive prefix sum over the lanes of the wave
+// inclusive prefix sum over the lanes of the wave, by DPP: row_shr 1, 2, 4,
+// 8 (lanes reading before their row's start get 0) scan each row, then
+// row_bcast:15 adds row 0's total into row 1 and row 2's into row 3, and
+// row_bcast:31 adds the total of rows 0-1 into rows 2 and 3
 __device__ __forceinline__ int wscan(int x, int lane)
 {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
+    (void)lane;
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
     return x;
 }
 
@@ -818,7 +856,7 @@ __device__ __forceinline__ void tier_stat(const Ctx& C, int tier, bool f, int fi
         }
         return;
     }
-    const int tn = __shfl_down(tier, 1);
+    const int tn = __builtin_amdgcn_update_dpp(tier, tier, 0x130, 0xF, 0xF, false);  // wave_shl:1 (lane 63 keeps its own)
     const bool last = lane == 63 || tn != tier;
     const unsigned long long bm = ballot(last), fm = ballot(f);
     if (last && tier < kTiers) {
@@ -1433,15 +1471,19 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 // demand, num and F in LDS at once: only that instance's lane
                 // touches them until the write-back)
                 double key[IPL];
-                int live_r[IPL], nadd[IPL], pend_r[IPL];
+                int live_r[IPL], nadd[IPL], pend_r[IPL], num_r[IPL], hold_r[IPL];
                 unsigned long long hk_r[IPL];
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
                     const uint32_t i = lane + 64 * j;
                     nadd[j] = 0;
                     pend_r[j] = -1;
+                    num_r[j] = 0;
+                    hold_r[j] = 0;
                     if (i < I) {
                         live_r[j] = C.live[i];
+                        num_r[j] = C.num[i];
+                        hold_r[j] = C.hold[i];
                         hk_r[j] = C.hols[i] == kNoHol ? kNone : C.holk[i];
                         key[j] = live_r[j] < int(S) && !C.drn[i] ? (infaas ? -infaas_cost(C, P, int(i), 0) : C.fd[i])
                                                                  : -__builtin_inf();
@@ -1464,7 +1506,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             double lb = key[0];
 #pragma unroll
                             for (int j = 1; j < IPL; ++j) lb = fmax(lb, key[j]);
-                            double mv = wave_max_f64(lb);
+                            double mv = wave_max_f64<(IM < 64 ? IM : 64)>(lb);
                             if (mv == -__builtin_inf() && !drain_mode) {
                                 // no non-draining instance has a free slot: the least
                                 // loaded draining one (largest F without the sentinel);
@@ -1480,7 +1522,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                 lb = key[0];
 #pragma unroll
                                 for (int j = 1; j < IPL; ++j) lb = fmax(lb, key[j]);
-                                mv = wave_max_f64(lb);
+                                mv = wave_max_f64<(IM < 64 ? IM : 64)>(lb);
                             }
                             if (mv == -__builtin_inf()) { full = true; break; }
 #pragma unroll
@@ -1517,14 +1559,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                     hk_r[j] = hk;
                                     pend_r[j] = int(k0 + k);
                                     // Eq. 1-2: F moves by the change of head-of-line demand
-                                    const int ii = lc + 64 * j;
+                                    // (num and the demand stay in registers until the write-back)
                                     const int dem = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
-                                    const int num = C.num[ii] - 256 * (dem - C.hold[ii]);
-                                    const double f = double(num) / double(C.den[ii]);
-                                    C.hold[ii] = dem;
-                                    C.num[ii] = num;
-                                    C.fd[ii] = f;
-                                    if (!infaas) key[j] = f;
+                                    num_r[j] -= 256 * (dem - hold_r[j]);
+                                    hold_r[j] = dem;
+                                    if (!infaas) key[j] = double(num_r[j]) / double(C.den[lc + 64 * j]);
                                 }
                                 if (infaas) key[j] -= double(P.alpha256) * double(m);
                                 if (nl >= int(S)) key[j] = -__builtin_inf();
@@ -1542,6 +1581,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         if (i >= I) continue;
                         C.live[i] = live_r[j];
                         C.nwait[i] += nadd[j];
+                        if (pend_r[j] >= 0) {
+                            C.num[i] = num_r[j];
+                            C.hold[i] = hold_r[j];
+                            C.fd[i] = double(num_r[j]) / double(C.den[i]);
+                        }
                         if (C.ext && nadd[j] > 0) wlb(C)[i] = t < wlb(C)[i] ? t : wlb(C)[i];
                         if (C.td && nadd[j] > 0) {
                             // queue cache: an arrival that became the head of line pushes
