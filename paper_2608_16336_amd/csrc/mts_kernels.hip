@@ -788,7 +788,9 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
         if (C.fsum) { atomicAdd(&C.fsum[i], static_cast<unsigned long long>(t - ta)); atomicAdd(&C.fcnt[i], 1); }
         c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
         tier_dec(C, i, tier);
-        if (m & kMigrating) atomicOr(&C.flags[i], kFlagAbort);
+        // being copied out: the source of its instance's migration record (the
+        // slot's meta may predate the migration's start)
+        if (C.mig[4 * i] >= 0 && C.mig[4 * i + 1] == s) atomicOr(&C.flags[i], kFlagAbort);
         atomicAnd(&C.occ[i * C.W + (s >> 6)], ~(1ull << (s & 63)));
         atomicAdd(&C.freeb[i], bl);
         atomicSub(&C.held[i], bl);
@@ -1227,13 +1229,20 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         // a tick's count is a lane read of a register, so no tick waits for
         // a load (and for the stores before it) to make its count uniform
         uint32_t cnt64 = uint32_t(lane) < nt ? cnts[lane] : 0u;
-        // the next tick's finish visit, loaded ahead: the entries of its bucket
-        // right after this tick's visit (pf_n of them; kNoPf: none), their
-        // slots' word, meta and arrival tick at the end of this tick.  It is
-        // used when the bucket still holds exactly pf_n entries and no
-        // preemption touched a slot in between; otherwise the visit loads again.
+        // The finish visits are loaded ahead in two stages, both right after a
+        // tick's own visit: the entries of the bucket two ticks ahead (pf2_n of
+        // them; kNoPf: none), and the slots' word, meta and arrival tick of the
+        // entries loaded a tick earlier for the next tick's bucket (pf_n, pf_e,
+        // pf_v, pf_m, pf_a).  A visit uses them when its bucket still holds
+        // exactly pf_n entries (appends, such as a committed migration's new
+        // entry, change the count) and no preemption touched a slot in between
+        // (victims' entries are dropped, more victims than the list holds drop
+        // the whole set); otherwise it loads again.  A running request's word,
+        // tier and arrival tick never change while it runs, and whether it is
+        // being copied out is read from the migration records at the visit.
         constexpr uint32_t kNoPf = 0xFFFFFFFFu;
         uint32_t pf_n = kNoPf, pf_e = 0, pf_v = 0, pf_m = 0, pf_a = 0;
+        uint32_t pf2_n = kNoPf, pf2_e = 0;
         unsigned long long a_nx = uint32_t(lane) < lim ? recs[lane] : 0ull;
         for (uint32_t tl = 0; tl < nt; ++tl) {
             const uint32_t t = t0u + tl;
@@ -1284,15 +1293,17 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 preempting = preempting || pre[j] != 0;
                 for (unsigned long long m = pre[j]; m; m &= m - 1) preempt(C, 64 * j + ffs64(m), t, lane);
             }
-            // a preempted request is waiting now: its prefetched entry is dropped
-            // (its wheel entry was erased); more victims than the list holds
-            // make the visit load again
+            // a preempted request is waiting now: its prefetched entries (for this
+            // tick's and the next tick's visit) are dropped (its wheel entry was
+            // erased); more victims than the list holds make both visits load again
             bool pf_lost = false;
             if (preempting) {
                 const int nv = *C.nvic;
                 pf_lost = nv > kVic;
-                for (int v = 0; v < nv && v < kVic; ++v)
+                for (int v = 0; v < nv && v < kVic; ++v) {
                     if (pf_e == C.vic[v]) pf_e = kTomb;
+                    if (pf2_e == C.vic[v]) pf2_e = kTomb;
+                }
             }
             for (uint32_t i = lane; i < I; i += 64) {
                 const int G = C.gtmp[i];
@@ -1311,12 +1322,23 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 } else {
                     finish_tick(C, t, lane);
                 }
-                // entries of the next tick's bucket
-                const uint32_t b1 = (t + 1u) & C.wmask;
-                const uint32_t n1 = (C.wc[b1 >> 1] >> ((b1 & 1u) * 16u)) & 0xFFFFu;
-                const bool ov1 = (C.wov[b1 >> 5] >> (b1 & 31u)) & 1u;
-                pf_n = !ov1 && n1 <= 64u && b1 != bk ? n1 : kNoPf;
-                pf_e = pf_n != kNoPf && uint32_t(lane) < pf_n ? C.wheel[size_t(b1) * C.wcap + lane] : 0u;
+                // slots of the next tick's bucket, from the entries loaded a tick ago
+                pf_n = pf_lost ? kNoPf : pf2_n;
+                pf_e = pf2_e;
+                if (pf_n != kNoPf) {
+                    const uint32_t pi = pf_e >> 16, ps = pf_e & 0xFFFFu;
+                    const bool ok = uint32_t(lane) < pf_n && pi < I && ps < S;
+                    const size_t idx = size_t(pi) * S + ps;
+                    pf_v = ok ? C.hot[idx] : 0u;
+                    pf_m = ok ? C.meta[idx] : 0u;
+                    pf_a = ok ? C.tarr[idx] : 0u;
+                }
+                // entries of the bucket two ticks ahead (three distinct buckets needed)
+                const uint32_t b2 = (t + 2u) & C.wmask;
+                const uint32_t n2 = (C.wc[b2 >> 1] >> ((b2 & 1u) * 16u)) & 0xFFFFu;
+                const bool ov2 = (C.wov[b2 >> 5] >> (b2 & 31u)) & 1u;
+                pf2_n = !ov2 && n2 <= 64u && C.wmask >= 3u ? n2 : kNoPf;
+                pf2_e = pf2_n != kNoPf && uint32_t(lane) < pf2_n ? C.wheel[size_t(b2) * C.wcap + lane] : 0u;
             }
             bool any_abort = false;
             for (uint32_t i = lane; i < I; i += 64) any_abort |= (C.flags[i] & kFlagAbort) != 0;
@@ -1896,15 +1918,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             }
 
             // ===================== end of tick =====================
-            // slots of the next tick's prefetched wheel entries
-            if (pf_n != kNoPf) {
-                const uint32_t pi = pf_e >> 16, ps = pf_e & 0xFFFFu;
-                const bool ok = uint32_t(lane) < pf_n && pi < I && ps < S;
-                const size_t idx = size_t(pi) * S + ps;
-                pf_v = ok ? C.hot[idx] : 0u;
-                pf_m = ok ? C.meta[idx] : 0u;
-                pf_a = ok ? C.tarr[idx] : 0u;
-            }
             for (uint32_t i = lane; i < I; i += 64) {
                 run_acc += unsigned(C.B[i]);
                 wait_acc += unsigned(C.nwait[i]);
