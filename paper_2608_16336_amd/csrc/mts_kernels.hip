@@ -123,7 +123,7 @@ struct Ctx {
     unsigned* vic;             // [kVic] instance << 16 | slot of this tick's preemption victims
     int* nvic;                 // their number (kVic + 1: more than the list holds)
     unsigned *hwd, *hmt, *hta; // [I] head of line: slot word, meta, arrival tick
-    unsigned* res;             // [I][RB] running requests per growth residue (u16 pairs)
+    unsigned* res;             // [RB][I] running requests per growth residue (u16 pairs)
     unsigned* tcnt;            // [I][10] running requests per tier (u16 pairs)
     int* mig;                  // [I][4] dst, src slot, dst slot, copied
     unsigned* wc;              // [wsz / 2] entries filed per wheel bucket, two u16 per word
@@ -353,6 +353,10 @@ __device__ inline void set_f(const Ctx& C, int i)
     C.den[i] = den;
     C.fd[i] = double(num) / double(den);
 }
+
+// running requests of instance i whose length is r mod block_tokens: laid out
+// residue-major, so that the lanes of one residue read consecutive counters
+__device__ __forceinline__ uint32_t res_idx(const Ctx& C, int i, uint32_t r) { return r * C.I + uint32_t(i); }
 
 // Counters of running requests, two u16 per LDS word (an instance holds at
 // most 2048 running requests, so no half ever carries into the other).  All
@@ -694,7 +698,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
             const int nv = *C.nvic;
             if (nv < kVic) C.vic[nv] = (uint32_t(i) << 16) | uint32_t(vs);
             *C.nvic = nv < kVic ? nv + 1 : kVic + 1;
-            c16_dec(C.res, i * C.RB + vr);
+            c16_dec(C.res, res_idx(C, i, vr));
             tier_dec(C, i, vt);
             stat(C, vt * 8 + kPreempted, 1);
             if (vm) C.flags[i] |= kFlagAbort;
@@ -734,7 +738,7 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
             stat(C, tier * 8 + kE2e, e2e);
             hist_add(C, kHistE2e, tier, e2e);
             if (C.fsum) { atomicAdd(&C.fsum[i], static_cast<unsigned long long>(e2e)); atomicAdd(&C.fcnt[i], 1); }
-            c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
+            c16_dec(C.res, res_idx(C, i, (lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
             if (m & kMigrating) ab = true;
             C.hot[b + s] = 0; C.meta[b + s] = 0; C.seq[b + s] = 0; C.tarr[b + s] = 0;
@@ -786,7 +790,7 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
         stat(C, tier * 8 + kE2e, t - ta);
         hist_add(C, kHistE2e, tier, t - ta);
         if (C.fsum) { atomicAdd(&C.fsum[i], static_cast<unsigned long long>(t - ta)); atomicAdd(&C.fcnt[i], 1); }
-        c16_dec(C.res, i * C.RB + ((lenf - t - 1u) & C.bmask));
+        c16_dec(C.res, res_idx(C, i, (lenf - t - 1u) & C.bmask));
         tier_dec(C, i, tier);
         // being copied out: the source of its instance's migration record (the
         // slot's meta may predate the migration's start)
@@ -897,7 +901,7 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
             stat(C, tier * 8 + kQdelay, t - ta);
             hist_add(C, kHistQdelay, tier, t - ta);
         }
-        c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
+        c16_inc(C.res, res_idx(C, i, (len - t - 1u) & C.bmask));
         tier_inc(C, i, tier);
         wheel_put(C, fin, i, slot);
     }
@@ -1184,7 +1188,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 if (st == 2u) {
                     const uint32_t lenf = wlo(v), fin = fin_of(v, t0u);
                     held += blocks_of(lenf - (fin - t0u + 1u), C.shift);
-                    c16_inc(C.res, i * C.RB + ((lenf - fin - 1u) & C.bmask));
+                    c16_inc(C.res, res_idx(C, i, (lenf - fin - 1u) & C.bmask));
                     const int tier = int((C.meta[b + s] >> 2) & 15u);
                     c16_inc(C.tcnt, i * kTiers + tier);
                     wheel_put(C, fin, int(i), s);
@@ -1277,7 +1281,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 const uint32_t i = lane + 64 * j;
                 bool np = false;
                 if (i < I) {
-                    const int G = int(c16_get(C.res, i * C.RB + cres));
+                    const int G = int(c16_get(C.res, res_idx(C, i, cres)));
                     C.gtmp[i] = G;
                     np = G > C.freeb[i];
                     if (C.flags[i] & kFlagIntf) C.flags[i] &= ~kFlagIntf;
@@ -1405,7 +1409,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                 C.held[i] += dem;
                                 C.B[i] += 1;
                                 C.nwait[i] -= 1;
-                                c16_inc(C.res, i * C.RB + ((len - t - 1u) & C.bmask));
+                                c16_inc(C.res, res_idx(C, i, (len - t - 1u) & C.bmask));
                                 tier_inc(C, int(i), tier);
                                 wheel_put(C, fin, int(i), h);
                                 hol_pop(C, int(i));
@@ -1746,8 +1750,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     C.inb[d] = 0;
                     C.B[i] -= 1;
                     C.B[d] += 1;
-                    c16_dec(C.res, i * C.RB + rr);
-                    c16_inc(C.res, d * C.RB + rr);
+                    c16_dec(C.res, res_idx(C, i, rr));
+                    c16_inc(C.res, res_idx(C, d, rr));
                     tier_dec(C, int(i), tier);
                     tier_inc(C, d, tier);
                     wheel_put(C, fin, d, m[2]);
