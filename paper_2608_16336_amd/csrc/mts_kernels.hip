@@ -644,10 +644,11 @@ __device__ inline void rescan_hol(const Ctx& C, int i, int lane)
 
 // memory pressure: preempt the largest (tier, seq) running request until the
 // growth of this tick fits (Section 2.2; recompute semantics)
-__device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
+__device__ inline bool preempt(const Ctx& C, int i, uint32_t t, int lane)
 {
     const size_t b = size_t(i) * C.S;
     int G = C.gtmp[i], fr = C.freeb[i];
+    bool aborted = false;
     while (G > fr) {
         const int nch = live_chunks(C, i, lane);
         unsigned long long bk = 0;
@@ -689,6 +690,7 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
         wheel_erase(C, vfin, i, vs, lane);
         fr += vb;
         G -= vg;
+        aborted = aborted || vm != 0;
         if (lane == 0) {
             C.held[i] -= vb;
             C.B[i] -= 1;
@@ -708,14 +710,16 @@ __device__ inline void preempt(const Ctx& C, int i, uint32_t t, int lane)
         }
         wave_sync();
     }
-    if (lane == 0) { C.gtmp[i] = G; C.freeb[i] = fr; }
+    // this tick's growth, now that it fits
+    if (lane == 0) { C.freeb[i] = fr - G; C.held[i] += G; }
     wave_sync();
+    return aborted;
 }
 
 // Exact finish scan of instance i, used when a wheel bucket overflowed:
 // finishes the requests whose last token is at t and files again the running
 // requests that share the bucket of t but finish later.
-__device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
+__device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane, bool& abort_any)
 {
     const size_t b = size_t(i) * C.S;
     const int nch = live_chunks(C, i, lane);
@@ -752,6 +756,7 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
     }
     freed = wsum(freed);
     const bool any_ab = ballot(ab) != 0;
+    abort_any = abort_any || any_ab;
     if (lane == 0) {
         C.freeb[i] += freed;
         C.held[i] -= freed;
@@ -768,7 +773,7 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane)
 // position kept on; returns the new kept count), tombstones and entries whose
 // slot changed since are dropped.
 __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint32_t* ent, uint32_t kept, bool inb,
-                                        uint32_t e, uint32_t v, uint32_t m, uint32_t ta)
+                                        uint32_t e, uint32_t v, uint32_t m, uint32_t ta, bool& abort_any)
 {
     const uint32_t bk = t & C.wmask;
     const int i = int(e >> 16), s = int(e & 0xFFFFu);
@@ -781,6 +786,7 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
     const unsigned long long km = ballot(k);
     if (k) ent[kept + __popcll(km & lanemask_lt())] = e;
     kept += __popcll(km);
+    bool ab = false;
     if (f) {
         const size_t idx = size_t(i) * C.S + s;
         const uint32_t lenf = wlo(v);
@@ -794,7 +800,8 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
         tier_dec(C, i, tier);
         // being copied out: the source of its instance's migration record (the
         // slot's meta may predate the migration's start)
-        if (C.mig[4 * i] >= 0 && C.mig[4 * i + 1] == s) atomicOr(&C.flags[i], kFlagAbort);
+        ab = C.mig[4 * i] >= 0 && C.mig[4 * i + 1] == s;
+        if (ab) atomicOr(&C.flags[i], kFlagAbort);
         atomicAnd(&C.occ[i * C.W + (s >> 6)], ~(1ull << (s & 63)));
         atomicAdd(&C.freeb[i], bl);
         atomicSub(&C.held[i], bl);
@@ -802,6 +809,7 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
         atomicSub(&C.live[i], 1);
         C.hot[idx] = 0; C.meta[idx] = 0; C.seq[idx] = 0; C.tarr[idx] = 0;
     }
+    abort_any = abort_any || ballot(ab) != 0;
     wave_sync();
     return kept;
 }
@@ -815,7 +823,7 @@ __device__ __forceinline__ void wheel_set_count(const Ctx& C, uint32_t b, uint32
 
 // Requests that emit their last token at tick t: the bucket t mod wsz lists
 // every running request with fin = t (mod wsz).
-__device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
+__device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane, bool& abort_any)
 {
     const uint32_t bk = t & C.wmask;
     const uint32_t sh = (bk & 1u) * 16u;
@@ -830,7 +838,7 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
         for (uint32_t j = 0; j < (C.I + 63) / 64; ++j) {
             const uint32_t i = lane + 64 * j;
             for (unsigned long long m = ballot(i < C.I && C.B[i] > 0); m; m &= m - 1)
-                finish_scan(C, int(64 * j + ffs64(m)), t, lane);
+                finish_scan(C, int(64 * j + ffs64(m)), t, lane, abort_any);
         }
         return;
     }
@@ -844,7 +852,7 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane)
         const size_t idx = size_t(i) * C.S + s;
         uint32_t v = 0, m = 0, ta = 0;
         if (valid) { v = C.hot[idx]; m = C.meta[idx]; ta = C.tarr[idx]; }
-        kept = finish_batch(C, t, lane, ent, kept, inb, e, v, m, ta);
+        kept = finish_batch(C, t, lane, ent, kept, inb, e, v, m, ta, abort_any);
     }
     wheel_set_count(C, bk, kept, lane);
 }
@@ -1274,28 +1282,40 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             }
 
             // ===================== A: growth, preemption, finish =====================
+            // an instance whose growth fits takes its blocks at once; the others
+            // preempt first (and take them at the end of preempt)
             const uint32_t cres = (0u - t) & C.bmask;
             unsigned long long pre[IPL];
+            bool preempting = false;
 #pragma unroll
             for (int j = 0; j < IPL; ++j) {
                 const uint32_t i = lane + 64 * j;
                 bool np = false;
                 if (i < I) {
                     const int G = int(c16_get(C.res, res_idx(C, i, cres)));
-                    C.gtmp[i] = G;
-                    np = G > C.freeb[i];
+                    const int fr = C.freeb[i];
+                    np = G > fr;
+                    if (np) {
+                        C.gtmp[i] = G;
+                    } else {
+                        C.freeb[i] = fr - G;
+                        C.held[i] += G;
+                    }
                     if (C.flags[i] & kFlagIntf) C.flags[i] &= ~kFlagIntf;
                     if (C.fsum) { C.fsum[i] = 0; C.fcnt[i] = 0; }
                 }
                 pre[j] = ballot(np);
+                preempting = preempting || pre[j] != 0;
             }
             if (lane == 0) *C.nvic = 0;
-            wave_sync();
-            bool preempting = false;
+            // migrations to abort: set by preemption and finish, kept in a register
+            bool abort_any = false;
+            if (preempting) {
+                wave_sync();
 #pragma unroll
-            for (int j = 0; j < IPL; ++j) {
-                preempting = preempting || pre[j] != 0;
-                for (unsigned long long m = pre[j]; m; m &= m - 1) preempt(C, 64 * j + ffs64(m), t, lane);
+                for (int j = 0; j < IPL; ++j)
+                    for (unsigned long long m = pre[j]; m; m &= m - 1)
+                        abort_any = preempt(C, 64 * j + ffs64(m), t, lane) || abort_any;
             }
             // a preempted request is waiting now: its prefetched entries (for this
             // tick's and the next tick's visit) are dropped (its wheel entry was
@@ -1309,11 +1329,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     if (pf2_e == C.vic[v]) pf2_e = kTomb;
                 }
             }
-            for (uint32_t i = lane; i < I; i += 64) {
-                const int G = C.gtmp[i];
-                C.freeb[i] -= G;
-                C.held[i] += G;
-            }
             wave_sync();
             {
                 const uint32_t bk = t & C.wmask;
@@ -1321,10 +1336,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 const bool ov = (C.wov[bk >> 5] >> (bk & 31u)) & 1u;
                 if (pf_n != kNoPf && !pf_lost && !ov && nb == pf_n) {
                     uint32_t* ent = C.wheel + size_t(bk) * C.wcap;
-                    const uint32_t kept = finish_batch(C, t, lane, ent, 0, uint32_t(lane) < pf_n, pf_e, pf_v, pf_m, pf_a);
+                    const uint32_t kept = finish_batch(C, t, lane, ent, 0, uint32_t(lane) < pf_n, pf_e, pf_v, pf_m, pf_a,
+                                                       abort_any);
                     wheel_set_count(C, bk, kept, lane);
                 } else {
-                    finish_tick(C, t, lane);
+                    finish_tick(C, t, lane, abort_any);
                 }
                 // slots of the next tick's bucket, from the entries loaded a tick ago
                 pf_n = pf_lost ? kNoPf : pf2_n;
@@ -1344,10 +1360,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 pf2_n = !ov2 && n2 <= 64u && C.wmask >= 3u ? n2 : kNoPf;
                 pf2_e = pf2_n != kNoPf && uint32_t(lane) < pf2_n ? C.wheel[size_t(b2) * C.wcap + lane] : 0u;
             }
-            bool any_abort = false;
-            for (uint32_t i = lane; i < I; i += 64) any_abort |= (C.flags[i] & kFlagAbort) != 0;
             // ===================== A2: release reservations of aborted migrations =====================
-            if (ballot(any_abort)) {
+            if (abort_any) {
                 for (uint32_t i = lane; i < I; i += 64) {
                     if (!(C.flags[i] & kFlagAbort)) continue;
                     C.flags[i] &= ~kFlagAbort;
@@ -1436,6 +1450,12 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             long long fsum = 0;
             for (uint32_t i = lane; i < I; i += 64) {
                 set_f(C, int(i));
+                // slot-ticks: running and waiting requests at the end of the tick.
+                // Later phases move running and waiting requests between
+                // instances (commits, queued moves) and add only the arrivals
+                // the dispatch places, counted there
+                run_acc += unsigned(C.B[i]);
+                wait_acc += unsigned(C.nwait[i]);
                 if (C.freeb[i] < 0 || C.freeb[i] + C.held[i] + C.inb[i] != int(C.M)) stat(C, kInvariant, 1);
                 // floor(x 2^20 / den): x 2^20 is exact in a double (|x| < 2^22) and
                 // the correctly rounded quotient never crosses an integer (the
@@ -1479,9 +1499,10 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             // ===================== D: tier-ordered dispatch =====================
             // an instance with an empty queue now holds, after this dispatch, only
             // this tick's arrivals; they are recorded in LDS when they fit one wave
-            for (uint32_t i = lane; i < I; i += 64) C.frs[i] = C.nwait[i] == 0 && n <= uint32_t(kLast);
+            // (frs is written with the dispatch's write-back, from the queue length before it)
             if (lane == 0) *C.lastn = 0;
-            wave_sync();
+            if (n == 0)
+                for (uint32_t i = lane; i < I; i += 64) C.frs[i] = C.nwait[i] == 0;
             if (n > 0) {
                 for (uint32_t k0 = 0; k0 < n; k0 += 64) {
                     const unsigned long long a = k0 == 0 ? a0 : (k0 + lane < n ? rec[k0 + lane] : 0);
@@ -1606,7 +1627,10 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         const uint32_t i = lane + 64 * j;
                         if (i >= I) continue;
                         C.live[i] = live_r[j];
-                        C.nwait[i] += nadd[j];
+                        const int nw0 = C.nwait[i];
+                        if (k0 == 0) C.frs[i] = nw0 == 0 && n <= uint32_t(kLast);
+                        C.nwait[i] = nw0 + nadd[j];
+                        wait_acc += unsigned(nadd[j]);
                         if (pend_r[j] >= 0) {
                             C.num[i] = num_r[j];
                             C.hold[i] = hold_r[j];
@@ -1922,10 +1946,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             }
 
             // ===================== end of tick =====================
-            for (uint32_t i = lane; i < I; i += 64) {
-                run_acc += unsigned(C.B[i]);
-                wait_acc += unsigned(C.nwait[i]);
-            }
             if (lane == 0) C.stats[kTicks] += 1;
         }
 
