@@ -541,15 +541,28 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     auto get = [&](void* dst, size_t off, size_t n) {
         if (e == hipSuccess && dst && n) e = hipMemcpy(dst, h->dev + off, n, hipMemcpyDeviceToHost);
     };
-    if (v->lr) {
-        std::vector<uint32_t> w(size_t(nr) * IS);
+    // the device marks an empty slot by its word alone, and an inbound
+    // reservation by its word and meta; their other fields are zero in the
+    // canonical state
+    std::vector<uint32_t> w;
+    if (v->lr || v->meta || v->seq || v->tarr) {
+        w.resize(size_t(nr) * IS);
         get(w.data(), L.hot + size_t(r0) * IS * 4, w.size() * 4);
-        if (e == hipSuccess)
-            for (size_t k = 0; k < w.size(); ++k) v->lr[k] = word_to_lr(w[k], h->tick);
     }
+    if (v->lr && e == hipSuccess)
+        for (size_t k = 0; k < w.size(); ++k) v->lr[k] = word_to_lr(w[k], h->tick);
     get(v->meta, L.meta + size_t(r0) * IS, size_t(nr) * IS);
     get(v->seq, L.seq + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
     get(v->tarr, L.tarr + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
+    if (e == hipSuccess)
+        for (size_t k = 0; k < w.size(); ++k) {
+            const uint32_t st = w[k] >> 30;
+            if (w[k] == 0 && v->meta) v->meta[k] = 0;
+            if (w[k] == 0 || st == kInbound) {
+                if (v->seq) v->seq[k] = 0;
+                if (v->tarr) v->tarr[k] = 0;
+            }
+        }
     get(v->free, L.freeb + size_t(r0) * I * 4, size_t(nr) * I * 4);
     get(v->mig, L.mig + size_t(r0) * I * 16, size_t(nr) * I * 16);
     get(v->next_seq, L.next_seq + size_t(r0) * 4, size_t(nr) * 4);

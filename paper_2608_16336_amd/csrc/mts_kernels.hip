@@ -11,8 +11,11 @@
 // Slot word ("hot", u32, bits 31..30 = status):
 //   waiting   01 | rem (14 bits) | len (16 bits)
 //   running   10 | fin mod 2^14  | final length (16 bits)
-//   inbound   11 | 0
-//   empty     0
+//   inbound   11 | 0 (with meta; seq and arrival tick keep whatever the slot
+//             held last and are read as zero by the export and the digest)
+//   empty     0 (the word alone marks an empty slot: meta, seq and arrival
+//             tick keep whatever the slot held last; the export and the
+//             digest read them as zero)
 // A running request's word never changes while it runs: the tick at which it
 // emits its last token (fin) and its final length determine its length at
 // any tick t (final - (fin - t + 1) before the decode of t), so decoding
@@ -745,7 +748,7 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane, bo
             c16_dec(C.res, res_idx(C, i, (lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
             if (m & kMigrating) ab = true;
-            C.hot[b + s] = 0; C.meta[b + s] = 0; C.seq[b + s] = 0; C.tarr[b + s] = 0;
+            C.hot[b + s] = 0;  // the word alone marks the slot empty
         } else if (run && (fin & C.wmask) == bk) {
             wheel_put(C, fin, i, s);
         }
@@ -807,7 +810,7 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
         atomicSub(&C.held[i], bl);
         atomicSub(&C.B[i], 1);
         atomicSub(&C.live[i], 1);
-        C.hot[idx] = 0; C.meta[idx] = 0; C.seq[idx] = 0; C.tarr[idx] = 0;
+        C.hot[idx] = 0;  // the word alone marks the slot empty
     }
     abort_any = abort_any || ballot(ab) != 0;
     wave_sync();
@@ -1371,7 +1374,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     C.freeb[d] += m[3];
                     C.inb[d] = 0;
                     const size_t db = size_t(d) * S + m[2];
-                    C.hot[db] = 0; C.meta[db] = 0;
+                    C.hot[db] = 0;
                     C.occ[d * W + (m[2] >> 6)] &= ~(1ull << (m[2] & 63));
                     C.live[d] -= 1;
                     m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
@@ -1745,7 +1748,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 if (w > C.freeb[d]) {
                     C.freeb[d] += m[3];
                     C.inb[d] = 0;
-                    C.hot[db] = 0; C.meta[db] = 0;
+                    C.hot[db] = 0;
                     C.occ[d * W + (m[2] >> 6)] &= ~(1ull << (m[2] & 63));
                     C.live[d] -= 1;
                     C.meta[sb] = uint8_t(C.meta[sb] & ~kMigrating);
@@ -1765,7 +1768,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     C.meta[db] = uint8_t((mm & ~(3u | kMigrating)) | kRunning);
                     C.seq[db] = C.seq[sb];
                     C.tarr[db] = C.tarr[sb];
-                    C.hot[sb] = 0; C.meta[sb] = 0; C.seq[sb] = 0; C.tarr[sb] = 0;
+                    C.hot[sb] = 0;
                     C.occ[i * W + (m[1] >> 6)] &= ~(1ull << (m[1] & 63));
                     C.live[i] -= 1;
                     C.freeb[i] += bl;
@@ -1889,7 +1892,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             const unsigned long long key = C.holk[src];
                             C.hot[dsb] = hw; C.meta[dsb] = uint8_t(hm);
                             C.seq[dsb] = uint32_t(key); C.tarr[dsb] = ht;
-                            C.hot[hb] = 0; C.meta[hb] = 0; C.seq[hb] = 0; C.tarr[hb] = 0;
+                            C.hot[hb] = 0;
                             C.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
                             C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
                             C.live[src] -= 1; C.nwait[src] -= 1;
@@ -2035,11 +2038,15 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t 
     const unsigned long long gm = mix64(P.id_base + r);
     unsigned long long d = 0;
     for (size_t s = threadIdx.x; s < IS; s += blockDim.x) {
+        // an empty slot has a zero word; an inbound reservation's seq and
+        // arrival tick are zero in the canonical state (the device leaves them)
+        const uint32_t hw = P.hot[rb + s];
+        if (hw == 0u) continue;
+        const bool inb = wst(hw) == kInbound;
         const unsigned m = P.meta[rb + s];
-        if ((m & 3u) == kEmpty) continue;
-        const unsigned long long a = static_cast<unsigned long long>(canonical_lr(P.hot[rb + s], tick)) |
-                                     (static_cast<unsigned long long>(P.seq[rb + s]) << 32);
-        const unsigned long long b = static_cast<unsigned long long>(P.tarr[rb + s]) |
+        const unsigned long long a = static_cast<unsigned long long>(canonical_lr(hw, tick)) |
+                                     (static_cast<unsigned long long>(inb ? 0u : P.seq[rb + s]) << 32);
+        const unsigned long long b = static_cast<unsigned long long>(inb ? 0u : P.tarr[rb + s]) |
                                      (static_cast<unsigned long long>(m) << 32);
         const unsigned long long p = mix64(gm + 2ull * s + 1ull);
         d += mix64(p ^ a) + mix64(p ^ b);
