@@ -3,6 +3,7 @@
 No GPU.  Each test names the passage or the closed form it checks.
 """
 import math
+import os
 from fractions import Fraction
 
 import numpy as np
@@ -14,6 +15,7 @@ from exact_sim import exact_headroom
 from workloads import preset, scaled
 
 TWO32 = 1 << 32
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
 # ---------------------------------------------------------------------------
@@ -48,18 +50,34 @@ def _cfg_one(**over):
     return c
 
 
+def _golden(name):
+    """key -> list of numbers from a fixture under tests/golden/."""
+    out = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].split()
+            if line:
+                out[line[0]] = [float(v) for v in line[1:]]
+    return out
+
+
 def test_headroom_matches_fig3_printed_values():
-    # Fig. 3: K = 4, h_max = 0.20, lambda = 1.0 -> H_p / M = 20.0, 7.36, 2.71,
-    # 1.00 % and 31.1 % in total (Section 3.3).  Fig. 3 charges the lowest
-    # tier too, so the lowest-tier zeroing is switched off here.
+    # Fig. 3 (Section 3.3): the printed per-tier headroom of Eq. 3 as a share
+    # of M.  Fig. 3 charges the lowest tier too, so the lowest-tier zeroing is
+    # switched off here.
+    g = _golden("fig3_headroom.txt")
+    K = int(g["K"][0])
     M = 10000
-    c = _cfg_one(kv_blocks=M, headroom_base=0.20 * M, headroom_decay=math.exp(-1.0), zero_lowest_tier=0)
-    c["groups"] = [dict(n_replicas=1, K=4, tiers=dict(kind="uniform"))]
-    H = oracle.Oracle(c, 0, 1).headroom(0)[:4]
+    c = _cfg_one(kv_blocks=M, headroom_base=g["h_max"][0] * M, headroom_decay=math.exp(-g["lambda"][0]),
+                 zero_lowest_tier=0)
+    c["groups"] = [dict(n_replicas=1, K=K, tiers=dict(kind="uniform"))]
+    H = oracle.Oracle(c, 0, 1).headroom(0)[:K]
     pct = [h / 256 / M * 100 for h in H]
-    for got, printed in zip(pct, [20.0, 7.36, 2.71, 1.00]):
-        assert abs(got - printed) <= 0.005
-    assert abs(sum(pct) - 31.1) <= 0.05
+    for p in range(K):
+        printed, tol = g["H%d_pct" % p]
+        assert abs(pct[p] - printed) <= tol, (p, pct[p], printed)
+    printed, tol = g["total_pct"]
+    assert abs(sum(pct) - printed) <= tol
 
 
 @pytest.mark.parametrize("name", ["tiny", "enterprise", "gauss10", "sweep", "wide"])
@@ -86,14 +104,19 @@ def test_single_tier_has_no_headroom():
 # Freeness, Eq. 1 / Eq. 2 / Eq. 4 and the Fig. 2 worked example
 # ---------------------------------------------------------------------------
 def _fig2_state(extra_running=()):
-    """Instance 0 of a 2-instance cluster with M = 2000 blocks of 16 tokens.
-    Two tier-0 requests run with 350 blocks each (35 % of M), one request
-    waits needing 300 blocks (15 %), tier-0 headroom is 400 blocks (20 %)."""
-    c = _cfg_one(n_instances=2, kv_blocks=2000, headroom_base=400.0, headroom_decay=0.5)
+    """Instance 0 of a 2-instance cluster with M = 2000 blocks of 16 tokens,
+    filled as Fig. 2's bar: two tier-0 requests run with half of the physical
+    share each, one request waits with the head-of-line share, tier-0
+    headroom is the headroom share."""
+    g = _golden("fig2_freeness.txt")
+    M = 2000
+    blocks = lambda key: int(round(g[key][0] / 100 * M))
+    phys, hol, head = blocks("phys_pct"), blocks("hol_pct"), blocks("headroom_pct")
+    assert phys % 2 == 0
+    c = _cfg_one(n_instances=2, kv_blocks=M, headroom_base=float(head), headroom_decay=0.5)
     o = oracle.Oracle(c, 0, 1)
     st = o.export()
-    S = c["slots_per_instance"]
-    reqs = [(2, 0, 350 * 16, 5, 1), (2, 0, 350 * 16, 5, 2), (1, 0, 300 * 16, 5, 3)]
+    reqs = [(2, 0, phys // 2 * 16, 5, 1), (2, 0, phys // 2 * 16, 5, 2), (1, 0, hol * 16, 5, 3)]
     reqs += list(extra_running)
     held = 0
     for s, (status, tier, length, rem, seq) in enumerate(reqs):
@@ -102,7 +125,7 @@ def _fig2_state(extra_running=()):
         st["seq"][s] = seq
         if status == 2:
             held += -(-length // 16)
-    st["free"][0] = 2000 - held
+    st["free"][0] = M - held
     st["next_seq"][0] = 100
     o.import_state(st)
     assert o.check(0) == 0
@@ -110,11 +133,14 @@ def _fig2_state(extra_running=()):
 
 
 def test_fig2_worked_example():
-    # Fig. 2: phys 35 %, HoL 15 %, H_p 20 %, free 30 % -> F = 0.30 M / B.
+    # Fig. 2 (Section 3.2): the bar's free share over B running requests is
+    # the freeness, F = free_pct / 100 * M / B.
+    g = _golden("fig2_freeness.txt")
+    assert sum(g[k][0] for k in ("phys_pct", "hol_pct", "headroom_pct", "free_pct")) == 100
     o, c = _fig2_state()
     num, den = o.freeness(0, 0)
     assert den == 2
-    assert Fraction(num, 256 * den) == Fraction(30, 100) * c["kv_blocks"] / 2
+    assert Fraction(num, 256 * den) == Fraction(int(g["free_pct"][0]), 100) * c["kv_blocks"] / 2
     # the empty instance: F = M / max(B, 1) (B = 0 read as 1)
     num1, den1 = o.freeness(0, 1)
     assert (num1, den1) == (256 * 2000, 1)
