@@ -579,72 +579,6 @@ __device__ inline void wheel_erase(const Ctx& C, uint32_t fin, int i, int s, int
     }
 }
 
-// Head of line of instance i from its slots, and behind it as many of the
-// next smallest (tier, seq) waiting requests as the queue cache holds.  Each
-// lane keeps the two smallest keys of its slots; the wave then takes the
-// minimum over the lanes' first keys round by round (the winner moves its
-// second key up), and stops when the winner had more waiting slots than the
-// two it kept (its next key is unknown).  A second read fetches the fields
-// of the requests taken.  GR chunks of 64 slots are read per memory round
-// trip (more for the large instances of the kernels with registers to spare).
-template <int GR>
-__device__ inline void rescan_hol(const Ctx& C, int i, int lane)
-{
-    const size_t b = size_t(i) * C.S;
-    const int nch = live_chunks(C, i, lane);
-    unsigned long long k1 = kNone, k2 = kNone;
-    int s1 = 0, s2 = 0, cnt = 0;
-    for (int c0 = 0; c0 < nch; c0 += GR) {
-        uint32_t v[GR], m[GR], q[GR];
-#pragma unroll
-        for (int g = 0; g < GR; ++g) {
-            const bool in = c0 + g < nch;
-            v[g] = in ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
-            m[g] = in ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
-            q[g] = in ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
-        }
-#pragma unroll
-        for (int g = 0; g < GR; ++g) {
-            if (wst(v[g]) != 1u) continue;
-            ++cnt;
-            const unsigned long long k = (rank_of(C, (m[g] >> 2) & 15u) << 32) | q[g];
-            const int sl = (c0 + g) * 64 + lane;
-            if (k < k1) { k2 = k1; s2 = s1; k1 = k; s1 = sl; }
-            else if (k < k2) { k2 = k; s2 = sl; }
-        }
-    }
-    unsigned long long myk = kNone;
-    int mys = 0, got = 0, taken = 0;
-    for (int r = 0; r <= C.td; ++r) {
-        const unsigned long long mn = wmin64(k1);
-        if (mn == kNone) break;
-        const int wl = ffs64(ballot(k1 == mn));
-        const int sl = rl(s1, wl);
-        if (lane == r) { myk = mn; mys = sl; }
-        got = r + 1;
-        bool unknown = false;
-        if (lane == wl) {
-            k1 = k2; s1 = s2; k2 = kNone;
-            ++taken;
-            unknown = taken >= 2 && cnt > 2;
-        }
-        if (ballot(unknown)) break;
-    }
-    if (got == 0) {
-        if (lane == 0) clear_hol(C, i);
-        wave_sync();
-        return;
-    }
-    uint32_t w = 0, mt = 0, ta = 0;
-    if (lane < got) { w = C.hot[b + mys]; mt = C.meta[b + mys]; ta = C.tarr[b + mys]; }
-    if (lane == 0) {
-        set_hol(C, i, mys, myk, w, mt, ta);
-        if (C.td) { C.qn[i] = got - 1; C.qh[i] = 0; }
-    }
-    if (lane >= 1 && lane < got) C.qt[i * C.td + lane - 1] = qc_pack(myk, mys, w, mt, ta);
-    wave_sync();
-}
-
 // memory pressure: preempt the largest (tier, seq) running request until the
 // growth of this tick fits (Section 2.2; recompute semantics)
 __device__ inline bool preempt(const Ctx& C, int i, uint32_t t, int lane)
@@ -890,9 +824,11 @@ __device__ __forceinline__ void tier_stat(const Ctx& C, int tier, bool f, int fi
 // whose summed demand fits the free blocks, and makes the next one the head
 // of line (Section 3.1: the local queue is served in priority order while
 // the head fits; the result equals admitting the head of line one request at
-// a time).
+// a time).  The list holds every waiting request of i (complete) or the w
+// smallest keys of a longer queue; when all w of those fit, the head of line
+// is unknown afterwards (the next rescan finds it).
 __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, int w, unsigned long long key,
-                                    uint32_t word, uint32_t meta, uint32_t ta, int slot)
+                                    uint32_t word, uint32_t meta, uint32_t ta, int slot, bool complete = true)
 {
     const size_t b = size_t(i) * C.S;
     const int dem = lane < w ? blocks_of(wlo(word), C.shift) : 0;
@@ -926,15 +862,106 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
         C.held[i] += used;
         C.B[i] += na;
         C.nwait[i] -= na;
-        if (w != C.nwait[i] + na) stat(C, kInvariant, 1);
-        if (na < w) set_hol(C, i, hs, hk, hw, hm, ht);
-        else clear_hol(C, i);
+        if (complete ? w != C.nwait[i] + na : w >= C.nwait[i] + na) stat(C, kInvariant, 1);
+        if (na < w) {
+            set_hol(C, i, hs, hk, hw, hm, ht);
+        } else if (complete) {
+            clear_hol(C, i);
+        } else {
+            C.hols[i] = kHolUnknown;
+            if (C.td) C.qn[i] = 0;
+        }
         if (C.td && na < w) { C.qn[i] = min(w - na - 1, C.td); C.qh[i] = 0; }
     }
-    // every waiting request is in the ranked list: the ones after the new head fill the cache
+    // the ranked list holds the smallest keys: the ones after the new head fill the cache
     if (C.td && lane > na && lane < w && lane - na - 1 < C.td)
         C.qt[i * C.td + lane - na - 1] = qc_pack(key, slot, word, meta, ta);
     wave_sync();
+}
+
+// Head of line of instance i from its slots, with admission (Section 3.1:
+// the local queue is served in (tier, seq) order while the head fits).  Each
+// lane keeps the MK smallest keys of its slots, with their demand; the wave
+// then takes minima round by round, lane r receiving the request of rank r,
+// and stops when the winning lane had more waiting slots than it kept (its
+// next key is unknown), after 64 requests, or qdepth requests after the first
+// one whose cumulative demand exceeds the free blocks (the new head of line
+// and the cache behind it).  A second read fetches the fields of the requests
+// taken, and the longest fitting prefix is admitted at once (admit_ranked).
+// GR chunks of 64 slots are read per memory round trip.  Returns true when
+// every request taken was admitted and more wait (the head of line is still
+// unknown).  Uniform.
+template <int GR, int MK>
+__device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
+{
+    const size_t b = size_t(i) * C.S;
+    const int nch = live_chunks(C, i, lane);
+    unsigned long long k[MK];
+    int ks[MK], kd[MK];
+#pragma unroll
+    for (int x = 0; x < MK; ++x) { k[x] = kNone; ks[x] = 0; kd[x] = 0; }
+    int cnt = 0;
+    for (int c0 = 0; c0 < nch; c0 += GR) {
+        uint32_t v[GR], m[GR], q[GR];
+#pragma unroll
+        for (int g = 0; g < GR; ++g) {
+            const bool in = c0 + g < nch;
+            v[g] = in ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
+            m[g] = in ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
+            q[g] = in ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
+        }
+#pragma unroll
+        for (int g = 0; g < GR; ++g) {
+            if (wst(v[g]) != 1u) continue;
+            ++cnt;
+            unsigned long long ck = (rank_of(C, (m[g] >> 2) & 15u) << 32) | q[g];
+            if (ck >= k[MK - 1]) continue;
+            int cs = (c0 + g) * 64 + lane, cd = blocks_of(wlo(v[g]), C.shift);
+            // insertion into the lane's sorted list (the largest drops out)
+#pragma unroll
+            for (int x = 0; x < MK; ++x) {
+                if (ck < k[x]) {
+                    const unsigned long long tk = k[x]; k[x] = ck; ck = tk;
+                    const int ts = ks[x]; ks[x] = cs; cs = ts;
+                    const int tdm = kd[x]; kd[x] = cd; cd = tdm;
+                }
+            }
+        }
+    }
+    const int fr = C.freeb[i];
+    unsigned long long myk = kNone;
+    int mys = 0, got = 0, taken = 0, cum = 0, lim = 64;
+    for (int r = 0; r < lim; ++r) {
+        const unsigned long long mn = wmin64(k[0]);
+        if (mn == kNone) break;
+        const int wl = ffs64(ballot(k[0] == mn));
+        if (lane == r) { myk = mn; mys = rl(ks[0], wl); }
+        got = r + 1;
+        cum += rl(kd[0], wl);
+        // the first request that does not fit is the new head of line; the
+        // cache takes the qdepth after it
+        if (cum > fr && lim == 64) lim = min(64, r + 1 + C.td);
+        bool unknown = false;
+        if (lane == wl) {
+#pragma unroll
+            for (int x = 0; x + 1 < MK; ++x) { k[x] = k[x + 1]; ks[x] = ks[x + 1]; kd[x] = kd[x + 1]; }
+            k[MK - 1] = kNone;
+            ++taken;
+            unknown = taken >= MK && cnt > MK;
+        }
+        if (ballot(unknown)) break;
+    }
+    if (got == 0) {
+        if (lane == 0) clear_hol(C, i);
+        wave_sync();
+        return false;
+    }
+    uint32_t w = 0, mt = 0, ta = 0;
+    if (lane < got) { w = C.hot[b + mys]; mt = C.meta[b + mys]; ta = C.tarr[b + mys]; }
+    const bool complete = got >= C.nwait[i];
+    if (lane == 0) C.frs[i] = 0;
+    admit_ranked(C, i, t, lane, got, myk, w, mt, ta, mys, complete);
+    return C.hols[i] == kHolUnknown;
 }
 
 // Admission of instance i when its head of line fits and 2..64 requests wait
@@ -1385,13 +1412,15 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
 
             // ===================== B: admission (lane-parallel rounds); C: freeness =====================
             for (;;) {
+                // heads of line left unknown: found by a rescan, which admits at once
+                bool unk = false;
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
                     const uint32_t i = lane + 64 * j;
                     for (unsigned long long m = ballot(i < I && C.hols[i] == kHolUnknown); m; m &= m - 1)
-                        rescan_hol<(IM >= 128 ? 16 : 4)>(C, 64 * j + ffs64(m), lane);
+                        unk = rescan_admit<(IM >= 128 ? 16 : 4), (IM >= 128 ? 4 : 2)>(C, 64 * j + ffs64(m), t, lane) || unk;
                 }
-                bool any = false;
+                bool any = unk;
                 unsigned long long bat[IPL], frm[IPL];
 #pragma unroll
                 for (int j = 0; j < IPL; ++j) {
