@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 
 # HBM bytes per k_step launch (mean over the timed launches of the default
-# sweep run: 1000-tick steps in launches of at most 431 ticks), from rocprofv3
+# sweep run: one launch per 1000-tick step), from rocprofv3
 # FETCH_SIZE (x2.0) and WRITE_SIZE (x1.0) passes scaled against a 1 GiB device
 # copy, keyed by the SHA-256 prefix of the step-kernel source they were taken
 # on; any other kernel source reports null.

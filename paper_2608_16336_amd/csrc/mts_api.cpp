@@ -51,7 +51,7 @@ uint32_t total_replicas(const mts_cfg& c)
 }
 
 // device bytes reserved for pre-sampled arrivals; sets the ticks per batch
-constexpr size_t kArrivalBudget = size_t(512) << 20;
+constexpr size_t kArrivalBudget = size_t(2048) << 20;
 
 uint32_t chunk_for(uint32_t R, uint32_t cap)
 {

@@ -1208,55 +1208,79 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         }
         wave_sync();
         const uint32_t t0u = uint32_t(t0);
-        for (uint32_t i = 0; i < I; ++i) {
-            const size_t b = size_t(i) * S;
+        {
+            // The slots are read as one flat run of I * W chunks of 64 (chunk c
+            // of instance i is flat chunk i W + c), GP chunks per memory round
+            // trip; an instance is summed up after its last chunk.  The arrival
+            // ticks of the heads of line are read afterwards, lane-parallel.
+            constexpr int GP = IM >= 128 ? 16 : 8;
+            const uint32_t nfl = I * W;
             int nB = 0, nlive = 0, nw = 0, held = 0;
             unsigned long long bk = kNone;
             int bs = 0;
             uint32_t bv = 0, bm = 0;
-            for (uint32_t c = 0; c < W; ++c) {
-                const int s = int(c) * 64 + lane;
-                const uint32_t v = C.hot[b + s];
-                const uint32_t st = wst(v);
-                const unsigned long long ow = ballot(v != 0);
-                nlive += __popcll(ow);
-                nB += __popcll(ballot(st == 2u));
-                nw += __popcll(ballot(st == 1u));
-                if (lane == 0) C.occ[i * W + c] = ow;
-                if (st == 2u) {
-                    const uint32_t lenf = wlo(v), fin = fin_of(v, t0u);
-                    held += blocks_of(lenf - (fin - t0u + 1u), C.shift);
-                    c16_inc(C.res, res_idx(C, i, (lenf - fin - 1u) & C.bmask));
-                    const int tier = int((C.meta[b + s] >> 2) & 15u);
-                    c16_inc(C.tcnt, i * kTiers + tier);
-                    wheel_put(C, fin, int(i), s);
-                } else if (st == 1u) {
-                    const uint32_t m = C.meta[b + s];
-                    const unsigned long long k = (rank_of(C, (m >> 2) & 15u) << 32) | C.seq[b + s];
-                    if (k < bk) { bk = k; bs = s; bv = v; bm = m; }
+            for (uint32_t f0 = 0; f0 < nfl; f0 += GP) {
+                uint32_t v[GP], m[GP], q[GP];
+#pragma unroll
+                for (int g = 0; g < GP; ++g) {
+                    const bool in = f0 + g < nfl;
+                    const size_t fs = size_t(f0 + g) * 64 + lane;
+                    v[g] = in ? C.hot[fs] : 0u;
+                    m[g] = in ? C.meta[fs] : 0u;
+                    q[g] = in ? C.seq[fs] : 0u;
+                }
+#pragma unroll
+                for (int g = 0; g < GP; ++g) {
+                    const uint32_t f = f0 + g;
+                    if (f >= nfl) continue;
+                    const uint32_t i = f / W, c = f - i * W;
+                    const int s = int(c) * 64 + lane;
+                    const uint32_t st = wst(v[g]);
+                    const unsigned long long ow = ballot(v[g] != 0);
+                    nlive += __popcll(ow);
+                    nB += __popcll(ballot(st == 2u));
+                    nw += __popcll(ballot(st == 1u));
+                    if (lane == 0) C.occ[i * W + c] = ow;
+                    if (st == 2u) {
+                        const uint32_t lenf = wlo(v[g]), fin = fin_of(v[g], t0u);
+                        held += blocks_of(lenf - (fin - t0u + 1u), C.shift);
+                        c16_inc(C.res, res_idx(C, i, (lenf - fin - 1u) & C.bmask));
+                        c16_inc(C.tcnt, i * kTiers + int((m[g] >> 2) & 15u));
+                        wheel_put(C, fin, int(i), s);
+                    } else if (st == 1u) {
+                        const unsigned long long k = (rank_of(C, (m[g] >> 2) & 15u) << 32) | q[g];
+                        if (k < bk) { bk = k; bs = s; bv = v[g]; bm = m[g]; }
+                    }
+                    if (c + 1 == W) {
+                        held = wsum(held);
+                        const unsigned long long mn = wmin64(bk);
+                        int hs = kNoHol;
+                        uint32_t hw = 0, hm = 0;
+                        if (mn != kNone) {
+                            const int wl = ffs64(ballot(bk == mn));
+                            hs = rl(bs, wl);
+                            hw = rlu(bv, wl);
+                            hm = rlu(bm, wl);
+                        }
+                        if (lane == 0) {
+                            C.B[i] = nB; C.live[i] = nlive; C.nwait[i] = nw;
+                            C.held[i] = held;
+                            if (hs >= 0) set_hol(C, int(i), hs, mn, hw, hm, 0u);
+                            else clear_hol(C, int(i));
+                            int tm = 0;
+                            for (int p = 0; p < kTiers; ++p) tm |= c16_get(C.tcnt, i * kTiers + p) ? (1 << p) : 0;
+                            C.tmask[i] = tm;
+                        }
+                        wave_sync();
+                        nB = 0; nlive = 0; nw = 0; held = 0;
+                        bk = kNone; bs = 0; bv = 0; bm = 0;
+                    }
                 }
             }
-            held = wsum(held);
-            const unsigned long long mn = wmin64(bk);
-            int hs = kNoHol;
-            uint32_t hw = 0, hm = 0, ht = 0;
-            if (mn != kNone) {
-                const int wl = ffs64(ballot(bk == mn));
-                hs = rl(bs, wl);
-                hw = rlu(bv, wl);
-                hm = rlu(bm, wl);
-                ht = rlu(lane == wl ? C.tarr[b + bs] : 0u, wl);
+            for (uint32_t i = lane; i < I; i += 64) {
+                const int h = C.hols[i];
+                if (h >= 0) C.hta[i] = C.tarr[size_t(i) * S + h];
             }
-            if (lane == 0) {
-                C.B[i] = nB; C.live[i] = nlive; C.nwait[i] = nw;
-                C.held[i] = held;
-                if (hs >= 0) set_hol(C, int(i), hs, mn, hw, hm, ht);
-                else clear_hol(C, int(i));
-                int tm = 0;
-                for (int p = 0; p < kTiers; ++p) tm |= c16_get(C.tcnt, i * kTiers + p) ? (1 << p) : 0;
-                C.tmask[i] = tm;
-            }
-            wave_sync();
         }
         unsigned next_seq = P.next_seq[r];
         uint32_t run_acc = 0, wait_acc = 0;  // per lane, at most 1024 ticks x 4 x 2048
