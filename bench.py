@@ -32,7 +32,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 # copy, keyed by the SHA-256 prefix of the step-kernel source they were taken
 # on; any other kernel source reports null.
 MEASURED_TRAFFIC = {
-    "a3aaf58a0605a62b": 1.0055e10,
+    "b80343d1b59c1061": 2.9082e10,
 }
 
 
