@@ -896,10 +896,12 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
 {
     const size_t b = size_t(i) * C.S;
     const int nch = live_chunks(C, i, lane);
+    // per lane: its MK smallest keys, ascending, each with slot | demand << 12
+    // (slot < 4096, demand < 2^16 blocks)
     unsigned long long k[MK];
-    int ks[MK], kd[MK];
+    uint32_t sd[MK];
 #pragma unroll
-    for (int x = 0; x < MK; ++x) { k[x] = kNone; ks[x] = 0; kd[x] = 0; }
+    for (int x = 0; x < MK; ++x) { k[x] = kNone; sd[x] = 0; }
     int cnt = 0;
     for (int c0 = 0; c0 < nch; c0 += GR) {
         uint32_t v[GR], m[GR], q[GR];
@@ -916,46 +918,51 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
             ++cnt;
             unsigned long long ck = (rank_of(C, (m[g] >> 2) & 15u) << 32) | q[g];
             if (ck >= k[MK - 1]) continue;
-            int cs = (c0 + g) * 64 + lane, cd = blocks_of(wlo(v[g]), C.shift);
+            uint32_t cs = uint32_t((c0 + g) * 64 + lane) | (uint32_t(blocks_of(wlo(v[g]), C.shift)) << 12);
             // insertion into the lane's sorted list (the largest drops out)
 #pragma unroll
             for (int x = 0; x < MK; ++x) {
                 if (ck < k[x]) {
                     const unsigned long long tk = k[x]; k[x] = ck; ck = tk;
-                    const int ts = ks[x]; ks[x] = cs; cs = ts;
-                    const int tdm = kd[x]; kd[x] = cd; cd = tdm;
+                    const uint32_t ts = sd[x]; sd[x] = cs; cs = ts;
                 }
             }
         }
     }
+    // rank extraction, branch-free per round: the winning lane's list moves up
     const int fr = C.freeb[i];
     unsigned long long myk = kNone;
-    int mys = 0, got = 0, taken = 0, cum = 0, lim = 64;
+    uint32_t mysd = 0;
+    int got = 0, taken = 0, cum = 0, lim = 64;
+    const bool more = cnt > MK;
     for (int r = 0; r < lim; ++r) {
         const unsigned long long mn = wmin64(k[0]);
         if (mn == kNone) break;
         const int wl = ffs64(ballot(k[0] == mn));
-        if (lane == r) { myk = mn; mys = rl(ks[0], wl); }
+        const uint32_t wsd = rlu(sd[0], wl);
+        myk = lane == r ? mn : myk;
+        mysd = lane == r ? wsd : mysd;
         got = r + 1;
-        cum += rl(kd[0], wl);
+        cum += int(wsd >> 12);
         // the first request that does not fit is the new head of line; the
         // cache takes the qdepth after it
         if (cum > fr && lim == 64) lim = min(64, r + 1 + C.td);
-        bool unknown = false;
-        if (lane == wl) {
+        const bool win = lane == wl;
 #pragma unroll
-            for (int x = 0; x + 1 < MK; ++x) { k[x] = k[x + 1]; ks[x] = ks[x + 1]; kd[x] = kd[x + 1]; }
-            k[MK - 1] = kNone;
-            ++taken;
-            unknown = taken >= MK && cnt > MK;
+        for (int x = 0; x + 1 < MK; ++x) {
+            k[x] = win ? k[x + 1] : k[x];
+            sd[x] = win ? sd[x + 1] : sd[x];
         }
-        if (ballot(unknown)) break;
+        k[MK - 1] = win ? kNone : k[MK - 1];
+        taken += win ? 1 : 0;
+        if (ballot(win && more && taken >= MK)) break;  // the winner's next key is unknown
     }
     if (got == 0) {
         if (lane == 0) clear_hol(C, i);
         wave_sync();
         return false;
     }
+    const int mys = int(mysd & 0xFFFu);
     uint32_t w = 0, mt = 0, ta = 0;
     if (lane < got) { w = C.hot[b + mys]; mt = C.meta[b + mys]; ta = C.tarr[b + mys]; }
     const bool complete = got >= C.nwait[i];
