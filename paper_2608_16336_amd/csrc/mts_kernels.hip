@@ -1889,32 +1889,83 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         avm[j] = ballot(av);
                         n2 += __popcll(avm[j]);
                     }
-                    int rk[IPL];
+                    // Pairs stop at the first source that is neither draining nor
+                    // below zero freeness, so with nneg such instances only L[0..nneg]
+                    // and L[n2 - 1 - nneg .. n2 - 1] are ever read.  The kernels for
+                    // 128+ instances take just those ends by repeated wave minima and
+                    // maxima when they are disjoint; otherwise every rank is counted.
+                    int nneg = 0;
 #pragma unroll
-                    for (int j = 0; j < IPL; ++j) rk[j] = 0;
+                    for (int j = 0; j < IPL; ++j) {
+                        const uint32_t i = lane + 64 * j;
+                        nneg += __popcll(avm[j] & ballot(i < I && (C.num[i] < 0 || C.drn[i])));
+                    }
+                    int npairs = min(int(P.mig_max_pairs), n2 / 2);
+                    if (IM >= 128 && 2 * (nneg + 1) <= n2 && nneg + 1 < npairs) {
+                        unsigned long long lo[IPL], hi[IPL];
 #pragma unroll
-                    for (int jj = 0; jj < IPL; ++jj) {
-                        for (unsigned long long mm = avm[jj]; mm; mm &= mm - 1) {
-                            const int l = ffs64(mm);
-                            const unsigned long long kl = rl64(fk[jj], l);
-                            const int il = 64 * jj + l;
+                        for (int j = 0; j < IPL; ++j) {
+                            const bool av = (avm[j] >> lane) & 1ull;
+                            lo[j] = av ? fk[j] : kNone;  // no key reaches either bound
+                            hi[j] = av ? fk[j] : 0ull;
+                        }
+                        for (int k = 0; k <= nneg; ++k) {
+                            // k-th in (F, index) order: smallest key, lowest index
+                            unsigned long long lb = lo[0];
+#pragma unroll
+                            for (int j = 1; j < IPL; ++j) lb = tmin(lb, lo[j]);
+                            const unsigned long long mn = wmin64(lb);
+                            int idx = -1;
 #pragma unroll
                             for (int j = 0; j < IPL; ++j) {
-                                const int i = lane + 64 * j;
-                                rk[j] += (kl < fk[j] || (kl == fk[j] && il < i)) ? 1 : 0;
+                                const unsigned long long bm = ballot(lo[j] == mn);
+                                if (idx < 0 && bm) idx = 64 * j + ffs64(bm);
+                            }
+#pragma unroll
+                            for (int j = 0; j < IPL; ++j) lo[j] = lane + 64 * j == idx ? kNone : lo[j];
+                            // (n2 - 1 - k)-th: largest key, highest index
+                            unsigned long long hb = hi[0];
+#pragma unroll
+                            for (int j = 1; j < IPL; ++j) hb = tmax(hb, hi[j]);
+                            const unsigned long long mx = wmax64(hb);
+                            int hdx = -1;
+#pragma unroll
+                            for (int j = IPL - 1; j >= 0; --j) {
+                                const unsigned long long bm = ballot(hi[j] == mx);
+                                if (hdx < 0 && bm) hdx = 64 * j + 63 - __clzll(static_cast<long long>(bm));
+                            }
+#pragma unroll
+                            for (int j = 0; j < IPL; ++j) hi[j] = lane + 64 * j == hdx ? 0ull : hi[j];
+                            if (lane == 0) { C.order[k] = idx; C.order[n2 - 1 - k] = hdx; }
+                        }
+                        npairs = nneg + 1;
+                    } else {
+                        int rk[IPL];
+#pragma unroll
+                        for (int j = 0; j < IPL; ++j) rk[j] = 0;
+#pragma unroll
+                        for (int jj = 0; jj < IPL; ++jj) {
+                            for (unsigned long long mm = avm[jj]; mm; mm &= mm - 1) {
+                                const int l = ffs64(mm);
+                                const unsigned long long kl = rl64(fk[jj], l);
+                                const int il = 64 * jj + l;
+#pragma unroll
+                                for (int j = 0; j < IPL; ++j) {
+                                    const int i = lane + 64 * j;
+                                    rk[j] += (kl < fk[j] || (kl == fk[j] && il < i)) ? 1 : 0;
+                                }
                             }
                         }
-                    }
 #pragma unroll
-                    for (int j = 0; j < IPL; ++j)
-                        if ((avm[j] >> lane) & 1ull) C.order[rk[j]] = lane + 64 * j;
+                        for (int j = 0; j < IPL; ++j)
+                            if ((avm[j] >> lane) & 1ull) C.order[rk[j]] = lane + 64 * j;
+                    }
                     wave_sync();
                     // Pairs (L[k], L[n2 - 1 - k]) use disjoint instances and one
                     // snapshot of F, so the stopping pair is found for all pairs at
                     // once (lane k tests pair k), the queued moves of the pairs
                     // before it run in parallel, and only the staged copies, which
                     // scan a source's slots with the whole wave, go one at a time.
-                    const int npairs = min(int(P.mig_max_pairs), n2 / 2);
                     for (int k0 = 0; k0 < npairs; k0 += 64) {
                         const int k = k0 + lane;
                         const bool in = k < npairs;

@@ -749,3 +749,48 @@ def test_extension_state_export_import_resumes_exactly():
     bad["hq"][9] = 5  # the lowest of 10 tiers under zero_lowest_tier
     with pytest.raises(MtsError):
         h2.import_state(bad)
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_large_clusters_pairing_ends(case):
+    # Clusters of 65..256 instances, overloaded so that many instances are
+    # below zero freeness: pairing reads only the two ends of the (F, index)
+    # order, which the kernels for 128+ instances take by wave minima and
+    # maxima when they are disjoint (Section 3.5); pair caps from 1 to I/2,
+    # thresholds 0 and 3/10, some instances draining.
+    rng = random.Random(12000 + case)
+    I = [65, 96, 128, 129, 200, 256][case % 6]
+    c = preset("tiny")
+    c.update(n_instances=I, slots_per_instance=rng.choice([64, 128]), kv_blocks=rng.choice([64, 256]),
+             block_tokens=16, headroom_base=rng.choice([0.0, 40.0]), headroom_decay=0.6,
+             mig_interval=1, mig_stage_blocks=rng.choice([2, 32]),
+             mig_max_pairs=rng.choice([1, 2, I // 4, I // 2]), theta_num=rng.choice([0, 3]), theta_den=10,
+             arrival=dict(kind="poisson", mean=float(rng.choice([I // 2, 2 * I]))),
+             prompt=dict(kind="uniform_int", lo=16, hi=rng.choice([400, 2000])),
+             output=dict(kind="geometric", mean=rng.choice([30.0, 120.0])),
+             groups=[dict(n_replicas=2, K=rng.randint(1, 10), tiers=dict(kind="uniform"))],
+             seed=rng.randrange(2**63), replica_id_base=rng.randrange(1000))
+    g = Scheduler(c)
+    orc = [oracle.Oracle(c, r, 1) for r in range(g.R)]
+    g.step(60)
+    for o in orc:
+        o.step(60)
+    if case % 3 == 0:
+        flags = np.zeros((g.R, I), np.uint8)
+        drained = rng.sample(range(I), 5)
+        flags[:, drained] = 1
+        g.set_draining(flags)
+        for o in orc:
+            for i in drained:
+                o.set_drain(0, i, True)
+    g.step(90)
+    for o in orc:
+        o.step(90)
+    moved = 0
+    for r, o in enumerate(orc):
+        e = o.export()
+        assert_same(g.export(r, 1), e, "case %d replica %d" % (case, r))
+        assert np.array_equal(g.digests(r, 1), o.digests())
+        moved += int(e["stats"][80:82].sum())
+    assert moved > 0, "no migration started"
+    assert g.stats()["raw"][86] == 0
