@@ -581,71 +581,115 @@ __device__ inline void wheel_erase(const Ctx& C, uint32_t fin, int i, int s, int
 
 // memory pressure: preempt the largest (tier, seq) running request until the
 // growth of this tick fits (Section 2.2; recompute semantics)
+template <int GR, int MK>
 __device__ inline bool preempt(const Ctx& C, int i, uint32_t t, int lane)
 {
     const size_t b = size_t(i) * C.S;
     int G = C.gtmp[i], fr = C.freeb[i];
     bool aborted = false;
-    while (G > fr) {
+    bool scan = G > fr;
+    while (scan) {
+        // Each lane keeps the MK largest (tier, seq) keys of its running slots,
+        // descending, with the slot, its word and its meta (a running
+        // request's word and meta do not change while it runs); GR chunks of
+        // 64 slots are read per memory round trip.
         const int nch = live_chunks(C, i, lane);
-        unsigned long long bk = 0;
-        int bs = 0;
-        for (int c = 0; c < nch; ++c) {
-            const int s = c * 64 + lane;
-            const uint32_t v = C.hot[b + s];
-            if (wst(v) == 2u) {
-                const unsigned long long k = ((rank_of(C, (C.meta[b + s] >> 2) & 15u) + 1ull) << 32) | C.seq[b + s];
-                if (k > bk) { bk = k; bs = s; }
+        unsigned long long k[MK];
+        uint32_t kw[MK], km[MK];
+        int ks[MK];
+#pragma unroll
+        for (int x = 0; x < MK; ++x) { k[x] = 0; kw[x] = 0; km[x] = 0; ks[x] = 0; }
+        int cnt = 0;
+        for (int c0 = 0; c0 < nch; c0 += GR) {
+            uint32_t v[GR], m[GR], q[GR];
+#pragma unroll
+            for (int g = 0; g < GR; ++g) {
+                const bool in = c0 + g < nch;
+                v[g] = in ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
+                m[g] = in ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
+                q[g] = in ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
+            }
+#pragma unroll
+            for (int g = 0; g < GR; ++g) {
+                if (wst(v[g]) != 2u) continue;
+                ++cnt;
+                unsigned long long ck = ((rank_of(C, (m[g] >> 2) & 15u) + 1ull) << 32) | q[g];
+                if (ck <= k[MK - 1]) continue;
+                uint32_t cw = v[g], cm = m[g];
+                int cs = (c0 + g) * 64 + lane;
+#pragma unroll
+                for (int x = 0; x < MK; ++x) {
+                    if (ck > k[x]) {
+                        const unsigned long long tk = k[x]; k[x] = ck; ck = tk;
+                        const uint32_t tw = kw[x]; kw[x] = cw; cw = tw;
+                        const uint32_t tm = km[x]; km[x] = cm; cm = tm;
+                        const int ts = ks[x]; ks[x] = cs; cs = ts;
+                    }
+                }
             }
         }
-        const unsigned long long mx = wmax64(bk);
-        if (mx == 0) break;
-        const int vs = rl(bs, ffs64(ballot(bk == mx)));
-        const int owner = vs & 63;
-        int vb = 0, vg = 0, vt = 0, vr = 0, vm = 0;
-        uint32_t vw = 0, vmeta = 0, vta = 0, vfin = 0;
-        if (lane == owner) {
-            const uint32_t v = C.hot[b + vs];
+        const bool more = cnt > MK;
+        int taken = 0;
+        scan = false;
+        while (G > fr) {
+            const unsigned long long mx = wmax64(k[0]);
+            if (mx == 0) break;  // nothing runs
+            const int wl = ffs64(ballot(k[0] == mx));
+            const int vs = rl(ks[0], wl);
+            const uint32_t v = rlu(kw[0], wl), m = rlu(km[0], wl);
+            const bool win = lane == wl;
+#pragma unroll
+            for (int x = 0; x + 1 < MK; ++x) {
+                k[x] = win ? k[x + 1] : k[x];
+                kw[x] = win ? kw[x + 1] : kw[x];
+                km[x] = win ? km[x + 1] : km[x];
+                ks[x] = win ? ks[x + 1] : ks[x];
+            }
+            k[MK - 1] = win ? 0ull : k[MK - 1];
+            taken += win ? 1 : 0;
+            const bool unknown = ballot(win && more && taken >= MK) != 0;
+            // the victim returns to the queue (recompute semantics: len, rem and
+            // seq kept, its blocks freed)
             const uint32_t lenf = wlo(v), fin = fin_of(v, t);
             const uint32_t remb = fin - t + 1u, lenb = lenf - remb;
-            vfin = fin;
-            vw = kWaitW | (remb << 16) | lenb;
-            C.hot[b + vs] = vw;
-            const uint32_t m = C.meta[b + vs];
-            vmeta = (m & ~(3u | kMigrating)) | kWaiting;
-            C.meta[b + vs] = uint8_t(vmeta);
-            vta = C.tarr[b + vs];
-            vb = blocks_of(lenb, C.shift);
-            vg = (lenb & C.bmask) == 0;
-            vt = int((m >> 2) & 15u);
-            vr = int((lenf - fin - 1u) & C.bmask);
-            vm = (m & kMigrating) ? 1 : 0;
+            const uint32_t vw = kWaitW | (remb << 16) | lenb;
+            const uint32_t vmeta = (m & ~(3u | kMigrating)) | kWaiting;
+            const int vb = blocks_of(lenb, C.shift);
+            const int vg = (lenb & C.bmask) == 0;
+            const int vt = int((m >> 2) & 15u);
+            const int vr = int((lenf - fin - 1u) & C.bmask);
+            const bool vm = (m & kMigrating) != 0;
+            uint32_t vta = 0;
+            if (lane == (vs & 63)) {
+                C.hot[b + vs] = vw;
+                C.meta[b + vs] = uint8_t(vmeta);
+                vta = C.tarr[b + vs];
+            }
+            vta = rlu(vta, vs & 63);
+            wheel_erase(C, fin, i, vs, lane);
+            fr += vb;
+            G -= vg;
+            aborted = aborted || vm;
+            if (lane == 0) {
+                C.held[i] -= vb;
+                C.B[i] -= 1;
+                C.nwait[i] += 1;
+                C.frs[i] = 0;
+                C.flags[i] |= kFlagIntf;
+                const int nv = *C.nvic;
+                if (nv < kVic) C.vic[nv] = (uint32_t(i) << 16) | uint32_t(vs);
+                *C.nvic = nv < kVic ? nv + 1 : kVic + 1;
+                c16_dec(C.res, res_idx(C, i, vr));
+                tier_dec(C, i, vt);
+                stat(C, vt * 8 + kPreempted, 1);
+                if (vm) C.flags[i] |= kFlagAbort;
+                const unsigned long long key = (rank_of(C, uint32_t(vt)) << 32) | static_cast<unsigned>(mx);
+                hol_insert(C, i, key, vs, vw, vmeta, vta);
+                if (C.ext) wlb(C)[i] = vta < wlb(C)[i] ? vta : wlb(C)[i];
+            }
+            wave_sync();
+            if (unknown) { scan = G > fr; break; }  // the winner's next key is unknown: read again
         }
-        vb = rl(vb, owner); vg = rl(vg, owner); vt = rl(vt, owner); vr = rl(vr, owner); vm = rl(vm, owner);
-        vw = rlu(vw, owner); vmeta = rlu(vmeta, owner); vta = rlu(vta, owner);
-        vfin = rlu(vfin, owner);
-        wheel_erase(C, vfin, i, vs, lane);
-        fr += vb;
-        G -= vg;
-        aborted = aborted || vm != 0;
-        if (lane == 0) {
-            C.held[i] -= vb;
-            C.B[i] -= 1;
-            C.nwait[i] += 1;
-            C.frs[i] = 0;
-            C.flags[i] |= kFlagIntf;
-            const int nv = *C.nvic;
-            if (nv < kVic) C.vic[nv] = (uint32_t(i) << 16) | uint32_t(vs);
-            *C.nvic = nv < kVic ? nv + 1 : kVic + 1;
-            c16_dec(C.res, res_idx(C, i, vr));
-            tier_dec(C, i, vt);
-            stat(C, vt * 8 + kPreempted, 1);
-            if (vm) C.flags[i] |= kFlagAbort;
-            const unsigned long long key = (rank_of(C, uint32_t(vt)) << 32) | static_cast<unsigned>(mx);
-            hol_insert(C, i, key, vs, vw, vmeta, vta);
-            if (C.ext) wlb(C)[i] = vta < wlb(C)[i] ? vta : wlb(C)[i];
-        }
-        wave_sync();
     }
     // this tick's growth, now that it fits
     if (lane == 0) { C.freeb[i] = fr - G; C.held[i] += G; }
@@ -1376,7 +1420,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
 #pragma unroll
                 for (int j = 0; j < IPL; ++j)
                     for (unsigned long long m = pre[j]; m; m &= m - 1)
-                        abort_any = preempt(C, 64 * j + ffs64(m), t, lane) || abort_any;
+                        abort_any = preempt<(IM >= 128 ? 16 : 4), (IM >= 128 ? 4 : 2)>(C, 64 * j + ffs64(m), t, lane) || abort_any;
             }
             // a preempted request is waiting now: its prefetched entries (for this
             // tick's and the next tick's visit) are dropped (its wheel entry was
