@@ -1653,7 +1653,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 for (uint32_t k0 = 0; k0 < n; k0 += 64) {
                     const uint32_t cn = n - k0 < 64 ? n - k0 : 64;
                     const unsigned long long a = k0 == 0 ? a0 : (lane < int(cn) ? rec[k0 + lane] : 0);
-                    int tgt = -1;
+                    int tgt = -1, rank = 0;  // rank: among this batch's arrivals bound for tgt
                     uint32_t k = 0;
                     while (k < cn && !full) {
                         if (cur < 0) {
@@ -1686,11 +1686,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             }
                         }
                         const int jc = cur >> 6, lc = cur & 63;
-                        int lv = 0;
+                        int lv = 0, na0 = 0;
                         unsigned long long hkc = 0;
 #pragma unroll
                         for (int j = 0; j < IPL; ++j)
-                            if (j == jc) { lv = rl(live_r[j], lc); hkc = rl64(hk_r[j], lc); }
+                            if (j == jc) { lv = rl(live_r[j], lc); hkc = rl64(hk_r[j], lc); na0 = rl(nadd[j], lc); }
                         const unsigned long long ak = rl64(a, int(k));
                         const unsigned long long hk = rank_of(C, uint32_t(ak >> 32) & 15u) << 32 | (seq0 + unsigned(ak >> 36));
                         const bool becomes = hk < hkc;
@@ -1723,7 +1723,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                                 if (nl >= int(S)) key[j] = -__builtin_inf();
                             }
                         }
-                        if (lane >= int(k) && lane < int(k) + m) tgt = cur;
+                        if (lane >= int(k) && lane < int(k) + m) { tgt = cur; rank = na0 + lane - int(k); }
                         if (step1 || nl >= int(S)) cur = -1;
                         if (drain_mode) nfall += m;
                         k += uint32_t(m);
@@ -1765,13 +1765,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     wave_sync();
                     // slot assignment: the arrivals bound for one instance take its
                     // lowest empty slots in arrival order
-                    int rank = 0;
-                    for (unsigned long long pend = ballot(tgt >= 0); pend;) {
-                        const int tv = rl(tgt, ffs64(pend));
-                        const unsigned long long same = ballot(tgt == tv);
-                        if (tgt == tv) rank = __popcll(same & lanemask_lt());
-                        pend &= ~same;
-                    }
                     const int tier = int((a >> 32) & 15u);
                     int s = -1;
                     if (tgt >= 0) {
