@@ -45,13 +45,13 @@ def test_state_bytes(name):
     R = sum(g["n_replicas"] for g in c["groups"])
     n_slots = R * c["n_instances"] * c["slots_per_instance"]
     b = mts.mts_state_bytes(c)
-    # slot arrays (13 B per slot), at most 512 MiB of pre-sampled arrivals, a
+    # slot arrays (13 B per slot), at most 2 GiB of pre-sampled arrivals, a
     # finish wheel of at most 512 buckets per replica and small tables
     a = c["arrival"]
     cv = a.get("cv", 0.0) if a["kind"] == "gamma_poisson" else 0.0
     wcap = min(2048, math.ceil((2 * a["mean"] * (1 + cv) + 24) / 16) * 16)
     wheel = R * 512 * wcap * 4 + 2**20
-    assert 13 * n_slots <= b < 13 * n_slots + wheel + 600 * 2**20
+    assert 13 * n_slots <= b < 13 * n_slots + wheel + 2136 * 2**20
 
 
 def _bad(**over):
