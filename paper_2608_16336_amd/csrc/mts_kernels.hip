@@ -2096,8 +2096,6 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 wave_sync();
             }
 
-            // ===================== end of tick =====================
-            if (lane == 0) C.stats[kTicks] += 1;
         }
 
         // ---------------- epilogue ----------------
@@ -2105,6 +2103,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         if (lane == 0) {
             C.stats[kRunSlotTicks] += run_sum;
             C.stats[kWaitSlotTicks] += wait_sum;
+            C.stats[kTicks] += nt;
         }
         wave_sync();
         for (int j = lane; j < kNstat; j += 64) P.stats[size_t(r) * kNstat + j] = C.stats[j];
