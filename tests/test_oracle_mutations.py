@@ -108,6 +108,14 @@ MUTATIONS = {
                              "h = h < c->adapt_up ? 0 : h - c->adapt_up;")],
     # Section 6.5 adaptive headroom: the lowest tier adapts under zero_lowest
     "adapt_lowest_tier": [("if ((c->zero_lowest && p == K - 1) || a == 0) continue;", "if (a == 0) continue;")],
+    # Section 4.4 workloads: prompt lengths drawn from the output table and output
+    # lengths from the prompt table
+    "length_tables_swapped": [
+        ("a[1] = x->prompt_tab.base + sample(&x->prompt_tab, (uint32_t)r[1]);\n        a[2] = x->out_tab.base + sample(&x->out_tab, (uint32_t)r[2]);",
+         "a[1] = x->out_tab.base + sample(&x->out_tab, (uint32_t)r[1]);\n        a[2] = x->prompt_tab.base + sample(&x->prompt_tab, (uint32_t)r[2]);")],
+    # the output length drawn from the prompt's random word (correlated lengths)
+    "length_shared_word": [("a[2] = x->out_tab.base + sample(&x->out_tab, (uint32_t)r[2]);",
+                            "a[2] = x->out_tab.base + sample(&x->out_tab, (uint32_t)r[1]);")],
     # Section 6.5 adaptive headroom: counters never re-based (cumulative means)
     "adapt_cumulative": [("        rp->snap_adm[p] = adm;\n        rp->snap_qd[p] = qd;\n", "")],
 }
@@ -127,6 +135,7 @@ def test_mutation_is_caught(name, tmp_path):
     env = dict(os.environ, MTS_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_sampling_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_drain_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_hist_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_infaas_pins.py"),
