@@ -180,7 +180,8 @@ enum { MTS_POLICY_LLUMNIX = 0, MTS_POLICY_INFAAS = 1 };
 /* Counters summed over all replicas (mts_stats) or per replica
  * (mts_export_state).  Index layout of the raw arrays: per_tier[p][f] is
  * element p * 8 + f, the scalar counters follow at 80..90 in the order of
- * the fields below, 91..95 are zero. */
+ * the fields below, 91..95 are zero in the canonical state (the device keeps
+ * a diagnostic at 91, see mts_get_wheel). */
 enum { MTS_F_ARRIVED = 0, MTS_F_REJECTED, MTS_F_DISPATCHED, MTS_F_ADMITTED,
        MTS_F_FINISHED, MTS_F_PREEMPTED, MTS_F_QDELAY_SUM, MTS_F_E2E_SUM };
 typedef struct mts_stats_t {
@@ -346,6 +347,20 @@ int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks);
  * mts_step; MTS_EINVAL for a depth above 15 or one whose LDS does not fit. */
 int mts_set_queue_cache(mts_handle h, uint32_t depth);
 int mts_get_queue_cache(mts_handle h, uint32_t* depth);
+
+/* Finish wheel of the step kernel (a test hook): every running request is
+ * filed under its finish tick in a per-replica wheel of buckets holding up to
+ * `cap` entries each; a bucket that fills is rebuilt at its visit by an exact
+ * scan of the slots, so results never depend on the capacity.  mts_create
+ * picks cap_max from the arrival rate; mts_set_wheel_cap lowers it (1 ..
+ * cap_max, else MTS_EINVAL) from the next mts_step on, so that tests reach the
+ * rebuild.  mts_get_wheel reports the capacity in use, the reserved one and
+ * the number of bucket rebuilds summed over the replicas (a device counter
+ * kept at index 91 of the per-replica counters; it is not part of the
+ * canonical state: mts_export_state reports it as 0 and mts_import_state
+ * resets it).  Any pointer may be NULL. */
+int mts_set_wheel_cap(mts_handle h, uint32_t cap);
+int mts_get_wheel(mts_handle h, uint32_t* cap, uint32_t* cap_max, uint64_t* rebuilds);
 
 /* Kernel timing with HIP events recorded on the launch stream (off by
  * default; costs three events per chunk of ticks).  With on = 1, every later

@@ -25,6 +25,7 @@ struct mts_ctx {
     uint64_t seq_bound = 0;            // no replica's sequence counter exceeds this
     uint32_t chunk = 0;                // ticks per arrival batch
     uint32_t wsz = 0, wcap = 0;        // finish wheel: buckets, entries per bucket
+    uint32_t wcap_max = 0;             // entries per bucket the layout reserves
     uint32_t blocks = 0;               // step-kernel blocks (one wave each); 0 = automatic
     uint32_t qdepth = 0;               // queue-cache entries per instance (chosen at create)
     int device = 0;
@@ -247,6 +248,7 @@ int prepare(const mts_cfg* cfg, mts_ctx& x)
     x.arr_cap = uint32_t(x.tables.count.base + x.tables.count.q.size());
     x.chunk = chunk_for(x.R, x.arr_cap);
     wheel_size(x.cfg, x.tables, x.wsz, x.wcap);
+    x.wcap_max = x.wcap;
     x.lay = make_layout(x.cfg, x.tables, x.R, x.chunk, x.arr_cap, x.wsz, x.wcap);
     return MTS_OK;
 }
@@ -567,6 +569,9 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     get(v->mig, L.mig + size_t(r0) * I * 16, size_t(nr) * I * 16);
     get(v->next_seq, L.next_seq + size_t(r0) * 4, size_t(nr) * 4);
     get(v->stats, L.stats + size_t(r0) * MTS_NSTAT * 8, size_t(nr) * MTS_NSTAT * 8);
+    // device diagnostics are not part of the canonical state
+    if (e == hipSuccess && v->stats)
+        for (uint32_t r = 0; r < nr; ++r) v->stats[size_t(r) * MTS_NSTAT + kWheelRebuilds] = 0;
     get(v->drain, L.drain + size_t(r0) * I, size_t(nr) * I);
     get(v->hist, L.hist + size_t(r0) * kHistPerReplica * 4, size_t(nr) * kHistPerReplica * 4);
     get(v->svc, L.svc + size_t(r0) * I * 8, size_t(nr) * I * 8);
@@ -731,6 +736,33 @@ int mts_set_tick(mts_handle h, uint64_t tick)
     if (launch_shift_clock(p, uint32_t(tick - h->tick), h->last) != 0) return MTS_EDEVICE;
     if (hipStreamSynchronize(h->last) != hipSuccess) return MTS_EDEVICE;
     h->tick = tick;
+    return MTS_OK;
+}
+
+int mts_set_wheel_cap(mts_handle h, uint32_t cap)
+{
+    if (!h || cap == 0 || cap > h->wcap_max) return MTS_EINVAL;
+    // every step-kernel launch files the running requests into the wheel
+    // afresh, so the capacity can change between steps
+    if (hipStreamSynchronize(h->last) != hipSuccess) return MTS_EDEVICE;
+    h->wcap = cap;
+    return MTS_OK;
+}
+
+int mts_get_wheel(mts_handle h, uint32_t* cap, uint32_t* cap_max, uint64_t* rebuilds)
+{
+    if (!h) return MTS_EINVAL;
+    if (cap) *cap = h->wcap;
+    if (cap_max) *cap_max = h->wcap_max;
+    if (rebuilds) {
+        std::vector<uint64_t> st(size_t(h->R) * MTS_NSTAT);
+        hipError_t e = hipStreamSynchronize(h->last);
+        if (e == hipSuccess) e = hipMemcpy(st.data(), h->dev + h->lay.stats, st.size() * 8, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return MTS_EDEVICE;
+        uint64_t n = 0;
+        for (uint32_t r = 0; r < h->R; ++r) n += st[size_t(r) * MTS_NSTAT + kWheelRebuilds];
+        *rebuilds = n;
+    }
     return MTS_OK;
 }
 

@@ -32,6 +32,9 @@ constexpr int kArrived = 0, kRejected = 1, kDispatched = 2, kAdmittedCnt = 3, kF
 constexpr int kMigQueued = 80, kMigStarted = 81, kMigCommitted = 82, kMigAborted = 83,
               kRunSlotTicks = 84, kWaitSlotTicks = 85, kInvariant = 86, kTicks = 87,
               kScaleOut = 88, kScaleIn = 89, kDrainFallback = 90;
+// device diagnostic, not part of the canonical state: finish-wheel buckets
+// rebuilt by a scan after they overflowed
+constexpr int kWheelRebuilds = 91;
 // latency histograms: queue delay and end-to-end, per tier
 constexpr int kHistQdelay = 0, kHistE2e = 1;
 constexpr size_t kHistPerReplica = size_t(2) * MTS_MAX_TIERS * MTS_HIST_BINS;
@@ -129,5 +132,6 @@ int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t bl
 int step_blocks_per_cu(const Params& p);
 int launch_digest(const Params& p, uint32_t r0, uint32_t nr, uint32_t tick, hipStream_t stream);
 int launch_shift_clock(const Params& p, uint32_t delta, hipStream_t stream);
+
 
 }  // namespace mts

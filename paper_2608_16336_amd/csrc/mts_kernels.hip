@@ -725,7 +725,9 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane, bo
             if (C.fsum) { atomicAdd(&C.fsum[i], static_cast<unsigned long long>(e2e)); atomicAdd(&C.fcnt[i], 1); }
             c16_dec(C.res, res_idx(C, i, (lenf - t - 1u) & C.bmask));
             tier_dec(C, i, tier);
-            if (m & kMigrating) ab = true;
+            // being copied out: the source of its instance's migration record
+            // (the same test as the wheel visit's)
+            if (C.mig[4 * i] >= 0 && C.mig[4 * i + 1] == s) ab = true;
             C.hot[b + s] = 0;  // the word alone marks the slot empty
         } else if (run && (fin & C.wmask) == bk) {
             wheel_put(C, fin, i, s);
@@ -814,6 +816,7 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane, bool& abo
         if (lane == 0) {
             C.wc[bk >> 1] &= ~(0xFFFFu << sh);
             C.wov[bk >> 5] &= ~(1u << (bk & 31u));
+            stat(C, kWheelRebuilds, 1);
         }
         wave_sync();
         for (uint32_t j = 0; j < (C.I + 63) / 64; ++j) {

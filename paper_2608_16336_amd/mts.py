@@ -89,7 +89,7 @@ EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_diges
             "mts_export_state", "mts_import_state", "mts_get_table", "mts_get_headroom",
             "mts_tick", "mts_set_tick", "mts_set_launch", "mts_get_launch", "mts_set_timing",
             "mts_get_timing", "mts_set_draining", "mts_set_queue_cache", "mts_get_queue_cache",
-            "mts_destroy", "mts_strerror")
+            "mts_set_wheel_cap", "mts_get_wheel", "mts_destroy", "mts_strerror")
 
 _lib = None
 
@@ -123,6 +123,8 @@ def load_library(path=LIB_PATH):
     L.mts_set_draining.argtypes = [vp, u32, u32, vp]
     L.mts_set_queue_cache.argtypes = [vp, u32]
     L.mts_get_queue_cache.argtypes = [vp, ctypes.POINTER(u32)]
+    L.mts_set_wheel_cap.argtypes = [vp, u32]
+    L.mts_get_wheel.argtypes = [vp, ctypes.POINTER(u32), ctypes.POINTER(u32), ctypes.POINTER(u64)]
     L.mts_get_timing.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                  ctypes.POINTER(u32)]
     L.mts_destroy.argtypes = [vp]
@@ -132,7 +134,7 @@ def load_library(path=LIB_PATH):
     for f in ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest", "mts_export_state",
               "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch", "mts_get_launch",
               "mts_set_timing", "mts_get_timing", "mts_set_draining", "mts_set_queue_cache",
-              "mts_get_queue_cache"):
+              "mts_get_queue_cache", "mts_set_wheel_cap", "mts_get_wheel"):
         getattr(L, f).restype = ci
     _lib = L
     return L
@@ -336,6 +338,17 @@ class Scheduler:
     @queue_cache.setter
     def queue_cache(self, depth):
         _check("mts_set_queue_cache", load_library().mts_set_queue_cache(self._h, depth))
+
+    def set_wheel_cap(self, cap):
+        """Entries per finish-wheel bucket from the next step on (test hook)."""
+        _check("mts_set_wheel_cap", load_library().mts_set_wheel_cap(self._h, cap))
+
+    def wheel(self):
+        """(capacity in use, reserved capacity, bucket rebuilds so far)."""
+        c, m, n = ctypes.c_uint32(0), ctypes.c_uint32(0), ctypes.c_uint64(0)
+        _check("mts_get_wheel", load_library().mts_get_wheel(self._h, ctypes.byref(c), ctypes.byref(m),
+                                                             ctypes.byref(n)))
+        return c.value, m.value, n.value
 
     def set_draining(self, flags, r0=0, nr=None):
         """flags: 0/1 per (replica, instance) of replicas [r0, r0 + nr)."""
