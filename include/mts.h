@@ -277,6 +277,21 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
  * stepped since, times the most arrivals one tick can hold). */
 int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream);
 
+/* For callers that cannot allocate device memory while stepping (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * mts_step with the arrival staging (per-tick counts and tier-sorted records
+ * of a chunk of ticks) in a static device array of 64 MiB per GPU instead of
+ * the handle's buffer.  It calls no allocating routine and records no timing
+ * events; results are identical to mts_step's.  The array's device address is
+ * looked up once per device by mts_create.  Ticks run in launches of as many
+ * ticks as fit the array (at most 1024): MTS_ENOMEM when even one tick's
+ * records (replicas x the largest arrival count x 8 bytes) do not fit, and
+ * nothing is launched.  MTS_EDEVICE if the lookup failed.  Every call on one
+ * GPU shares that GPU's array: calls on different handles that overlap on one
+ * GPU (other streams, other threads) race and must be serialised by the
+ * caller.  Otherwise as mts_step. */
+int mts_step_noalloc(mts_handle h, uint64_t n_ticks, hipStream_t stream);
+
 /* Synchronise with the last stream used on h, sum the per-replica counters
  * and compute the state digest.  Returns MTS_ESTATE (with *out filled) when
  * a device-side invariant check failed. */

@@ -6,7 +6,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "_lib", "libmts.so")
 SOURCES = [os.path.join(HERE, "csrc", f)
-           for f in ("mts_api.cpp", "mts_tables.cpp", "mts_kernels.hip", "mts_arrivals.hip")]
+           for f in ("mts_api.cpp", "mts_tables.cpp", "mts_kernels.hip", "mts_arrivals.hip", "mts_noalloc.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC",

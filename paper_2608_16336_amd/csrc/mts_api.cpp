@@ -382,6 +382,9 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
     if (e != hipSuccess) { delete x; return MTS_EDEVICE; }
     const Params p = make_params(x);
     if (launch_init(p, stream) != 0) { delete x; return MTS_EDEVICE; }
+    // address of this device's static scratch for mts_step_noalloc; a failed
+    // lookup leaves that entry point unavailable (MTS_EDEVICE), not the handle
+    (void)scratch_setup(x->device);
     x->last = stream;
     *out = x;
     return MTS_OK;
@@ -466,6 +469,40 @@ int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)
         if (h->timing && hipEventRecord(e[1], stream) != hipSuccess) return MTS_EDEVICE;
         if (launch_step(p, t, nt, blocks, stream) != 0) return MTS_EDEVICE;
         if (h->timing && hipEventRecord(e[2], stream) != hipSuccess) return MTS_EDEVICE;
+    }
+    h->tick = end;
+    h->seq_bound = seq_end;
+    h->last = stream;
+    return MTS_OK;
+}
+
+int mts_step_noalloc(mts_handle h, uint64_t n_ticks, hipStream_t stream)
+{
+    if (!h) return MTS_EINVAL;
+    if (n_ticks == 0) return MTS_OK;
+    char* base = scratch_ptr(h->device);
+    if (!base) return MTS_EDEVICE;
+    // ticks per launch: the counts [R][c] (u32) and records [R][c][cap] (u64)
+    // of c ticks must fit the static scratch
+    const size_t R = h->R, cap = h->arr_cap;
+    auto need = [&](size_t c) { return up256(R * c * 4) + R * c * cap * 8; };
+    size_t c = std::min<size_t>(1024, kNoallocScratchBytes / (R * cap * 8 + R * 4));
+    while (c > 0 && need(c) > kNoallocScratchBytes) --c;
+    if (c == 0) return MTS_ENOMEM;
+    const uint64_t end = h->tick + n_ticks;
+    const uint64_t seq_end = h->seq_bound + n_ticks * uint64_t(h->arr_cap);
+    if (end > 0xFFFF0000ull || seq_end > 0xFFFFFFFFull) return MTS_ERANGE;
+    Params p = make_params(h);
+    p.chunk = uint32_t(c);
+    p.arr_cnt = reinterpret_cast<uint32_t*>(base);
+    p.arr_rec = reinterpret_cast<unsigned long long*>(base + up256(R * c * 4));
+    uint32_t blocks = 0;
+    const int rc = auto_blocks(h, p, &blocks);
+    if (rc) return rc;
+    for (uint64_t t = h->tick; t < end; t += c) {
+        const uint32_t nt = uint32_t(std::min<uint64_t>(c, end - t));
+        if (launch_arrivals(p, t, nt, stream) != 0) return MTS_EDEVICE;
+        if (launch_step(p, t, nt, blocks, stream) != 0) return MTS_EDEVICE;
     }
     h->tick = end;
     h->seq_bound = seq_end;

@@ -133,5 +133,11 @@ int step_blocks_per_cu(const Params& p);
 int launch_digest(const Params& p, uint32_t r0, uint32_t nr, uint32_t tick, hipStream_t stream);
 int launch_shift_clock(const Params& p, uint32_t delta, hipStream_t stream);
 
+// static device scratch of mts_step_noalloc (mts_noalloc.hip): its size, the
+// once-per-device lookup of its address (with that device current) and the
+// address found (null before the lookup or after it failed)
+constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
+int scratch_setup(int device);
+char* scratch_ptr(int device);
 
 }  // namespace mts

@@ -89,7 +89,7 @@ EXPORTED = ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_diges
             "mts_export_state", "mts_import_state", "mts_get_table", "mts_get_headroom",
             "mts_tick", "mts_set_tick", "mts_set_launch", "mts_get_launch", "mts_set_timing",
             "mts_get_timing", "mts_set_draining", "mts_set_queue_cache", "mts_get_queue_cache",
-            "mts_set_wheel_cap", "mts_get_wheel", "mts_destroy", "mts_strerror")
+            "mts_set_wheel_cap", "mts_get_wheel", "mts_step_noalloc", "mts_destroy", "mts_strerror")
 
 _lib = None
 
@@ -107,6 +107,7 @@ def load_library(path=LIB_PATH):
     L.mts_state_bytes.argtypes = [ctypes.POINTER(mts_cfg), ctypes.POINTER(ctypes.c_size_t)]
     L.mts_create.argtypes = [ctypes.POINTER(mts_cfg), vp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]
     L.mts_step.argtypes = [vp, u64, vp]
+    L.mts_step_noalloc.argtypes = [vp, u64, vp]
     L.mts_stats.argtypes = [vp, ctypes.POINTER(mts_stats_t)]
     L.mts_digest.argtypes = [vp, u32, u32, vp]
     L.mts_export_state.argtypes = [vp, u32, u32, ctypes.POINTER(mts_state_view)]
@@ -131,7 +132,7 @@ def load_library(path=LIB_PATH):
     L.mts_destroy.restype = None
     L.mts_strerror.argtypes = [ci]
     L.mts_strerror.restype = ctypes.c_char_p
-    for f in ("mts_state_bytes", "mts_create", "mts_step", "mts_stats", "mts_digest", "mts_export_state",
+    for f in ("mts_state_bytes", "mts_create", "mts_step", "mts_step_noalloc", "mts_stats", "mts_digest", "mts_export_state",
               "mts_import_state", "mts_get_table", "mts_get_headroom", "mts_set_launch", "mts_get_launch",
               "mts_set_timing", "mts_get_timing", "mts_set_draining", "mts_set_queue_cache",
               "mts_get_queue_cache", "mts_set_wheel_cap", "mts_get_wheel"):
@@ -276,6 +277,11 @@ class Scheduler:
 
     def step(self, n_ticks, stream=None):
         _check("mts_step", load_library().mts_step(self._h, n_ticks, _stream_handle(stream)))
+
+    def step_noalloc(self, n_ticks, stream=None):
+        """step() with the arrival staging in the library's static device
+        scratch: allocates nothing (mts_step_noalloc)."""
+        _check("mts_step_noalloc", load_library().mts_step_noalloc(self._h, n_ticks, _stream_handle(stream)))
 
     def set_launch(self, threads=0, blocks=0):
         _check("mts_set_launch", load_library().mts_set_launch(self._h, threads, blocks))
