@@ -178,7 +178,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="sweep")
     ap.add_argument("--ticks-per-step", type=int, default=1000)
-    ap.add_argument("--blocks", type=int, default=0, help="waves of the step kernel (0: automatic)")
+    ap.add_argument("--blocks", type=int, default=0, help="blocks of the step kernel (0: automatic)")
     ap.add_argument("--cpu-replicas", type=int, default=16, help="oracle replicas of the single-thread run")
     ap.add_argument("--cpu-replicas-per-core", type=int, default=12,
                     help="oracle replicas per process of the one-process-per-core run")
@@ -222,7 +222,7 @@ def main():
     if W > 0:
         warm = Scheduler(cfg)
         if args.blocks:
-            warm.set_launch(64, args.blocks)
+            warm.set_launch(0, args.blocks)
         for _ in range(W):
             warm.step(T)
         torch.cuda.synchronize()
@@ -238,7 +238,7 @@ def main():
 
     sch = Scheduler(cfg)
     if args.blocks:
-        sch.set_launch(64, args.blocks)
+        sch.set_launch(0, args.blocks)
     torch.cuda.synchronize()
     s0 = sch.stats()["raw"].astype(np.int64)
     stream = torch.cuda.current_stream()

@@ -343,14 +343,17 @@ uint64_t mts_tick(mts_handle h);
  * the tick does not fit the 32-bit tick fields. */
 int mts_set_tick(mts_handle h, uint64_t tick);
 
-/* Force the launch shape of the step kernel: threads per block (0 or 64:
- * one wave per replica) and number of blocks (0: automatic, else at most the
- * replica count; each wave runs replicas r, r + blocks, ...). */
+/* Force the launch shape of the step kernel: threads per block (0, or the
+ * block size mts_get_launch reports: one 64-lane wave per replica, eight
+ * waves per replica for 128 or more instances) and number of blocks (0:
+ * automatic, else at most the replica count; each block runs replicas r,
+ * r + blocks, ...). */
 int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks);
 
-/* Launch shape mts_step uses now: *threads = 64 and *blocks = the forced
- * count, or the automatic one (replicas, capped at the step-kernel blocks the
- * device holds at once).  Queries the current device's occupancy. */
+/* Launch shape mts_step uses now: *threads = the block size (64, or 512 for
+ * 128 or more instances) and *blocks = the forced count, or the automatic one
+ * (replicas, capped at the step-kernel blocks the device holds at once).
+ * Queries the current device's occupancy. */
 int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks);
 
 /* Queue cache of the step kernel: per instance, the waiting requests that

@@ -393,7 +393,8 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
 int mts_set_launch(mts_handle h, uint32_t threads, uint32_t blocks)
 {
     if (!h) return MTS_EINVAL;
-    if (threads != 0 && threads != 64) return MTS_EINVAL;  // one wave per replica
+    // the block is the replica's waves: its size is fixed by the instance count
+    if (threads != 0 && int(threads) != step_threads(make_params(h))) return MTS_EINVAL;
     if (blocks > h->R) return MTS_EINVAL;
     h->blocks = blocks;
     return MTS_OK;
@@ -439,8 +440,9 @@ int mts_get_queue_cache(mts_handle h, uint32_t* depth)
 int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks)
 {
     if (!h || !threads || !blocks) return MTS_EINVAL;
-    *threads = 64;
-    return auto_blocks(h, make_params(h), blocks);
+    const Params p = make_params(h);
+    *threads = uint32_t(step_threads(p));
+    return auto_blocks(h, p, blocks);
 }
 
 int mts_step(mts_handle h, uint64_t n_ticks, hipStream_t stream)

@@ -128,8 +128,10 @@ size_t lds_bytes(uint32_t I, uint32_t S, uint32_t RB, uint32_t wsz, uint32_t pol
 int launch_init(const Params& p, hipStream_t stream);
 int launch_arrivals(const Params& p, unsigned long long t0, uint32_t nt, hipStream_t stream);
 int launch_step(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, hipStream_t stream);
-// resident step-kernel blocks per CU (0 if the runtime cannot tell)
+// resident step-kernel blocks per CU (0 if the runtime cannot tell); threads
+// per block (one wave per replica, or eight for 128 or more instances)
 int step_blocks_per_cu(const Params& p);
+int step_threads(const Params& p);
 int launch_digest(const Params& p, uint32_t r0, uint32_t nr, uint32_t tick, hipStream_t stream);
 int launch_shift_clock(const Params& p, uint32_t delta, hipStream_t stream);
 

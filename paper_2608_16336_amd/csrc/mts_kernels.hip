@@ -61,8 +61,13 @@ enum { kXSlo = 0, kXAge = 10, kXPromoMin = 20, kXPromoPeriod, kXAdaptEpoch, kXAd
 static_assert(kXWords == MTS_EXT_WORDS, "extension table size");
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, ext, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, ext, blk, total;
 };
+
+// Waves per replica: the kernels for 128 or more instances run a workgroup of
+// eight waves per replica (the per-instance phases are spread over the waves,
+// the serial ones stay on wave 0); the others one wave.
+__host__ __device__ constexpr int waves_for(uint32_t IM) { return IM >= 128 ? 8 : 1; }
 
 __host__ __device__ inline uint32_t al8(uint32_t x) { return (x + 7u) & ~7u; }
 
@@ -107,6 +112,10 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     // in HBM: it is touched only on pass and update ticks)
     o = al8(o);
     L.ext = o;   o += ext ? 8 + IM * 4 : 0;
+    // multi-wave kernels: values the waves combine (the auto-scaling sum, an
+    // abort flag)
+    o = al8(o);
+    L.blk = o;   o += waves_for(IM) > 1 ? 16 : 0;
     L.total = al8(o);
     return L;
 }
@@ -124,7 +133,7 @@ struct Ctx {
                                // instance << 16 | tier << 12 | slot, seq
     int* lastn;                // number of those placements
     unsigned* vic;             // [kVic] instance << 16 | slot of this tick's preemption victims
-    int* nvic;                 // their number (kVic + 1: more than the list holds)
+    int* nvic;                 // their number (above kVic: more than the list holds)
     unsigned *hwd, *hmt, *hta; // [I] head of line: slot word, meta, arrival tick
     unsigned* res;             // [RB][I] running requests per growth residue (u16 pairs)
     unsigned* tcnt;            // [I][10] running requests per tier (u16 pairs)
@@ -145,6 +154,10 @@ struct Ctx {
     // adaptive headroom and promotion (null when both are off): the LDS
     // region read through the accessors below
     unsigned char* ext;
+    // multi-wave kernels only (null otherwise): the block area, a 64-bit sum
+    // and a flag the waves combine
+    long long* bsum;
+    int* bflag;
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -228,6 +241,8 @@ __device__ inline Ctx carve(char* base, const Params& P)
         C.fsum = nullptr; C.svc = nullptr; C.fcnt = nullptr; C.pen = nullptr;
     }
     C.ext = EXT ? reinterpret_cast<unsigned char*>(base + Y.ext) : nullptr;
+    C.bsum = waves_for(IM) > 1 ? reinterpret_cast<long long*>(base + Y.blk) : nullptr;
+    C.bflag = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 8) : nullptr;
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
@@ -448,6 +463,15 @@ __device__ __forceinline__ int wscan(int x, int lane)
     x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
     x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
     return x;
+}
+
+// value of lane src (any lane, through the LDS crossbar without LDS storage)
+__device__ __forceinline__ int perm32(int v, int src) { return __builtin_amdgcn_ds_bpermute(src << 2, v); }
+__device__ __forceinline__ unsigned long long perm64(unsigned long long v, int src)
+{
+    const unsigned lo = unsigned(perm32(int(unsigned(v)), src));
+    const unsigned hi = unsigned(perm32(int(unsigned(v >> 32)), src));
+    return (static_cast<unsigned long long>(hi) << 32) | lo;
 }
 
 // ---------------------------------------------------------------------------
@@ -676,9 +700,10 @@ __device__ inline bool preempt(const Ctx& C, int i, uint32_t t, int lane)
                 C.nwait[i] += 1;
                 C.frs[i] = 0;
                 C.flags[i] |= kFlagIntf;
-                const int nv = *C.nvic;
+                // (several waves may preempt at once; a count above kVic means
+                // the list missed some)
+                const int nv = atomicAdd(C.nvic, 1);
                 if (nv < kVic) C.vic[nv] = (uint32_t(i) << 16) | uint32_t(vs);
-                *C.nvic = nv < kVic ? nv + 1 : kVic + 1;
                 c16_dec(C.res, res_idx(C, i, vr));
                 tier_dec(C, i, vt);
                 stat(C, vt * 8 + kPreempted, 1);
@@ -1023,7 +1048,9 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
 // fits).  The waiting requests are gathered into lanes, ranked by (tier, seq),
 // and the longest prefix of the ranked list whose summed demand fits is
 // admitted in one step; the next ranked request becomes the head of line.
-// The result equals admitting the head of line one request at a time.
+// The result equals admitting the head of line one request at a time.  GR
+// chunks of 64 slots are read per memory round trip.
+template <int GR>
 __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
 {
     const size_t b = size_t(i) * C.S;
@@ -1031,11 +1058,11 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
     unsigned long long key = kNone;
     uint32_t word = 0, meta = 0, ta = 0;
     int slot = 0, w = 0;
-    for (int c0 = 0; c0 < nch; c0 += 4) {
-        uint32_t v[4], m[4], q[4], a[4];
+    for (int c0 = 0; c0 < nch; c0 += GR) {
+        uint32_t v[GR], m[GR], q[GR], a[GR];
         // all loads of the group are issued together (one memory round trip)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int g = 0; g < GR; ++g) {
             const bool in = c0 + g < nch;
             const size_t sb = b + (c0 + g) * 64 + lane;
             v[g] = in ? C.hot[sb] : 0u;
@@ -1044,7 +1071,7 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
             a[g] = in ? C.tarr[sb] : 0u;
         }
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int g = 0; g < GR; ++g) {
             const unsigned long long wm = ballot(wst(v[g]) == 1u);
             if (!wm) continue;
             const int cnt = __popcll(wm);
@@ -1076,6 +1103,31 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
     slot = __builtin_amdgcn_ds_permute(ad, slot);
     key = (static_cast<unsigned long long>(k_hi) << 32) | k_lo;
     admit_ranked(C, i, t, lane, w, key, word, meta, ta, slot);
+}
+
+// Admission of instance i from its head of line and the requests cached behind
+// it, which are the smallest keys of its queue in order: the longest fitting
+// prefix is admitted at once (admit_ranked).  When all of them fit and more
+// wait, the head of line is unknown afterwards.
+__device__ inline void admit_cached(const Ctx& C, int i, uint32_t t, int lane)
+{
+    const int n = C.qn[i];
+    unsigned long long key = kNone;
+    uint32_t word = 0, meta = 0, ta = 0;
+    int slot = 0;
+    if (lane == 0) {
+        key = C.holk[i]; word = C.hwd[i]; meta = C.hmt[i]; ta = C.hta[i]; slot = C.hols[i];
+    } else if (lane <= n) {
+        const uint4 e = C.qt[qc_at(C, i, lane - 1)];
+        const uint32_t tier = (e.w >> 12) & 15u;
+        key = qc_key(C, e);
+        word = e.y;
+        meta = kWaiting | (tier << 2) | (((e.w >> 16) & 1u) << 6);
+        ta = e.z;
+        slot = int(e.w & 0xFFFu);
+    }
+    const bool complete = C.nwait[i] == n + 1;
+    admit_ranked(C, i, t, lane, n + 1, key, word, meta, ta, slot, complete);
 }
 
 // Admission of instance i whose waiting requests all arrived in the previous
@@ -1203,13 +1255,30 @@ __device__ inline void adapt_headroom(const Ctx& C, const Params& P, uint32_t r,
 // ---------------------------------------------------------------------------
 // k_step
 // ---------------------------------------------------------------------------
-template <int IM, bool INF, bool EXT>
-__global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigned long long t0, uint32_t nt)
+// A barrier of the replica's waves (a wave-level one when a replica has one
+// wave): every LDS and memory write before it is seen by every wave after it.
+template <int NW>
+__device__ __forceinline__ void block_sync()
 {
+    if (NW > 1) __syncthreads();
+    else wave_sync();
+}
+
+template <int IM, bool INF, bool EXT>
+__global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(Params P, unsigned long long t0, uint32_t nt)
+{
+    // IPL: instances per lane when one wave covers every instance (the serial
+    // phases, run by wave 0); OPL: instances per lane of the instances a wave
+    // owns in the per-instance phases, instance (64 j + lane) NW + wid
+    constexpr int NW = waves_for(IM);
     constexpr int IPL = (IM + 63) / 64;
+    constexpr int OPL = (IM + 64 * NW - 1) / (64 * NW);
     extern __shared__ __align__(16) char lds_raw[];
     Ctx C = carve<IM, INF, EXT>(lds_raw, P);
     const int lane = lane_id();
+    const int wid = NW > 1 ? int(threadIdx.x >> 6) : 0;
+    const uint32_t tid = threadIdx.x;
+    constexpr uint32_t NT = 64u * NW;
     const uint32_t I = P.I, S = P.S, W = P.W;
     const uint32_t wsz = P.wsz;
     constexpr bool infaas = INF;  // the global policy: INFaaS cost, else Llumnix freeness
@@ -1223,12 +1292,12 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             // none of them stays in registers through the tick loop)
             const int32_t* hqr = ext_hqr(P);
             if (hqr) hq = hqr + size_t(r) * kTiers;
-            if (lane == 0) {
+            if (tid == 0) {
                 const uint32_t t0u = uint32_t(t0), per = P.ext[kXPromoPeriod], ep = P.ext[kXAdaptEpoch];
                 xleft(C)[0] = per ? int(t0u % per) : 0;
                 xleft(C)[1] = ep ? int(t0u % ep) : 0;
             }
-            for (uint32_t i = lane; i < P.I; i += 64) wlb(C)[i] = 0u;  // unknown: the first pass reads them
+            for (uint32_t i = tid; i < P.I; i += NT) wlb(C)[i] = 0u;  // unknown: the first pass reads them
         }
 #pragma unroll
         for (int p = 0; p < kTiers; ++p) C.hq[p] = hq[p];
@@ -1238,8 +1307,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         C.hist = P.hist + size_t(r) * kHistPerReplica;
 
         // ---------------- prologue: derived per-instance state ----------------
-        for (int j = lane; j < kNstat; j += 64) C.stats[j] = P.stats[size_t(r) * kNstat + j];
-        for (uint32_t i = lane; i < I; i += 64) {
+        for (uint32_t j = tid; j < uint32_t(kNstat); j += NT) C.stats[j] = P.stats[size_t(r) * kNstat + j];
+        for (uint32_t i = tid; i < I; i += NT) {
             C.freeb[i] = P.freeb[size_t(r) * I + i];
             C.drn[i] = P.drain[size_t(r) * I + i];
             for (int k = 0; k < 4; ++k) C.mig[4 * i + k] = P.mig[(size_t(r) * I + i) * 4 + k];
@@ -1250,25 +1319,27 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             if (C.td) { C.qn[i] = 0; C.qh[i] = 0; }
             if (C.svc) C.svc[i] = P.svc[size_t(r) * I + i];
         }
-        for (uint32_t b = lane; b < wsz / 2; b += 64) C.wc[b] = 0;
-        if (lane == 0) *C.lastn = 0;
-        for (uint32_t b = lane; b < (I * C.RB + 1) / 2; b += 64) C.res[b] = 0;
-        for (uint32_t b = lane; b < (I * kTiers + 1) / 2; b += 64) C.tcnt[b] = 0;
-        for (uint32_t b = lane; b < (wsz + 31) / 32; b += 64) C.wov[b] = 0;
-        wave_sync();
-        for (uint32_t i = lane; i < I; i += 64) {
+        for (uint32_t b = tid; b < wsz / 2; b += NT) C.wc[b] = 0;
+        if (tid == 0) { *C.lastn = 0; *C.nvic = 0; }
+        for (uint32_t b = tid; b < (I * C.RB + 1) / 2; b += NT) C.res[b] = 0;
+        for (uint32_t b = tid; b < (I * kTiers + 1) / 2; b += NT) C.tcnt[b] = 0;
+        for (uint32_t b = tid; b < (wsz + 31) / 32; b += NT) C.wov[b] = 0;
+        block_sync<NW>();
+        for (uint32_t i = tid; i < I; i += NT) {
             const int d = C.mig[4 * i];
             if (d >= 0) C.inb[d] = C.mig[4 * i + 3];
         }
-        wave_sync();
+        block_sync<NW>();
         const uint32_t t0u = uint32_t(t0);
         {
             // The slots are read as one flat run of I * W chunks of 64 (chunk c
             // of instance i is flat chunk i W + c), GP chunks per memory round
             // trip; an instance is summed up after its last chunk.  The arrival
             // ticks of the heads of line are read afterwards, lane-parallel.
+            // (each wave reads the chunks of the instances it owns: wid, wid + NW, ...)
             constexpr int GP = IM >= 128 ? 16 : 8;
-            const uint32_t nfl = I * W;
+            const uint32_t nown = NW > 1 ? (I > uint32_t(wid) ? (I - uint32_t(wid) + NW - 1) / NW : 0u) : I;
+            const uint32_t nfl = nown * W;
             int nB = 0, nlive = 0, nw = 0, held = 0;
             unsigned long long bk = kNone;
             int bs = 0;
@@ -1278,7 +1349,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
 #pragma unroll
                 for (int g = 0; g < GP; ++g) {
                     const bool in = f0 + g < nfl;
-                    const size_t fs = size_t(f0 + g) * 64 + lane;
+                    const uint32_t fo = (f0 + g) / W;
+                    const size_t fs = (size_t(fo * NW + wid) * W + (f0 + g - fo * W)) * 64 + lane;
                     v[g] = in ? C.hot[fs] : 0u;
                     m[g] = in ? C.meta[fs] : 0u;
                     q[g] = in ? C.seq[fs] : 0u;
@@ -1287,7 +1359,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 for (int g = 0; g < GP; ++g) {
                     const uint32_t f = f0 + g;
                     if (f >= nfl) continue;
-                    const uint32_t i = f / W, c = f - i * W;
+                    const uint32_t io = f / W, c = f - io * W, i = io * NW + uint32_t(wid);
                     const int s = int(c) * 64 + lane;
                     const uint32_t st = wst(v[g]);
                     const unsigned long long ow = ballot(v[g] != 0);
@@ -1331,7 +1403,8 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     }
                 }
             }
-            for (uint32_t i = lane; i < I; i += 64) {
+            block_sync<NW>();
+            for (uint32_t i = tid; i < I; i += NT) {
                 const int h = C.hols[i];
                 if (h >= 0) C.hta[i] = C.tarr[size_t(i) * S + h];
             }
@@ -1340,7 +1413,7 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
         uint32_t run_acc = 0, wait_acc = 0;  // per lane, at most 1024 ticks x 4 x 2048
         const unsigned long long* recs = P.arr_rec + size_t(r) * P.chunk * P.arr_cap;
         const uint32_t* cnts = P.arr_cnt + size_t(r) * P.chunk;
-        wave_sync();
+        block_sync<NW>();
 
         // the arrivals of the next tick are loaded one tick ahead; records past
         // the tick's count are never used
@@ -1376,14 +1449,17 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             if (EXT) {
                 const int pl = xleft(C)[0], al = xleft(C)[1];
                 const int per = int(P.ext[kXPromoPeriod]), ep = int(P.ext[kXAdaptEpoch]);
-                if (per && pl == 0) promote_waiting(C, P, t, lane);
+                if (wid == 0) {
+                    if (per && pl == 0) promote_waiting(C, P, t, lane);
+                    if (ep && al == 0) adapt_headroom(C, P, r, lane);
+                }
+                block_sync<NW>();
                 if (ep && al == 0) {
-                    adapt_headroom(C, P, r, lane);
                     const int32_t* hq = ext_hqr(P) + size_t(r) * kTiers;
 #pragma unroll
                     for (int p = 0; p < kTiers; ++p) C.hq[p] = hq[p];
                 }
-                if (lane == 0) {
+                if (tid == 0) {
                     xleft(C)[0] = per && pl + 1 < per ? pl + 1 : 0;
                     xleft(C)[1] = ep && al + 1 < ep ? al + 1 : 0;
                 }
@@ -1393,11 +1469,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             // an instance whose growth fits takes its blocks at once; the others
             // preempt first (and take them at the end of preempt)
             const uint32_t cres = (0u - t) & C.bmask;
-            unsigned long long pre[IPL];
+            unsigned long long pre[OPL];
             bool preempting = false;
 #pragma unroll
-            for (int j = 0; j < IPL; ++j) {
-                const uint32_t i = lane + 64 * j;
+            for (int j = 0; j < OPL; ++j) {
+                const uint32_t i = (uint32_t(lane) + 64u * j) * NW + uint32_t(wid);
                 bool np = false;
                 if (i < I) {
                     const int G = int(c16_get(C.res, res_idx(C, i, cres)));
@@ -1415,21 +1491,31 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 pre[j] = ballot(np);
                 preempting = preempting || pre[j] != 0;
             }
-            if (lane == 0) *C.nvic = 0;
             // migrations to abort: set by preemption and finish, kept in a register
+            // (multi-wave kernels: another wave's preemption sets the block flag)
             bool abort_any = false;
             if (preempting) {
                 wave_sync();
 #pragma unroll
-                for (int j = 0; j < IPL; ++j)
+                for (int j = 0; j < OPL; ++j)
                     for (unsigned long long m = pre[j]; m; m &= m - 1)
-                        abort_any = preempt<(IM >= 128 ? 16 : 4), (IM >= 128 ? 4 : 2)>(C, 64 * j + ffs64(m), t, lane) || abort_any;
+                        abort_any = preempt<(IM >= 128 ? 16 : 4), (IM >= 128 ? 4 : 2)>(
+                                        C, int((64u * j + ffs64(m)) * NW + uint32_t(wid)), t, lane) || abort_any;
+            }
+            if (NW > 1) {
+                if (abort_any && lane == 0) *C.bflag = 1;
+                if (tid == 0) *C.bsum = 0;  // the auto-scaling sum of this tick (phase C)
+                block_sync<NW>();
+                if (wid == 0) {
+                    preempting = *C.nvic != 0;
+                    abort_any = *C.bflag != 0;
+                }
             }
             // a preempted request is waiting now: its prefetched entries (for this
             // tick's and the next tick's visit) are dropped (its wheel entry was
             // erased); more victims than the list holds make both visits load again
             bool pf_lost = false;
-            if (preempting) {
+            if (preempting && wid == 0) {
                 const int nv = *C.nvic;
                 pf_lost = nv > kVic;
                 for (int v = 0; v < nv && v < kVic; ++v) {
@@ -1438,6 +1524,9 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 }
             }
             wave_sync();
+            // the finish visit and the release of aborted migrations: wave 0
+            if (wid == 0) {
+            if (lane == 0) *C.nvic = 0;
             {
                 const uint32_t bk = t & C.wmask;
                 const uint32_t nb = (C.wc[bk >> 1] >> ((bk & 1u) * 16u)) & 0xFFFFu;
@@ -1487,23 +1576,28 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 }
                 wave_sync();
             }
+            if (NW > 1 && lane == 0) *C.bflag = 0;
+            }  // wave 0
+            block_sync<NW>();
 
             // ===================== B: admission (lane-parallel rounds); C: freeness =====================
+            // (each wave admits on the instances it owns)
             for (;;) {
                 // heads of line left unknown: found by a rescan, which admits at once
                 bool unk = false;
 #pragma unroll
-                for (int j = 0; j < IPL; ++j) {
-                    const uint32_t i = lane + 64 * j;
+                for (int j = 0; j < OPL; ++j) {
+                    const uint32_t i = (uint32_t(lane) + 64u * j) * NW + uint32_t(wid);
                     for (unsigned long long m = ballot(i < I && C.hols[i] == kHolUnknown); m; m &= m - 1)
-                        unk = rescan_admit<(IM >= 128 ? 16 : 4), (IM >= 128 ? 4 : 2)>(C, 64 * j + ffs64(m), t, lane) || unk;
+                        unk = rescan_admit<(IM >= 128 ? 16 : 4), (IM >= 128 ? 4 : 2)>(
+                                  C, int((64u * j + ffs64(m)) * NW + uint32_t(wid)), t, lane) || unk;
                 }
                 bool any = unk;
-                unsigned long long bat[IPL], frm[IPL];
+                unsigned long long bat[OPL], frm[OPL], cch[OPL];
 #pragma unroll
-                for (int j = 0; j < IPL; ++j) {
-                    const uint32_t i = lane + 64 * j;
-                    bool batch = false, fresh = false;
+                for (int j = 0; j < OPL; ++j) {
+                    const uint32_t i = (uint32_t(lane) + 64u * j) * NW + uint32_t(wid);
+                    bool batch = false, fresh = false, cachd = false;
                     if (i < I && C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]) {
                         const int nw = C.nwait[i];
                         const bool cached = C.td && C.qn[i] > 0;
@@ -1511,6 +1605,11 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             fresh = true;
                         } else if (nw >= 2 && nw <= 64 && !cached) {
                             batch = true;
+                        } else if (IM >= 128 && cached) {
+                            // the kernels for 128+ instances admit a cached run at
+                            // once (the head of line may be unknown afterwards)
+                            cachd = true;
+                            any = true;
                         } else {
                             // the only waiting request, a queue longer than a wave or one
                             // whose next requests are cached: admit heads of line one at a
@@ -1544,12 +1643,17 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     }
                     bat[j] = ballot(batch);
                     frm[j] = ballot(fresh);
+                    cch[j] = ballot(cachd);
                 }
                 wave_sync();
 #pragma unroll
-                for (int j = 0; j < IPL; ++j) {
-                    for (unsigned long long m = frm[j]; m; m &= m - 1) admit_fresh(C, 64 * j + ffs64(m), t, lane);
-                    for (unsigned long long m = bat[j]; m; m &= m - 1) admit_batch(C, 64 * j + ffs64(m), t, lane);
+                for (int j = 0; j < OPL; ++j) {
+                    for (unsigned long long m = frm[j]; m; m &= m - 1)
+                        admit_fresh(C, int((64u * j + ffs64(m)) * NW + uint32_t(wid)), t, lane);
+                    for (unsigned long long m = bat[j]; m; m &= m - 1)
+                        admit_batch<(IM >= 128 ? 16 : 4)>(C, int((64u * j + ffs64(m)) * NW + uint32_t(wid)), t, lane);
+                    for (unsigned long long m = cch[j]; m; m &= m - 1)
+                        admit_cached(C, int((64u * j + ffs64(m)) * NW + uint32_t(wid)), t, lane);
                 }
                 if (!ballot(any)) break;
             }
@@ -1558,7 +1662,10 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             // max(B, 1) -- no headroom, no draining sentinel -- in fixed point,
             // floor(F_normal * 2^20) per instance, against -1/2 and 3/2
             long long fsum = 0;
-            for (uint32_t i = lane; i < I; i += 64) {
+#pragma unroll
+            for (int j = 0; j < OPL; ++j) {
+                const uint32_t i = (uint32_t(lane) + 64u * j) * NW + uint32_t(wid);
+                if (i >= I) continue;
                 set_f(C, int(i));
                 // slot-ticks: running and waiting requests at the end of the tick.
                 // Later phases move running and waiting requests between
@@ -1583,7 +1690,10 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
             if (C.svc) {
                 // INFaaS: service-time estimate from this tick's finishes, then
                 // the state penalty (OVERLOADED before INTERFERED before ACTIVE)
-                for (uint32_t i = lane; i < I; i += 64) {
+#pragma unroll
+                for (int j = 0; j < OPL; ++j) {
+                    const uint32_t i = (uint32_t(lane) + 64u * j) * NW + uint32_t(wid);
+                    if (i >= I) continue;
                     const int c = C.fcnt[i];
                     if (c > 0) {
                         // floor(256 sum / c): sum < 2^43, so 256 sum is exact in a
@@ -1599,13 +1709,20 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                              : (C.flags[i] & kFlagIntf) ? int(P.pen_intf) : 0;
                 }
             }
-            if (lane == 0) {
+            if (NW > 1) {
+                if (lane == 0) atomicAdd(reinterpret_cast<unsigned long long*>(C.bsum), static_cast<unsigned long long>(fsum));
+                block_sync<NW>();
+                fsum = *C.bsum;
+            }
+            if (tid == 0) {
                 const long long half = static_cast<long long>(I) << 19;
                 if (fsum < -half) stat(C, kScaleOut, 1);
                 else if (fsum > 3 * half) stat(C, kScaleIn, 1);
             }
             wave_sync();
 
+            // the dispatch and the migrations (phases D and E): wave 0
+            if (wid == 0) {
             // ===================== D: tier-ordered dispatch =====================
             // an instance with an empty queue now holds, after this dispatch, only
             // this tick's arrivals; they are recorded in LDS when they fit one wave
@@ -1771,14 +1888,19 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                     const int tier = int((a >> 32) & 15u);
                     int s = -1;
                     if (tgt >= 0) {
+                        // the rank-th empty slot, four occupancy words per step
                         int rk = rank;
-                        for (uint32_t w = 0; w < W && s < 0; ++w) {
-                            const unsigned long long word = C.occ[tgt * W + w];
-                            const int z = 64 - __popcll(word);
-                            if (rk < z) {
-                                s = int(w) * 64 + kth_set_bit(~word, rk);
-                            } else {
-                                rk -= z;
+                        for (uint32_t w0 = 0; w0 < W && s < 0; w0 += 4) {
+                            unsigned long long wd[4];
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) wd[k] = w0 + k < W ? C.occ[tgt * W + w0 + k] : kNone;
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) {
+                                const int z = 64 - __popcll(wd[k]);
+                                if (s < 0) {
+                                    if (rk < z) s = int(w0 + k) * 64 + kth_set_bit(~wd[k], rk);
+                                    else rk -= z;
+                                }
                             }
                         }
                         if (s < 0) {  // occupancy and live count disagree: flag, drop the arrival
@@ -1929,56 +2051,60 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                         avm[j] = ballot(av);
                         n2 += __popcll(avm[j]);
                     }
-                    // Pairs stop at the first source that is neither draining nor
-                    // below zero freeness, so with nneg such instances only L[0..nneg]
-                    // and L[n2 - 1 - nneg .. n2 - 1] are ever read.  The kernels for
-                    // 128+ instances take just those ends by repeated wave minima and
-                    // maxima when they are disjoint; otherwise every rank is counted.
-                    int nneg = 0;
-#pragma unroll
-                    for (int j = 0; j < IPL; ++j) {
-                        const uint32_t i = lane + 64 * j;
-                        nneg += __popcll(avm[j] & ballot(i < I && (C.num[i] < 0 || C.drn[i])));
-                    }
-                    int npairs = min(int(P.mig_max_pairs), n2 / 2);
-                    if (IM >= 128 && 2 * (nneg + 1) <= n2 && nneg + 1 < npairs) {
-                        unsigned long long lo[IPL], hi[IPL];
+                    // L: the kernels for 128+ instances sort all keys at once;
+                    // the others count every instance's rank
+                    const int npairs = min(int(P.mig_max_pairs), n2 / 2);
+                    if (IM >= 128) {
+                        // the whole order at once: a bitonic sort of the IM
+                        // (key, index) pairs, element e = lane + 64 j in register j
+                        // (the instances in a migration carry the largest key and
+                        // sort after the n2 available ones)
+                        unsigned long long sk[IPL];
+                        int si[IPL];
 #pragma unroll
                         for (int j = 0; j < IPL; ++j) {
-                            const bool av = (avm[j] >> lane) & 1ull;
-                            lo[j] = av ? fk[j] : kNone;  // no key reaches either bound
-                            hi[j] = av ? fk[j] : 0ull;
+                            sk[j] = (avm[j] >> lane) & 1ull ? fk[j] : kNone;
+                            si[j] = lane + 64 * j;
                         }
-                        for (int k = 0; k <= nneg; ++k) {
-                            // k-th in (F, index) order: smallest key, lowest index
-                            unsigned long long lb = lo[0];
 #pragma unroll
-                            for (int j = 1; j < IPL; ++j) lb = tmin(lb, lo[j]);
-                            const unsigned long long mn = wmin64(lb);
-                            int idx = -1;
+                        for (int size = 2; size <= 64 * IPL; size <<= 1) {
 #pragma unroll
-                            for (int j = 0; j < IPL; ++j) {
-                                const unsigned long long bm = ballot(lo[j] == mn);
-                                if (idx < 0 && bm) idx = 64 * j + ffs64(bm);
+                            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                                if (stride >= 64) {
+                                    // between registers of a lane
+                                    const int js = stride >> 6;
+#pragma unroll
+                                    for (int j = 0; j < IPL; ++j) {
+                                        if (j & js) continue;
+                                        const bool asc = ((lane + 64 * j) & size) == 0;
+                                        const unsigned long long ka = sk[j], kb = sk[j + js];
+                                        const int ia = si[j], ib = si[j + js];
+                                        const bool gt = ka > kb || (ka == kb && ia > ib);
+                                        const bool sw = asc ? gt : !gt;
+                                        sk[j] = sw ? kb : ka; si[j] = sw ? ib : ia;
+                                        sk[j + js] = sw ? ka : kb; si[j + js] = sw ? ia : ib;
+                                    }
+                                } else {
+                                    // between lanes: the lower lane of an ascending pair
+                                    // keeps the smaller (key, index)
+                                    const int partner = lane ^ stride;
+                                    const bool low = (lane & stride) == 0;
+#pragma unroll
+                                    for (int j = 0; j < IPL; ++j) {
+                                        const unsigned long long pk = perm64(sk[j], partner);
+                                        const int pi = perm32(si[j], partner);
+                                        const bool asc = ((lane + 64 * j) & size) == 0;
+                                        const bool plt = pk < sk[j] || (pk == sk[j] && pi < si[j]);
+                                        const bool take = low == asc ? plt : !plt;
+                                        sk[j] = take ? pk : sk[j];
+                                        si[j] = take ? pi : si[j];
+                                    }
+                                }
                             }
-#pragma unroll
-                            for (int j = 0; j < IPL; ++j) lo[j] = lane + 64 * j == idx ? kNone : lo[j];
-                            // (n2 - 1 - k)-th: largest key, highest index
-                            unsigned long long hb = hi[0];
-#pragma unroll
-                            for (int j = 1; j < IPL; ++j) hb = tmax(hb, hi[j]);
-                            const unsigned long long mx = wmax64(hb);
-                            int hdx = -1;
-#pragma unroll
-                            for (int j = IPL - 1; j >= 0; --j) {
-                                const unsigned long long bm = ballot(hi[j] == mx);
-                                if (hdx < 0 && bm) hdx = 64 * j + 63 - __clzll(static_cast<long long>(bm));
-                            }
-#pragma unroll
-                            for (int j = 0; j < IPL; ++j) hi[j] = lane + 64 * j == hdx ? 0ull : hi[j];
-                            if (lane == 0) { C.order[k] = idx; C.order[n2 - 1 - k] = hdx; }
                         }
-                        npairs = nneg + 1;
+#pragma unroll
+                        for (int j = 0; j < IPL; ++j)
+                            if (lane + 64 * j < n2) C.order[lane + 64 * j] = si[j];
                     } else {
                         int rk[IPL];
 #pragma unroll
@@ -2064,17 +2190,28 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                             const int nch = live_chunks(C, psrc, lane);
                             unsigned long long bk = 0;
                             int bs = 0;
-                            for (int c = 0; c < nch; ++c) {
-                                const int s = c * 64 + lane;
-                                const uint32_t v = C.hot[sbase + s];
-                                const uint32_t m = C.meta[sbase + s];
-                                if (wst(v) == 2u && !(m & kMigrating)) {
-                                    const uint32_t fin = fin_of(v, t);
-                                    const unsigned long long kk =
-                                        ((rank_of(C, (m >> 2) & 15u) + 1ull) << 48) |
-                                        (static_cast<unsigned long long>(65535 - blocks_of(wlo(v) - (fin - t), C.shift)) << 32) |
-                                        C.seq[sbase + s];
-                                    if (kk > bk) { bk = kk; bs = s; }
+                            // GC chunks of 64 slots per memory round trip
+                            constexpr int GC = IM >= 128 ? 16 : 4;
+                            for (int c0 = 0; c0 < nch; c0 += GC) {
+                                uint32_t v[GC], m[GC], q[GC];
+#pragma unroll
+                                for (int g = 0; g < GC; ++g) {
+                                    const bool in = c0 + g < nch;
+                                    const size_t sb = sbase + (c0 + g) * 64 + lane;
+                                    v[g] = in ? C.hot[sb] : 0u;
+                                    m[g] = in ? C.meta[sb] : 0u;
+                                    q[g] = in ? C.seq[sb] : 0u;
+                                }
+#pragma unroll
+                                for (int g = 0; g < GC; ++g) {
+                                    if (wst(v[g]) == 2u && !(m[g] & kMigrating)) {
+                                        const uint32_t fin = fin_of(v[g], t);
+                                        const unsigned long long kk =
+                                            ((rank_of(C, (m[g] >> 2) & 15u) + 1ull) << 48) |
+                                            (static_cast<unsigned long long>(65535 - blocks_of(wlo(v[g]) - (fin - t), C.shift)) << 32) |
+                                            q[g];
+                                        if (kk > bk) { bk = kk; bs = (c0 + g) * 64 + lane; }
+                                    }
                                 }
                             }
                             const unsigned long long mx = wmax64(bk);
@@ -2098,25 +2235,26 @@ __global__ __launch_bounds__(64, IM <= 64 ? 4 : 1) void k_step(Params P, unsigne
                 }
                 wave_sync();
             }
-
+            }  // wave 0
+            block_sync<NW>();
         }
 
         // ---------------- epilogue ----------------
         const unsigned long long run_sum = wsum64(run_acc), wait_sum = wsum64(wait_acc);
         if (lane == 0) {
-            C.stats[kRunSlotTicks] += run_sum;
-            C.stats[kWaitSlotTicks] += wait_sum;
-            C.stats[kTicks] += nt;
+            stat(C, kRunSlotTicks, run_sum);
+            stat(C, kWaitSlotTicks, wait_sum);
+            if (wid == 0) stat(C, kTicks, nt);
         }
-        wave_sync();
-        for (int j = lane; j < kNstat; j += 64) P.stats[size_t(r) * kNstat + j] = C.stats[j];
-        for (uint32_t i = lane; i < I; i += 64) {
+        block_sync<NW>();
+        for (uint32_t j = tid; j < uint32_t(kNstat); j += NT) P.stats[size_t(r) * kNstat + j] = C.stats[j];
+        for (uint32_t i = tid; i < I; i += NT) {
             P.freeb[size_t(r) * I + i] = C.freeb[i];
             if (C.svc) P.svc[size_t(r) * I + i] = C.svc[i];
             for (int k = 0; k < 4; ++k) P.mig[(size_t(r) * I + i) * 4 + k] = C.mig[4 * i + k];
         }
-        if (lane == 0) P.next_seq[r] = next_seq;
-        wave_sync();
+        if (tid == 0) P.next_seq[r] = next_seq;
+        block_sync<NW>();
     }
 }
 
@@ -2260,11 +2398,11 @@ template <bool INF, bool EXT>
 void launch_step_t(const Params& p, unsigned long long t0, uint32_t nt, uint32_t blocks, size_t lds, hipStream_t stream)
 {
     switch (imax_for(p.I)) {
-    case 16: hipLaunchKernelGGL((k_step<16, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 32: hipLaunchKernelGGL((k_step<32, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 64: hipLaunchKernelGGL((k_step<64, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    case 128: hipLaunchKernelGGL((k_step<128, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
-    default: hipLaunchKernelGGL((k_step<256, INF, EXT>), dim3(blocks), dim3(64), lds, stream, p, t0, nt); break;
+    case 16: hipLaunchKernelGGL((k_step<16, INF, EXT>), dim3(blocks), dim3(64 * waves_for(16)), lds, stream, p, t0, nt); break;
+    case 32: hipLaunchKernelGGL((k_step<32, INF, EXT>), dim3(blocks), dim3(64 * waves_for(32)), lds, stream, p, t0, nt); break;
+    case 64: hipLaunchKernelGGL((k_step<64, INF, EXT>), dim3(blocks), dim3(64 * waves_for(64)), lds, stream, p, t0, nt); break;
+    case 128: hipLaunchKernelGGL((k_step<128, INF, EXT>), dim3(blocks), dim3(64 * waves_for(128)), lds, stream, p, t0, nt); break;
+    default: hipLaunchKernelGGL((k_step<256, INF, EXT>), dim3(blocks), dim3(64 * waves_for(256)), lds, stream, p, t0, nt); break;
     }
 }
 
@@ -2281,11 +2419,13 @@ size_t step_lds(const Params& p)
 
 }  // namespace
 
+int step_threads(const Params& p) { return 64 * waves_for(imax_for(p.I)); }
+
 int step_blocks_per_cu(const Params& p)
 {
     const size_t lds = step_lds(p);
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, step_fn(p), 64, lds) != hipSuccess) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, step_fn(p), step_threads(p), lds) != hipSuccess) {
         (void)hipGetLastError();
         return 0;
     }

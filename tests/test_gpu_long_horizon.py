@@ -106,6 +106,22 @@ def test_wide_across_the_finish_field_wrap():
     g.close()
 
 
+@pytest.mark.parametrize("blocks", [1, 3])
+def test_wide_launch_shape_does_not_change_results(blocks):
+    # fewer workgroups than replicas: each runs several replicas in turn
+    cfg = preset("wide")
+    ref = Scheduler(cfg)
+    threads, nb = ref.launch()
+    assert threads == 512 and nb == ref.R
+    ref.step(300)
+    g = Scheduler(cfg)
+    g.set_launch(0, blocks)
+    assert g.launch() == (512, blocks)
+    g.step(300)
+    assert_same(g.export(), ref.export(), "wide in %d blocks" % blocks)
+    assert np.array_equal(g.digests(), ref.digests())
+
+
 def _random_cfg(case):
     from test_oracle_exact import _random_cfg as rc
     return rc(random.Random(7000 + case))
