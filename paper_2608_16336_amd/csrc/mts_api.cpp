@@ -120,10 +120,7 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.prompt_g = o; o = up256(o + guide_bytes(T.prompt));
     L.output_g = o; o = up256(o + guide_bytes(T.output));
     L.group_of = o; o = up256(o + size_t(R) * 2);
-    L.meta = o;     o = up256(o + N);
-    L.hot = o;      o = up256(o + N * 4);
-    L.seq = o;      o = up256(o + N * 4);
-    L.tarr = o;     o = up256(o + N * 4);
+    L.slot = o;     o = up256(o + N * 16);
     L.freeb = o;    o = up256(o + size_t(R) * I * 4);
     L.mig = o;      o = up256(o + size_t(R) * I * 16);
     L.drain = o;    o = up256(o + size_t(R) * I);
@@ -201,10 +198,7 @@ Params make_params(const mts_ctx* h)
     p.prompt_g = reinterpret_cast<const uint32_t*>(d + L.prompt_g);
     p.output_g = reinterpret_cast<const uint32_t*>(d + L.output_g);
     p.group_of = reinterpret_cast<const uint16_t*>(d + L.group_of);
-    p.meta = reinterpret_cast<uint8_t*>(d + L.meta);
-    p.hot = reinterpret_cast<uint32_t*>(d + L.hot);
-    p.seq = reinterpret_cast<uint32_t*>(d + L.seq);
-    p.tarr = reinterpret_cast<uint32_t*>(d + L.tarr);
+    p.slot = reinterpret_cast<uint4*>(d + L.slot);
     p.freeb = reinterpret_cast<int32_t*>(d + L.freeb);
     p.mig = reinterpret_cast<int32_t*>(d + L.mig);
     p.drain = reinterpret_cast<uint8_t*>(d + L.drain);
@@ -582,28 +576,22 @@ int mts_export_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     auto get = [&](void* dst, size_t off, size_t n) {
         if (e == hipSuccess && dst && n) e = hipMemcpy(dst, h->dev + off, n, hipMemcpyDeviceToHost);
     };
-    // the device marks an empty slot by its word alone, and an inbound
-    // reservation by its word and meta; their other fields are zero in the
-    // canonical state
-    std::vector<uint32_t> w;
+    // slot records {word, meta, seq, arrival tick}; the device marks an empty
+    // slot by its word alone, and an inbound reservation by its word and
+    // meta; their other fields are zero in the canonical state
     if (v->lr || v->meta || v->seq || v->tarr) {
-        w.resize(size_t(nr) * IS);
-        get(w.data(), L.hot + size_t(r0) * IS * 4, w.size() * 4);
-    }
-    if (v->lr && e == hipSuccess)
-        for (size_t k = 0; k < w.size(); ++k) v->lr[k] = word_to_lr(w[k], h->tick);
-    get(v->meta, L.meta + size_t(r0) * IS, size_t(nr) * IS);
-    get(v->seq, L.seq + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
-    get(v->tarr, L.tarr + size_t(r0) * IS * 4, size_t(nr) * IS * 4);
-    if (e == hipSuccess)
-        for (size_t k = 0; k < w.size(); ++k) {
-            const uint32_t st = w[k] >> 30;
-            if (w[k] == 0 && v->meta) v->meta[k] = 0;
-            if (w[k] == 0 || st == kInbound) {
-                if (v->seq) v->seq[k] = 0;
-                if (v->tarr) v->tarr[k] = 0;
+        std::vector<uint32_t> rec(size_t(nr) * IS * 4);
+        get(rec.data(), L.slot + size_t(r0) * IS * 16, rec.size() * 4);
+        if (e == hipSuccess)
+            for (size_t k = 0; k < size_t(nr) * IS; ++k) {
+                const uint32_t w = rec[4 * k], st = w >> 30;
+                const bool gone = w == 0 || st == kInbound;
+                if (v->lr) v->lr[k] = word_to_lr(w, h->tick);
+                if (v->meta) v->meta[k] = w == 0 ? 0 : uint8_t(rec[4 * k + 1]);
+                if (v->seq) v->seq[k] = gone ? 0 : rec[4 * k + 2];
+                if (v->tarr) v->tarr[k] = gone ? 0 : rec[4 * k + 3];
             }
-        }
+    }
     get(v->free, L.freeb + size_t(r0) * I * 4, size_t(nr) * I * 4);
     get(v->mig, L.mig + size_t(r0) * I * 16, size_t(nr) * I * 16);
     get(v->next_seq, L.next_seq + size_t(r0) * 4, size_t(nr) * 4);
@@ -634,6 +622,7 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     if (r0 > h->R || nr > h->R - r0) return MTS_ERANGE;
     const size_t IS = size_t(h->I) * h->S, I = h->I;
     std::vector<uint32_t> w(size_t(nr) * IS);
+    std::vector<uint32_t> rec(size_t(nr) * IS * 4);
     // structural checks keep every index the kernel derives from the state in
     // range; running requests are re-encoded relative to the handle's tick
     for (uint32_t r = 0; r < nr; ++r) {
@@ -682,10 +671,13 @@ int mts_import_state(mts_handle h, uint32_t r0, uint32_t nr, const mts_state_vie
     auto put = [&](size_t off, const void* src, size_t n) {
         if (e == hipSuccess && n) e = hipMemcpy(h->dev + off, src, n, hipMemcpyHostToDevice);
     };
-    put(L.meta + size_t(r0) * IS, v->meta, size_t(nr) * IS);
-    put(L.hot + size_t(r0) * IS * 4, w.data(), w.size() * 4);
-    put(L.seq + size_t(r0) * IS * 4, v->seq, size_t(nr) * IS * 4);
-    put(L.tarr + size_t(r0) * IS * 4, v->tarr, size_t(nr) * IS * 4);
+    for (size_t k = 0; k < w.size(); ++k) {
+        rec[4 * k] = w[k];
+        rec[4 * k + 1] = v->meta[k];
+        rec[4 * k + 2] = v->seq[k];
+        rec[4 * k + 3] = v->tarr[k];
+    }
+    put(L.slot + size_t(r0) * IS * 16, rec.data(), rec.size() * 4);
     put(L.freeb + size_t(r0) * I * 4, v->free, size_t(nr) * I * 4);
     put(L.mig + size_t(r0) * I * 16, v->mig, size_t(nr) * I * 16);
     put(L.next_seq + size_t(r0) * 4, v->next_seq, size_t(nr) * 4);

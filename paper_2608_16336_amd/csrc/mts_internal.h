@@ -57,7 +57,7 @@ int build_tables(const mts_cfg& c, Tables& T);
 struct Layout {
     size_t tier_q, hq, group_K, count_q, prompt_q, output_q, group_of;  // tables
     size_t count_g, prompt_g, output_g;                                 // guide tables
-    size_t meta, hot, seq, tarr;                                        // [R][I][S]
+    size_t slot;                                                        // [R][I][S] uint4 records
     size_t freeb, mig, drain;                                           // [R][I], [R][I][4], [R][I] u8
     size_t hist;                                                        // [R][2][10][MTS_HIST_BINS] u32
     size_t svc;                                                         // [R][I] i64 INFaaS estimate
@@ -103,10 +103,7 @@ struct Params {
     const uint32_t* prompt_g;
     const uint32_t* output_g;
     const uint16_t* group_of;      // [R]
-    uint8_t* meta;
-    uint32_t* hot;
-    uint32_t* seq;
-    uint32_t* tarr;
+    uint4* slot;                   // [R][I][S] {slot word, meta, seq, arrival tick}
     int32_t* freeb;
     int32_t* mig;
     uint8_t* drain;

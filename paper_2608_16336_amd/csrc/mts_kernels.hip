@@ -8,7 +8,9 @@
 //               state lives in HBM and is touched only by events.
 //   k_init      empty clusters; k_digest the canonical state digest.
 //
-// Slot word ("hot", u32, bits 31..30 = status):
+// Slot record (uint4 per slot): x = slot word, y = meta, z = seq, w = arrival
+// tick, so that an event reads or writes one 16-byte record.  Slot word (u32,
+// bits 31..30 = status):
 //   waiting   01 | rem (14 bits) | len (16 bits)
 //   running   10 | fin mod 2^14  | final length (16 bits)
 //   inbound   11 | 0 (with meta; seq and arrival tick keep whatever the slot
@@ -162,10 +164,7 @@ struct Ctx {
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
     uint32_t wmask, wcap;
-    uint32_t* hot;
-    uint8_t* meta;
-    uint32_t* seq;
-    uint32_t* tarr;
+    uint4* slot;               // [I][S] slot records of this replica
     uint32_t I, S, W, RB, shift, bmask, M, K;
     int hq[kTiers];
 };
@@ -176,6 +175,16 @@ struct Ctx {
 // (0: unknown, the next pass reads the instance)
 __device__ __forceinline__ int* xleft(const Ctx& C) { return reinterpret_cast<int*>(C.ext); }
 __device__ __forceinline__ unsigned* wlb(const Ctx& C) { return reinterpret_cast<unsigned*>(C.ext + 8); }
+// fields of slot record x
+__device__ __forceinline__ uint32_t& s_word(const Ctx& C, size_t x) { return reinterpret_cast<uint32_t*>(C.slot + x)[0]; }
+__device__ __forceinline__ uint32_t& s_meta(const Ctx& C, size_t x) { return reinterpret_cast<uint32_t*>(C.slot + x)[1]; }
+__device__ __forceinline__ uint32_t& s_tarr(const Ctx& C, size_t x) { return reinterpret_cast<uint32_t*>(C.slot + x)[3]; }
+// word and meta of slot record x in one 8-byte store
+__device__ __forceinline__ void s_set_wm(const Ctx& C, size_t x, uint32_t w, uint32_t m)
+{
+    *reinterpret_cast<uint2*>(C.slot + x) = make_uint2(w, m);
+}
+
 // addresses of the per-replica headroom and snapshot arrays (null: static headroom)
 __device__ __forceinline__ int32_t* ext_hqr(const Params& P)
 {
@@ -629,9 +638,8 @@ __device__ inline bool preempt(const Ctx& C, int i, uint32_t t, int lane)
 #pragma unroll
             for (int g = 0; g < GR; ++g) {
                 const bool in = c0 + g < nch;
-                v[g] = in ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
-                m[g] = in ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
-                q[g] = in ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
+                const uint4 rr = in ? C.slot[b + (c0 + g) * 64 + lane] : make_uint4(0u, 0u, 0u, 0u);
+                v[g] = rr.x; m[g] = rr.y; q[g] = rr.z;
             }
 #pragma unroll
             for (int g = 0; g < GR; ++g) {
@@ -685,9 +693,8 @@ __device__ inline bool preempt(const Ctx& C, int i, uint32_t t, int lane)
             const bool vm = (m & kMigrating) != 0;
             uint32_t vta = 0;
             if (lane == (vs & 63)) {
-                C.hot[b + vs] = vw;
-                C.meta[b + vs] = uint8_t(vmeta);
-                vta = C.tarr[b + vs];
+                s_set_wm(C, b + vs, vw, vmeta);
+                vta = s_tarr(C, b + vs);
             }
             vta = rlu(vta, vs & 63);
             wheel_erase(C, fin, i, vs, lane);
@@ -734,17 +741,18 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane, bo
     bool ab = false;
     for (int c = 0; c < nch; ++c) {
         const int s = c * 64 + lane;
-        const uint32_t v = C.hot[b + s];
+        const uint4 rec = C.slot[b + s];
+        const uint32_t v = rec.x;
         const bool run = wst(v) == 2u;
         const uint32_t fin = fin_of(v, t);
         const bool f = run && fin == t;
         if (f) {
             const uint32_t lenf = wlo(v);
             freed += blocks_of(lenf, C.shift);
-            const uint32_t m = C.meta[b + s];
+            const uint32_t m = rec.y;
             const int tier = int((m >> 2) & 15u);
             stat(C, tier * 8 + kFinished, 1);
-            const uint32_t e2e = t - C.tarr[b + s];
+            const uint32_t e2e = t - rec.w;
             stat(C, tier * 8 + kE2e, e2e);
             hist_add(C, kHistE2e, tier, e2e);
             if (C.fsum) { atomicAdd(&C.fsum[i], static_cast<unsigned long long>(e2e)); atomicAdd(&C.fcnt[i], 1); }
@@ -753,7 +761,7 @@ __device__ inline void finish_scan(const Ctx& C, int i, uint32_t t, int lane, bo
             // being copied out: the source of its instance's migration record
             // (the same test as the wheel visit's)
             if (C.mig[4 * i] >= 0 && C.mig[4 * i + 1] == s) ab = true;
-            C.hot[b + s] = 0;  // the word alone marks the slot empty
+            s_word(C, b + s) = 0;  // the word alone marks the slot empty
         } else if (run && (fin & C.wmask) == bk) {
             wheel_put(C, fin, i, s);
         }
@@ -815,7 +823,7 @@ __device__ inline uint32_t finish_batch(const Ctx& C, uint32_t t, int lane, uint
         atomicSub(&C.held[i], bl);
         atomicSub(&C.B[i], 1);
         atomicSub(&C.live[i], 1);
-        C.hot[idx] = 0;  // the word alone marks the slot empty
+        s_word(C, idx) = 0;  // the word alone marks the slot empty
     }
     abort_any = abort_any || ballot(ab) != 0;
     wave_sync();
@@ -860,7 +868,7 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane, bool& abo
         const bool valid = inb && uint32_t(i) < C.I && uint32_t(s) < C.S;
         const size_t idx = size_t(i) * C.S + s;
         uint32_t v = 0, m = 0, ta = 0;
-        if (valid) { v = C.hot[idx]; m = C.meta[idx]; ta = C.tarr[idx]; }
+        if (valid) { const uint4 rec = C.slot[idx]; v = rec.x; m = rec.y; ta = rec.w; }
         kept = finish_batch(C, t, lane, ent, kept, inb, e, v, m, ta, abort_any);
     }
     wheel_set_count(C, bk, kept, lane);
@@ -912,8 +920,7 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
         const uint32_t len = wlo(word), rem = wmid(word);
         const uint32_t fin = t + rem;
         const size_t hb = b + slot;
-        C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
-        C.meta[hb] = uint8_t((meta & ~3u) | kRunning | kAdmitted);
+        s_set_wm(C, hb, kRunW | ((fin & kFin) << 16) | (len + rem), (meta & ~3u) | kRunning | kAdmitted);
         const int tier = int((meta >> 2) & 15u);
         if (!(meta & kAdmitted)) {
             stat(C, tier * 8 + kAdmittedCnt, 1);
@@ -980,9 +987,8 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
 #pragma unroll
         for (int g = 0; g < GR; ++g) {
             const bool in = c0 + g < nch;
-            v[g] = in ? C.hot[b + (c0 + g) * 64 + lane] : 0u;
-            m[g] = in ? C.meta[b + (c0 + g) * 64 + lane] : 0u;
-            q[g] = in ? C.seq[b + (c0 + g) * 64 + lane] : 0u;
+            const uint4 rr = in ? C.slot[b + (c0 + g) * 64 + lane] : make_uint4(0u, 0u, 0u, 0u);
+            v[g] = rr.x; m[g] = rr.y; q[g] = rr.z;
         }
 #pragma unroll
         for (int g = 0; g < GR; ++g) {
@@ -1036,7 +1042,7 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
     }
     const int mys = int(mysd & 0xFFFu);
     uint32_t w = 0, mt = 0, ta = 0;
-    if (lane < got) { w = C.hot[b + mys]; mt = C.meta[b + mys]; ta = C.tarr[b + mys]; }
+    if (lane < got) { const uint4 rec = C.slot[b + mys]; w = rec.x; mt = rec.y; ta = rec.w; }
     const bool complete = got >= C.nwait[i];
     if (lane == 0) C.frs[i] = 0;
     admit_ranked(C, i, t, lane, got, myk, w, mt, ta, mys, complete);
@@ -1065,10 +1071,8 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
         for (int g = 0; g < GR; ++g) {
             const bool in = c0 + g < nch;
             const size_t sb = b + (c0 + g) * 64 + lane;
-            v[g] = in ? C.hot[sb] : 0u;
-            m[g] = in ? C.meta[sb] : 0u;
-            q[g] = in ? C.seq[sb] : 0u;
-            a[g] = in ? C.tarr[sb] : 0u;
+            const uint4 rr = in ? C.slot[sb] : make_uint4(0u, 0u, 0u, 0u);
+            v[g] = rr.x; m[g] = rr.y; q[g] = rr.z; a[g] = rr.w;
         }
 #pragma unroll
         for (int g = 0; g < GR; ++g) {
@@ -1187,17 +1191,18 @@ __device__ inline void promote_waiting(const Ctx& C, const Params& P, uint32_t t
         unsigned long long kmin = kNone;
         for (int c = 0; c < nch; ++c) {
             const int s = c * 64 + lane;
-            if (wst(C.hot[b + s]) != 1u) continue;
-            const uint32_t m = C.meta[b + s], tier = (m >> 2) & 15u, ta = C.tarr[b + s];
+            const uint4 rec = C.slot[b + s];
+            if (wst(rec.x) != 1u) continue;
+            const uint32_t m = rec.y, tier = (m >> 2) & 15u, ta = rec.w;
             lo = ta < lo ? ta : lo;
             late = late || ta > t;
             if (tier == 0) continue;
             const uint32_t q = P.ext[kXAge + tier];
             if (q != 0 && t - ta >= q) {
-                C.meta[b + s] = uint8_t(m - 4u);  // tier field at bits 2..5
+                s_meta(C, b + s) = m - 4u;  // tier field at bits 2..5
                 any = true;
                 head = head || s == h;
-                const unsigned long long k = (rank_of(C, tier - 1u) << 32) | C.seq[b + s];
+                const unsigned long long k = (rank_of(C, tier - 1u) << 32) | rec.z;
                 kmin = k < kmin ? k : kmin;
             }
         }
@@ -1302,7 +1307,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
 #pragma unroll
         for (int p = 0; p < kTiers; ++p) C.hq[p] = hq[p];
         const size_t rb = size_t(r) * I * S;
-        C.hot = P.hot + rb; C.meta = P.meta + rb; C.seq = P.seq + rb; C.tarr = P.tarr + rb;
+        C.slot = P.slot + rb;
         C.wheel = P.wheel + size_t(r) * wsz * P.wcap;
         C.hist = P.hist + size_t(r) * kHistPerReplica;
 
@@ -1351,9 +1356,8 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                     const bool in = f0 + g < nfl;
                     const uint32_t fo = (f0 + g) / W;
                     const size_t fs = (size_t(fo * NW + wid) * W + (f0 + g - fo * W)) * 64 + lane;
-                    v[g] = in ? C.hot[fs] : 0u;
-                    m[g] = in ? C.meta[fs] : 0u;
-                    q[g] = in ? C.seq[fs] : 0u;
+                    const uint4 rr = in ? C.slot[fs] : make_uint4(0u, 0u, 0u, 0u);
+                    v[g] = rr.x; m[g] = rr.y; q[g] = rr.z;
                 }
 #pragma unroll
                 for (int g = 0; g < GP; ++g) {
@@ -1406,7 +1410,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             block_sync<NW>();
             for (uint32_t i = tid; i < I; i += NT) {
                 const int h = C.hols[i];
-                if (h >= 0) C.hta[i] = C.tarr[size_t(i) * S + h];
+                if (h >= 0) C.hta[i] = s_tarr(C, size_t(i) * S + h);
             }
         }
         unsigned next_seq = P.next_seq[r];
@@ -1546,9 +1550,8 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                     const uint32_t pi = pf_e >> 16, ps = pf_e & 0xFFFFu;
                     const bool ok = uint32_t(lane) < pf_n && pi < I && ps < S;
                     const size_t idx = size_t(pi) * S + ps;
-                    pf_v = ok ? C.hot[idx] : 0u;
-                    pf_m = ok ? C.meta[idx] : 0u;
-                    pf_a = ok ? C.tarr[idx] : 0u;
+                    const uint4 rec = ok ? C.slot[idx] : make_uint4(0u, 0u, 0u, 0u);
+                    pf_v = rec.x; pf_m = rec.y; pf_a = rec.w;
                 }
                 // entries of the bucket two ticks ahead (three distinct buckets needed)
                 const uint32_t b2 = (t + 2u) & C.wmask;
@@ -1568,7 +1571,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                     C.freeb[d] += m[3];
                     C.inb[d] = 0;
                     const size_t db = size_t(d) * S + m[2];
-                    C.hot[db] = 0;
+                    s_word(C, db) = 0;
                     C.occ[d * W + (m[2] >> 6)] &= ~(1ull << (m[2] & 63));
                     C.live[d] -= 1;
                     m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
@@ -1620,8 +1623,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                                 const uint32_t len = wlo(w), rem = wmid(w);
                                 const uint32_t fin = t + rem;
                                 const size_t hb = size_t(i) * S + h;
-                                C.hot[hb] = kRunW | ((fin & kFin) << 16) | (len + rem);
-                                C.meta[hb] = uint8_t((m & ~3u) | kRunning | kAdmitted);
+                                s_set_wm(C, hb, kRunW | ((fin & kFin) << 16) | (len + rem), (m & ~3u) | kRunning | kAdmitted);
                                 const int tier = int((m >> 2) & 15u);
                                 if (!(m & kAdmitted)) {
                                     stat(C, tier * 8 + kAdmittedCnt, 1);
@@ -1925,10 +1927,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                         const size_t sb = size_t(tgt) * S + s;
                         const uint32_t word = kWaitW | (uint32_t((a >> 16) & 0xFFFFu) << 16) | uint32_t(a & 0xFFFFu);
                         const uint32_t meta = kWaiting | (unsigned(tier) << 2);
-                        C.hot[sb] = word;
-                        C.meta[sb] = uint8_t(meta);
-                        C.seq[sb] = seq0 + unsigned(a >> 36);
-                        C.tarr[sb] = t;
+                        C.slot[sb] = make_uint4(word, meta, seq0 + unsigned(a >> 36), t);
                         if (C.hols[tgt] == kHolPending && C.pend[tgt] == int(k0) + lane) {
                             C.hols[tgt] = s;
                             C.hwd[tgt] = word;
@@ -1962,7 +1961,8 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                 const int d = m[0];
                 if (d < 0) continue;
                 const size_t sb = size_t(i) * S + m[1], db = size_t(d) * S + m[2];
-                const uint32_t v = C.hot[sb];
+                const uint4 srec = C.slot[sb];
+                const uint32_t v = srec.x;
                 const uint32_t fin = fin_of(v, t);
                 const int bl = blocks_of(wlo(v) - (fin - t), C.shift);
                 int w = bl - m[3];
@@ -1970,10 +1970,10 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                 if (w > C.freeb[d]) {
                     C.freeb[d] += m[3];
                     C.inb[d] = 0;
-                    C.hot[db] = 0;
+                    s_word(C, db) = 0;
                     C.occ[d * W + (m[2] >> 6)] &= ~(1ull << (m[2] & 63));
                     C.live[d] -= 1;
-                    C.meta[sb] = uint8_t(C.meta[sb] & ~kMigrating);
+                    s_meta(C, sb) = srec.y & ~kMigrating;
                     m[0] = -1; m[1] = 0; m[2] = 0; m[3] = 0;
                     stat(C, kMigAborted, 1);
                     set_f(C, d);
@@ -1983,14 +1983,11 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                 m[3] += w;
                 C.inb[d] += w;
                 if (m[3] == bl) {
-                    const uint32_t mm = C.meta[sb];
+                    const uint32_t mm = srec.y;
                     const int tier = int((mm >> 2) & 15u);
                     const int rr = int((wlo(v) - fin - 1u) & C.bmask);
-                    C.hot[db] = v;
-                    C.meta[db] = uint8_t((mm & ~(3u | kMigrating)) | kRunning);
-                    C.seq[db] = C.seq[sb];
-                    C.tarr[db] = C.tarr[sb];
-                    C.hot[sb] = 0;
+                    C.slot[db] = make_uint4(v, (mm & ~(3u | kMigrating)) | kRunning, srec.z, srec.w);
+                    s_word(C, sb) = 0;
                     C.occ[i * W + (m[1] >> 6)] &= ~(1ull << (m[1] & 63));
                     C.live[i] -= 1;
                     C.freeb[i] += bl;
@@ -2167,9 +2164,8 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                             const size_t dsb = size_t(dst) * S + ds, hb = size_t(src) * S + h;
                             const uint32_t hw = C.hwd[src], hm = C.hmt[src], ht = C.hta[src];
                             const unsigned long long key = C.holk[src];
-                            C.hot[dsb] = hw; C.meta[dsb] = uint8_t(hm);
-                            C.seq[dsb] = uint32_t(key); C.tarr[dsb] = ht;
-                            C.hot[hb] = 0;
+                            C.slot[dsb] = make_uint4(hw, hm, uint32_t(key), ht);
+                            s_word(C, hb) = 0;
                             C.occ[src * W + (h >> 6)] &= ~(1ull << (h & 63));
                             C.occ[dst * W + (ds >> 6)] |= 1ull << (ds & 63);
                             C.live[src] -= 1; C.nwait[src] -= 1;
@@ -2198,9 +2194,8 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                                 for (int g = 0; g < GC; ++g) {
                                     const bool in = c0 + g < nch;
                                     const size_t sb = sbase + (c0 + g) * 64 + lane;
-                                    v[g] = in ? C.hot[sb] : 0u;
-                                    m[g] = in ? C.meta[sb] : 0u;
-                                    q[g] = in ? C.seq[sb] : 0u;
+                                    const uint4 rr = in ? C.slot[sb] : make_uint4(0u, 0u, 0u, 0u);
+                                    v[g] = rr.x; m[g] = rr.y; q[g] = rr.z;
                                 }
 #pragma unroll
                                 for (int g = 0; g < GC; ++g) {
@@ -2219,11 +2214,10 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                             const int cs = rl(bs, ffs64(ballot(bk == mx)));
                             if (lane == 0) {
                                 const size_t dsb = size_t(pdst) * S + pds;
-                                C.hot[dsb] = kInbW;
-                                C.meta[dsb] = uint8_t(kInbound);
+                                s_set_wm(C, dsb, kInbW, kInbound);
                                 C.occ[pdst * W + (pds >> 6)] |= 1ull << (pds & 63);
                                 C.live[pdst] += 1;
-                                C.meta[sbase + cs] = uint8_t(C.meta[sbase + cs] | kMigrating);
+                                s_meta(C, sbase + cs) |= kMigrating;
                                 int* m = &C.mig[4 * psrc];
                                 m[0] = pdst; m[1] = cs; m[2] = pds; m[3] = 0;
                                 stat(C, kMigStarted, 1);
@@ -2266,7 +2260,7 @@ __global__ void k_init(Params P)
     const size_t nslots = size_t(P.R) * P.I * P.S;
     const size_t stride = size_t(gridDim.x) * blockDim.x;
     const size_t t0 = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    for (size_t s = t0; s < nslots; s += stride) { P.meta[s] = 0; P.hot[s] = 0; P.seq[s] = 0; P.tarr[s] = 0; }
+    for (size_t s = t0; s < nslots; s += stride) P.slot[s] = make_uint4(0u, 0u, 0u, 0u);
     for (size_t j = t0; j < size_t(P.R) * P.I; j += stride) {
         P.freeb[j] = int32_t(P.M);
         P.mig[4 * j] = -1; P.mig[4 * j + 1] = 0; P.mig[4 * j + 2] = 0; P.mig[4 * j + 3] = 0;
@@ -2289,8 +2283,9 @@ __global__ void k_shift_clock(Params P, uint32_t delta)
     const size_t nslots = size_t(P.R) * P.I * P.S;
     const size_t stride = size_t(gridDim.x) * blockDim.x;
     for (size_t s = size_t(blockIdx.x) * blockDim.x + threadIdx.x; s < nslots; s += stride) {
-        const uint32_t v = P.hot[s];
-        if (wst(v) == 2u) P.hot[s] = (v & ~(kFin << 16)) | (((wmid(v) + delta) & kFin) << 16);
+        uint32_t* w = reinterpret_cast<uint32_t*>(P.slot + s);
+        const uint32_t v = *w;
+        if (wst(v) == 2u) *w = (v & ~(kFin << 16)) | (((wmid(v) + delta) & kFin) << 16);
     }
 }
 
@@ -2328,13 +2323,14 @@ __global__ __launch_bounds__(256) void k_digest(Params P, uint32_t r0, uint32_t 
     for (size_t s = threadIdx.x; s < IS; s += blockDim.x) {
         // an empty slot has a zero word; an inbound reservation's seq and
         // arrival tick are zero in the canonical state (the device leaves them)
-        const uint32_t hw = P.hot[rb + s];
+        const uint4 rec = P.slot[rb + s];
+        const uint32_t hw = rec.x;
         if (hw == 0u) continue;
         const bool inb = wst(hw) == kInbound;
-        const unsigned m = P.meta[rb + s];
+        const unsigned m = rec.y;
         const unsigned long long a = static_cast<unsigned long long>(canonical_lr(hw, tick)) |
-                                     (static_cast<unsigned long long>(inb ? 0u : P.seq[rb + s]) << 32);
-        const unsigned long long b = static_cast<unsigned long long>(inb ? 0u : P.tarr[rb + s]) |
+                                     (static_cast<unsigned long long>(inb ? 0u : rec.z) << 32);
+        const unsigned long long b = static_cast<unsigned long long>(inb ? 0u : rec.w) |
                                      (static_cast<unsigned long long>(m) << 32);
         const unsigned long long p = mix64(gm + 2ull * s + 1ull);
         d += mix64(p ^ a) + mix64(p ^ b);
