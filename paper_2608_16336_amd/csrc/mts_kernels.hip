@@ -874,28 +874,39 @@ __device__ inline void finish_tick(const Ctx& C, uint32_t t, int lane, bool& abo
     wheel_set_count(C, bk, kept, lane);
 }
 
-// Adds to stats[tier * 8 + field], for every tier, the number of lanes with f
-// set among the lanes of that tier.  The lanes' tiers are non-decreasing
-// (arrivals are sorted by tier) unless scheduling is tier-blind; lanes that
-// hold no arrival carry tier 15.
-__device__ __forceinline__ void tier_stat(const Ctx& C, int tier, bool f, int field, int lane)
+// Adds to stats[tier * 8 + fd0], for every tier, the number of lanes of that
+// tier with f0 set, and likewise for (f1, fd1) and (f2, fd2): the boundaries
+// of the tiers' runs of lanes are found once.  The lanes' tiers are
+// non-decreasing (arrivals are sorted by tier) unless scheduling is
+// tier-blind; lanes that hold no arrival carry tier 15.
+__device__ __forceinline__ void tier_stat3(const Ctx& C, int tier, bool f0, int fd0, bool f1, int fd1, bool f2, int fd2,
+                                           int lane)
 {
+    const unsigned long long m0 = ballot(f0), m1 = ballot(f1), m2 = ballot(f2);
     if (C.blind) {
         for (int p = 0; p < int(C.K); ++p) {
-            const int c = __popcll(ballot(f && tier == p));
-            if (lane == 0 && c) stat(C, p * 8 + field, c);
+            const unsigned long long tp = ballot(tier == p);
+            const int c0 = __popcll(m0 & tp), c1 = __popcll(m1 & tp), c2 = __popcll(m2 & tp);
+            if (lane == 0) {
+                if (c0) stat(C, p * 8 + fd0, c0);
+                if (c1) stat(C, p * 8 + fd1, c1);
+                if (c2) stat(C, p * 8 + fd2, c2);
+            }
         }
         return;
     }
     const int tn = __builtin_amdgcn_update_dpp(tier, tier, 0x130, 0xF, 0xF, false);  // wave_shl:1 (lane 63 keeps its own)
     const bool last = lane == 63 || tn != tier;
-    const unsigned long long bm = ballot(last), fm = ballot(f);
+    const unsigned long long bm = ballot(last);
     if (last && tier < kTiers) {
         const unsigned long long below = bm & lanemask_lt();
         const int start = below ? 64 - __clzll(static_cast<long long>(below)) : 0;
         const unsigned long long upto = lane == 63 ? ~0ull : (1ull << (lane + 1)) - 1ull;
-        const int c = __popcll(fm & upto & ~((1ull << start) - 1ull));
-        if (c) stat(C, tier * 8 + field, c);
+        const unsigned long long run = upto & ~((1ull << start) - 1ull);
+        const int c0 = __popcll(m0 & run), c1 = __popcll(m1 & run), c2 = __popcll(m2 & run);
+        if (c0) stat(C, tier * 8 + fd0, c0);
+        if (c1) stat(C, tier * 8 + fd1, c1);
+        if (c2) stat(C, tier * 8 + fd2, c2);
     }
 }
 
@@ -1440,6 +1451,12 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
         constexpr uint32_t kNoPf = 0xFFFFFFFFu;
         uint32_t pf_n = kNoPf, pf_e = 0, pf_v = 0, pf_m = 0, pf_a = 0;
         uint32_t pf2_n = kNoPf, pf2_e = 0;
+        // (wave 0) ticks to the next pairing round, and whether a migration
+        // record may be active (the staged-copy phase is skipped otherwise)
+        uint32_t mig_left = (P.mig_interval - t0u % P.mig_interval) % P.mig_interval;
+        bool migs = false;
+        for (uint32_t i = lane; i < I; i += 64) migs = migs || C.mig[4 * i] >= 0;
+        migs = ballot(migs) != 0;
         unsigned long long a_nx = uint32_t(lane) < lim ? recs[lane] : 0ull;
         for (uint32_t tl = 0; tl < nt; ++tl) {
             const uint32_t t = t0u + tl;
@@ -1733,11 +1750,6 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             if (n == 0)
                 for (uint32_t i = lane; i < I; i += 64) C.frs[i] = C.nwait[i] == 0;
             if (n > 0) {
-                for (uint32_t k0 = 0; k0 < n; k0 += 64) {
-                    const unsigned long long a = k0 == 0 ? a0 : (k0 + lane < n ? rec[k0 + lane] : 0);
-                    const int tier = k0 + lane < n ? int((a >> 32) & 15u) : 15;
-                    tier_stat(C, tier, true, kArrived, lane);
-                }
                 const unsigned seq0 = next_seq;
                 next_seq += n;
                 // per-instance dispatch state in registers: lane l, register j <-> instance 64 j + l
@@ -1746,7 +1758,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                 // (an arrival that becomes an instance's head of line updates its
                 // demand, num and F in LDS at once: only that instance's lane
                 // touches them until the write-back)
-                double key[IPL];
+                double key[IPL], fnew[IPL];
                 int live_r[IPL], nadd[IPL], pend_r[IPL], num_r[IPL], hold_r[IPL];
                 unsigned long long hk_r[IPL];
 #pragma unroll
@@ -1756,6 +1768,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                     pend_r[j] = -1;
                     num_r[j] = 0;
                     hold_r[j] = 0;
+                    fnew[j] = 0.0;
                     if (i < I) {
                         live_r[j] = C.live[i];
                         num_r[j] = C.num[i];
@@ -1839,7 +1852,8 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                                     const int dem = blocks_of(uint32_t(ak & 0xFFFFu), C.shift);
                                     num_r[j] -= 256 * (dem - hold_r[j]);
                                     hold_r[j] = dem;
-                                    if (!infaas) key[j] = double(num_r[j]) / double(C.den[lc + 64 * j]);
+                                    fnew[j] = double(num_r[j]) / double(C.den[lc + 64 * j]);
+                                    if (!infaas) key[j] = fnew[j];
                                 }
                                 if (infaas) key[j] -= double(P.alpha256) * double(m);
                                 if (nl >= int(S)) key[j] = -__builtin_inf();
@@ -1863,7 +1877,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                         if (pend_r[j] >= 0) {
                             C.num[i] = num_r[j];
                             C.hold[i] = hold_r[j];
-                            C.fd[i] = double(num_r[j]) / double(C.den[i]);
+                            C.fd[i] = fnew[j];
                         }
                         if (C.ext && nadd[j] > 0) wlb(C)[i] = t < wlb(C)[i] ? t : wlb(C)[i];
                         if (C.td && nadd[j] > 0) {
@@ -1935,9 +1949,12 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                             C.hta[tgt] = t;
                         }
                     }
+                    // every arrival is dispatched (tgt >= 0) or rejected: no free slot
+                    // anywhere (-1), or dropped by the occupancy check (-2, counted
+                    // above)
                     const int vt = lane < int(cn) ? tier : 15;
-                    tier_stat(C, vt, tgt >= 0, kDispatched, lane);
-                    tier_stat(C, vt, tgt == -1 && lane < int(cn), kRejected, lane);
+                    tier_stat3(C, vt, lane < int(cn), kArrived, tgt >= 0, kDispatched, tgt == -1 && lane < int(cn),
+                               kRejected, lane);
                     wave_sync();
                 }
                 if (lane == 0 && nfall) stat(C, kDrainFallback, unsigned(nfall));
@@ -1955,6 +1972,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             // ===================== E1: staged copies =====================
             // a commit leaves the source slot: its wheel entry (source slot in
             // gtmp, finish tick in pend) is erased after the loop
+            if (migs) {
             for (uint32_t i = lane; i < I; i += 64) C.gtmp[i] = -1;
             for (uint32_t i = lane; i < I; i += 64) {
                 int* m = &C.mig[4 * i];
@@ -2019,9 +2037,15 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                 }
             }
             wave_sync();
+            bool live = false;
+            for (uint32_t i = lane; i < I; i += 64) live = live || C.mig[4 * i] >= 0;
+            migs = ballot(live) != 0;
+            }
 
             // ===================== E2: pairing on interval ticks =====================
-            if (!infaas && t % P.mig_interval == 0) {
+            const bool mig_tick = mig_left == 0;
+            mig_left = mig_tick ? P.mig_interval - 1u : mig_left - 1u;
+            if (!infaas && mig_tick) {
                 bool neg = false;
                 for (uint32_t i = lane; i < I; i += 64) neg |= C.num[i] < 0 || C.drn[i];
                 if (ballot(neg)) {
@@ -2222,6 +2246,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                                 m[0] = pdst; m[1] = cs; m[2] = pds; m[3] = 0;
                                 stat(C, kMigStarted, 1);
                             }
+                            migs = true;
                             wave_sync();
                         }
                         if (sm) break;
