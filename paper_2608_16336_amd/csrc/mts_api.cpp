@@ -292,15 +292,18 @@ int mts_create(const mts_cfg* cfg, void* dev_buf, size_t bytes, hipStream_t stre
         return MTS_EDEVICE;
     }
     if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, 0, ext_state(x->cfg)) > size_t(max_lds)) { delete x; return MTS_EINVAL; }
-    // queue cache depth: the deepest of 7, 3, 1 that keeps the step kernel's
-    // blocks per CU (the cache only saves rescans; a lost block per CU costs
-    // more: with no spare room per CU the dispatcher cannot place every
-    // block at once)
+    // queue cache depth: the deepest of 7, 3, 1 (15, 11, 7, 3, 1 for 128 or
+    // more instances, whose long burst queues it spares rescans of 2048
+    // slots) that keeps the step kernel's blocks per CU (the cache only saves
+    // rescans; a lost block per CU costs more: with no spare room per CU the
+    // dispatcher cannot place every block at once; and for small instances a
+    // deeper cache costs more in insertions than it saves)
     {
         Params p = make_params(x);
         p.qdepth = 0;
         const int base = step_blocks_per_cu(p);
-        for (uint32_t d : {7u, 3u, 1u}) {
+        for (uint32_t d : {15u, 11u, 7u, 3u, 1u}) {
+            if (d > 7 && x->I < 128) continue;
             p.qdepth = d;
             if (lds_bytes(x->I, x->S, x->cfg.block_tokens, x->wsz, x->cfg.dispatch_policy, d, ext_state(x->cfg)) > size_t(max_lds)) continue;
             if (step_blocks_per_cu(p) >= base) { x->qdepth = d; break; }

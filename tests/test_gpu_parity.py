@@ -444,7 +444,8 @@ def test_queue_cache_depth_does_not_change_results(depth):
 
 def test_queue_cache_depth_is_validated():
     g = Scheduler(preset("tiny"))
-    assert 0 <= g.queue_cache <= 7
+    # the automatic depth: at most 7, 15 for 128 or more instances
+    assert 0 <= g.queue_cache <= (15 if g.I >= 128 else 7)
     with pytest.raises(MtsError):
         g.queue_cache = 16
 
