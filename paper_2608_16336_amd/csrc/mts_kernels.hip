@@ -115,9 +115,9 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     o = al8(o);
     L.ext = o;   o += ext ? 8 + IM * 4 : 0;
     // multi-wave kernels: values the waves combine (the auto-scaling sum, an
-    // abort flag)
+    // abort flag, the admission work list's length and next entry)
     o = al8(o);
-    L.blk = o;   o += waves_for(IM) > 1 ? 16 : 0;
+    L.blk = o;   o += waves_for(IM) > 1 ? 32 : 0;
     L.total = al8(o);
     return L;
 }
@@ -157,9 +157,12 @@ struct Ctx {
     // region read through the accessors below
     unsigned char* ext;
     // multi-wave kernels only (null otherwise): the block area, a 64-bit sum
-    // and a flag the waves combine
+    // and a flag the waves combine, the admission work list's length and the
+    // next entry to hand out (the list itself is kept in order[])
     long long* bsum;
     int* bflag;
+    int* wln;
+    int* wlnext;
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -252,6 +255,8 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.ext = EXT ? reinterpret_cast<unsigned char*>(base + Y.ext) : nullptr;
     C.bsum = waves_for(IM) > 1 ? reinterpret_cast<long long*>(base + Y.blk) : nullptr;
     C.bflag = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 8) : nullptr;
+    C.wln = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 12) : nullptr;
+    C.wlnext = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 16) : nullptr;
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
@@ -1172,6 +1177,66 @@ __device__ inline void admit_fresh(const Ctx& C, int i, uint32_t t, int lane)
     admit_ranked(C, i, t, lane, w, key, word, meta, ta, slot);
 }
 
+// Admission of instance i's known head of line, which fits (per lane: the
+// lane-parallel rounds call it for their lanes' instances; the next head of
+// line comes from the queue cache or is left unknown).
+__device__ inline void admit_head(const Ctx& C, int i, uint32_t t)
+{
+    const int h = C.hols[i], dem = C.hold[i];
+    const uint32_t w = C.hwd[i], m = C.hmt[i];
+    const uint32_t len = wlo(w), rem = wmid(w);
+    const uint32_t fin = t + rem;
+    const size_t hb = size_t(i) * C.S + h;
+    s_set_wm(C, hb, kRunW | ((fin & kFin) << 16) | (len + rem), (m & ~3u) | kRunning | kAdmitted);
+    const int tier = int((m >> 2) & 15u);
+    if (!(m & kAdmitted)) {
+        stat(C, tier * 8 + kAdmittedCnt, 1);
+        stat(C, tier * 8 + kQdelay, t - C.hta[i]);
+        hist_add(C, kHistQdelay, tier, t - C.hta[i]);
+    }
+    C.freeb[i] -= dem;
+    C.held[i] += dem;
+    C.B[i] += 1;
+    C.nwait[i] -= 1;
+    c16_inc(C.res, res_idx(C, i, (len - t - 1u) & C.bmask));
+    tier_inc(C, i, tier);
+    wheel_put(C, fin, i, h);
+    hol_pop(C, i);
+}
+
+// The whole admission of instance i (uniform): requests are admitted in
+// (tier, seq) order while the head of line fits (Section 3.1), through the
+// same steps as the lane-parallel rounds -- a rescan when the head of line
+// is unknown, the previous tick's placements, a gather of a short queue, a
+// cached run, or one head of line -- until the head of line does not fit or
+// nothing waits.  Every step admits at least one request, or finds the head
+// of line, so the loop ends.  (The kernels for 128+ instances hand instances
+// to waves dynamically with it.)
+template <int GR, int MK>
+__device__ inline void admit_all(const Ctx& C, int i, uint32_t t, int lane)
+{
+    for (;;) {
+        const int h = C.hols[i];
+        if (h == kHolUnknown) {
+            rescan_admit<GR, MK>(C, i, t, lane);
+            continue;
+        }
+        if (h < 0 || C.hold[i] > C.freeb[i]) break;
+        const int nw = C.nwait[i];
+        const bool cached = C.td && C.qn[i] > 0;
+        if (nw >= 2 && nw <= 64 && C.frs[i]) {
+            admit_fresh(C, i, t, lane);
+        } else if (nw >= 2 && nw <= 64 && !cached) {
+            admit_batch<GR>(C, i, t, lane);
+        } else if (cached) {
+            admit_cached(C, i, t, lane);
+        } else {
+            if (lane == 0) admit_head(C, i, t);
+            wave_sync();
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Section 6.5 extensions, run at the start of a tick (uniform)
 // ---------------------------------------------------------------------------
@@ -1525,7 +1590,11 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             }
             if (NW > 1) {
                 if (abort_any && lane == 0) *C.bflag = 1;
-                if (tid == 0) *C.bsum = 0;  // the auto-scaling sum of this tick (phase C)
+                if (tid == 0) {
+                    *C.bsum = 0;  // the auto-scaling sum of this tick (phase C)
+                    *C.wln = 0;   // the admission work list (phase B)
+                    *C.wlnext = 0;
+                }
                 block_sync<NW>();
                 if (wid == 0) {
                     preempting = *C.nvic != 0;
@@ -1601,7 +1670,32 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             block_sync<NW>();
 
             // ===================== B: admission (lane-parallel rounds); C: freeness =====================
-            // (each wave admits on the instances it owns)
+            // Eight-wave kernels: the instances with admission work (an unknown
+            // head of line, or a known one that fits) are listed, and the waves
+            // take them one at a time from the list, each admitting on its
+            // instance to the end: a few long queues no longer load one wave.
+            // Admissions on different instances touch only their own state and
+            // shared counters, so the order does not matter.
+            if (NW > 1) {
+#pragma unroll
+                for (int j = 0; j < OPL; ++j) {
+                    const uint32_t i = (uint32_t(lane) + 64u * j) * NW + uint32_t(wid);
+                    const bool need = i < I && (C.hols[i] == kHolUnknown || (C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]));
+                    if (need) C.order[atomicAdd(C.wln, 1)] = int(i);
+                }
+                block_sync<NW>();
+                const int nl = *C.wln;
+                for (;;) {
+                    int k = 0;
+                    if (lane == 0) k = atomicAdd(C.wlnext, 1);
+                    k = rl(k, 0);
+                    if (k >= nl) break;
+                    admit_all<16, 4>(C, C.order[k], t, lane);
+                }
+                // phase C reads the instances each wave owns, which any wave
+                // may have admitted on
+                block_sync<NW>();
+            } else
             for (;;) {
                 // heads of line left unknown: found by a rescan, which admits at once
                 bool unk = false;
@@ -1635,26 +1729,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                             // whose next requests are cached: admit heads of line one at a
                             // time while they fit and are known
                             do {
-                                const int h = C.hols[i], dem = C.hold[i];
-                                const uint32_t w = C.hwd[i], m = C.hmt[i];
-                                const uint32_t len = wlo(w), rem = wmid(w);
-                                const uint32_t fin = t + rem;
-                                const size_t hb = size_t(i) * S + h;
-                                s_set_wm(C, hb, kRunW | ((fin & kFin) << 16) | (len + rem), (m & ~3u) | kRunning | kAdmitted);
-                                const int tier = int((m >> 2) & 15u);
-                                if (!(m & kAdmitted)) {
-                                    stat(C, tier * 8 + kAdmittedCnt, 1);
-                                    stat(C, tier * 8 + kQdelay, t - C.hta[i]);
-                                    hist_add(C, kHistQdelay, tier, t - C.hta[i]);
-                                }
-                                C.freeb[i] -= dem;
-                                C.held[i] += dem;
-                                C.B[i] += 1;
-                                C.nwait[i] -= 1;
-                                c16_inc(C.res, res_idx(C, i, (len - t - 1u) & C.bmask));
-                                tier_inc(C, int(i), tier);
-                                wheel_put(C, fin, int(i), h);
-                                hol_pop(C, int(i));
+                                admit_head(C, int(i), t);
                             } while (C.hols[i] >= 0 && C.hold[i] <= C.freeb[i]);
                             // an unknown head of line is found by the next round's rescan
                             any = any || C.hols[i] == kHolUnknown;
