@@ -163,6 +163,8 @@ struct Ctx {
     int* bflag;
     int* wln;
     int* wlnext;
+    int* e2go;                 // pairing runs this tick (set by wave 0)
+    int* e2n2;                 // instances that can pair
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -257,6 +259,8 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.bflag = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 8) : nullptr;
     C.wln = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 12) : nullptr;
     C.wlnext = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 16) : nullptr;
+    C.e2go = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 20) : nullptr;
+    C.e2n2 = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 24) : nullptr;
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
@@ -1815,7 +1819,10 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             }
             wave_sync();
 
-            // the dispatch and the migrations (phases D and E): wave 0
+            // the dispatch and the migrations (phases D and E): wave 0 (pairing:
+            // whether it runs this tick and how many instances can pair)
+            bool e2 = false;
+            int n2 = 0;
             if (wid == 0) {
             // ===================== D: tier-ordered dispatch =====================
             // an instance with an empty queue now holds, after this dispatch, only
@@ -1978,7 +1985,35 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                     // lowest empty slots in arrival order
                     const int tier = int((a >> 32) & 15u);
                     int s = -1;
-                    if (tgt >= 0) {
+                    bool searched = false;
+                    const unsigned long long tgm = ballot(tgt >= 0);
+                    if (W > 8 && W <= uint32_t(IM) && tgm) {
+                        const int ft = rl(tgt, ffs64(tgm));
+                        if (!ballot(tgt >= 0 && tgt != ft)) {
+                            // the whole batch goes to one instance (a burst): the
+                            // inclusive prefix of its free slots per occupancy word
+                            // (gtmp, free during the dispatch), and each arrival's
+                            // word by binary search
+                            const unsigned long long wdl = uint32_t(lane) < W ? C.occ[ft * W + lane] : kNone;
+                            const int pre = wscan(64 - __popcll(wdl), lane);
+                            if (uint32_t(lane) < W) C.gtmp[lane] = pre;
+                            wave_sync();
+                            if (tgt >= 0) {
+                                int lo = 0, hi = int(W) - 1;
+                                while (lo < hi) {
+                                    const int mid = (lo + hi) >> 1;
+                                    if (C.gtmp[mid] > rank) hi = mid;
+                                    else lo = mid + 1;
+                                }
+                                if (C.gtmp[lo] > rank) {
+                                    const int before = lo ? C.gtmp[lo - 1] : 0;
+                                    s = lo * 64 + kth_set_bit(~C.occ[ft * W + lo], rank - before);
+                                }
+                            }
+                            searched = true;
+                        }
+                    }
+                    if (tgt >= 0 && !searched) {
                         // the rank-th empty slot, four occupancy words per step
                         int rk = rank;
                         for (uint32_t w0 = 0; w0 < W && s < 0; w0 += 4) {
@@ -1994,11 +2029,11 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                                 }
                             }
                         }
-                        if (s < 0) {  // occupancy and live count disagree: flag, drop the arrival
-                            stat(C, kInvariant, 1);
-                            stat(C, tier * 8 + kRejected, 1);
-                            tgt = -2;
-                        }
+                    }
+                    if (tgt >= 0 && s < 0) {  // occupancy and live count disagree: flag, drop the arrival
+                        stat(C, kInvariant, 1);
+                        stat(C, tier * 8 + kRejected, 1);
+                        tgt = -2;
                     }
                     wave_sync();
                     if (n <= uint32_t(kLast)) {
@@ -2120,10 +2155,14 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             // ===================== E2: pairing on interval ticks =====================
             const bool mig_tick = mig_left == 0;
             mig_left = mig_tick ? P.mig_interval - 1u : mig_left - 1u;
+            // pairing in three parts: which instances can pair and their keys
+            // (wave 0), their order (wave 0 by counting ranks; in the
+            // eight-wave kernels every thread counts), the pairs (wave 0)
             if (!infaas && mig_tick) {
                 bool neg = false;
                 for (uint32_t i = lane; i < I; i += 64) neg |= C.num[i] < 0 || C.drn[i];
                 if (ballot(neg)) {
+                    e2 = true;
                     for (uint32_t i = lane; i < I; i += 64) C.flags[i] &= ~kFlagBusy;
                     wave_sync();
                     for (uint32_t i = lane; i < I; i += 64) {
@@ -2133,10 +2172,9 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                     wave_sync();
                     // rank the instances not in a migration by (F, index): F as an
                     // order-preserving 64-bit key (a draining instance's F is minus
-                    // infinity), compared with every other lane's key through readlane
+                    // infinity)
                     unsigned long long fk[IPL];
                     unsigned long long avm[IPL];
-                    int n2 = 0;
 #pragma unroll
                     for (int j = 0; j < IPL; ++j) {
                         const uint32_t i = lane + 64 * j;
@@ -2147,61 +2185,18 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                         avm[j] = ballot(av);
                         n2 += __popcll(avm[j]);
                     }
-                    // L: the kernels for 128+ instances sort all keys at once;
-                    // the others count every instance's rank
-                    const int npairs = min(int(P.mig_max_pairs), n2 / 2);
-                    if (IM >= 128) {
-                        // the whole order at once: a bitonic sort of the IM
-                        // (key, index) pairs, element e = lane + 64 j in register j
-                        // (the instances in a migration carry the largest key and
-                        // sort after the n2 available ones)
-                        unsigned long long sk[IPL];
-                        int si[IPL];
+                    if (NW > 1) {
+                        // the keys for the workgroup's count, in the freeness array
+                        // (set again in phase C before its next use); an instance in
+                        // a migration carries the largest key
 #pragma unroll
                         for (int j = 0; j < IPL; ++j) {
-                            sk[j] = (avm[j] >> lane) & 1ull ? fk[j] : kNone;
-                            si[j] = lane + 64 * j;
+                            const uint32_t i = lane + 64 * j;
+                            if (i < I)
+                                reinterpret_cast<unsigned long long*>(C.fd)[i] = (avm[j] >> lane) & 1ull ? fk[j] : kNone;
                         }
-#pragma unroll
-                        for (int size = 2; size <= 64 * IPL; size <<= 1) {
-#pragma unroll
-                            for (int stride = size >> 1; stride > 0; stride >>= 1) {
-                                if (stride >= 64) {
-                                    // between registers of a lane
-                                    const int js = stride >> 6;
-#pragma unroll
-                                    for (int j = 0; j < IPL; ++j) {
-                                        if (j & js) continue;
-                                        const bool asc = ((lane + 64 * j) & size) == 0;
-                                        const unsigned long long ka = sk[j], kb = sk[j + js];
-                                        const int ia = si[j], ib = si[j + js];
-                                        const bool gt = ka > kb || (ka == kb && ia > ib);
-                                        const bool sw = asc ? gt : !gt;
-                                        sk[j] = sw ? kb : ka; si[j] = sw ? ib : ia;
-                                        sk[j + js] = sw ? ka : kb; si[j + js] = sw ? ia : ib;
-                                    }
-                                } else {
-                                    // between lanes: the lower lane of an ascending pair
-                                    // keeps the smaller (key, index)
-                                    const int partner = lane ^ stride;
-                                    const bool low = (lane & stride) == 0;
-#pragma unroll
-                                    for (int j = 0; j < IPL; ++j) {
-                                        const unsigned long long pk = perm64(sk[j], partner);
-                                        const int pi = perm32(si[j], partner);
-                                        const bool asc = ((lane + 64 * j) & size) == 0;
-                                        const bool plt = pk < sk[j] || (pk == sk[j] && pi < si[j]);
-                                        const bool take = low == asc ? plt : !plt;
-                                        sk[j] = take ? pk : sk[j];
-                                        si[j] = take ? pi : si[j];
-                                    }
-                                }
-                            }
-                        }
-#pragma unroll
-                        for (int j = 0; j < IPL; ++j)
-                            if (lane + 64 * j < n2) C.order[lane + 64 * j] = si[j];
                     } else {
+                        // L: every instance's rank, from every other lane's key
                         int rk[IPL];
 #pragma unroll
                         for (int j = 0; j < IPL; ++j) rk[j] = 0;
@@ -2222,7 +2217,45 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                         for (int j = 0; j < IPL; ++j)
                             if ((avm[j] >> lane) & 1ull) C.order[rk[j]] = lane + 64 * j;
                     }
-                    wave_sync();
+                }
+            }
+            if (NW > 1 && lane == 0) { *C.e2go = e2 ? 1 : 0; *C.e2n2 = n2; }
+            wave_sync();
+            }  // wave 0
+            block_sync<NW>();
+            if (NW > 1 && *C.e2go) {
+                // L in the eight-wave kernels: each instance's rank in (F, index)
+                // order counted by NT / IM threads over parts of the instances,
+                // summed in pend[] (free at this point of the tick)
+                const unsigned long long* key = reinterpret_cast<const unsigned long long*>(C.fd);
+                constexpr uint32_t kParts = NT / uint32_t(IM);
+                for (uint32_t i = tid; i < I; i += NT) C.pend[i] = 0;
+                block_sync<NW>();
+                {
+                    const uint32_t i = tid % uint32_t(IM), part = tid / uint32_t(IM);
+                    const uint32_t chunk = (I + kParts - 1) / kParts;
+                    const uint32_t j0 = part * chunk, j1 = min(I, j0 + chunk);
+                    if (i < I) {
+                        const unsigned long long ki = key[i];
+                        if (ki != kNone) {
+                            int rk = 0;
+                            for (uint32_t jx = j0; jx < j1; ++jx) {
+                                const unsigned long long kj = key[jx];
+                                rk += (kj < ki || (kj == ki && jx < i)) ? 1 : 0;
+                            }
+                            if (rk) atomicAdd(&C.pend[i], rk);
+                        }
+                    }
+                }
+                block_sync<NW>();
+                for (uint32_t i = tid; i < I; i += NT)
+                    if (key[i] != kNone) C.order[C.pend[i]] = int(i);
+                block_sync<NW>();
+            }
+            if (wid == 0) {
+                if (NW > 1) { e2 = *C.e2go != 0; n2 = *C.e2n2; }
+                if (e2) {
+                    const int npairs = min(int(P.mig_max_pairs), n2 / 2);
                     // Pairs (L[k], L[n2 - 1 - k]) use disjoint instances and one
                     // snapshot of F, so the stopping pair is found for all pairs at
                     // once (lane k tests pair k), the queued moves of the pairs
@@ -2329,7 +2362,6 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                 }
                 wave_sync();
             }
-            }  // wave 0
             block_sync<NW>();
         }
 
