@@ -332,6 +332,14 @@ __device__ __forceinline__ uint32_t wmin32(uint32_t x)
     x = tmin(x, uint32_t(dpp_row<0x140>(int(x))));
     return tmin(tmin(rlu(x, 0), rlu(x, 16)), tmin(rlu(x, 32), rlu(x, 48)));
 }
+__device__ __forceinline__ uint32_t wmax32(uint32_t x)
+{
+    x = tmax(x, uint32_t(dpp_row<0xB1>(int(x))));
+    x = tmax(x, uint32_t(dpp_row<0x4E>(int(x))));
+    x = tmax(x, uint32_t(dpp_row<0x141>(int(x))));
+    x = tmax(x, uint32_t(dpp_row<0x140>(int(x))));
+    return tmax(tmax(rlu(x, 0), rlu(x, 16)), tmax(rlu(x, 32), rlu(x, 48)));
+}
 
 // wave-wide max of a double through DPP lane moves; every lane gets the result
 template <int kCtrl, int kRowMask>
@@ -978,6 +986,51 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
     wave_sync();
 }
 
+// The ranked prefix of a rescan, taken minimum by minimum from the lanes'
+// ascending lists k (MK each, with slot | demand << 12 in sd): lane r
+// receives the key and sd of rank r.  The extraction stops when nothing is
+// left, after 64 requests, qdepth requests after the first one whose summed
+// demand exceeds the free blocks fr (the new head of line and the cache
+// behind it), or when the winning lane had more waiting slots than it kept
+// (more: its next key is unknown).  Returns the number taken.  KT is the key
+// type: the 64-bit keys or an order-preserving 32-bit form of them, with
+// all-ones as "none".
+__device__ __forceinline__ uint32_t wmin_k(uint32_t x) { return wmin32(x); }
+__device__ __forceinline__ unsigned long long wmin_k(unsigned long long x) { return wmin64(x); }
+__device__ __forceinline__ uint32_t rl_k(uint32_t x, int l) { return rlu(x, l); }
+__device__ __forceinline__ unsigned long long rl_k(unsigned long long x, int l) { return rl64(x, l); }
+
+template <typename KT, int MK>
+__device__ inline int rank_extract(KT (&k)[MK], uint32_t (&sd)[MK], bool more, int fr, int td, int lane, KT& myk,
+                                   uint32_t& mysd)
+{
+    const KT none = static_cast<KT>(~static_cast<KT>(0));
+    myk = none;
+    mysd = 0;
+    int got = 0, taken = 0, cum = 0, lim = 64;
+    for (int r = 0; r < lim; ++r) {
+        const KT mn = wmin_k(k[0]);
+        if (mn == none) break;
+        const int wl = ffs64(ballot(k[0] == mn));
+        const uint32_t wsd = rlu(sd[0], wl);
+        myk = lane == r ? mn : myk;
+        mysd = lane == r ? wsd : mysd;
+        got = r + 1;
+        cum += int(wsd >> 12);
+        if (cum > fr && lim == 64) lim = min(64, r + 1 + td);
+        const bool win = lane == wl;
+#pragma unroll
+        for (int x = 0; x + 1 < MK; ++x) {
+            k[x] = win ? k[x + 1] : k[x];
+            sd[x] = win ? sd[x + 1] : sd[x];
+        }
+        k[MK - 1] = win ? none : k[MK - 1];
+        taken += win ? 1 : 0;
+        if (ballot(win && more && taken >= MK)) break;  // the winner's next key is unknown
+    }
+    return got;
+}
+
 // Head of line of instance i from its slots, with admission (Section 3.1:
 // the local queue is served in (tier, seq) order while the head fits).  Each
 // lane keeps the MK smallest keys of its slots, with their demand; the wave
@@ -1027,33 +1080,32 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
             }
         }
     }
-    // rank extraction, branch-free per round: the winning lane's list moves up
+    // rank extraction on 32-bit keys rank << 27 | (seq - lowest seq) when the
+    // candidates' seqs span less than 2^27 (the order is the same; a 32-bit
+    // wave minimum is a third of the 64-bit one), else on the keys themselves
     const int fr = C.freeb[i];
-    unsigned long long myk = kNone;
-    uint32_t mysd = 0;
-    int got = 0, taken = 0, cum = 0, lim = 64;
     const bool more = cnt > MK;
-    for (int r = 0; r < lim; ++r) {
-        const unsigned long long mn = wmin64(k[0]);
-        if (mn == kNone) break;
-        const int wl = ffs64(ballot(k[0] == mn));
-        const uint32_t wsd = rlu(sd[0], wl);
-        myk = lane == r ? mn : myk;
-        mysd = lane == r ? wsd : mysd;
-        got = r + 1;
-        cum += int(wsd >> 12);
-        // the first request that does not fit is the new head of line; the
-        // cache takes the qdepth after it
-        if (cum > fr && lim == 64) lim = min(64, r + 1 + C.td);
-        const bool win = lane == wl;
+    uint32_t slo = 0xFFFFFFFFu, shi = 0;
 #pragma unroll
-        for (int x = 0; x + 1 < MK; ++x) {
-            k[x] = win ? k[x + 1] : k[x];
-            sd[x] = win ? sd[x + 1] : sd[x];
-        }
-        k[MK - 1] = win ? kNone : k[MK - 1];
-        taken += win ? 1 : 0;
-        if (ballot(win && more && taken >= MK)) break;  // the winner's next key is unknown
+    for (int x = 0; x < MK; ++x) {
+        if (k[x] != kNone) { slo = tmin(slo, uint32_t(k[x])); shi = tmax(shi, uint32_t(k[x])); }
+    }
+    slo = wmin32(slo);
+    shi = wmax32(shi);
+    unsigned long long myk;
+    uint32_t mysd;
+    int got;
+    if (shi - slo < (1u << 27) || slo > shi) {
+        uint32_t k32[MK];
+#pragma unroll
+        for (int x = 0; x < MK; ++x)
+            k32[x] = k[x] == kNone ? 0xFFFFFFFFu : (uint32_t(k[x] >> 32) << 27) | (uint32_t(k[x]) - slo);
+        uint32_t my32;
+        got = rank_extract<uint32_t, MK>(k32, sd, more, fr, C.td, lane, my32, mysd);
+        myk = my32 == 0xFFFFFFFFu ? kNone
+                                  : (static_cast<unsigned long long>(my32 >> 27) << 32) | ((my32 & 0x7FFFFFFu) + slo);
+    } else {
+        got = rank_extract<unsigned long long, MK>(k, sd, more, fr, C.td, lane, myk, mysd);
     }
     if (got == 0) {
         if (lane == 0) clear_hol(C, i);
