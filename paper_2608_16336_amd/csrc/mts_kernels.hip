@@ -63,7 +63,7 @@ enum { kXSlo = 0, kXAge = 10, kXPromoMin = 20, kXPromoPeriod, kXAdaptEpoch, kXAd
 static_assert(kXWords == MTS_EXT_WORDS, "extension table size");
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, ext, blk, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, ext, blk, rsel, total;
 };
 
 // Waves per replica: the kernels for 128 or more instances run a workgroup of
@@ -118,6 +118,9 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     // abort flag, the admission work list's length and next entry)
     o = al8(o);
     L.blk = o;   o += waves_for(IM) > 1 ? 32 : 0;
+    // multi-wave kernels: per wave 64 (key, slot | demand) pairs, the rescan's
+    // selected requests before they are ranked
+    L.rsel = o;  o += waves_for(IM) > 1 ? waves_for(IM) * 64 * 8 : 0;
     L.total = al8(o);
     return L;
 }
@@ -165,6 +168,7 @@ struct Ctx {
     int* wlnext;
     int* e2go;                 // pairing runs this tick (set by wave 0)
     int* e2n2;                 // instances that can pair
+    uint2* rsel;               // this wave's 64 entries of the rescan selection buffer
     // HBM: timing wheel of this replica, slot arrays, latency histograms
     uint32_t* wheel;           // [wsz][wcap] instance << 16 | slot
     uint32_t* hist;            // [2][10][MTS_HIST_BINS] queue delay, end-to-end
@@ -261,6 +265,7 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.wlnext = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 16) : nullptr;
     C.e2go = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 20) : nullptr;
     C.e2n2 = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.blk + 24) : nullptr;
+    C.rsel = waves_for(IM) > 1 ? reinterpret_cast<uint2*>(base + Y.rsel) + 64 * (threadIdx.x >> 6) : nullptr;
     C.I = P.I; C.S = P.S; C.W = P.W; C.RB = P.RB;
     C.shift = P.blk_shift;
     C.bmask = (1u << P.blk_shift) - 1u;
@@ -1031,6 +1036,76 @@ __device__ inline int rank_extract(KT (&k)[MK], uint32_t (&sd)[MK], bool more, i
     return got;
 }
 
+// The same ranked prefix as rank_extract on 32-bit keys, found by selection
+// instead of minimum by minimum: the candidates the extraction can reach are
+// the keys up to the smallest last kept key of a lane with more waiting slots
+// (bnd; all keys when no lane has more); of those, the 64 smallest are the
+// keys up to a threshold found by bisection over key values (the keys are
+// distinct, counted by ballots); they are gathered into this wave's buffer,
+// ranked by counting and sent to the lane of their rank, and the prefix stops
+// qdepth requests after the first one whose summed demand exceeds fr.  The
+// latency chain is a few dozen scalar steps instead of one wave reduction per
+// request.
+template <int MK>
+__device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd)[MK], bool more, int fr, int lane,
+                                  uint32_t& myk, uint32_t& mysd)
+{
+    constexpr uint32_t none = 0xFFFFFFFFu;
+    const uint32_t bnd = wmin32(more ? k[MK - 1] : none);
+    bool vx[MK];
+    int nvalid = 0;
+#pragma unroll
+    for (int x = 0; x < MK; ++x) {
+        vx[x] = k[x] != none && k[x] <= bnd;
+        nvalid += __popcll(ballot(vx[x]));
+    }
+    myk = none;
+    mysd = 0;
+    const int want = min(64, nvalid);
+    if (want == 0) return 0;
+    uint32_t thr = none;
+    if (nvalid > 64) {
+        // the smallest value with 64 candidates at or below it
+        uint32_t hi = 0;
+#pragma unroll
+        for (int x = 0; x < MK; ++x) hi = vx[x] ? tmax(hi, k[x]) : hi;
+        uint32_t lo = wmin32(k[0]);
+        hi = wmax32(hi);
+        while (lo < hi) {
+            const uint32_t mid = lo + ((hi - lo) >> 1);
+            int c = 0;
+#pragma unroll
+            for (int x = 0; x < MK; ++x) c += __popcll(ballot(vx[x] && k[x] <= mid));
+            if (c >= 64) hi = mid;
+            else lo = mid + 1;
+        }
+        thr = lo;
+    }
+    // gather the want selected candidates
+    int base = 0;
+#pragma unroll
+    for (int x = 0; x < MK; ++x) {
+        const bool sel = vx[x] && k[x] <= thr;
+        const unsigned long long m = ballot(sel);
+        if (sel) C.rsel[base + __popcll(m & lanemask_lt())] = make_uint2(k[x], sd[x]);
+        base += __popcll(m);
+    }
+    wave_sync();
+    uint32_t ck = none, cs = 0;
+    if (lane < want) { const uint2 e = C.rsel[lane]; ck = e.x; cs = e.y; }
+    wave_sync();
+    int rank = 0;
+    for (int j = 0; j < want; ++j) rank += rlu(ck, j) < ck ? 1 : 0;
+    if (lane >= want) rank = lane;
+    const uint32_t sk = uint32_t(__builtin_amdgcn_ds_permute(rank * 4, int(ck)));
+    const uint32_t ss = uint32_t(__builtin_amdgcn_ds_permute(rank * 4, int(cs)));
+    const int cum = wscan(lane < want ? int(ss >> 12) : 0, lane);
+    const unsigned long long over = ballot(lane < want && cum > fr);
+    const int got = over ? min(want, ffs64(over) + 1 + C.td) : want;
+    if (lane < got) { myk = sk; mysd = ss; }
+    return got;
+}
+
 // Head of line of instance i from its slots, with admission (Section 3.1:
 // the local queue is served in (tier, seq) order while the head fits).  Each
 // lane keeps the MK smallest keys of its slots, with their demand; the wave
@@ -1043,7 +1118,7 @@ __device__ inline int rank_extract(KT (&k)[MK], uint32_t (&sd)[MK], bool more, i
 // GR chunks of 64 slots are read per memory round trip.  Returns true when
 // every request taken was admitted and more wait (the head of line is still
 // unknown).  Uniform.
-template <int GR, int MK>
+template <int GR, int MK, bool SEL = false>
 __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
 {
     const size_t b = size_t(i) * C.S;
@@ -1101,7 +1176,8 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
         for (int x = 0; x < MK; ++x)
             k32[x] = k[x] == kNone ? 0xFFFFFFFFu : (uint32_t(k[x] >> 32) << 27) | (uint32_t(k[x]) - slo);
         uint32_t my32;
-        got = rank_extract<uint32_t, MK>(k32, sd, more, fr, C.td, lane, my32, mysd);
+        if (SEL) got = rank_select<MK>(C, k32, sd, more, fr, lane, my32, mysd);
+        else got = rank_extract<uint32_t, MK>(k32, sd, more, fr, C.td, lane, my32, mysd);
         myk = my32 == 0xFFFFFFFFu ? kNone
                                   : (static_cast<unsigned long long>(my32 >> 27) << 32) | ((my32 & 0x7FFFFFFu) + slo);
     } else {
@@ -1274,7 +1350,7 @@ __device__ inline void admit_all(const Ctx& C, int i, uint32_t t, int lane)
     for (;;) {
         const int h = C.hols[i];
         if (h == kHolUnknown) {
-            rescan_admit<GR, MK>(C, i, t, lane);
+            rescan_admit<GR, MK, true>(C, i, t, lane);
             continue;
         }
         if (h < 0 || C.hold[i] > C.freeb[i]) break;
