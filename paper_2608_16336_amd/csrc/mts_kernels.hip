@@ -1094,8 +1094,16 @@ __device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd
     uint32_t ck = none, cs = 0;
     if (lane < want) { const uint2 e = C.rsel[lane]; ck = e.x; cs = e.y; }
     wave_sync();
-    int rank = 0;
-    for (int j = 0; j < want; ++j) rank += rlu(ck, j) < ck ? 1 : 0;
+    // (four independent counts, so that the lane reads overlap)
+    int rank = 0, r1 = 0, r2 = 0, r3 = 0, j = 0;
+    for (; j + 4 <= want; j += 4) {
+        rank += int(rlu(ck, j) < ck);
+        r1 += int(rlu(ck, j + 1) < ck);
+        r2 += int(rlu(ck, j + 2) < ck);
+        r3 += int(rlu(ck, j + 3) < ck);
+    }
+    for (; j < want; ++j) rank += int(rlu(ck, j) < ck);
+    rank += r1 + r2 + r3;
     if (lane >= want) rank = lane;
     const uint32_t sk = uint32_t(__builtin_amdgcn_ds_permute(rank * 4, int(ck)));
     const uint32_t ss = uint32_t(__builtin_amdgcn_ds_permute(rank * 4, int(cs)));
@@ -1822,7 +1830,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                     if (lane == 0) k = atomicAdd(C.wlnext, 1);
                     k = rl(k, 0);
                     if (k >= nl) break;
-                    admit_all<16, 4>(C, C.order[k], t, lane);
+                    admit_all<16, 3>(C, C.order[k], t, lane);
                 }
                 // phase C reads the instances each wave owns, which any wave
                 // may have admitted on
@@ -2360,20 +2368,35 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                 for (uint32_t i = tid; i < I; i += NT) C.pend[i] = 0;
                 block_sync<NW>();
                 {
-                    const uint32_t i = tid % uint32_t(IM), part = tid / uint32_t(IM);
+                    // (a wave's threads share one part: IM >= 64) the part's keys
+                    // come 64 at a time in one LDS read and are compared lane by lane
+                    const uint32_t i = tid % uint32_t(IM);
+                    const uint32_t part = uint32_t(__builtin_amdgcn_readfirstlane(int(tid / uint32_t(IM))));
                     const uint32_t chunk = (I + kParts - 1) / kParts;
                     const uint32_t j0 = part * chunk, j1 = min(I, j0 + chunk);
-                    if (i < I) {
-                        const unsigned long long ki = key[i];
-                        if (ki != kNone) {
-                            int rk = 0;
-                            for (uint32_t jx = j0; jx < j1; ++jx) {
-                                const unsigned long long kj = key[jx];
-                                rk += (kj < ki || (kj == ki && jx < i)) ? 1 : 0;
-                            }
-                            if (rk) atomicAdd(&C.pend[i], rk);
+                    const unsigned long long ki = i < I ? key[i] : kNone;
+                    int rk = 0;
+                    for (uint32_t jb = j0; jb < j1; jb += 64) {
+                        const unsigned long long kb = jb + uint32_t(lane) < j1 ? key[jb + uint32_t(lane)] : kNone;
+                        const uint32_t nb = uint32_t(__builtin_amdgcn_readfirstlane(int(min(64u, j1 - jb))));
+                        // four independent counts, so that the lane reads overlap
+                        int r1 = 0, r2 = 0, r3 = 0;
+                        uint32_t u = 0;
+                        for (; u + 4 <= nb; u += 4) {
+                            const unsigned long long k0 = rl64(kb, int(u)), k1 = rl64(kb, int(u + 1)),
+                                                     k2 = rl64(kb, int(u + 2)), k3 = rl64(kb, int(u + 3));
+                            rk += int((k0 < ki) | ((k0 == ki) & (jb + u < i)));
+                            r1 += int((k1 < ki) | ((k1 == ki) & (jb + u + 1 < i)));
+                            r2 += int((k2 < ki) | ((k2 == ki) & (jb + u + 2 < i)));
+                            r3 += int((k3 < ki) | ((k3 == ki) & (jb + u + 3 < i)));
                         }
+                        for (; u < nb; ++u) {
+                            const unsigned long long kj = rl64(kb, int(u));
+                            rk += int((kj < ki) | ((kj == ki) & (jb + u < i)));
+                        }
+                        rk += r1 + r2 + r3;
                     }
+                    if (i < I && ki != kNone && rk) atomicAdd(&C.pend[i], rk);
                 }
                 block_sync<NW>();
                 for (uint32_t i = tid; i < I; i += NT)
