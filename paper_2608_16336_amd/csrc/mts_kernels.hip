@@ -1725,7 +1725,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
 #pragma unroll
                 for (int j = 0; j < OPL; ++j)
                     for (unsigned long long m = pre[j]; m; m &= m - 1)
-                        abort_any = preempt<(IM >= 128 ? 16 : 4), (IM >= 128 ? 4 : 2)>(
+                        abort_any = preempt<(IM >= 128 ? 16 : 4), 2>(
                                         C, int((64u * j + ffs64(m)) * NW + uint32_t(wid)), t, lane) || abort_any;
             }
             if (NW > 1) {
