@@ -119,7 +119,9 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     o = al8(o);
     L.blk = o;   o += waves_for(IM) > 1 ? 32 : 0;
     // multi-wave kernels: per wave 64 (key, slot | demand) pairs, the rescan's
-    // selected requests before they are ranked
+    // selected requests before they are ranked (the pairing's sorted blocks
+    // of 64 (key, index) pairs use the same bytes later in the tick)
+    o = (o + 15u) & ~15u;
     L.rsel = o;  o += waves_for(IM) > 1 ? waves_for(IM) * 64 * 8 : 0;
     L.total = al8(o);
     return L;
@@ -2361,42 +2363,50 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             block_sync<NW>();
             if (NW > 1 && *C.e2go) {
                 // L in the eight-wave kernels: each instance's rank in (F, index)
-                // order counted by NT / IM threads over parts of the instances,
-                // summed in pend[] (free at this point of the tick)
+                // order, in two steps: waves 0..3 each sort a block of 64
+                // instances by counting (into the rescans' selection buffers,
+                // free at this point of the tick), then every instance adds its
+                // place in each block, found by bisection, summed in pend[]
                 const unsigned long long* key = reinterpret_cast<const unsigned long long*>(C.fd);
                 constexpr uint32_t kParts = NT / uint32_t(IM);
+                const uint32_t nblk = (I + 63u) / 64u;
+                ulonglong2* sblk = reinterpret_cast<ulonglong2*>(C.rsel - 64 * wid);
                 for (uint32_t i = tid; i < I; i += NT) C.pend[i] = 0;
+                if (uint32_t(wid) < nblk) {
+                    // (entries past I and unavailable instances carry the largest key)
+                    const uint32_t i = 64u * uint32_t(wid) + uint32_t(lane);
+                    const unsigned long long kb = i < I ? key[i] : kNone;
+                    int r0 = 0, r1 = 0, r2 = 0, r3 = 0;
+                    for (int j = 0; j < 64; j += 4) {
+                        const unsigned long long k0 = rl64(kb, j), k1 = rl64(kb, j + 1), k2 = rl64(kb, j + 2),
+                                                 k3 = rl64(kb, j + 3);
+                        r0 += int((k0 < kb) | ((k0 == kb) & (j < lane)));
+                        r1 += int((k1 < kb) | ((k1 == kb) & (j + 1 < lane)));
+                        r2 += int((k2 < kb) | ((k2 == kb) & (j + 2 < lane)));
+                        r3 += int((k3 < kb) | ((k3 == kb) & (j + 3 < lane)));
+                    }
+                    sblk[64 * wid + r0 + r1 + r2 + r3] = make_ulonglong2(kb, i);
+                }
                 block_sync<NW>();
                 {
-                    // (a wave's threads share one part: IM >= 64) the part's keys
-                    // come 64 at a time in one LDS read and are compared lane by lane
                     const uint32_t i = tid % uint32_t(IM);
                     const uint32_t part = uint32_t(__builtin_amdgcn_readfirstlane(int(tid / uint32_t(IM))));
-                    const uint32_t chunk = (I + kParts - 1) / kParts;
-                    const uint32_t j0 = part * chunk, j1 = min(I, j0 + chunk);
                     const unsigned long long ki = i < I ? key[i] : kNone;
-                    int rk = 0;
-                    for (uint32_t jb = j0; jb < j1; jb += 64) {
-                        const unsigned long long kb = jb + uint32_t(lane) < j1 ? key[jb + uint32_t(lane)] : kNone;
-                        const uint32_t nb = uint32_t(__builtin_amdgcn_readfirstlane(int(min(64u, j1 - jb))));
-                        // four independent counts, so that the lane reads overlap
-                        int r1 = 0, r2 = 0, r3 = 0;
-                        uint32_t u = 0;
-                        for (; u + 4 <= nb; u += 4) {
-                            const unsigned long long k0 = rl64(kb, int(u)), k1 = rl64(kb, int(u + 1)),
-                                                     k2 = rl64(kb, int(u + 2)), k3 = rl64(kb, int(u + 3));
-                            rk += int((k0 < ki) | ((k0 == ki) & (jb + u < i)));
-                            r1 += int((k1 < ki) | ((k1 == ki) & (jb + u + 1 < i)));
-                            r2 += int((k2 < ki) | ((k2 == ki) & (jb + u + 2 < i)));
-                            r3 += int((k3 < ki) | ((k3 == ki) & (jb + u + 3 < i)));
+                    if (ki != kNone) {
+                        int rk = 0;
+                        for (uint32_t bk = part; bk < nblk; bk += kParts) {
+                            // entries of block bk below (ki, i)
+                            int lo = 0, hi = 64;
+                            while (lo < hi) {
+                                const int mid = (lo + hi) >> 1;
+                                const ulonglong2 e = sblk[64 * bk + mid];
+                                if (e.x < ki || (e.x == ki && e.y < i)) lo = mid + 1;
+                                else hi = mid;
+                            }
+                            rk += lo;
                         }
-                        for (; u < nb; ++u) {
-                            const unsigned long long kj = rl64(kb, int(u));
-                            rk += int((kj < ki) | ((kj == ki) & (jb + u < i)));
-                        }
-                        rk += r1 + r2 + r3;
+                        if (rk) atomicAdd(&C.pend[i], rk);
                     }
-                    if (i < I && ki != kNone && rk) atomicAdd(&C.pend[i], rk);
                 }
                 block_sync<NW>();
                 for (uint32_t i = tid; i < I; i += NT)
