@@ -795,3 +795,35 @@ def test_large_clusters_pairing_ends(case):
         moved += int(e["stats"][80:82].sum())
     assert moved > 0, "no migration started"
     assert g.stats()["raw"][86] == 0
+
+
+@pytest.mark.parametrize("name,rpg,ticks", [("gauss10", 3, 300), ("enterprise", 3, 300), ("wide", 2, 150)])
+def test_waiting_seqs_spanning_more_than_2_27(name, rpg, ticks):
+    # The rescans rank on 32-bit keys (tier rank << 27 | seq - lowest seq)
+    # only when the candidates' seqs span less than 2^27, and on the 64-bit
+    # (tier, seq) keys otherwise.  Moving the seqs of the live requests in odd
+    # slots up by 2^28 puts both ranges in every queue (seqs stay distinct;
+    # next_seq moves past them); the imported state then runs as the oracle
+    # runs it.
+    cfg = scaled(name, replicas_per_group=rpg)
+    g = Scheduler(cfg)
+    g.step(ticks)
+    st = g.export()
+    R, I, S = g.R, cfg["n_instances"], cfg["slots_per_instance"]
+    seq = st["seq"].reshape(R, I, S).astype(np.int64)
+    live = (st["meta"].reshape(R, I, S) & 3) != 0
+    odd = (np.arange(S) % 2 == 1)[None, None, :]
+    assert ((st["meta"].reshape(R, I, S) & 3) == 1).sum() > 0, "no request waits"
+    seq = np.where(live & odd, seq + (1 << 28), seq)
+    st["seq"] = seq.reshape(-1).astype(np.uint32)
+    st["next_seq"] = (seq.reshape(R, -1).max(axis=1) + 1).astype(np.uint32)
+    g.import_state(st)
+    o = oracle.Oracle(cfg)
+    o.import_state(st)
+    o.tick = g.tick
+    g.step(200)
+    o.step(200)
+    assert_same(g.export(), o.export(), "%s with seqs spanning 2^28" % name)
+    assert np.array_equal(g.digests(), o.digests())
+    assert g.stats()["raw"][86] == 0
+    g.close()
