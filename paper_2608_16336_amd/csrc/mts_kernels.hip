@@ -1041,7 +1041,8 @@ __device__ inline int rank_extract(KT (&k)[MK], uint32_t (&sd)[MK], bool more, i
 // The same ranked prefix as rank_extract on 32-bit keys, found by selection
 // instead of minimum by minimum: the candidates the extraction can reach are
 // the keys up to the smallest last kept key of a lane with more waiting slots
-// (bnd; all keys when no lane has more); of those, the 64 smallest are the
+// (bnd, from the caller; all keys when no lane has more); the keys taken are
+// removed from the lists (set to none); of those, the 64 smallest are the
 // keys up to a threshold found by bisection over key values (the keys are
 // distinct, counted by ballots); they are gathered into this wave's buffer,
 // ranked by counting and sent to the lane of their rank, and the prefix stops
@@ -1049,11 +1050,10 @@ __device__ inline int rank_extract(KT (&k)[MK], uint32_t (&sd)[MK], bool more, i
 // latency chain is a few dozen scalar steps instead of one wave reduction per
 // request.
 template <int MK>
-__device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd)[MK], bool more, int fr, int lane,
+__device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd)[MK], uint32_t bnd, int fr, int lane,
                                   uint32_t& myk, uint32_t& mysd)
 {
     constexpr uint32_t none = 0xFFFFFFFFu;
-    const uint32_t bnd = wmin32(more ? k[MK - 1] : none);
     bool vx[MK];
     int nvalid = 0;
 #pragma unroll
@@ -1067,11 +1067,15 @@ __device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd
     if (want == 0) return 0;
     uint32_t thr = none;
     if (nvalid > 64) {
-        // the smallest value with 64 candidates at or below it
-        uint32_t hi = 0;
+        // the smallest value with 64 candidates at or below it (a lane's
+        // candidates need not start at k[0]: taken keys are none)
+        uint32_t lo = none, hi = 0;
 #pragma unroll
-        for (int x = 0; x < MK; ++x) hi = vx[x] ? tmax(hi, k[x]) : hi;
-        uint32_t lo = wmin32(k[0]);
+        for (int x = 0; x < MK; ++x) {
+            lo = vx[x] ? tmin(lo, k[x]) : lo;
+            hi = vx[x] ? tmax(hi, k[x]) : hi;
+        }
+        lo = wmin32(lo);
         hi = wmax32(hi);
         while (lo < hi) {
             const uint32_t mid = lo + ((hi - lo) >> 1);
@@ -1083,13 +1087,15 @@ __device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd
         }
         thr = lo;
     }
-    // gather the want selected candidates
+    // gather the want selected candidates (and take them out of the lists)
     int base = 0;
 #pragma unroll
     for (int x = 0; x < MK; ++x) {
         const bool sel = vx[x] && k[x] <= thr;
         const unsigned long long m = ballot(sel);
-        if (sel) C.rsel[base + __popcll(m & lanemask_lt())] = make_uint2(k[x], sd[x]);
+        const int at = base + __popcll(m & lanemask_lt());  // < want <= 64
+        if (sel && at < 64) C.rsel[at] = make_uint2(k[x], sd[x]);
+        if (sel) k[x] = none;
         base += __popcll(m);
     }
     wave_sync();
@@ -1177,33 +1183,46 @@ __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
     }
     slo = wmin32(slo);
     shi = wmax32(shi);
-    unsigned long long myk;
-    uint32_t mysd;
-    int got;
-    if (shi - slo < (1u << 27) || slo > shi) {
-        uint32_t k32[MK];
+    const bool c32 = shi - slo < (1u << 27) || slo > shi;
+    uint32_t k32[MK];
 #pragma unroll
-        for (int x = 0; x < MK; ++x)
-            k32[x] = k[x] == kNone ? 0xFFFFFFFFu : (uint32_t(k[x] >> 32) << 27) | (uint32_t(k[x]) - slo);
-        uint32_t my32;
-        if (SEL) got = rank_select<MK>(C, k32, sd, more, fr, lane, my32, mysd);
-        else got = rank_extract<uint32_t, MK>(k32, sd, more, fr, C.td, lane, my32, mysd);
-        myk = my32 == 0xFFFFFFFFu ? kNone
-                                  : (static_cast<unsigned long long>(my32 >> 27) << 32) | ((my32 & 0x7FFFFFFu) + slo);
-    } else {
-        got = rank_extract<unsigned long long, MK>(k, sd, more, fr, C.td, lane, myk, mysd);
+    for (int x = 0; x < MK; ++x)
+        k32[x] = k[x] == kNone ? 0xFFFFFFFFu : (uint32_t(k[x] >> 32) << 27) | (uint32_t(k[x]) - slo);
+    const uint32_t bnd = SEL && c32 ? wmin32(more ? k32[MK - 1] : 0xFFFFFFFFu) : 0u;
+    for (;;) {
+        unsigned long long myk;
+        uint32_t mysd;
+        int got;
+        if (c32) {
+            uint32_t my32;
+            if (SEL) got = rank_select<MK>(C, k32, sd, bnd, C.freeb[i], lane, my32, mysd);
+            else got = rank_extract<uint32_t, MK>(k32, sd, more, fr, C.td, lane, my32, mysd);
+            myk = my32 == 0xFFFFFFFFu
+                      ? kNone
+                      : (static_cast<unsigned long long>(my32 >> 27) << 32) | ((my32 & 0x7FFFFFFu) + slo);
+        } else {
+            got = rank_extract<unsigned long long, MK>(k, sd, more, fr, C.td, lane, myk, mysd);
+        }
+        if (got == 0) {
+            if (lane == 0) clear_hol(C, i);
+            wave_sync();
+            return false;
+        }
+        const int mys = int(mysd & 0xFFFu);
+        uint32_t w = 0, mt = 0, ta = 0;
+        if (lane < got) { const uint4 rec = C.slot[b + mys]; w = rec.x; mt = rec.y; ta = rec.w; }
+        const bool complete = got >= C.nwait[i];
+        if (lane == 0) C.frs[i] = 0;
+        admit_ranked(C, i, t, lane, got, myk, w, mt, ta, mys, complete);
+        // (selection) every request taken was admitted and more wait: the
+        // candidates left up to bnd are the next smallest keys of the queue,
+        // and are taken without reading the slots again
+        if (!(SEL && c32) || C.hols[i] != kHolUnknown) break;
+        bool left = false;
+#pragma unroll
+        for (int x = 0; x < MK; ++x) left = left || (k32[x] != 0xFFFFFFFFu && k32[x] <= bnd);
+        if (!ballot(left)) break;
     }
-    if (got == 0) {
-        if (lane == 0) clear_hol(C, i);
-        wave_sync();
-        return false;
-    }
-    const int mys = int(mysd & 0xFFFu);
-    uint32_t w = 0, mt = 0, ta = 0;
-    if (lane < got) { const uint4 rec = C.slot[b + mys]; w = rec.x; mt = rec.y; ta = rec.w; }
-    const bool complete = got >= C.nwait[i];
-    if (lane == 0) C.frs[i] = 0;
-    admit_ranked(C, i, t, lane, got, myk, w, mt, ta, mys, complete);
     return C.hols[i] == kHolUnknown;
 }
 
