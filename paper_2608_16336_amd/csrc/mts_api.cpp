@@ -136,6 +136,8 @@ Layout make_layout(const mts_cfg& c, const Tables& T, uint32_t R, uint32_t chunk
     L.arr_cnt = o;  o = up256(o + size_t(R) * chunk * 4);
     L.arr_rec = o;  o = up256(o + size_t(R) * chunk * cap * 8);
     L.wheel = o;    o = up256(o + size_t(R) * wsz * wcap * 4);
+    // the queue cache's extension, for the kernels of more than 64 instances
+    L.qx = o;       o = up256(o + (I > 64 ? size_t(R) * I * kQxDepth * 16 : 0));
     L.total = o;
     return L;
 }
@@ -210,6 +212,7 @@ Params make_params(const mts_ctx* h)
     p.arr_cnt = reinterpret_cast<uint32_t*>(d + L.arr_cnt);
     p.arr_rec = reinterpret_cast<unsigned long long*>(d + L.arr_rec);
     p.wheel = reinterpret_cast<uint32_t*>(d + L.wheel);
+    p.qx = h->I > 64 ? reinterpret_cast<uint4*>(d + L.qx) : nullptr;
     return p;
 }
 

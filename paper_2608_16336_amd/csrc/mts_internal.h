@@ -66,8 +66,13 @@ struct Layout {
     size_t next_seq, stats, digest;                                     // [R], [R][NSTAT], [R]
     size_t arr_cnt, arr_rec;                                            // [R][chunk], [R][chunk][cap]
     size_t wheel;                                                       // [R][wsz][wcap]
+    size_t qx;                                                          // [R][I][kQxDepth] uint4 (I > 64 only)
     size_t total;
 };
+
+// The kernels for more than 64 instances keep, behind each instance's queue
+// cache in LDS, up to this many further waiting requests in order in HBM.
+constexpr uint32_t kQxDepth = 64;
 
 // Everything a kernel launch needs, passed by value.
 struct Params {
@@ -115,6 +120,7 @@ struct Params {
     uint32_t* arr_cnt;
     unsigned long long* arr_rec;
     uint32_t* wheel;
+    uint4* qx;                     // [R][I][kQxDepth] queue cache extension (I > 64; null otherwise)
 };
 
 // LDS bytes of one wave (one replica) of the step kernel

@@ -63,7 +63,7 @@ enum { kXSlo = 0, kXAge = 10, kXPromoMin = 20, kXPromoPeriod, kXAdaptEpoch, kXAd
 static_assert(kXWords == MTS_EXT_WORDS, "extension table size");
 
 struct LdsLayout {
-    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, ext, blk, rsel, total;
+    uint32_t stats, occ, holk, fd, ints, res, tcnt, mig, last, vic, wc, wov, inf, qt, qn, xn, ext, blk, rsel, total;
 };
 
 // Waves per replica: the kernels for 128 or more instances run a workgroup of
@@ -108,6 +108,8 @@ __host__ __device__ inline LdsLayout lds_layout(uint32_t IM, uint32_t I, uint32_
     o = (o + 15u) & ~15u;
     L.qt = o;    o += IM * qdepth * 16;
     L.qn = o;    o += qdepth ? IM * 8 : 0;
+    // multi-wave kernels: per instance the queue cache extension's head << 16 | count
+    L.xn = o;    o += waves_for(IM) > 1 ? IM * 4 : 0;
     // adaptive headroom / promotion: the ticks left to the next promotion
     // pass and headroom update, and per instance a lower bound on the
     // arrival ticks of its waiting requests (the rest of their state stays
@@ -156,6 +158,10 @@ struct Ctx {
     uint4* qt;                 // [I][td] a ring: entry k at (qh + k) mod td
     int* qn;                   // [I] cached entries
     int* qh;                   // [I] ring position of the first entry
+    // kernels for 128+ instances (null otherwise): behind the ring, up to
+    // kQxDepth further waiting requests of the instance in order, in HBM
+    int* xn;                   // [I] head << 16 | count
+    uint4* qx;                 // [I][kQxDepth] this replica's extensions
     int td;
     uint32_t blind;            // 1: tiers order nothing (tier-blind scheduling)
     // adaptive headroom and promotion (null when both are off): the LDS
@@ -252,6 +258,8 @@ __device__ inline Ctx carve(char* base, const Params& P)
     C.qt = reinterpret_cast<uint4*>(base + Y.qt);
     C.qn = reinterpret_cast<int*>(base + Y.qn);
     C.qh = C.qn + IM;
+    C.xn = waves_for(IM) > 1 ? reinterpret_cast<int*>(base + Y.xn) : nullptr;
+    C.qx = nullptr;  // per replica, set with the slot records
     if (INF) {
         C.fsum = reinterpret_cast<unsigned long long*>(base + Y.inf);
         C.svc = reinterpret_cast<long long*>(base + Y.inf + IM * 8);
@@ -511,10 +519,17 @@ __device__ __forceinline__ unsigned long long perm64(unsigned long long v, int s
 // per-instance event handlers (uniform: the whole wave works on instance i)
 // ---------------------------------------------------------------------------
 
+__device__ __forceinline__ void qx_clear(const Ctx& C, int i)
+{
+    if (C.xn) C.xn[i] = 0;
+}
+__device__ __forceinline__ int qx_count(const Ctx& C, int i) { return C.xn ? (C.xn[i] & 0xFFFF) : 0; }
+
 __device__ __forceinline__ void clear_hol(const Ctx& C, int i)
 {
     C.hols[i] = kNoHol; C.holk[i] = kNone; C.hold[i] = 0;
     if (C.td) C.qn[i] = 0;
+    qx_clear(C, i);
 }
 
 __device__ __forceinline__ void set_hol(const Ctx& C, int i, int slot, unsigned long long key, uint32_t word,
@@ -524,9 +539,9 @@ __device__ __forceinline__ void set_hol(const Ctx& C, int i, int slot, unsigned 
     C.hwd[i] = word; C.hmt[i] = meta; C.hta[i] = tarr;
 }
 
-// Queue cache.  Invariant: the head of line and the qn[i] cached entries are
-// the qn[i] + 1 smallest (tier, seq) keys among instance i's waiting
-// requests, in order.  The functions below are per lane (lane-private
+// Queue cache.  Invariant: the head of line, the qn[i] cached entries and
+// (kernels for 128+ instances) the extension's entries are the smallest
+// (tier, seq) keys among instance i's waiting requests, in order.  The functions below are per lane (lane-private
 // instance i) and keep it: popping the head promotes the first cached entry
 // (or leaves the head unknown, to be found by a rescan), a new waiting
 // request becomes the head or enters the cache at its place when it is
@@ -556,6 +571,7 @@ __device__ __forceinline__ int qc_at(const Ctx& C, int i, int k)
 __device__ inline void qc_insert_at(const Ctx& C, int i, int p, uint4 e)
 {
     const int n = C.qn[i];
+    if (n >= C.td) qx_clear(C, i);  // the last entry drops out: the extension no longer follows
     if (p == 0) {
         // in front: the ring start moves back (over the last entry when full)
         const int h = C.qh[i];
@@ -574,7 +590,17 @@ __device__ inline void hol_pop(const Ctx& C, int i)
 {
     if (C.nwait[i] == 0) { clear_hol(C, i); return; }
     const int n = C.td ? C.qn[i] : 0;
-    if (n == 0) { C.hols[i] = kHolUnknown; return; }
+    if (n == 0) {
+        const int xv = C.xn ? C.xn[i] : 0;
+        if ((xv & 0xFFFF) == 0) { C.hols[i] = kHolUnknown; return; }
+        // the extension's first entry becomes the head of line
+        const int xh = xv >> 16;
+        const uint4 e = C.qx[size_t(i) * kQxDepth + xh];
+        const uint32_t tier = (e.w >> 12) & 15u;
+        set_hol(C, i, int(e.w & 0xFFFu), qc_key(C, e), e.y, kWaiting | (tier << 2) | (((e.w >> 16) & 1u) << 6), e.z);
+        C.xn[i] = ((xh + 1) << 16) | ((xv & 0xFFFF) - 1);
+        return;
+    }
     const uint4 e = C.qt[qc_at(C, i, 0)];
     const uint32_t tier = (e.w >> 12) & 15u;
     set_hol(C, i, int(e.w & 0xFFFu), qc_key(C, e), e.y, kWaiting | (tier << 2) | (((e.w >> 16) & 1u) << 6), e.z);
@@ -588,7 +614,7 @@ __device__ inline void hol_insert(const Ctx& C, int i, unsigned long long key, i
 {
     const int h = C.hols[i];
     if (h == kHolUnknown) return;
-    if (h == kNoHol) { set_hol(C, i, slot, key, word, meta, tarr); if (C.td) C.qn[i] = 0; return; }
+    if (h == kNoHol) { set_hol(C, i, slot, key, word, meta, tarr); if (C.td) C.qn[i] = 0; qx_clear(C, i); return; }
     if (key < C.holk[i]) {
         if (C.td) qc_insert_at(C, i, 0, qc_pack(C.holk[i], h, C.hwd[i], C.hmt[i], C.hta[i]));
         set_hol(C, i, slot, key, word, meta, tarr);
@@ -599,6 +625,7 @@ __device__ inline void hol_insert(const Ctx& C, int i, unsigned long long key, i
     int p = 0;
     while (p < n && qc_key(C, C.qt[qc_at(C, i, p)]) < key) ++p;
     if (p < n) qc_insert_at(C, i, p, qc_pack(key, slot, word, meta, tarr));
+    else qx_clear(C, i);  // beyond the cached run: it may fall inside the extension
 }
 
 // file a running request under its finish tick
@@ -986,10 +1013,14 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
             if (C.td) C.qn[i] = 0;
         }
         if (C.td && na < w) { C.qn[i] = min(w - na - 1, C.td); C.qh[i] = 0; }
+        if (C.xn) C.xn[i] = C.td && na < w && w - na - 1 > C.td ? w - na - 1 - C.td : 0;
     }
-    // the ranked list holds the smallest keys: the ones after the new head fill the cache
+    // the ranked list holds the smallest keys: the ones after the new head fill
+    // the cache, and the ones after those its extension
     if (C.td && lane > na && lane < w && lane - na - 1 < C.td)
         C.qt[i * C.td + lane - na - 1] = qc_pack(key, slot, word, meta, ta);
+    if (C.xn && C.td && lane > na + C.td && lane < w)
+        C.qx[size_t(i) * kQxDepth + (lane - na - 1 - C.td)] = qc_pack(key, slot, word, meta, ta);
     wave_sync();
 }
 
@@ -1041,14 +1072,13 @@ __device__ inline int rank_extract(KT (&k)[MK], uint32_t (&sd)[MK], bool more, i
 // The same ranked prefix as rank_extract on 32-bit keys, found by selection
 // instead of minimum by minimum: the candidates the extraction can reach are
 // the keys up to the smallest last kept key of a lane with more waiting slots
-// (bnd, from the caller; all keys when no lane has more); the keys taken are
-// removed from the lists (set to none); of those, the 64 smallest are the
-// keys up to a threshold found by bisection over key values (the keys are
-// distinct, counted by ballots); they are gathered into this wave's buffer,
-// ranked by counting and sent to the lane of their rank, and the prefix stops
-// qdepth requests after the first one whose summed demand exceeds fr.  The
-// latency chain is a few dozen scalar steps instead of one wave reduction per
-// request.
+// (bnd, from the caller; all keys when no lane has more).  Of those, the 64
+// smallest are the keys up to a threshold found by bisection over key values
+// (the keys are distinct, counted by ballots); they are gathered into this
+// wave's buffer, taken out of the lists (set to none), ranked by counting and
+// sent to the lane of their rank, and the prefix stops qdepth requests after
+// the first one whose summed demand exceeds fr.  The latency chain is a few
+// dozen scalar steps instead of one wave reduction per request.
 template <int MK>
 __device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd)[MK], uint32_t bnd, int fr, int lane,
                                   uint32_t& myk, uint32_t& mysd)
@@ -1117,7 +1147,9 @@ __device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd
     const uint32_t ss = uint32_t(__builtin_amdgcn_ds_permute(rank * 4, int(cs)));
     const int cum = wscan(lane < want ? int(ss >> 12) : 0, lane);
     const unsigned long long over = ballot(lane < want && cum > fr);
-    const int got = over ? min(want, ffs64(over) + 1 + C.td) : want;
+    // (with the extension every selected request is kept: the head of line,
+    // the cache and the extension take them)
+    const int got = over && !C.xn ? min(want, ffs64(over) + 1 + C.td) : want;
     if (lane < got) { myk = sk; mysd = ss; }
     return got;
 }
@@ -1131,9 +1163,13 @@ __device__ inline int rank_select(const Ctx& C, uint32_t (&k)[MK], uint32_t (&sd
 // one whose cumulative demand exceeds the free blocks (the new head of line
 // and the cache behind it).  A second read fetches the fields of the requests
 // taken, and the longest fitting prefix is admitted at once (admit_ranked).
-// GR chunks of 64 slots are read per memory round trip.  Returns true when
-// every request taken was admitted and more wait (the head of line is still
-// unknown).  Uniform.
+// The minima are taken on 32-bit keys when the candidates' seqs allow
+// (rank_extract); with SEL (the kernels for 128+ instances) the same prefix
+// is found by selection (rank_select), and when every request taken fits the
+// candidates left up to the exhaustion bound are taken next without reading
+// the slots again.  GR chunks of 64 slots are read per memory round trip.
+// Returns true when every request taken was admitted and more wait (the head
+// of line is still unknown).  Uniform.
 template <int GR, int MK, bool SEL = false>
 __device__ inline bool rescan_admit(const Ctx& C, int i, uint32_t t, int lane)
 {
@@ -1293,13 +1329,15 @@ __device__ inline void admit_batch(const Ctx& C, int i, uint32_t t, int lane)
 __device__ inline void admit_cached(const Ctx& C, int i, uint32_t t, int lane)
 {
     const int n = C.qn[i];
+    // (kernels for 128+ instances) the extension follows the ring: n + xc <= 63
+    const int xv = C.xn ? C.xn[i] : 0, xc = xv & 0xFFFF, xh = xv >> 16;
     unsigned long long key = kNone;
     uint32_t word = 0, meta = 0, ta = 0;
     int slot = 0;
     if (lane == 0) {
         key = C.holk[i]; word = C.hwd[i]; meta = C.hmt[i]; ta = C.hta[i]; slot = C.hols[i];
-    } else if (lane <= n) {
-        const uint4 e = C.qt[qc_at(C, i, lane - 1)];
+    } else if (lane <= n + xc) {
+        const uint4 e = lane <= n ? C.qt[qc_at(C, i, lane - 1)] : C.qx[size_t(i) * kQxDepth + xh + lane - n - 1];
         const uint32_t tier = (e.w >> 12) & 15u;
         key = qc_key(C, e);
         word = e.y;
@@ -1307,8 +1345,8 @@ __device__ inline void admit_cached(const Ctx& C, int i, uint32_t t, int lane)
         ta = e.z;
         slot = int(e.w & 0xFFFu);
     }
-    const bool complete = C.nwait[i] == n + 1;
-    admit_ranked(C, i, t, lane, n + 1, key, word, meta, ta, slot, complete);
+    const bool complete = C.nwait[i] == n + xc + 1;
+    admit_ranked(C, i, t, lane, n + xc + 1, key, word, meta, ta, slot, complete);
 }
 
 // Admission of instance i whose waiting requests all arrived in the previous
@@ -1384,7 +1422,7 @@ __device__ inline void admit_all(const Ctx& C, int i, uint32_t t, int lane)
         }
         if (h < 0 || C.hold[i] > C.freeb[i]) break;
         const int nw = C.nwait[i];
-        const bool cached = C.td && C.qn[i] > 0;
+        const bool cached = C.td && (C.qn[i] > 0 || qx_count(C, i) > 0);
         if (nw >= 2 && nw <= 64 && C.frs[i]) {
             admit_fresh(C, i, t, lane);
         } else if (nw >= 2 && nw <= 64 && !cached) {
@@ -1452,6 +1490,7 @@ __device__ inline void promote_waiting(const Ctx& C, const Params& P, uint32_t t
                 C.frs[i] = 0;
                 if (hit || h < 0 || kmin < C.holk[i]) C.hols[i] = kHolUnknown;
                 else if (C.td) C.qn[i] = 0;
+                qx_clear(C, i);
             }
         }
     }
@@ -1545,6 +1584,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
         for (int p = 0; p < kTiers; ++p) C.hq[p] = hq[p];
         const size_t rb = size_t(r) * I * S;
         C.slot = P.slot + rb;
+        if (C.xn) C.qx = P.qx + size_t(r) * I * kQxDepth;
         C.wheel = P.wheel + size_t(r) * wsz * P.wcap;
         C.hist = P.hist + size_t(r) * kHistPerReplica;
 
@@ -1559,6 +1599,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
             C.tmask[i] = 0;
             C.frs[i] = 0;
             if (C.td) { C.qn[i] = 0; C.qh[i] = 0; }
+            if (C.xn) C.xn[i] = 0;
             if (C.svc) C.svc[i] = P.svc[size_t(r) * I + i];
         }
         for (uint32_t b = tid; b < wsz / 2; b += NT) C.wc[b] = 0;
@@ -2125,6 +2166,7 @@ __global__ __launch_bounds__(64 * waves_for(IM), IM <= 64 ? 4 : 2) void k_step(P
                             // fall between cached entries, so the cache is emptied
                             if (nadd[j] > (pend_r[j] >= 0 ? 1 : 0)) {
                                 C.qn[i] = 0;
+                                qx_clear(C, int(i));
                             } else if (C.hols[i] >= 0) {
                                 qc_insert_at(C, int(i), 0, qc_pack(C.holk[i], C.hols[i], C.hwd[i], C.hmt[i], C.hta[i]));
                             }
