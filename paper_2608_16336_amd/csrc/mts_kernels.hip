@@ -969,8 +969,13 @@ __device__ __forceinline__ void tier_stat3(const Ctx& C, int tier, bool f0, int 
 // a time).  The list holds every waiting request of i (complete) or the w
 // smallest keys of a longer queue; when all w of those fit, the head of line
 // is unknown afterwards (the next rescan finds it).
+// xn0 >= 0: the list is the head of line, the xn0 cached entries and the
+// extension from its head xh0 on (admit_cached): the new extension is then
+// a suffix of the stored one (the cache never holds more than qdepth), so
+// only its head moves.
 __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, int w, unsigned long long key,
-                                    uint32_t word, uint32_t meta, uint32_t ta, int slot, bool complete = true)
+                                    uint32_t word, uint32_t meta, uint32_t ta, int slot, bool complete = true,
+                                    int xn0 = -1, int xh0 = 0)
 {
     const size_t b = size_t(i) * C.S;
     const int dem = lane < w ? blocks_of(wlo(word), C.shift) : 0;
@@ -1013,13 +1018,16 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
             if (C.td) C.qn[i] = 0;
         }
         if (C.td && na < w) { C.qn[i] = min(w - na - 1, C.td); C.qh[i] = 0; }
-        if (C.xn) C.xn[i] = C.td && na < w && w - na - 1 > C.td ? w - na - 1 - C.td : 0;
+        if (C.xn) {
+            const int xc = C.td && na < w && w - na - 1 > C.td ? w - na - 1 - C.td : 0;
+            C.xn[i] = xc && xn0 >= 0 ? ((xh0 + na + C.td - xn0) << 16) | xc : xc;
+        }
     }
     // the ranked list holds the smallest keys: the ones after the new head fill
     // the cache, and the ones after those its extension
     if (C.td && lane > na && lane < w && lane - na - 1 < C.td)
         C.qt[i * C.td + lane - na - 1] = qc_pack(key, slot, word, meta, ta);
-    if (C.xn && C.td && lane > na + C.td && lane < w)
+    if (C.xn && C.td && xn0 < 0 && lane > na + C.td && lane < w)
         C.qx[size_t(i) * kQxDepth + (lane - na - 1 - C.td)] = qc_pack(key, slot, word, meta, ta);
     wave_sync();
 }
@@ -1346,7 +1354,7 @@ __device__ inline void admit_cached(const Ctx& C, int i, uint32_t t, int lane)
         slot = int(e.w & 0xFFFu);
     }
     const bool complete = C.nwait[i] == n + xc + 1;
-    admit_ranked(C, i, t, lane, n + xc + 1, key, word, meta, ta, slot, complete);
+    admit_ranked(C, i, t, lane, n + xc + 1, key, word, meta, ta, slot, complete, C.xn ? n : -1, xh);
 }
 
 // Admission of instance i whose waiting requests all arrived in the previous
