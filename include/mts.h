@@ -361,8 +361,9 @@ int mts_get_launch(mts_handle h, uint32_t* threads, uint32_t* blocks);
  * admitting or moving the head does not rescan the instance's slots.
  * mts_create picks the deepest of 7, 3, 1 (15, 11, 7, 3, 1 for 128 or more
  * instances; else 0) entries that keeps the step kernel's blocks per compute
- * unit.  Results never depend on the depth (a performance
- * setting, also a test hook).  mts_set_queue_cache takes effect at the next
+ * unit.  For more than 64 instances the cache continues in the state buffer
+ * (up to 64 further requests per instance).  Results never depend on the
+ * depth (a performance setting, also a test hook).  mts_set_queue_cache takes effect at the next
  * mts_step; MTS_EINVAL for a depth above 15 or one whose LDS does not fit. */
 int mts_set_queue_cache(mts_handle h, uint32_t depth);
 int mts_get_queue_cache(mts_handle h, uint32_t* depth);

@@ -506,15 +506,6 @@ __device__ __forceinline__ int wscan(int x, int lane)
     return x;
 }
 
-// value of lane src (any lane, through the LDS crossbar without LDS storage)
-__device__ __forceinline__ int perm32(int v, int src) { return __builtin_amdgcn_ds_bpermute(src << 2, v); }
-__device__ __forceinline__ unsigned long long perm64(unsigned long long v, int src)
-{
-    const unsigned lo = unsigned(perm32(int(unsigned(v)), src));
-    const unsigned hi = unsigned(perm32(int(unsigned(v >> 32)), src));
-    return (static_cast<unsigned long long>(hi) << 32) | lo;
-}
-
 // ---------------------------------------------------------------------------
 // per-instance event handlers (uniform: the whole wave works on instance i)
 // ---------------------------------------------------------------------------
@@ -1043,8 +1034,6 @@ __device__ inline void admit_ranked(const Ctx& C, int i, uint32_t t, int lane, i
 // all-ones as "none".
 __device__ __forceinline__ uint32_t wmin_k(uint32_t x) { return wmin32(x); }
 __device__ __forceinline__ unsigned long long wmin_k(unsigned long long x) { return wmin64(x); }
-__device__ __forceinline__ uint32_t rl_k(uint32_t x, int l) { return rlu(x, l); }
-__device__ __forceinline__ unsigned long long rl_k(unsigned long long x, int l) { return rl64(x, l); }
 
 template <typename KT, int MK>
 __device__ inline int rank_extract(KT (&k)[MK], uint32_t (&sd)[MK], bool more, int fr, int td, int lane, KT& myk,
