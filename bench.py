@@ -43,7 +43,7 @@ VALU_PEAK_GINST = 256 * 2.4
 #   read, write   HBM bytes per launch from TCC_EA0_RDREQ_{32B,64B,128B} and
 #                 TCC_EA0_WRREQ{,_64B} (requests times their sizes)
 PROFILED = {
-    '4d316b5ba371f2f8': {"valu_per_rt": 891.04, "lane_util": 0.3672, "read": 9127152902, "write": 7658471955},
+    'e7eb6393498a72f8': {"valu_per_rt": 869.2, "lane_util": 0.3756, "read": 9133853824, "write": 7667387645},
 }
 
 
