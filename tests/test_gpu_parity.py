@@ -691,6 +691,40 @@ def test_random_clusters_with_adaptive_headroom_and_promotion(case):
     assert g.stats()["raw"][86] == 0
 
 
+@pytest.mark.parametrize("case", range(8))
+def test_large_random_clusters_with_adaptive_headroom_and_promotion(case):
+    # 65..256 instances: the eight-wave kernels, whose queue cache continues
+    # in HBM, under promotion (which drops that cache) and adaptive headroom;
+    # queue-cache depths from none to the deepest
+    rng = random.Random(15000 + case)
+    cfg = _wide_random_cfg(rng)
+    cfg["n_instances"] = rng.choice([65, 128, 200, 256])
+    cfg["slots_per_instance"] = rng.choice([128, 256, 512])
+    cfg["mig_max_pairs"] = rng.randint(0, cfg["n_instances"] // 2)
+    cfg["arrival"] = dict(kind="gamma_poisson", mean=rng.choice([20.0, 80.0]), cv=2.0)
+    cfg = _with_extensions(rng, cfg)
+    g = Scheduler(cfg)
+    depth = rng.choice([None, 0, 1, 7, 15])
+    if depth is not None:
+        g.queue_cache = depth
+    orc = [oracle.Oracle(cfg, r, 1) for r in range(g.R)]
+    for n in (1, 70, 129):  # launches start on and off the update ticks
+        g.step(n)
+        for o in orc:
+            o.step(n)
+    _compare(g, orc, "case %d" % case)
+    assert g.stats()["raw"][86] == 0
+
+
+def test_wide_with_adaptive_headroom_and_promotion():
+    cfg = scaled("wide", replicas_per_group=2)
+    cfg["adaptive"] = dict(epoch=25, step_up=2048, step_down=512, max=256 * cfg["kv_blocks"] // 4, margin=128,
+                           slo=[2, 6, 15, 40, 100])
+    cfg["promotion"] = dict(period=5, age=[0] + [40 + 10 * p for p in range(1, 10)])
+    g = run_both(cfg, 400)
+    assert g.stats()["raw"][86] == 0
+
+
 @pytest.mark.parametrize("name,rpg,ticks", [("gauss10", 3, 500), ("sweep", 1, 300), ("enterprise", 4, 400)])
 def test_extension_presets_reduced(name, rpg, ticks):
     cfg = scaled(name, replicas_per_group=rpg)
